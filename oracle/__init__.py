@@ -1,0 +1,13 @@
+"""fp64 CPU oracle for MSSA (test infrastructure only).
+
+Only the test suite, the smoke check and the benchmark's CPU-baseline leg may
+import this package.  The GPU library never imports it, and it imports
+nothing from the library.
+"""
+from .mssa_oracle import (  # noqa: F401
+    KIND_HIST, KIND_SINK, KIND_WIN, algorithmic_flops, attention,
+    brute_force_attention, context, context_rows, frame_tokens, grid,
+    mssa_attention, num_hist_tokens, num_sink_tokens, num_window_tokens,
+    pool_frame, pooled_kv, query_groups, scales_in_use, softmax_scale, tables,
+    window_frames,
+)
