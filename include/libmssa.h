@@ -1,0 +1,173 @@
+/*
+ * libmssa -- Multi-Scale Self-Attention (MSSA) over a Multi-Scale
+ * Patchification (MSP) rolling window, for AMD Instinct MI355X (gfx950).
+ *
+ * Method: Ms. Forcing, Sec. 4.1.  A rolling window (Sec. 3.1, Eq. 2) holds
+ * T states; state l carries F latent frames tokenized at patch scale p_l
+ * (a power-of-two multiple of the native patch, nondecreasing in l), so a
+ * frame of H x W native tokens becomes a ceil(H/p_l) x ceil(W/p_l) grid
+ * (Eq. 3).  Queries at scale s attend to (Eq. 4)
+ *     [ sink frames at native density
+ *     | history frames average-pooled to scale s
+ *     | every window frame b at scale max(s, p_b), pooled from p_b ]
+ * with softmax(scale * q k^T) v per head.  Frames coarser than the query keep
+ * their own scale; the sink is never resampled.  A pooled cell averages the
+ * cells of its f x f block that exist (ragged edges average fewer cells).
+ *
+ * Conventions shared by every entry point
+ *   - Tensors are token-major, contiguous [tokens, num_heads, head_dim], in
+ *     the plan's dtype (bf16 or fp32), 16-byte aligned device pointers.
+ *     Window tokens are ordered (state 1..T, frame, row, col) at the state's
+ *     scale; sink and history tokens are (frame, row, col) at native scale,
+ *     history oldest first.
+ *   - The caller owns all device memory (inputs, output, workspace).  The
+ *     library never allocates or frees device memory; a plan owns only host
+ *     memory.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     Device entry points only enqueue work on it and never synchronise; a
+ *     fault inside a kernel surfaces at the caller's next synchronisation.
+ *   - Every entry point validates its arguments before enqueuing anything
+ *     and returns a status; no C++ exception crosses this boundary.
+ *     mssa_last_error() returns a thread-local message for the last failure.
+ *   - A plan is immutable after creation and may be shared between threads
+ *     and streams; concurrent calls need one workspace each.
+ *   - Kernels use fixed reduction orders and no atomics: results are
+ *     bitwise reproducible run to run.
+ */
+#ifndef LIBMSSA_H
+#define LIBMSSA_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MSSA_MAX_STATES 8
+
+typedef struct mssa_plan_s* mssa_plan;
+
+typedef enum {
+  MSSA_OK = 0,
+  MSSA_ERR_INVALID_ARG = 1, /* null pointer, bad size, inconsistent argument */
+  MSSA_ERR_UNSUPPORTED = 2, /* valid descriptor this build does not run */
+  MSSA_ERR_WORKSPACE = 3,   /* workspace missing or smaller than required */
+  MSSA_ERR_DEVICE = 4,      /* HIP launch or runtime error */
+  MSSA_ERR_NO_MEMORY = 5    /* host allocation failed */
+} mssa_status;
+
+typedef enum { MSSA_BF16 = 0, MSSA_F32 = 1 } mssa_dtype;
+
+/* Static problem description (Sec. 4.1 problem statement; Sec. 5.1 sizes). */
+typedef struct {
+  int32_t num_states;               /* T, 1..MSSA_MAX_STATES */
+  int32_t scales[MSSA_MAX_STATES];  /* p_l / p for l = 1..T: powers of two in
+                                       [1, 64], nondecreasing (Sec. 4.1) */
+  int32_t grid_h, grid_w;           /* native token grid of a latent frame */
+  int32_t frames_per_state;         /* F latent frames per window state */
+  int32_t sink_frames;              /* S native sink frames (>= 0) */
+  int32_t hist_frames;              /* Hh native history frames (>= 0) */
+  int32_t num_heads;                /* >= 1 */
+  int32_t head_dim;                 /* 64 or 128 */
+  int32_t dtype;                    /* mssa_dtype of every tensor */
+  float softmax_scale;              /* <= 0 selects 1/sqrt(head_dim) */
+} mssa_plan_desc;
+
+/* Sizes derived by the plan.  Group g is the g-th distinct query scale in
+ * window token order; its queries are the contiguous range
+ * [q_begin[g], q_end[g]) and its context has n_kv[g] tokens per head.
+ * The pooled K/V that group g reads (history pooled to its scale, then the
+ * window frames finer than its scale pooled to it, in context order) live in
+ * the workspace at byte offsets pooled_k_offset[g] / pooled_v_offset[g],
+ * pooled_tokens[g] tokens each, laid out [tokens, num_heads, head_dim]. */
+typedef struct {
+  int64_t n_q;              /* window (query) tokens */
+  int64_t n_sink_tok;       /* sink_frames * grid_h * grid_w */
+  int64_t n_hist_tok;       /* hist_frames * grid_h * grid_w */
+  int64_t workspace_bytes;  /* minimum workspace for pool_kv / forward */
+  int64_t pairs_per_head;   /* sum over groups of queries * n_kv */
+  int64_t flops_alg;        /* 4 * head_dim * num_heads * pairs_per_head */
+  int64_t pool_bytes_alg;   /* bytes pool_kv must read once and write once */
+  int32_t n_groups;
+  int32_t group_scale[MSSA_MAX_STATES];
+  int32_t q_begin[MSSA_MAX_STATES];
+  int32_t q_end[MSSA_MAX_STATES];
+  int64_t n_kv[MSSA_MAX_STATES];
+  int64_t pooled_k_offset[MSSA_MAX_STATES];
+  int64_t pooled_v_offset[MSSA_MAX_STATES];
+  int64_t pooled_tokens[MSSA_MAX_STATES];
+} mssa_plan_info;
+
+/* Build the static plan: MSP grids (Eq. 3), query groups, the per-scale
+ * context segment tables (Eq. 4), pool jobs and the kernel work list.
+ * Host only.  Returns MSSA_ERR_INVALID_ARG for a malformed descriptor or
+ * null pointer, MSSA_ERR_UNSUPPORTED for a schedule that is not made of
+ * nondecreasing powers of two, head_dim not in {64, 128}, or sizes beyond
+ * the 32-bit token indexing of the kernels.  *out is set only on success;
+ * release it with mssa_plan_destroy. */
+mssa_status mssa_plan_create(const mssa_plan_desc* desc, mssa_plan* out);
+
+/* Release a plan (NULL is ignored).  The caller must not use it afterwards
+ * and must have no work using it still pending on any stream. */
+void mssa_plan_destroy(mssa_plan plan);
+
+/* Copy the derived sizes into *info (host). */
+mssa_status mssa_plan_query(mssa_plan plan, mssa_plan_info* info);
+
+/* Export the plan tables as int64 values (host):
+ *   [n_grid, n_qgrp, n_seg,
+ *    GRID rows  {scale, gh, gw, tokens}                        x n_grid,
+ *    QGRP rows  {q_scale, q_begin, q_end, n_kv}                x n_qgrp,
+ *    SEG rows   {q_scale, kind, frame, src_scale, eff_scale,
+ *                factor, n_tok, kv_begin}                      x n_seg,
+ *    TOTAL      {n_q, pairs_per_head}]
+ * kind: 0 sink, 1 history, 2 window; frame: index within its kind (window
+ * frames counted across states).  SEG rows are in context order: sink,
+ * history oldest first, window state 1..T (Eq. 4).  *needed receives the
+ * number of int64 values; if cap < *needed nothing is written and
+ * MSSA_ERR_INVALID_ARG is returned (dst may be NULL to query the size). */
+mssa_status mssa_plan_tables(mssa_plan plan, int64_t* dst, int64_t cap, int64_t* needed);
+
+/* K/V resampling (Eq. 4 "Subsample", read as an average pool): for every
+ * query scale s > 1, average-pool each history frame from native and each
+ * window frame with p_b < s from p_b to scale s, over the cells that exist
+ * in each block, for K and V alike, every head and channel.  fp32
+ * accumulation; results rounded to the plan dtype (round-to-nearest-even)
+ * into the workspace at the offsets mssa_plan_query reports.
+ *   k_hist, v_hist  [n_hist_tok, H, D] device (NULL iff hist_frames == 0)
+ *   k_win, v_win    [n_q, H, D] device
+ *   workspace       device, >= workspace_bytes, 256-byte aligned
+ * Enqueues on `stream`; a plan with a single query scale 1 enqueues
+ * nothing. */
+mssa_status mssa_pool_kv(mssa_plan plan, const void* k_hist, const void* v_hist,
+                         const void* k_win, const void* v_win, void* workspace,
+                         int64_t workspace_bytes, void* stream);
+
+/* Multi-scale self-attention forward (Eq. 4): for every head and query
+ * scale s, out = softmax(softmax_scale * q k^T) v over the context of s,
+ * reading sink/history/window K/V directly and the pooled K/V that
+ * mssa_pool_kv wrote to `workspace` earlier on the same stream.  bf16 plans
+ * use bf16 matrix cores with fp32 accumulation and an fp32 online softmax;
+ * fp32 plans compute in fp32 throughout.
+ *   q_win            [n_q, H, D] device
+ *   k_sink, v_sink   [n_sink_tok, H, D] device (NULL iff sink_frames == 0)
+ *   k_hist, v_hist   [n_hist_tok, H, D] device (NULL iff hist_frames == 0)
+ *   k_win, v_win     [n_q, H, D] device
+ *   workspace        as passed to mssa_pool_kv
+ *   out              [n_q, H, D] device, same dtype, must not alias inputs */
+mssa_status mssa_forward(mssa_plan plan, const void* q_win, const void* k_sink,
+                         const void* v_sink, const void* k_hist, const void* v_hist,
+                         const void* k_win, const void* v_win, const void* workspace,
+                         int64_t workspace_bytes, void* out, void* stream);
+
+/* Name of a status code (static string). */
+const char* mssa_status_string(mssa_status s);
+
+/* Detail of the last non-OK status returned on this thread ("" if none). */
+const char* mssa_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LIBMSSA_H */

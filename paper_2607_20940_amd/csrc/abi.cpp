@@ -1,0 +1,234 @@
+// C ABI of libmssa (declared in include/libmssa.h).  Validates every call
+// before enqueuing work, turns the immutable plan into kernel arguments, and
+// keeps C++ exceptions on this side of the boundary.
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "../../include/libmssa.h"
+#include "kernels.hpp"
+#include "plan.hpp"
+
+struct mssa_plan_s {
+  mssa::Plan p;
+  std::vector<int> order;  // groups, longest context first
+};
+
+namespace {
+
+thread_local std::string g_last_error;
+
+mssa_status fail(mssa_status s, const std::string& msg) {
+  g_last_error = msg;
+  return s;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+mssa_status check_device(hipError_t e, const char* what) {
+  if (e == hipSuccess) return MSSA_OK;
+  return fail(MSSA_ERR_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+}  // namespace
+
+extern "C" {
+
+mssa_status mssa_plan_create(const mssa_plan_desc* desc, mssa_plan* out) {
+  if (!desc || !out) return fail(MSSA_ERR_INVALID_ARG, "desc and out must be non-null");
+  try {
+    auto* h = new mssa_plan_s;
+    std::string err;
+    const mssa_status s = mssa::build_plan(*desc, h->p, err);
+    if (s != MSSA_OK) {
+      delete h;
+      return fail(s, err);
+    }
+    const int G = static_cast<int>(h->p.groups.size());
+    for (int g = 0; g < G; ++g) h->order.push_back(g);
+    std::stable_sort(h->order.begin(), h->order.end(),
+                     [&](int x, int y) { return h->p.groups[x].n_kv > h->p.groups[y].n_kv; });
+    *out = h;
+    return MSSA_OK;
+  } catch (const std::bad_alloc&) {
+    return fail(MSSA_ERR_NO_MEMORY, "host allocation failed");
+  } catch (...) {
+    return fail(MSSA_ERR_INVALID_ARG, "unexpected error while building the plan");
+  }
+}
+
+void mssa_plan_destroy(mssa_plan plan) { delete plan; }
+
+mssa_status mssa_plan_query(mssa_plan plan, mssa_plan_info* info) {
+  if (!plan || !info) return fail(MSSA_ERR_INVALID_ARG, "plan and info must be non-null");
+  const mssa::Plan& p = plan->p;
+  std::memset(info, 0, sizeof(*info));
+  info->n_q = p.n_q;
+  info->n_sink_tok = p.n_sink_tok;
+  info->n_hist_tok = p.n_hist_tok;
+  info->workspace_bytes = p.workspace_bytes;
+  info->pairs_per_head = p.pairs_per_head;
+  info->flops_alg = 4 * static_cast<int64_t>(p.desc.head_dim) * p.desc.num_heads * p.pairs_per_head;
+  info->pool_bytes_alg = p.pool_bytes_alg;
+  info->n_groups = static_cast<int32_t>(p.groups.size());
+  for (size_t g = 0; g < p.groups.size(); ++g) {
+    info->group_scale[g] = p.groups[g].scale;
+    info->q_begin[g] = p.groups[g].q_begin;
+    info->q_end[g] = p.groups[g].q_end;
+    info->n_kv[g] = p.groups[g].n_kv;
+    info->pooled_k_offset[g] = p.pooled_k_off[g];
+    info->pooled_v_offset[g] = p.pooled_v_off[g];
+    info->pooled_tokens[g] = p.pooled_tokens[g];
+  }
+  return MSSA_OK;
+}
+
+mssa_status mssa_plan_tables(mssa_plan plan, int64_t* dst, int64_t cap, int64_t* needed) {
+  if (!plan || !needed) return fail(MSSA_ERR_INVALID_ARG, "plan and needed must be non-null");
+  try {
+    const std::vector<int64_t> t = mssa::export_tables(plan->p);
+    *needed = static_cast<int64_t>(t.size());
+    if (!dst || cap < *needed) return fail(MSSA_ERR_INVALID_ARG, "table buffer too small");
+    std::memcpy(dst, t.data(), t.size() * sizeof(int64_t));
+    return MSSA_OK;
+  } catch (const std::bad_alloc&) {
+    return fail(MSSA_ERR_NO_MEMORY, "host allocation failed");
+  }
+}
+
+mssa_status mssa_pool_kv(mssa_plan plan, const void* k_hist, const void* v_hist, const void* k_win,
+                         const void* v_win, void* workspace, int64_t workspace_bytes, void* stream) {
+  if (!plan) return fail(MSSA_ERR_INVALID_ARG, "plan must be non-null");
+  const mssa::Plan& p = plan->p;
+  if (p.pool_jobs.empty()) return MSSA_OK;
+  if (!k_win || !v_win) return fail(MSSA_ERR_INVALID_ARG, "k_win and v_win must be non-null");
+  if (p.n_hist_tok > 0 && (!k_hist || !v_hist))
+    return fail(MSSA_ERR_INVALID_ARG, "k_hist and v_hist must be non-null when hist_frames > 0");
+  if (!workspace || workspace_bytes < p.workspace_bytes)
+    return fail(MSSA_ERR_WORKSPACE, "workspace smaller than mssa_plan_info.workspace_bytes");
+  if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
+    return fail(MSSA_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+  if (!aligned16(k_win) || !aligned16(v_win) || (k_hist && !aligned16(k_hist)) || (v_hist && !aligned16(v_hist)))
+    return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
+
+  const int64_t eb = p.elem_bytes;
+  const int64_t row_bytes = p.ld * eb;
+  mssa::PoolArgs a{};
+  a.ld = p.ld;
+  a.chunks_per_tok = static_cast<int32_t>(row_bytes / 16);
+  auto* ws = static_cast<char*>(workspace);
+  size_t j0 = 0;
+  while (j0 < p.pool_jobs.size()) {
+    const size_t nj = std::min<size_t>(mssa::kMaxPoolJobs, p.pool_jobs.size() - j0);
+    int64_t blocks = 0;
+    for (size_t i = 0; i < nj; ++i) {
+      const mssa::PoolJob& J = p.pool_jobs[j0 + i];
+      mssa::PoolJobArgs& A = a.jobs[i];
+      const char* sk = static_cast<const char*>(J.buffer == mssa::kBufHist ? k_hist : k_win);
+      const char* sv = static_cast<const char*>(J.buffer == mssa::kBufHist ? v_hist : v_win);
+      A.src_k = sk + J.src_tok * row_bytes;
+      A.src_v = sv + J.src_tok * row_bytes;
+      A.dst_k = ws + p.pooled_k_off[J.group] + J.dst_tok * row_bytes;
+      A.dst_v = ws + p.pooled_v_off[J.group] + J.dst_tok * row_bytes;
+      A.src_gh = J.src_gh;
+      A.src_gw = J.src_gw;
+      A.dst_gh = J.dst_gh;
+      A.dst_gw = J.dst_gw;
+      A.factor = J.factor;
+      A.n_frames = J.n_frames;
+      A.block_begin = static_cast<int32_t>(blocks);
+      const int64_t work = static_cast<int64_t>(J.n_frames) * J.dst_gh * J.dst_gw * a.chunks_per_tok;
+      blocks += (work + mssa::kPoolThreads - 1) / mssa::kPoolThreads;
+    }
+    if (blocks > 0x7fffffff) return fail(MSSA_ERR_UNSUPPORTED, "pool grid too large");
+    a.n_jobs = static_cast<int32_t>(nj);
+    const mssa_status s = check_device(
+        mssa::launch_pool(a, static_cast<int>(blocks), p.desc.dtype == MSSA_BF16, static_cast<hipStream_t>(stream)),
+        "pool kernel launch");
+    if (s != MSSA_OK) return s;
+    j0 += nj;
+  }
+  return MSSA_OK;
+}
+
+mssa_status mssa_forward(mssa_plan plan, const void* q_win, const void* k_sink, const void* v_sink,
+                         const void* k_hist, const void* v_hist, const void* k_win, const void* v_win,
+                         const void* workspace, int64_t workspace_bytes, void* out, void* stream) {
+  if (!plan) return fail(MSSA_ERR_INVALID_ARG, "plan must be non-null");
+  const mssa::Plan& p = plan->p;
+  if (!q_win || !k_win || !v_win || !out)
+    return fail(MSSA_ERR_INVALID_ARG, "q_win, k_win, v_win and out must be non-null");
+  if (p.n_sink_tok > 0 && (!k_sink || !v_sink))
+    return fail(MSSA_ERR_INVALID_ARG, "k_sink and v_sink must be non-null when sink_frames > 0");
+  if (p.n_hist_tok > 0 && (!k_hist || !v_hist))
+    return fail(MSSA_ERR_INVALID_ARG, "k_hist and v_hist must be non-null when hist_frames > 0");
+  if (p.workspace_bytes > 0 && (!workspace || workspace_bytes < p.workspace_bytes))
+    return fail(MSSA_ERR_WORKSPACE, "workspace smaller than mssa_plan_info.workspace_bytes");
+  for (const void* t : {q_win, k_sink, v_sink, k_hist, v_hist, k_win, v_win, static_cast<const void*>(out)})
+    if (t && !aligned16(t)) return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
+  if (out == q_win || out == k_win || out == v_win)
+    return fail(MSSA_ERR_INVALID_ARG, "out must not alias an input");
+
+  const bool bf16 = p.desc.dtype == MSSA_BF16;
+  const int bm = bf16 ? mssa::kFwdBM : mssa::kFwdF32BM;
+  const int64_t row_bytes = p.ld * p.elem_bytes;
+  mssa::FwdArgs a{};
+  a.q = q_win;
+  a.out = out;
+  a.ld = p.ld;
+  a.num_heads = p.desc.num_heads;
+  a.scale = p.softmax_scale;
+  a.scale_log2e = p.softmax_scale * 1.4426950408889634f;
+  const char* ws = static_cast<const char*>(workspace);
+  int64_t blocks = 0;
+  int gi = 0;
+  for (int g : plan->order) {
+    const mssa::QGroup& Q = p.groups[g];
+    mssa::FwdGroupArgs& A = a.groups[gi++];
+    A.q_begin = Q.q_begin;
+    A.q_end = Q.q_end;
+    A.n_qtiles = (Q.q_end - Q.q_begin + bm - 1) / bm;
+    A.block_begin = static_cast<int32_t>(blocks);
+    if (p.runs[g].size() > static_cast<size_t>(mssa::kMaxRuns))
+      return fail(MSSA_ERR_UNSUPPORTED, "too many context runs for one query scale");
+    A.n_runs = static_cast<int32_t>(p.runs[g].size());
+    for (size_t r = 0; r < p.runs[g].size(); ++r) {
+      const mssa::Run& R = p.runs[g][r];
+      const char *kb = nullptr, *vb = nullptr;
+      switch (R.buffer) {
+        case mssa::kBufSink: kb = static_cast<const char*>(k_sink); vb = static_cast<const char*>(v_sink); break;
+        case mssa::kBufHist: kb = static_cast<const char*>(k_hist); vb = static_cast<const char*>(v_hist); break;
+        case mssa::kBufWin: kb = static_cast<const char*>(k_win); vb = static_cast<const char*>(v_win); break;
+        default: kb = ws + p.pooled_k_off[g]; vb = ws + p.pooled_v_off[g]; break;
+      }
+      A.runs[r].k = kb + R.tok_offset * row_bytes;
+      A.runs[r].v = vb + R.tok_offset * row_bytes;
+      A.runs[r].n_tok = static_cast<int32_t>(R.n_tok);
+    }
+    blocks += static_cast<int64_t>(A.n_qtiles) * p.desc.num_heads;
+  }
+  if (blocks > 0x7fffffff) return fail(MSSA_ERR_UNSUPPORTED, "attention grid too large");
+  a.n_groups = gi;
+  a.n_blocks = static_cast<int32_t>(blocks);
+  return check_device(mssa::launch_forward(a, p.desc.head_dim, bf16, static_cast<hipStream_t>(stream)),
+                      "attention kernel launch");
+}
+
+const char* mssa_status_string(mssa_status s) {
+  switch (s) {
+    case MSSA_OK: return "MSSA_OK";
+    case MSSA_ERR_INVALID_ARG: return "MSSA_ERR_INVALID_ARG";
+    case MSSA_ERR_UNSUPPORTED: return "MSSA_ERR_UNSUPPORTED";
+    case MSSA_ERR_WORKSPACE: return "MSSA_ERR_WORKSPACE";
+    case MSSA_ERR_DEVICE: return "MSSA_ERR_DEVICE";
+    case MSSA_ERR_NO_MEMORY: return "MSSA_ERR_NO_MEMORY";
+  }
+  return "MSSA_ERR_UNKNOWN";
+}
+
+const char* mssa_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

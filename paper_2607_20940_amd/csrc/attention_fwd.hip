@@ -1,0 +1,252 @@
+// Multi-scale self-attention forward (Ms. Forcing, Sec. 4.1, Eq. 4): for
+// every head and query scale, softmax(scale q k^T) v over the concatenated
+// context runs of that scale (sink | history at the query scale | window at
+// max(query scale, own scale)).
+//
+// bf16 path (gfx950 matrix cores).  One block = 4 waves = 128 queries of one
+// (query scale, head); each wave owns 32 queries.  The block walks the
+// scale's runs in 64-key tiles staged through LDS.  Per tile and wave:
+//   S^T = K Q^T   with v_mfma_f32_32x32x16_bf16 (A = K rows from LDS,
+//                 B = the wave's Q fragment held in registers), so each lane
+//                 holds 16 keys of ONE query: the softmax row reductions are
+//                 in-lane plus one exchange between the two half-waves;
+//   online softmax in fp32 in the exp2 domain (scale * log2 e folded into
+//                 one FMA per score);
+//   O^T += V^T P^T with the same MFMA: the exponentiated scores are already
+//                 laid out as the B operand (their key order defines the
+//                 contraction order), and V^T comes from row-major V in LDS
+//                 through the gfx950 transposing LDS read ds_read_b64_tr_b16.
+// Keys past the end of a run are zero-filled in LDS and masked to -inf.
+//
+// fp32 path: one lane per query, plain fp32 FMA dot products and an online
+// softmax with expf; used for fp32 plans (correctness path).
+#include <hip/hip_runtime.h>
+
+#include "kernels.hpp"
+
+namespace mssa {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+
+// Logical block -> (group, head, query tile).  Groups are stored longest
+// context first; inside a group consecutive blocks share a head.
+struct Work {
+  int g, head, tile;
+};
+
+__device__ inline Work decode(const FwdArgs& a, int L) {
+  int g = 0;
+  while (g + 1 < a.n_groups && L >= a.groups[g + 1].block_begin) ++g;
+  const int idx = L - a.groups[g].block_begin;
+  const int nt = a.groups[g].n_qtiles;
+  return {g, idx / nt, idx % nt};
+}
+
+template <int D>
+__global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(FwdArgs a) {
+  constexpr int BM = kFwdBM, BN = kFwdBN;
+  constexpr int KS = D / 16;   // 16-wide k-steps of q k^T
+  constexpr int DB = D / 32;   // 32-row blocks of O^T
+  constexpr int KSTR = D + 8;  // LDS row strides (elements)
+  constexpr int VSTR = D + 16;
+  constexpr int CPR = D / 8;   // 16-byte chunks per row
+  __shared__ __attribute__((aligned(16))) __bf16 Ks[BN * KSTR];
+  __shared__ __attribute__((aligned(16))) __bf16 Vs[BN * VSTR];
+
+  const Work w = decode(a, blockIdx.x);
+  const FwdGroupArgs& G = a.groups[w.g];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int n = lane & 31;   // query column of this lane
+  const int hh = lane >> 5;  // half-wave
+  const int q_row = G.q_begin + w.tile * BM + wave * 32 + n;
+  const bool q_ok = q_row < G.q_end;
+  const int64_t ld = a.ld;
+  const int64_t hoff = static_cast<int64_t>(w.head) * D;
+
+  bf16x8 qf[KS];
+  {
+    const __bf16* qp = static_cast<const __bf16*>(a.q) + static_cast<int64_t>(q_ok ? q_row : G.q_begin) * ld +
+                       hoff + hh * 8;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      bf16x8 v = *reinterpret_cast<const bf16x8*>(qp + ks * 16);
+      if (!q_ok) v = bf16x8{};
+      qf[ks] = v;
+    }
+  }
+
+  f32x16 o[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) o[db] = f32x16{};
+  float m_run = -INFINITY;  // running max, exp2 domain
+  float l_part = 0.f;       // this lane's share of the row sum
+
+  // Transposing-read address pieces: 16-lane group gq, lane r4/c4 within it.
+  const int gq = lane >> 4;
+  const int r4 = (lane & 15) >> 2;
+  const int c4 = lane & 3;
+  const int v_lane_off = (4 * (gq >> 1) + r4) * VSTR + 16 * (gq & 1) + 4 * c4;
+
+  for (int r = 0; r < G.n_runs; ++r) {
+    const __bf16* Kg = static_cast<const __bf16*>(G.runs[r].k) + hoff;
+    const __bf16* Vg = static_cast<const __bf16*>(G.runs[r].v) + hoff;
+    const int ntok = G.runs[r].n_tok;
+    for (int t0 = 0; t0 < ntok; t0 += BN) {
+      const int nvalid = min(BN, ntok - t0);
+#pragma unroll
+      for (int c = threadIdx.x; c < BN * CPR; c += kFwdThreads) {
+        const int row = c / CPR, col = (c % CPR) * 8;
+        bf16x8 kv{}, vv{};
+        if (row < nvalid) {
+          const int64_t off = static_cast<int64_t>(t0 + row) * ld + col;
+          kv = *reinterpret_cast<const bf16x8*>(Kg + off);
+          vv = *reinterpret_cast<const bf16x8*>(Vg + off);
+        }
+        *reinterpret_cast<bf16x8*>(Ks + row * KSTR + col) = kv;
+        *reinterpret_cast<bf16x8*>(Vs + row * VSTR + col) = vv;
+      }
+      __syncthreads();
+
+      f32x16 s[BN / 32];
+#pragma unroll
+      for (int kb = 0; kb < BN / 32; ++kb) {
+        s[kb] = f32x16{};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          const bf16x8 ka = *reinterpret_cast<const bf16x8*>(Ks + (kb * 32 + n) * KSTR + ks * 16 + hh * 8);
+          s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[ks], s[kb], 0, 0, 0);
+        }
+      }
+      if (nvalid < BN) {
+#pragma unroll
+        for (int kb = 0; kb < BN / 32; ++kb)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const int key = kb * 32 + 8 * (e >> 2) + 4 * hh + (e & 3);
+            if (key >= nvalid) s[kb][e] = -INFINITY;
+          }
+      }
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kb = 0; kb < BN / 32; ++kb)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[kb][e]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float m_new = fmaxf(m_run, mx * a.scale_log2e);
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      m_run = m_new;
+      l_part *= alpha;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) o[db] *= alpha;
+
+      bf16x8 pb[BN / 32][2];
+#pragma unroll
+      for (int kb = 0; kb < BN / 32; ++kb)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][e], a.scale_log2e, -m_new));
+          l_part += p;
+          pb[kb][e >> 3][e & 7] = static_cast<__bf16>(p);
+        }
+
+#pragma unroll
+      for (int kb = 0; kb < BN / 32; ++kb)
+#pragma unroll
+        for (int cc = 0; cc < 2; ++cc) {
+          const __bf16* vrow = Vs + (kb * 32 + cc * 16) * VSTR + v_lane_off;
+#pragma unroll
+          for (int db = 0; db < DB; ++db) {
+            const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vrow + db * 32));
+            const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vrow + 8 * VSTR + db * 32));
+            const bf16x8 va = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+            o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[kb][cc], o[db], 0, 0, 0);
+          }
+        }
+      __syncthreads();
+    }
+  }
+
+  const float l_tot = l_part + __shfl_xor(l_part, 32);
+  const float inv = 1.0f / l_tot;
+  if (q_ok) {
+    __bf16* op = static_cast<__bf16*>(a.out) + static_cast<int64_t>(q_row) * ld + hoff + 4 * hh;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        bf16x4 v;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] = static_cast<__bf16>(o[db][4 * j + i] * inv);
+        *reinterpret_cast<bf16x4*>(op + db * 32 + 8 * j) = v;
+      }
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(kFwdF32BM) void fwd_f32_kernel(FwdArgs a) {
+  const Work w = decode(a, blockIdx.x);
+  const FwdGroupArgs& G = a.groups[w.g];
+  const int q_row = G.q_begin + w.tile * kFwdF32BM + threadIdx.x;
+  if (q_row >= G.q_end) return;
+  const int64_t ld = a.ld;
+  const int64_t hoff = static_cast<int64_t>(w.head) * D;
+  const float* qp = static_cast<const float*>(a.q) + static_cast<int64_t>(q_row) * ld + hoff;
+  float q[D], o[D];
+#pragma unroll
+  for (int d = 0; d < D; ++d) {
+    q[d] = qp[d];
+    o[d] = 0.f;
+  }
+  float m = -INFINITY, l = 0.f;
+  for (int r = 0; r < G.n_runs; ++r) {
+    const float* Kg = static_cast<const float*>(G.runs[r].k) + hoff;
+    const float* Vg = static_cast<const float*>(G.runs[r].v) + hoff;
+    for (int j = 0; j < G.runs[r].n_tok; ++j) {
+      const float* kp = Kg + static_cast<int64_t>(j) * ld;
+      const float* vp = Vg + static_cast<int64_t>(j) * ld;
+      float dot = 0.f;
+#pragma unroll
+      for (int d = 0; d < D; ++d) dot = __builtin_fmaf(q[d], kp[d], dot);
+      const float z = dot * a.scale;
+      if (z > m) {
+        const float alpha = expf(m - z);
+        l *= alpha;
+#pragma unroll
+        for (int d = 0; d < D; ++d) o[d] *= alpha;
+        m = z;
+      }
+      const float p = expf(z - m);
+      l += p;
+#pragma unroll
+      for (int d = 0; d < D; ++d) o[d] = __builtin_fmaf(p, vp[d], o[d]);
+    }
+  }
+  float* op = static_cast<float*>(a.out) + static_cast<int64_t>(q_row) * ld + hoff;
+#pragma unroll
+  for (int d = 0; d < D; ++d) op[d] = o[d] / l;
+}
+
+}  // namespace
+
+hipError_t launch_forward(const FwdArgs& a, int head_dim, bool bf16, hipStream_t stream) {
+  if (a.n_blocks <= 0) return hipSuccess;
+  if (bf16) {
+    if (head_dim == 128)
+      hipLaunchKernelGGL(fwd_bf16_kernel<128>, dim3(a.n_blocks), dim3(kFwdThreads), 0, stream, a);
+    else
+      hipLaunchKernelGGL(fwd_bf16_kernel<64>, dim3(a.n_blocks), dim3(kFwdThreads), 0, stream, a);
+  } else {
+    if (head_dim == 128)
+      hipLaunchKernelGGL(fwd_f32_kernel<128>, dim3(a.n_blocks), dim3(kFwdF32BM), 0, stream, a);
+    else
+      hipLaunchKernelGGL(fwd_f32_kernel<64>, dim3(a.n_blocks), dim3(kFwdF32BM), 0, stream, a);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace mssa

@@ -1,0 +1,16 @@
+// Host-side launchers of the MSSA HIP kernels (defined in the .hip files).
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+
+#include "kernel_args.hpp"
+
+namespace mssa {
+
+// Average-pool jobs; grid = (n_blocks, 2): y = 0 pools K, y = 1 pools V.
+hipError_t launch_pool(const PoolArgs& a, int n_blocks, bool bf16, hipStream_t stream);
+
+// Attention forward over the groups of `a` (a.n_blocks logical blocks).
+hipError_t launch_forward(const FwdArgs& a, int head_dim, bool bf16, hipStream_t stream);
+
+}  // namespace mssa

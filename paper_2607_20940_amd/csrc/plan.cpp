@@ -1,0 +1,230 @@
+// Static MSSA plan (host).  Every table follows Sec. 4.1 of Ms. Forcing:
+// MSP grids from Eq. 3 (ceil grid when a scale does not divide the native
+// grid), query groups per distinct scale, and the Eq. 4 context of each
+// query scale s:
+//   sink frames        native, never resampled;
+//   history frames     native, pooled by s;
+//   window frame of b  at max(s, p_b), pooled by max(1, s / p_b);
+// in the order sink, history (oldest first), window (state 1..T).
+#include "plan.hpp"
+
+#include <algorithm>
+#include <cmath>
+#include <limits>
+
+namespace mssa {
+namespace {
+
+bool is_pow2(int32_t x) { return x > 0 && (x & (x - 1)) == 0; }
+
+int32_t ceil_div(int32_t a, int32_t b) { return (a + b - 1) / b; }
+
+}  // namespace
+
+mssa_status build_plan(const mssa_plan_desc& d, Plan& p, std::string& err) {
+  const int32_t T = d.num_states;
+  if (T < 1 || T > MSSA_MAX_STATES) {
+    err = "num_states must be in [1, " + std::to_string(MSSA_MAX_STATES) + "]";
+    return MSSA_ERR_INVALID_ARG;
+  }
+  if (d.grid_h < 1 || d.grid_w < 1 || d.grid_h > 65536 || d.grid_w > 65536) {
+    err = "grid_h and grid_w must be in [1, 65536]";
+    return MSSA_ERR_INVALID_ARG;
+  }
+  if (d.frames_per_state < 1 || d.sink_frames < 0 || d.hist_frames < 0) {
+    err = "frames_per_state must be >= 1, sink_frames and hist_frames >= 0";
+    return MSSA_ERR_INVALID_ARG;
+  }
+  if (d.num_heads < 1) {
+    err = "num_heads must be >= 1";
+    return MSSA_ERR_INVALID_ARG;
+  }
+  if (d.dtype != MSSA_BF16 && d.dtype != MSSA_F32) {
+    err = "dtype must be MSSA_BF16 or MSSA_F32";
+    return MSSA_ERR_INVALID_ARG;
+  }
+  if (!std::isfinite(d.softmax_scale)) {
+    err = "softmax_scale must be finite";
+    return MSSA_ERR_INVALID_ARG;
+  }
+  for (int l = 0; l < T; ++l) {
+    if (!is_pow2(d.scales[l]) || d.scales[l] > 64) {
+      err = "scales must be powers of two in [1, 64]";
+      return MSSA_ERR_UNSUPPORTED;
+    }
+    if (l > 0 && d.scales[l] < d.scales[l - 1]) {
+      err = "scales must be nondecreasing (coarser patches for noisier states)";
+      return MSSA_ERR_UNSUPPORTED;
+    }
+  }
+  if (d.head_dim != 64 && d.head_dim != 128) {
+    err = "head_dim must be 64 or 128";
+    return MSSA_ERR_UNSUPPORTED;
+  }
+
+  p = Plan{};
+  p.desc = d;
+  p.softmax_scale = d.softmax_scale > 0.f ? d.softmax_scale
+                                          : 1.0f / std::sqrt(static_cast<float>(d.head_dim));
+  const int32_t F = d.frames_per_state;
+  auto tok_at = [&](int32_t s) {
+    return static_cast<int64_t>(ceil_div(d.grid_h, s)) * ceil_div(d.grid_w, s);
+  };
+  p.tok1 = tok_at(1);
+  p.ld = static_cast<int64_t>(d.num_heads) * d.head_dim;
+  p.elem_bytes = d.dtype == MSSA_BF16 ? 2 : 4;
+  p.n_sink_tok = p.tok1 * d.sink_frames;
+  p.n_hist_tok = p.tok1 * d.hist_frames;
+
+  // GRID: native scale plus every scheduled scale, ascending.
+  std::vector<int32_t> sc{1};
+  for (int l = 0; l < T; ++l) sc.push_back(d.scales[l]);
+  std::sort(sc.begin(), sc.end());
+  sc.erase(std::unique(sc.begin(), sc.end()), sc.end());
+  for (int32_t s : sc)
+    p.grids.push_back({s, ceil_div(d.grid_h, s), ceil_div(d.grid_w, s), static_cast<int32_t>(tok_at(s))});
+
+  // Window frames in token order and the query groups (contiguous per scale
+  // because the schedule is nondecreasing).
+  struct WinFrame { int32_t w, p; int64_t first, n; };
+  std::vector<WinFrame> wf;
+  int64_t pos = 0;
+  for (int l = 0; l < T; ++l)
+    for (int f = 0; f < F; ++f) {
+      const int64_t n = tok_at(d.scales[l]);
+      wf.push_back({l * F + f, d.scales[l], pos, n});
+      pos += n;
+    }
+  p.n_q = pos;
+  for (const WinFrame& w : wf) {
+    if (!p.groups.empty() && p.groups.back().scale == w.p)
+      p.groups.back().q_end = static_cast<int32_t>(w.first + w.n);
+    else
+      p.groups.push_back({w.p, static_cast<int32_t>(w.first), static_cast<int32_t>(w.first + w.n), 0});
+  }
+
+  const int64_t kIdxMax = std::numeric_limits<int32_t>::max();
+  if (p.n_q > kIdxMax || p.n_sink_tok > kIdxMax || p.n_hist_tok > kIdxMax) {
+    err = "token counts exceed 32-bit indexing";
+    return MSSA_ERR_UNSUPPORTED;
+  }
+
+  // SEG rows per group, their placement, runs and pool jobs.
+  const int G = static_cast<int>(p.groups.size());
+  p.runs.assign(G, {});
+  p.pooled_tokens.assign(G, 0);
+  p.pooled_k_off.assign(G, 0);
+  p.pooled_v_off.assign(G, 0);
+  p.pairs_per_head = 0;
+  int64_t ws = 0;
+  auto align256 = [](int64_t x) { return (x + 255) / 256 * 256; };
+  std::vector<char> win_read(wf.size(), 0);
+  bool hist_read = false;
+
+  for (int g = 0; g < G; ++g) {
+    QGroup& grp = p.groups[g];
+    const int32_t s = grp.scale;
+    int64_t kv = 0, pooled = 0;
+    std::vector<SegRow> rows;
+    for (int f = 0; f < d.sink_frames; ++f)
+      rows.push_back({s, kSink, f, 1, 1, 1, static_cast<int32_t>(p.tok1), 0, kBufSink, f * p.tok1});
+    for (int f = 0; f < d.hist_frames; ++f) {
+      SegRow r{s, kHist, f, 1, s, s, static_cast<int32_t>(tok_at(s)), 0, kBufHist, f * p.tok1};
+      if (s > 1) { r.buffer = kBufPooled; r.tok_offset = pooled; pooled += r.n_tok; hist_read = true; }
+      rows.push_back(r);
+    }
+    for (size_t i = 0; i < wf.size(); ++i) {
+      const WinFrame& w = wf[i];
+      const int32_t eff = std::max(s, w.p);
+      const int32_t fac = std::max(1, s / w.p);
+      SegRow r{s, kWin, w.w, w.p, eff, fac, static_cast<int32_t>(tok_at(eff)), 0, kBufWin, w.first};
+      if (fac > 1) { r.buffer = kBufPooled; r.tok_offset = pooled; pooled += r.n_tok; win_read[i] = 1; }
+      rows.push_back(r);
+    }
+    for (SegRow& r : rows) { r.kv_begin = kv; kv += r.n_tok; }
+    if (kv > kIdxMax) {
+      err = "context length exceeds 32-bit indexing";
+      return MSSA_ERR_UNSUPPORTED;
+    }
+    grp.n_kv = kv;
+    p.pairs_per_head += static_cast<int64_t>(grp.q_end - grp.q_begin) * kv;
+
+    // Runs: merge rows that are contiguous in one buffer.
+    for (const SegRow& r : rows) {
+      std::vector<Run>& rs = p.runs[g];
+      if (!rs.empty() && rs.back().buffer == r.buffer &&
+          rs.back().tok_offset + rs.back().n_tok == r.tok_offset)
+        rs.back().n_tok += r.n_tok;
+      else
+        rs.push_back({r.buffer, r.tok_offset, r.n_tok});
+    }
+
+    // Pool jobs: merge consecutive pooled rows of one source kind, source
+    // scale and factor whose source and destination frames are contiguous.
+    for (const SegRow& r : rows) {
+      if (r.buffer != kBufPooled) continue;
+      const int32_t src_buf = r.kind == kHist ? kBufHist : kBufWin;
+      int64_t src_tok;
+      int64_t src_n;
+      if (r.kind == kHist) {
+        src_tok = r.frame * p.tok1;
+        src_n = p.tok1;
+      } else {
+        src_tok = wf[r.frame].first;
+        src_n = wf[r.frame].n;
+      }
+      const int32_t sgh = ceil_div(d.grid_h, r.src_scale), sgw = ceil_div(d.grid_w, r.src_scale);
+      if (!p.pool_jobs.empty()) {
+        PoolJob& j = p.pool_jobs.back();
+        const int64_t jsrc_n = static_cast<int64_t>(j.src_gh) * j.src_gw;
+        const int64_t jdst_n = static_cast<int64_t>(j.dst_gh) * j.dst_gw;
+        if (j.group == g && j.buffer == src_buf && j.factor == r.factor && j.src_gh == sgh &&
+            j.src_gw == sgw && j.src_tok + j.n_frames * jsrc_n == src_tok &&
+            j.dst_tok + j.n_frames * jdst_n == r.tok_offset) {
+          j.n_frames += 1;
+          continue;
+        }
+      }
+      (void)src_n;
+      p.pool_jobs.push_back({g, src_buf, src_tok, sgh, sgw, r.factor, 1,
+                             ceil_div(sgh, r.factor), ceil_div(sgw, r.factor), r.tok_offset});
+    }
+
+    p.pooled_tokens[g] = pooled;
+    if (pooled > 0) {
+      const int64_t bytes = align256(pooled * p.ld * p.elem_bytes);
+      p.pooled_k_off[g] = ws;
+      ws += bytes;
+      p.pooled_v_off[g] = ws;
+      ws += bytes;
+    }
+    for (SegRow& r : rows) p.segs.push_back(r);
+  }
+  p.workspace_bytes = ws;
+
+  // Algorithmic pool traffic: each pooled source frame read once, each
+  // pooled frame written once, for K and V.
+  int64_t read_tok = hist_read ? p.n_hist_tok : 0;
+  for (size_t i = 0; i < wf.size(); ++i)
+    if (win_read[i]) read_tok += wf[i].n;
+  int64_t write_tok = 0;
+  for (int64_t t : p.pooled_tokens) write_tok += t;
+  p.pool_bytes_alg = 2 * (read_tok + write_tok) * p.ld * p.elem_bytes;
+  return MSSA_OK;
+}
+
+std::vector<int64_t> export_tables(const Plan& p) {
+  std::vector<int64_t> t;
+  t.push_back(static_cast<int64_t>(p.grids.size()));
+  t.push_back(static_cast<int64_t>(p.groups.size()));
+  t.push_back(static_cast<int64_t>(p.segs.size()));
+  for (const GridRow& g : p.grids) t.insert(t.end(), {g.scale, g.gh, g.gw, g.tok});
+  for (const QGroup& g : p.groups) t.insert(t.end(), {g.scale, g.q_begin, g.q_end, g.n_kv});
+  for (const SegRow& r : p.segs)
+    t.insert(t.end(), {r.q_scale, r.kind, r.frame, r.src_scale, r.eff_scale, r.factor, r.n_tok, r.kv_begin});
+  t.push_back(p.n_q);
+  t.push_back(p.pairs_per_head);
+  return t;
+}
+
+}  // namespace mssa

@@ -1,0 +1,84 @@
+// Static MSSA plan: MSP grids, query groups, Eq. 4 context tables, pool jobs
+// and the kernel launch descriptions.  Host-only C++17; no HIP types, so the
+// scheduler builds and runs without a GPU.
+#pragma once
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "../../include/libmssa.h"
+
+namespace mssa {
+
+enum Kind : int32_t { kSink = 0, kHist = 1, kWin = 2 };
+
+// Where a run of context tokens lives.
+enum Buffer : int32_t { kBufSink = 0, kBufHist = 1, kBufWin = 2, kBufPooled = 3 };
+
+struct GridRow {
+  int32_t scale, gh, gw, tok;
+};
+
+struct QGroup {
+  int32_t scale, q_begin, q_end;
+  int64_t n_kv;
+};
+
+struct SegRow {
+  int32_t q_scale, kind, frame, src_scale, eff_scale, factor, n_tok;
+  int64_t kv_begin;
+  // placement used by the kernels (not exported)
+  int32_t buffer;
+  int64_t tok_offset;  // first token inside `buffer` (pooled: inside the group block)
+};
+
+// A maximal stretch of context tokens that is contiguous in one buffer.
+struct Run {
+  int32_t buffer;
+  int64_t tok_offset;
+  int64_t n_tok;
+};
+
+// One average-pool job: n_frames consecutive frames of grid (src_gh, src_gw)
+// starting at src_tok of `buffer` (history or window) -> factor x factor
+// pooled frames of grid (dst_gh, dst_gw) at dst_tok of group `group`'s
+// pooled block.
+struct PoolJob {
+  int32_t group;
+  int32_t buffer;
+  int64_t src_tok;
+  int32_t src_gh, src_gw;
+  int32_t factor;
+  int32_t n_frames;
+  int32_t dst_gh, dst_gw;
+  int64_t dst_tok;
+};
+
+struct Plan {
+  mssa_plan_desc desc;
+  float softmax_scale;
+  int64_t tok1;  // native tokens per frame
+  int64_t n_q, n_sink_tok, n_hist_tok;
+  int64_t ld;          // elements between consecutive tokens: heads * head_dim
+  int64_t elem_bytes;  // 2 (bf16) or 4 (fp32)
+  std::vector<GridRow> grids;
+  std::vector<QGroup> groups;
+  std::vector<SegRow> segs;             // all groups, context order
+  std::vector<std::vector<Run>> runs;   // per group
+  std::vector<PoolJob> pool_jobs;
+  std::vector<int64_t> pooled_tokens;   // per group
+  std::vector<int64_t> pooled_k_off, pooled_v_off;  // bytes, per group
+  int64_t workspace_bytes;
+  int64_t pairs_per_head;
+  int64_t pool_bytes_alg;
+};
+
+// Validates `d` and fills `p`.  Returns MSSA_OK or an error status with a
+// message in `err`.
+mssa_status build_plan(const mssa_plan_desc& d, Plan& p, std::string& err);
+
+// Flat int64 export of GRID / QGRP / SEG / TOTAL (layout in libmssa.h).
+std::vector<int64_t> export_tables(const Plan& p);
+
+}  // namespace mssa

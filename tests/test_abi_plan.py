@@ -1,0 +1,158 @@
+"""C-ABI checks that need no GPU: the library loads and exports every
+declared symbol, the scheduler's tables equal the oracle's bit for bit, and
+invalid calls are rejected before anything is enqueued."""
+
+import os
+import re
+
+import numpy as np
+import pytest
+from hypothesis import given, settings, strategies as st
+
+import oracle
+from paper_2607_20940_amd import mssa
+from paper_2607_20940_amd.workloads import STREAMING, WORKLOADS
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    src = open(os.path.join(ROOT, "include", "libmssa.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(mssa_[a-z_]+)\s*\(", src)))
+
+
+def test_exports_every_declared_symbol():
+    names = _declared_functions()
+    assert set(names) == set(mssa.EXPORTS)
+    for name in names:
+        assert hasattr(mssa.lib, name), name
+
+
+def _plan(desc, **kw):
+    d = dict(desc)
+    d.update(kw)
+    return mssa.mssa_plan_create(d)
+
+
+def _assert_tables_equal(desc):
+    got = _plan(desc).tables()
+    want = oracle.tables(desc)
+    for key in ("GRID", "QGRP", "SEG", "TOTAL"):
+        assert np.array_equal(got[key], want[key]), key
+
+
+@pytest.mark.parametrize("name", sorted(WORKLOADS))
+def test_tables_bit_exact_workloads(name):
+    _assert_tables_equal(WORKLOADS[name]["desc"])
+
+
+@pytest.mark.parametrize("hist", [6, 9, 12, 15, 18, 21])
+def test_tables_bit_exact_streaming_history_lengths(hist):
+    _assert_tables_equal(dict(STREAMING["layer"], hist_frames=hist))
+
+
+@settings(max_examples=150, deadline=None)
+@given(H=st.integers(1, 70), W=st.integers(1, 90),
+       sched=st.lists(st.sampled_from([1, 2, 4, 8, 16]), min_size=1, max_size=8).map(sorted),
+       F=st.integers(1, 4), S=st.integers(0, 4), Hh=st.integers(0, 25),
+       nh=st.integers(1, 48), d=st.sampled_from([64, 128]))
+def test_tables_bit_exact_fuzz(H, W, sched, F, S, Hh, nh, d):
+    desc = dict(num_states=len(sched), scales=sched, grid_h=H, grid_w=W, frames_per_state=F,
+                sink_frames=S, hist_frames=Hh, num_heads=nh, head_dim=d)
+    _assert_tables_equal(desc)
+
+
+@pytest.mark.parametrize("name", sorted(WORKLOADS))
+def test_info_matches_oracle(name):
+    w = WORKLOADS[name]
+    desc = dict(w["desc"], dtype=w["dtype"])
+    info = _plan(desc).info()
+    assert info["n_q"] == oracle.num_window_tokens(desc)
+    assert info["n_sink_tok"] == oracle.num_sink_tokens(desc)
+    assert info["n_hist_tok"] == oracle.num_hist_tokens(desc)
+    assert info["flops_alg"] == oracle.algorithmic_flops(desc)
+    groups = oracle.tables(desc)["QGRP"]
+    assert info["group_scale"] == groups[:, 0].tolist()
+    assert info["n_kv"] == groups[:, 3].tolist()
+    # pooled tokens per scale: everything in the context that is resampled
+    for g, s in enumerate(info["group_scale"]):
+        rows = [r for r in oracle.context_rows(desc, s) if r[4] > 1 and r[0] != oracle.KIND_SINK]
+        assert info["pooled_tokens"][g] == sum(r[5] for r in rows)
+
+
+def test_pool_bytes_wan13b():
+    desc = WORKLOADS["wan13b_layer"]["desc"]
+    info = _plan(desc).info()
+    ld = 12 * 128 * 2
+    read = 9360 + 2 * 3 * 1560          # 6 history frames + window states 1-2
+    write = 6 * 390 + 6 * 390            # both pooled to 15x26
+    assert info["pool_bytes_alg"] == 2 * (read + write) * ld
+
+
+@pytest.mark.parametrize("bad, status", [
+    (dict(num_states=0), mssa.MSSA_ERR_INVALID_ARG),
+    (dict(num_states=9), mssa.MSSA_ERR_INVALID_ARG),
+    (dict(scales=[1, 1, 3, 3, 3]), mssa.MSSA_ERR_UNSUPPORTED),
+    (dict(scales=[2, 1, 2, 2, 2]), mssa.MSSA_ERR_UNSUPPORTED),
+    (dict(scales=[1, 1, 2, 2, 128]), mssa.MSSA_ERR_UNSUPPORTED),
+    (dict(head_dim=96), mssa.MSSA_ERR_UNSUPPORTED),
+    (dict(grid_h=0), mssa.MSSA_ERR_INVALID_ARG),
+    (dict(frames_per_state=0), mssa.MSSA_ERR_INVALID_ARG),
+    (dict(sink_frames=-1), mssa.MSSA_ERR_INVALID_ARG),
+    (dict(num_heads=0), mssa.MSSA_ERR_INVALID_ARG),
+    (dict(dtype=7), mssa.MSSA_ERR_INVALID_ARG),
+    (dict(softmax_scale=float("nan")), mssa.MSSA_ERR_INVALID_ARG),
+    (dict(grid_h=40000, grid_w=40000, hist_frames=4), mssa.MSSA_ERR_UNSUPPORTED),
+])
+def test_invalid_descriptors(bad, status):
+    with pytest.raises(mssa.MssaError) as e:
+        _plan(WORKLOADS["wan13b_layer"]["desc"], **bad)
+    assert e.value.status == status
+    assert mssa.lib.mssa_last_error().decode()
+
+
+def test_calls_rejected_before_launch():
+    """Every failure below is detected on the host; no kernel is enqueued
+    (no GPU is touched: all pointers are fake, misaligned or NULL)."""
+    plan = _plan(WORKLOADS["wan13b_layer"]["desc"])
+    info = plan.info()
+    fake = 1 << 20  # 256-byte aligned, never dereferenced
+    ws = info["workspace_bytes"]
+    with pytest.raises(mssa.MssaError) as e:
+        mssa.mssa_pool_kv(plan, fake, fake, fake, fake, fake, ws - 1, stream=0)
+    assert e.value.status == mssa.MSSA_ERR_WORKSPACE
+    with pytest.raises(mssa.MssaError) as e:
+        mssa.mssa_pool_kv(plan, None, fake, fake, fake, fake, ws, stream=0)
+    assert e.value.status == mssa.MSSA_ERR_INVALID_ARG
+    with pytest.raises(mssa.MssaError) as e:
+        mssa.mssa_pool_kv(plan, fake, fake, fake, fake, fake + 16, ws, stream=0)
+    assert e.value.status == mssa.MSSA_ERR_INVALID_ARG
+    with pytest.raises(mssa.MssaError) as e:
+        mssa.mssa_forward(plan, fake, fake, fake, fake, fake, fake, fake, fake, fake,
+                          workspace_bytes=0, stream=0)
+    assert e.value.status == mssa.MSSA_ERR_WORKSPACE
+    with pytest.raises(mssa.MssaError) as e:
+        mssa.mssa_forward(plan, fake, None, fake, fake, fake, fake, fake, fake, fake,
+                          workspace_bytes=ws, stream=0)
+    assert e.value.status == mssa.MSSA_ERR_INVALID_ARG
+    with pytest.raises(mssa.MssaError) as e:
+        mssa.mssa_forward(plan, fake + 8, fake, fake, fake, fake, fake, fake, fake, fake + 4096,
+                          workspace_bytes=ws, stream=0)
+    assert e.value.status == mssa.MSSA_ERR_INVALID_ARG
+    with pytest.raises(mssa.MssaError) as e:
+        mssa.mssa_forward(plan, fake, fake, fake, fake, fake, fake, fake, fake, fake,
+                          workspace_bytes=ws, stream=0)
+    assert e.value.status == mssa.MSSA_ERR_INVALID_ARG  # out aliases q_win
+    with pytest.raises(mssa.MssaError) as e:
+        mssa.mssa_plan_query(mssa.Plan(None, {}))
+    assert e.value.status == mssa.MSSA_ERR_INVALID_ARG
+
+
+def test_table_buffer_too_small():
+    import ctypes
+    plan = _plan(WORKLOADS["tiny_f32"]["desc"])
+    need = ctypes.c_int64()
+    buf = (ctypes.c_int64 * 4)()
+    st_ = mssa.lib.mssa_plan_tables(plan.handle, buf, 4, ctypes.byref(need))
+    assert st_ == mssa.MSSA_ERR_INVALID_ARG and need.value > 4
