@@ -1,0 +1,234 @@
+"""Benchmark of the MSSA hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+One step is one rolling pass of one layer: mssa_pool_kv (K/V resampling)
+followed by mssa_forward (multi-scale attention) over inputs already resident
+in HBM.  Input sets are rotated between steps (distinct device copies) so
+that the pool kernel reads from HBM rather than from the 256 MB last-level
+cache.  Kernel durations come from HIP events recorded around each launch on
+the stream the kernels run on.
+
+Prints one JSON line: effective TFLOP/s (algorithmic FLOP / pass time), ms per
+pass, the roofline of the attention kernel and the fp64 CPU oracle timed on a
+bounded sample of the same workload.
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 MFMA: 256 CU x 4096 flop/clk x 2.4 GHz
+PEAK_F32_TFLOPS = 157.3
+PEAK_HBM_GBPS = 8000.0
+METRIC = "MSSA effective TFLOP/s + ms per rolling pass; % of bf16 MFMA peak (1 GPU)"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "mssa_fwd_traffic_{workload}.txt")
+FWD_SOURCE = os.path.join(ROOT, "paper_2607_20940_amd", "csrc", "attention_fwd.hip")
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_source_hash():
+    with open(FWD_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def read_traffic(workload):
+    """HBM bytes per forward launch from the committed counter summary, if it
+    was taken on the current attention kernel source (else None)."""
+    path = TRAFFIC_FILE.format(workload=workload)
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                vals[k.strip()] = v.strip()
+    if vals.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(w, x, info, budget_s):
+    """Time the fp64 oracle (as it stands) on the host: whole heads of the
+    workload (pool + attention for every query), one at a time, until the
+    time budget is used.  Returns the oracle's effective TFLOP/s."""
+    import oracle
+    from paper_2607_20940_amd.inputs import to_f64
+
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # noqa: BLE001
+        threads = os.cpu_count() or 1
+    desc = dict(w["desc"])
+    nh = desc["num_heads"]
+    flops_per_head = info["flops_alg"] / nh
+    done, t_total = 0, 0.0
+    for h in range(nh):
+        xh = {k: (None if v is None else to_f64(v[:, [h]], w["dtype"])) for k, v in x.items()}
+        d1 = dict(desc, num_heads=1)
+        t0 = time.perf_counter()
+        oracle.mssa_attention(d1, xh["q_win"], xh["k_sink"], xh["v_sink"], xh["k_hist"],
+                              xh["v_hist"], xh["k_win"], xh["v_win"])
+        t_total += time.perf_counter() - t0
+        done += 1
+        log(f"cpu oracle head {h}: {t_total:.1f} s cumulative")
+        if t_total >= budget_s:
+            break
+    return {
+        "value": flops_per_head * done / t_total / 1e12,
+        "unit": "TFLOP/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": f"{done} of {nh} heads of {w['name']} (pool + attention, all {info['n_q']} queries), "
+                  f"fp64 numpy, {t_total:.1f} s",
+        "ms_per_pass_extrapolated": 1e3 * t_total / done * nh,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="wan13b_layer")
+    ap.add_argument("--input-sets", type=int, default=4,
+                    help="distinct device copies of the inputs rotated between steps")
+    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py runs on one GPU only: MSSA here is a single-GPU kernel path with no "
+              f"collectives (asked for --gpus {args.gpus}, WORLD_SIZE={world}).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2607_20940_amd import mssa
+    from paper_2607_20940_amd.inputs import make_inputs
+    from paper_2607_20940_amd.workloads import WORKLOADS, input_shapes
+
+    w = dict(WORKLOADS[args.workload], name=args.workload)
+    desc = w["desc"]
+    dtype = w["dtype"]
+    plan = mssa.mssa_plan_create(dict(desc, dtype=dtype))
+    info = plan.info()
+    shapes = input_shapes(desc, info["n_q"], info["n_sink_tok"], info["n_hist_tok"])
+    log(f"workload {args.workload}: n_q={info['n_q']} n_kv={info['n_kv']} flops={info['flops_alg']:.4e}")
+    t0 = time.perf_counter()
+    x = make_inputs(shapes, w["seed"], w["amplitude"], dtype)
+    log(f"inputs generated in {time.perf_counter() - t0:.1f} s")
+
+    def dev(a):
+        if a is None:
+            return None
+        if dtype == "bf16":
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
+        return torch.from_numpy(a).cuda()
+
+    base = {k: dev(v) for k, v in x.items()}
+    sets = [base] + [{k: (None if v is None else v.clone()) for k, v in base.items()}
+                     for _ in range(args.input_sets - 1)]
+    ws = [torch.empty(max(256, info["workspace_bytes"]), dtype=torch.uint8, device="cuda")
+          for _ in sets]
+    outs = [torch.empty_like(base["q_win"]) for _ in sets]
+    stream = torch.cuda.current_stream()
+
+    def step(i, ev=None):
+        s = sets[i % len(sets)]
+        if ev is not None:
+            ev[0].record(stream)
+        mssa.mssa_pool_kv(plan, s["k_hist"], s["v_hist"], s["k_win"], s["v_win"], ws[i % len(sets)])
+        if ev is not None:
+            ev[1].record(stream)
+        mssa.mssa_forward(plan, s["q_win"], s["k_sink"], s["v_sink"], s["k_hist"], s["v_hist"],
+                          s["k_win"], s["v_win"], ws[i % len(sets)], outs[i % len(sets)])
+        if ev is not None:
+            ev[2].record(stream)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    log(f"warmup {args.warmup} steps done")
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for i in range(args.steps):
+        step(i, evs[i])
+    end.record(stream)
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(end)
+    pool_ms = np.array([e[0].elapsed_time(e[1]) for e in evs])
+    fwd_ms = np.array([e[1].elapsed_time(e[2]) for e in evs])
+    ms_per_step = total_ms / args.steps
+    log(f"timed {args.steps} steps: {ms_per_step:.4f} ms/pass, forward mean {fwd_ms.mean():.4f} ms, "
+        f"pool mean {pool_ms.mean():.4f} ms")
+
+    flops = info["flops_alg"]
+    value = flops / (ms_per_step * 1e-3) / 1e12
+    fwd_tflops = flops / (fwd_ms.mean() * 1e-3) / 1e12
+    peak = PEAK_BF16_TFLOPS if dtype == "bf16" else PEAK_F32_TFLOPS
+    pool_gbps = info["pool_bytes_alg"] / (pool_ms.mean() * 1e-3) / 1e9 if pool_ms.mean() > 0 else None
+
+    result = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": dtype,
+        "data": "synthetic",
+        "config": {
+            "workload": args.workload,
+            "heads": desc["num_heads"], "head_dim": desc["head_dim"],
+            "grid": f"{desc['grid_h']}x{desc['grid_w']}", "schedule": desc["scales"],
+            "sink_frames": desc["sink_frames"], "hist_frames": desc["hist_frames"],
+            "states": desc["num_states"], "frames_per_state": desc["frames_per_state"],
+            "n_q": info["n_q"], "n_kv": info["n_kv"], "flops_alg": flops,
+            "input_sets_rotated": len(sets),
+        },
+        "pct_of_bf16_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
+        "forward_ms": round(float(fwd_ms.mean()), 4),
+        "forward_ms_p10_p90": [round(float(np.percentile(fwd_ms, 10)), 4),
+                               round(float(np.percentile(fwd_ms, 90)), 4)],
+        "pool_ms": round(float(pool_ms.mean()), 4),
+        "pool": {"bound": "hbm", "achieved": None if pool_gbps is None else round(pool_gbps, 1),
+                 "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                 "frac": None if pool_gbps is None else round(pool_gbps / PEAK_HBM_GBPS, 4),
+                 "bytes_alg": info["pool_bytes_alg"]},
+        "roofline": {"kernel": "mssa_forward (fwd_bf16_kernel)" if dtype == "bf16" else "fwd_f32_kernel",
+                     "bound": "mfma", "achieved": round(fwd_tflops, 2), "peak": peak,
+                     "unit": "TFLOP/s", "frac": round(fwd_tflops / peak, 4),
+                     "traffic": read_traffic(args.workload)},
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(w, x, info, args.cpu_budget)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()
