@@ -30,7 +30,10 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+
+__device__ constexpr bf16x2 kOnes2 = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
 
 // Logical block -> (group, head, query tile).  Groups are stored longest
 // context first; inside a group consecutive blocks share a head.
@@ -46,27 +49,38 @@ __device__ inline Work decode(const FwdArgs& a, int L) {
   return {g, idx / nt, idx % nt};
 }
 
+// Lazy rescaling threshold (log2 units): the running max used for the
+// exponentials is raised only when a tile's max exceeds it by more than this,
+// so exponentials stay <= 2^8 and most tiles skip the O rescale.  The final
+// O / l is unchanged; only rounding differs.
+constexpr float kRescaleLog2 = 8.0f;
+
 template <int D>
-__global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(FwdArgs a) {
+__global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void fwd_bf16_kernel(FwdArgs a) {
   constexpr int BM = kFwdBM, BN = kFwdBN;
-  constexpr int KS = D / 16;   // 16-wide k-steps of q k^T
-  constexpr int DB = D / 32;   // 32-row blocks of O^T
-  constexpr int KSTR = D + 8;  // LDS row strides (elements)
-  constexpr int VSTR = D + 16;
-  constexpr int CPR = D / 8;   // 16-byte chunks per row
-  __shared__ __attribute__((aligned(16))) __bf16 Ks[BN * KSTR];
-  __shared__ __attribute__((aligned(16))) __bf16 Vs[BN * VSTR];
+  constexpr int KS = D / 16;    // 16-wide k-steps of q k^T
+  constexpr int DB = D / 32;    // 32-row blocks of O^T
+  constexpr int CPR = D / 8;    // 16-byte chunks per K/V row
+  constexpr int KSTR = D + 8;   // K row stride: 16 consecutive rows hit disjoint banks (b128 reads)
+  constexpr int VSTR = D + 32;  // V row stride: the 4x16 transposing reads of 32 lanes hit disjoint banks
+  constexpr int NLD = BN * CPR / kFwdThreads;  // 16-byte chunks per thread per tile and tensor
+  static_assert(NLD * kFwdThreads == BN * CPR, "tile load must divide evenly");
+  __shared__ __attribute__((aligned(16))) __bf16 Ks[2][BN * KSTR];
+  __shared__ __attribute__((aligned(16))) __bf16 Vs[2][BN * VSTR];
 
   const Work w = decode(a, blockIdx.x);
   const FwdGroupArgs& G = a.groups[w.g];
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
   const int n = lane & 31;   // query column of this lane
   const int hh = lane >> 5;  // half-wave
   const int q_row = G.q_begin + w.tile * BM + wave * 32 + n;
   const bool q_ok = q_row < G.q_end;
   const int64_t ld = a.ld;
   const int64_t hoff = static_cast<int64_t>(w.head) * D;
+  const float c = a.scale_log2e;
 
   bf16x8 qf[KS];
   {
@@ -83,92 +97,137 @@ __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(FwdArgs a) {
   f32x16 o[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db) o[db] = f32x16{};
-  float m_run = -INFINITY;  // running max, exp2 domain
+  float m_run = -INFINITY;  // running max in the exp2 domain (shared by both half-waves)
   float l_part = 0.f;       // this lane's share of the row sum
 
-  // Transposing-read address pieces: 16-lane group gq, lane r4/c4 within it.
+  // Transposing-read address of this lane inside a 16-key slab of V.
   const int gq = lane >> 4;
-  const int r4 = (lane & 15) >> 2;
-  const int c4 = lane & 3;
-  const int v_lane_off = (4 * (gq >> 1) + r4) * VSTR + 16 * (gq & 1) + 4 * c4;
+  const int v_lane_off = (4 * (gq >> 1) + ((lane & 15) >> 2)) * VSTR + 16 * (gq & 1) + 4 * (lane & 3);
 
-  for (int r = 0; r < G.n_runs; ++r) {
+  // Global -> register prefetch of one tile, then register -> LDS.
+  bf16x8 pk[NLD], pv[NLD];
+  auto issue = [&](int r, int t0) {
     const __bf16* Kg = static_cast<const __bf16*>(G.runs[r].k) + hoff;
     const __bf16* Vg = static_cast<const __bf16*>(G.runs[r].v) + hoff;
-    const int ntok = G.runs[r].n_tok;
-    for (int t0 = 0; t0 < ntok; t0 += BN) {
-      const int nvalid = min(BN, ntok - t0);
+    const int nv = G.runs[r].n_tok - t0;
 #pragma unroll
-      for (int c = threadIdx.x; c < BN * CPR; c += kFwdThreads) {
-        const int row = c / CPR, col = (c % CPR) * 8;
-        bf16x8 kv{}, vv{};
-        if (row < nvalid) {
-          const int64_t off = static_cast<int64_t>(t0 + row) * ld + col;
-          kv = *reinterpret_cast<const bf16x8*>(Kg + off);
-          vv = *reinterpret_cast<const bf16x8*>(Vg + off);
-        }
-        *reinterpret_cast<bf16x8*>(Ks + row * KSTR + col) = kv;
-        *reinterpret_cast<bf16x8*>(Vs + row * VSTR + col) = vv;
+    for (int i = 0; i < NLD; ++i) {
+      const int ch = i * kFwdThreads + tid;
+      const int row = ch / CPR, col = (ch % CPR) * 8;
+      bf16x8 kv{}, vv{};
+      if (row < nv) {
+        const int64_t off = static_cast<int64_t>(t0 + row) * ld + col;
+        kv = *reinterpret_cast<const bf16x8*>(Kg + off);
+        vv = *reinterpret_cast<const bf16x8*>(Vg + off);
       }
-      __syncthreads();
+      pk[i] = kv;
+      pv[i] = vv;
+    }
+  };
+  auto commit = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < NLD; ++i) {
+      const int ch = i * kFwdThreads + tid;
+      const int row = ch / CPR, col = (ch % CPR) * 8;
+      *reinterpret_cast<bf16x8*>(&Ks[buf][row * KSTR + col]) = pk[i];
+      *reinterpret_cast<bf16x8*>(&Vs[buf][row * VSTR + col]) = pv[i];
+    }
+  };
 
-      f32x16 s[BN / 32];
+  int r = 0, t0 = 0;
+  while (r < G.n_runs && G.runs[r].n_tok == 0) ++r;
+  if (r < G.n_runs) {
+    issue(r, 0);
+    commit(0);
+  }
+  __syncthreads();
+  int buf = 0;
+  while (r < G.n_runs) {
+    const int nvalid = min(BN, G.runs[r].n_tok - t0);
+    // next tile (possibly in the next non-empty run)
+    int rn = r, tn = t0 + BN;
+    if (tn >= G.runs[r].n_tok) {
+      rn = r + 1;
+      tn = 0;
+      while (rn < G.n_runs && G.runs[rn].n_tok == 0) ++rn;
+    }
+    const bool has_next = rn < G.n_runs;
+    if (has_next) issue(rn, tn);
+
+    const __bf16* Kb = Ks[buf];
+    const __bf16* Vb = Vs[buf];
+    f32x16 s[BN / 32];
 #pragma unroll
-      for (int kb = 0; kb < BN / 32; ++kb) {
-        s[kb] = f32x16{};
+    for (int kb = 0; kb < BN / 32; ++kb) {
+      s[kb] = f32x16{};
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          const bf16x8 ka = *reinterpret_cast<const bf16x8*>(Ks + (kb * 32 + n) * KSTR + ks * 16 + hh * 8);
-          s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[ks], s[kb], 0, 0, 0);
-        }
+      for (int ks = 0; ks < KS; ++ks) {
+        const bf16x8 ka = *reinterpret_cast<const bf16x8*>(Kb + (kb * 32 + n) * KSTR + ks * 16 + hh * 8);
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[ks], s[kb], 0, 0, 0);
       }
-      if (nvalid < BN) {
-#pragma unroll
-        for (int kb = 0; kb < BN / 32; ++kb)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            const int key = kb * 32 + 8 * (e >> 2) + 4 * hh + (e & 3);
-            if (key >= nvalid) s[kb][e] = -INFINITY;
-          }
-      }
-      float mx = -INFINITY;
+    }
+    if (nvalid < BN) {
 #pragma unroll
       for (int kb = 0; kb < BN / 32; ++kb)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[kb][e]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m_run, mx * a.scale_log2e);
+        for (int e = 0; e < 16; ++e) {
+          const int key = kb * 32 + 8 * (e >> 2) + 4 * hh + (e & 3);
+          if (key >= nvalid) s[kb][e] = -INFINITY;
+        }
+    }
+    float mx = s[0][0];
+#pragma unroll
+    for (int kb = 0; kb < BN / 32; ++kb)
+#pragma unroll
+      for (int e = (kb == 0 ? 1 : 0); e < 16; e += 2) {
+        if (e + 1 < 16)
+          mx = fmaxf(fmaxf(mx, s[kb][e]), s[kb][e + 1]);
+        else
+          mx = fmaxf(mx, s[kb][e]);
+      }
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float mt = mx * c;
+    if (__any(mt > m_run + kRescaleLog2)) {
+      const float m_new = fmaxf(m_run, mt);
       const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
       m_run = m_new;
       l_part *= alpha;
 #pragma unroll
       for (int db = 0; db < DB; ++db) o[db] *= alpha;
-
-      bf16x8 pb[BN / 32][2];
-#pragma unroll
-      for (int kb = 0; kb < BN / 32; ++kb)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][e], a.scale_log2e, -m_new));
-          l_part += p;
-          pb[kb][e >> 3][e & 7] = static_cast<__bf16>(p);
-        }
-
-#pragma unroll
-      for (int kb = 0; kb < BN / 32; ++kb)
-#pragma unroll
-        for (int cc = 0; cc < 2; ++cc) {
-          const __bf16* vrow = Vs + (kb * 32 + cc * 16) * VSTR + v_lane_off;
-#pragma unroll
-          for (int db = 0; db < DB; ++db) {
-            const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vrow + db * 32));
-            const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vrow + 8 * VSTR + db * 32));
-            const bf16x8 va = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-            o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[kb][cc], o[db], 0, 0, 0);
-          }
-        }
-      __syncthreads();
     }
+    const float mneg = -m_run;
+    bf16x8 pb[BN / 32][2];
+#pragma unroll
+    for (int kb = 0; kb < BN / 32; ++kb)
+#pragma unroll
+      for (int e = 0; e < 16; e += 2) {
+        bf16x2 pair;
+        pair[0] = static_cast<__bf16>(__builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][e], c, mneg)));
+        pair[1] = static_cast<__bf16>(__builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][e + 1], c, mneg)));
+        l_part = __builtin_amdgcn_fdot2_f32_bf16(pair, kOnes2, l_part, false);
+        pb[kb][e >> 3][e & 7] = pair[0];
+        pb[kb][e >> 3][(e & 7) + 1] = pair[1];
+      }
+
+#pragma unroll
+    for (int kb = 0; kb < BN / 32; ++kb)
+#pragma unroll
+      for (int cc = 0; cc < 2; ++cc) {
+        const __bf16* vrow = Vb + (kb * 32 + cc * 16) * VSTR + v_lane_off;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+          const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vrow + db * 32));
+          const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vrow + 8 * VSTR + db * 32));
+          const bf16x8 va = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[kb][cc], o[db], 0, 0, 0);
+        }
+      }
+
+    if (has_next) commit(buf ^ 1);
+    __syncthreads();
+    r = rn;
+    t0 = tn;
+    buf ^= 1;
   }
 
   const float l_tot = l_part + __shfl_xor(l_part, 32);
