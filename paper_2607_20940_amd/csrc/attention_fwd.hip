@@ -22,6 +22,8 @@
 // softmax with expf; used for fp32 plans (correctness path).
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "kernels.hpp"
 
 namespace mssa {
@@ -55,6 +57,14 @@ __device__ inline Work decode(const FwdArgs& a, int L) {
 // O / l is unchanged; only rounding differs.
 constexpr float kRescaleLog2 = 8.0f;
 
+// Buffer resource (gfx9 layout) over `bytes` bytes from `base`: loads past
+// the end return zeros, which is how ragged K/V tiles are zero-filled without
+// per-element selects.
+__device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0),
+                                           static_cast<int>(bytes), 0x00020000);
+}
+
 template <int D>
 __global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void fwd_bf16_kernel(FwdArgs a) {
@@ -62,12 +72,14 @@ void fwd_bf16_kernel(FwdArgs a) {
   constexpr int KS = D / 16;    // 16-wide k-steps of q k^T
   constexpr int DB = D / 32;    // 32-row blocks of O^T
   constexpr int CPR = D / 8;    // 16-byte chunks per K/V row
+  constexpr int RPL = kFwdThreads / CPR;  // rows covered by one pass of the block
   constexpr int KSTR = D + 8;   // K row stride: 16 consecutive rows hit disjoint banks (b128 reads)
   constexpr int VSTR = D + 32;  // V row stride: the 4x16 transposing reads of 32 lanes hit disjoint banks
-  constexpr int NLD = BN * CPR / kFwdThreads;  // 16-byte chunks per thread per tile and tensor
-  static_assert(NLD * kFwdThreads == BN * CPR, "tile load must divide evenly");
-  __shared__ __attribute__((aligned(16))) __bf16 Ks[2][BN * KSTR];
-  __shared__ __attribute__((aligned(16))) __bf16 Vs[2][BN * VSTR];
+  constexpr int NLD = BN / RPL; // 16-byte chunks per thread per tile and tensor
+  constexpr int KT = BN * KSTR, VT = BN * VSTR;  // elements per LDS tile
+  static_assert(NLD * RPL == BN, "tile load must divide evenly");
+  // [K buf0 | K buf1 | V buf0 | V buf1]; every offset fits a ds instruction's immediate.
+  __shared__ __attribute__((aligned(16))) __bf16 lds[2 * KT + 2 * VT];
 
   const Work w = decode(a, blockIdx.x);
   const FwdGroupArgs& G = a.groups[w.g];
@@ -80,6 +92,7 @@ void fwd_bf16_kernel(FwdArgs a) {
   const bool q_ok = q_row < G.q_end;
   const int64_t ld = a.ld;
   const int64_t hoff = static_cast<int64_t>(w.head) * D;
+  const uint32_t row_bytes = static_cast<uint32_t>(ld) * 2;
   const float c = a.scale_log2e;
 
   bf16x8 qf[KS];
@@ -100,69 +113,54 @@ void fwd_bf16_kernel(FwdArgs a) {
   float m_run = -INFINITY;  // running max in the exp2 domain (shared by both half-waves)
   float l_part = 0.f;       // this lane's share of the row sum
 
-  // Transposing-read address of this lane inside a 16-key slab of V.
+  // Per-thread constants of the tile copy: global byte offset inside a tile
+  // and LDS element offset of chunk 0 (chunk i adds i * RPL rows).
+  const int ld_row = tid / CPR, ld_col = (tid % CPR) * 8;
+  const uint32_t g_off = ld_row * row_bytes + ld_col * 2;
+  const int k_st = ld_row * KSTR + ld_col;
+  const int v_st = ld_row * VSTR + ld_col;
+  // Transposing-read offset of this lane inside a 16-key slab of V.
   const int gq = lane >> 4;
-  const int v_lane_off = (4 * (gq >> 1) + ((lane & 15) >> 2)) * VSTR + 16 * (gq & 1) + 4 * (lane & 3);
+  const int v_rd = (4 * (gq >> 1) + ((lane & 15) >> 2)) * VSTR + 16 * (gq & 1) + 4 * (lane & 3);
+  const int k_rd = n * KSTR + hh * 8;
 
-  // Global -> register prefetch of one tile, then register -> LDS.
   bf16x8 pk[NLD], pv[NLD];
+  // Issue the loads of the tile starting at token t0 of run r (zero past the run's end).
   auto issue = [&](int r, int t0) {
-    const __bf16* Kg = static_cast<const __bf16*>(G.runs[r].k) + hoff;
-    const __bf16* Vg = static_cast<const __bf16*>(G.runs[r].v) + hoff;
-    const int nv = G.runs[r].n_tok - t0;
+    const int nv = min(G.runs[r].n_tok - t0, BN);
+    const uint32_t bytes = static_cast<uint32_t>(nv - 1) * row_bytes + D * 2;
+    const int64_t base = static_cast<int64_t>(t0) * ld + hoff;
+    const auto rk = make_rsrc(static_cast<const __bf16*>(G.runs[r].k) + base, bytes);
+    const auto rv = make_rsrc(static_cast<const __bf16*>(G.runs[r].v) + base, bytes);
 #pragma unroll
     for (int i = 0; i < NLD; ++i) {
-      const int ch = i * kFwdThreads + tid;
-      const int row = ch / CPR, col = (ch % CPR) * 8;
-      bf16x8 kv{}, vv{};
-      if (row < nv) {
-        const int64_t off = static_cast<int64_t>(t0 + row) * ld + col;
-        kv = *reinterpret_cast<const bf16x8*>(Kg + off);
-        vv = *reinterpret_cast<const bf16x8*>(Vg + off);
-      }
-      pk[i] = kv;
-      pv[i] = vv;
+      const uint32_t off = g_off + i * RPL * row_bytes;
+      pk[i] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rk, off, 0, 0));
+      pv[i] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rv, off, 0, 0));
     }
   };
-  auto commit = [&](int buf) {
+  auto commit = [&](auto bufc) {
+    constexpr int buf = decltype(bufc)::value;
 #pragma unroll
     for (int i = 0; i < NLD; ++i) {
-      const int ch = i * kFwdThreads + tid;
-      const int row = ch / CPR, col = (ch % CPR) * 8;
-      *reinterpret_cast<bf16x8*>(&Ks[buf][row * KSTR + col]) = pk[i];
-      *reinterpret_cast<bf16x8*>(&Vs[buf][row * VSTR + col]) = pv[i];
+      *reinterpret_cast<bf16x8*>(&lds[buf * KT + k_st + i * RPL * KSTR]) = pk[i];
+      *reinterpret_cast<bf16x8*>(&lds[2 * KT + buf * VT + v_st + i * RPL * VSTR]) = pv[i];
     }
   };
 
-  int r = 0, t0 = 0;
-  while (r < G.n_runs && G.runs[r].n_tok == 0) ++r;
-  if (r < G.n_runs) {
-    issue(r, 0);
-    commit(0);
-  }
-  __syncthreads();
-  int buf = 0;
-  while (r < G.n_runs) {
-    const int nvalid = min(BN, G.runs[r].n_tok - t0);
-    // next tile (possibly in the next non-empty run)
-    int rn = r, tn = t0 + BN;
-    if (tn >= G.runs[r].n_tok) {
-      rn = r + 1;
-      tn = 0;
-      while (rn < G.n_runs && G.runs[rn].n_tok == 0) ++rn;
-    }
-    const bool has_next = rn < G.n_runs;
-    if (has_next) issue(rn, tn);
-
-    const __bf16* Kb = Ks[buf];
-    const __bf16* Vb = Vs[buf];
+  // One 64-key tile from LDS buffer `buf`: S^T = K Q^T, online softmax, O^T += V^T P^T.
+  auto compute = [&](auto bufc, int nvalid) {
+    constexpr int buf = decltype(bufc)::value;
+    const __bf16* Kb = lds + buf * KT;
+    const __bf16* Vb = lds + 2 * KT + buf * VT;
     f32x16 s[BN / 32];
 #pragma unroll
     for (int kb = 0; kb < BN / 32; ++kb) {
-      s[kb] = f32x16{};
+      const bf16x8 ka0 = *reinterpret_cast<const bf16x8*>(Kb + k_rd + kb * 32 * KSTR);
+      s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka0, qf[0], f32x16{}, 0, 0, 0);
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const bf16x8 ka = *reinterpret_cast<const bf16x8*>(Kb + (kb * 32 + n) * KSTR + ks * 16 + hh * 8);
+      for (int ks = 1; ks < KS; ++ks) {
+        const bf16x8 ka = *reinterpret_cast<const bf16x8*>(Kb + k_rd + kb * 32 * KSTR + ks * 16);
         s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[ks], s[kb], 0, 0, 0);
       }
     }
@@ -175,16 +173,13 @@ void fwd_bf16_kernel(FwdArgs a) {
           if (key >= nvalid) s[kb][e] = -INFINITY;
         }
     }
-    float mx = s[0][0];
+    float mx = fmaxf(s[0][0], s[0][1]);
 #pragma unroll
-    for (int kb = 0; kb < BN / 32; ++kb)
+    for (int e = 2; e < 16; e += 2) mx = fmaxf(fmaxf(mx, s[0][e]), s[0][e + 1]);
 #pragma unroll
-      for (int e = (kb == 0 ? 1 : 0); e < 16; e += 2) {
-        if (e + 1 < 16)
-          mx = fmaxf(fmaxf(mx, s[kb][e]), s[kb][e + 1]);
-        else
-          mx = fmaxf(mx, s[kb][e]);
-      }
+    for (int kb = 1; kb < BN / 32; ++kb)
+#pragma unroll
+      for (int e = 0; e < 16; e += 2) mx = fmaxf(fmaxf(mx, s[kb][e]), s[kb][e + 1]);
     mx = fmaxf(mx, __shfl_xor(mx, 32));
     const float mt = mx * c;
     if (__any(mt > m_run + kRescaleLog2)) {
@@ -208,12 +203,11 @@ void fwd_bf16_kernel(FwdArgs a) {
         pb[kb][e >> 3][e & 7] = pair[0];
         pb[kb][e >> 3][(e & 7) + 1] = pair[1];
       }
-
 #pragma unroll
     for (int kb = 0; kb < BN / 32; ++kb)
 #pragma unroll
       for (int cc = 0; cc < 2; ++cc) {
-        const __bf16* vrow = Vb + (kb * 32 + cc * 16) * VSTR + v_lane_off;
+        const __bf16* vrow = Vb + v_rd + (kb * 32 + cc * 16) * VSTR;
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
           const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vrow + db * 32));
@@ -222,12 +216,43 @@ void fwd_bf16_kernel(FwdArgs a) {
           o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[kb][cc], o[db], 0, 0, 0);
         }
       }
+  };
 
-    if (has_next) commit(buf ^ 1);
+  // Walk the runs tile by tile; the loop body is unrolled over the two LDS
+  // buffers so that every LDS address is a per-thread constant plus an
+  // immediate.
+  int r = 0, t0 = 0;
+  while (r < G.n_runs && G.runs[r].n_tok == 0) ++r;
+  auto advance = [&](int& rr, int& tt) {
+    tt += BN;
+    if (tt >= G.runs[rr].n_tok) {
+      tt = 0;
+      ++rr;
+      while (rr < G.n_runs && G.runs[rr].n_tok == 0) ++rr;
+    }
+  };
+  if (r < G.n_runs) {
+    issue(r, 0);
+    commit(std::integral_constant<int, 0>{});
+  }
+  __syncthreads();
+  auto step = [&](auto bufc) -> bool {
+    constexpr int buf = decltype(bufc)::value;
+    const int nvalid = min(BN, G.runs[r].n_tok - t0);
+    int rn = r, tn = t0;
+    advance(rn, tn);
+    const bool has_next = rn < G.n_runs;
+    if (has_next) issue(rn, tn);
+    compute(bufc, nvalid);
+    if (has_next) commit(std::integral_constant<int, buf ^ 1>{});
     __syncthreads();
     r = rn;
     t0 = tn;
-    buf ^= 1;
+    return has_next;
+  };
+  if (r < G.n_runs) {
+    while (step(std::integral_constant<int, 0>{}) && step(std::integral_constant<int, 1>{})) {
+    }
   }
 
   const float l_tot = l_part + __shfl_xor(l_part, 32);
