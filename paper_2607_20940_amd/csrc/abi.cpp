@@ -4,6 +4,7 @@
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
+#include <cstdlib>
 #include <cstring>
 #include <new>
 #include <string>
@@ -14,7 +15,6 @@
 
 struct mssa_plan_s {
   mssa::Plan p;
-  std::vector<int> order;  // groups, longest context first
 };
 
 namespace {
@@ -27,6 +27,26 @@ mssa_status fail(mssa_status s, const std::string& msg) {
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Attention blocks resident at once on the current device (CUs x blocks per
+// CU), or 0 when there is no usable device (the plan then assumes 512).
+int resident_attention_blocks(int head_dim) {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return 0;
+  }
+  const int per_cu = mssa::forward_blocks_per_cu(head_dim);
+  return per_cu > 0 ? cus * per_cu : 0;
+}
+
+// MSSA_FWD_RANGES=<n> forces the number of attention tile ranges (used by the
+// tests to make items split across several ranges).
+int ranges_override() {
+  const char* e = std::getenv("MSSA_FWD_RANGES");
+  return e ? std::atoi(e) : 0;
+}
 
 mssa_status check_device(hipError_t e, const char* what) {
   if (e == hipSuccess) return MSSA_OK;
@@ -42,15 +62,12 @@ mssa_status mssa_plan_create(const mssa_plan_desc* desc, mssa_plan* out) {
   try {
     auto* h = new mssa_plan_s;
     std::string err;
-    const mssa_status s = mssa::build_plan(*desc, h->p, err);
+    const mssa_status s = mssa::build_plan(*desc, resident_attention_blocks(desc->head_dim),
+                                           ranges_override(), h->p, err);
     if (s != MSSA_OK) {
       delete h;
       return fail(s, err);
     }
-    const int G = static_cast<int>(h->p.groups.size());
-    for (int g = 0; g < G; ++g) h->order.push_back(g);
-    std::stable_sort(h->order.begin(), h->order.end(),
-                     [&](int x, int y) { return h->p.groups[x].n_kv > h->p.groups[y].n_kv; });
     *out = h;
     return MSSA_OK;
   } catch (const std::bad_alloc&) {
@@ -182,16 +199,23 @@ mssa_status mssa_forward(mssa_plan plan, const void* q_win, const void* k_sink, 
   a.num_heads = p.desc.num_heads;
   a.scale = p.softmax_scale;
   a.scale_log2e = p.softmax_scale * 1.4426950408889634f;
+  a.n_ranges = p.n_ranges;
+  a.total_tiles = p.total_tiles;
+  a.tail_begin = p.tail_begin;
+  a.dp_rounds = p.dp_rounds;
   const char* ws = static_cast<const char*>(workspace);
+  a.partial = p.partial_bytes > 0 ? reinterpret_cast<float*>(const_cast<char*>(ws) + p.partial_off) : nullptr;
   int64_t blocks = 0;
   int gi = 0;
-  for (int g : plan->order) {
+  for (int g : p.order) {
     const mssa::QGroup& Q = p.groups[g];
     mssa::FwdGroupArgs& A = a.groups[gi++];
     A.q_begin = Q.q_begin;
     A.q_end = Q.q_end;
     A.n_qtiles = (Q.q_end - Q.q_begin + bm - 1) / bm;
     A.block_begin = static_cast<int32_t>(blocks);
+    A.tiles_per_item = p.tiles_per_item[g];
+    A.tile_begin = p.tile_begin[g];
     if (p.runs[g].size() > static_cast<size_t>(mssa::kMaxRuns))
       return fail(MSSA_ERR_UNSUPPORTED, "too many context runs for one query scale");
     A.n_runs = static_cast<int32_t>(p.runs[g].size());

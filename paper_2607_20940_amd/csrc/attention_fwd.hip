@@ -32,6 +32,7 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
@@ -57,6 +58,60 @@ __device__ inline Work decode(const FwdArgs& a, int L) {
 // O / l is unchanged; only rounding differs.
 constexpr float kRescaleLog2 = 8.0f;
 
+// ---------------------------------------------------------------------------
+// Persistent schedule.  An item is one (query scale, head, 128-query tile); its
+// context is tiles_per_item 64-key tiles.  Items are numbered group by group
+// (longest context first), head-major, and laid out in a linear tile space of
+// total_tiles tiles.  Each of the n_ranges blocks first attends dp_rounds
+// whole items (item r * n_ranges + rho in round r), in lockstep with the
+// blocks of its XCD, which work on neighbouring query tiles of the same head
+// and so share K/V in L2.  The remaining items (from tail_begin) are cut into
+// one contiguous tail range per block, sized so that every block's total is
+// total_tiles / n_ranges.  A tail range may begin or end inside an item: that
+// piece writes a partial record (O unnormalised, running max, row sum) and
+// combine_kernel merges the pieces of each split item in range order.  Record
+// of the piece of an item inside tail range j: 2j if the item began at or
+// before the range start (the range's first piece), else 2j + 1.
+
+// First tile of item i (i may be the total item count).
+__device__ inline int64_t item_tile(const FwdArgs& a, int64_t i) {
+  int g = 0;
+  while (g + 1 < a.n_groups && i >= a.groups[g + 1].block_begin) ++g;
+  return a.groups[g].tile_begin + (i - a.groups[g].block_begin) * a.groups[g].tiles_per_item;
+}
+
+// Start of tail range rho: tail_begin + rho * total / n_ranges minus the
+// tiles that the ranges before it spent on whole-item rounds.
+__device__ inline int64_t range_begin(const FwdArgs& a, int rho) {
+  const int B = a.n_ranges;
+  int64_t dp = 0;
+  for (int r = 0; r < a.dp_rounds; ++r)
+    dp += item_tile(a, static_cast<int64_t>(r) * B + rho) - item_tile(a, static_cast<int64_t>(r) * B);
+  return a.tail_begin + static_cast<int64_t>(rho) * a.total_tiles / B - dp;
+}
+
+// Blocks are dispatched round-robin over the 8 XCDs; give each XCD a
+// contiguous eighth of the range indices so that its L2 serves few heads.
+__device__ inline int range_of_block(int b, int B) {
+  const int q = B / 8, r = B % 8, x = b % 8, j = b / 8;
+  return (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + j;
+}
+
+struct Loc {
+  int g, item, k;      // group, item within the group, tile within the item
+  int64_t item_begin;  // linear tile of the item's first tile
+};
+
+__device__ inline Loc locate(const FwdArgs& a, int64_t t) {
+  int g = 0;
+  while (g + 1 < a.n_groups && t >= a.groups[g + 1].tile_begin) ++g;
+  const FwdGroupArgs& G = a.groups[g];
+  const int64_t rel = t - G.tile_begin;
+  const int item = static_cast<int>(rel / G.tiles_per_item);
+  const int k = static_cast<int>(rel - static_cast<int64_t>(item) * G.tiles_per_item);
+  return {g, item, k, G.tile_begin + static_cast<int64_t>(item) * G.tiles_per_item};
+}
+
 // Buffer resource (gfx9 layout) over `bytes` bytes from `base`: loads past
 // the end return zeros, which is how ragged K/V tiles are zero-filled without
 // per-element selects.
@@ -66,32 +121,73 @@ __device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t by
 }
 
 template <int D>
-__global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
-void fwd_bf16_kernel(FwdArgs a) {
-  constexpr int BM = kFwdBM, BN = kFwdBN;
-  constexpr int KS = D / 16;    // 16-wide k-steps of q k^T
-  constexpr int DB = D / 32;    // 32-row blocks of O^T
-  constexpr int CPR = D / 8;    // 16-byte chunks per K/V row
-  constexpr int RPL = kFwdThreads / CPR;  // rows covered by one pass of the block
-  constexpr int KSTR = D + 8;   // K row stride: 16 consecutive rows hit disjoint banks (b128 reads)
-  constexpr int VSTR = D + 32;  // V row stride: the 4x16 transposing reads of 32 lanes hit disjoint banks
-  constexpr int NLD = BN / RPL; // 16-byte chunks per thread per tile and tensor
-  constexpr int KT = BN * KSTR, VT = BN * VSTR;  // elements per LDS tile
+struct FwdTile {
+  static constexpr int BM = kFwdBM, BN = kFwdBN;
+  static constexpr int KS = D / 16;    // 16-wide k-steps of q k^T
+  static constexpr int DB = D / 32;    // 32-row blocks of O^T
+  static constexpr int CPR = D / 8;    // 16-byte chunks per K/V row
+  static constexpr int RPL = kFwdThreads / CPR;  // rows covered by one pass of the block
+  static constexpr int KSTR = D + 8;   // K row stride: 16 consecutive rows hit disjoint banks
+  static constexpr int VSTR = D + 32;  // V row stride: transposing reads of 32 lanes hit disjoint banks
+  static constexpr int NLD = BN / RPL; // 16-byte chunks per thread per tile and tensor
+  static constexpr int KT = BN * KSTR, VT = BN * VSTR;  // elements per LDS tile
   static_assert(NLD * RPL == BN, "tile load must divide evenly");
-  // [K buf0 | K buf1 | V buf0 | V buf1]; every offset fits a ds instruction's immediate.
-  __shared__ __attribute__((aligned(16))) __bf16 lds[2 * KT + 2 * VT];
+};
 
-  const Work w = decode(a, blockIdx.x);
-  const FwdGroupArgs& G = a.groups[w.g];
+// Position of a 64-key tile inside an item's run list.
+struct TilePos {
+  int r, t0;
+};
+
+// Value of lane l ^ 32.  v_permlane32_swap exchanges the upper half of its
+// first operand with the lower half of its second; whether the compiler gives
+// the two operands one register or two, lane l < 32 finds lane l + 32 in the
+// second result and lane l >= 32 finds lane l - 32 in the first.
+__device__ inline float other_half(float v) {
+  const int b = __builtin_bit_cast(int, v);
+  const auto sw = __builtin_amdgcn_permlane32_swap(b, b, false, false);
+  return __builtin_bit_cast(float, (threadIdx.x & 32) ? sw[0] : sw[1]);
+}
+
+__device__ inline float halfwave_max(float v) { return fmaxf(v, other_half(v)); }
+
+__device__ inline float halfwave_sum(float v) { return v + other_half(v); }
+
+// One piece: tiles [k, k + nt) of item `item` of group G, by the whole block.
+// Writes the final output if the piece is the whole item, else partial
+// record `rec`.
+//
+// The 8 waves form two groups of 4 (waves w and w + 4 share a SIMD); group 0
+// owns queries 0..127 of the item's tile, group 1 queries 128..255.  Phases
+// are separated by block barriers; in phase 2j group 0 runs its matrix-core
+// step M(j) = {O += P_{j-1} V_{j-1}; S_j = K_j Q^T} while group 1 runs its
+// softmax step on S_{j-1}, and in phase 2j + 1 the roles swap.  Each SIMD
+// thus has one wave issuing MFMAs while the other issues VALU work.  K_j is
+// loaded from global memory during phase 2j - 2 and stored to LDS at the end
+// of phase 2j - 1; V_j is loaded during phase 2j - 1 and stored at the end of
+// phase 2j; two LDS buffers each suffice.
+template <int D>
+__device__ __forceinline__ void attend_piece(const FwdArgs& a, const FwdGroupArgs& G, int item, int k,
+                                             int nt, bool whole, int rec, __bf16* lds) {
+  using P = FwdTile<D>;
+  constexpr int BM = P::BM, BN = P::BN, KS = P::KS, DB = P::DB, CPR = P::CPR, RPL = P::RPL;
+  constexpr int KSTR = P::KSTR, VSTR = P::VSTR, NLD = P::NLD, KT = P::KT, VT = P::VT;
+
+  const int head = item / G.n_qtiles;
+  const int qtile = item - head * G.n_qtiles;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int n = lane & 31;   // query column of this lane
-  const int hh = lane >> 5;  // half-wave
-  const int q_row = G.q_begin + w.tile * BM + wave * 32 + n;
+  // Wave-uniform values go through readfirstlane so that branches on them are
+  // scalar branches: MFMA instructions ignore EXEC, so a lane-masked branch
+  // around the matrix-core step would still run its MFMAs.
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int grp = wave >> 2;  // 0: matrix core in even phases; 1: in odd phases
+  const int n = lane & 31;    // query column of this lane
+  const int hh = lane >> 5;   // half-wave
+  const int q_row = G.q_begin + qtile * BM + wave * 32 + n;
   const bool q_ok = q_row < G.q_end;
   const int64_t ld = a.ld;
-  const int64_t hoff = static_cast<int64_t>(w.head) * D;
+  const int64_t hoff = static_cast<int64_t>(head) * D;
   const uint32_t row_bytes = static_cast<uint32_t>(ld) * 2;
   const float c = a.scale_log2e;
 
@@ -112,58 +208,113 @@ void fwd_bf16_kernel(FwdArgs a) {
   for (int db = 0; db < DB; ++db) o[db] = f32x16{};
   float m_run = -INFINITY;  // running max in the exp2 domain (shared by both half-waves)
   float l_part = 0.f;       // this lane's share of the row sum
+  f32x16 s[BN / 32];
+  bf16x8 pb[BN / 32][2];
 
-  // Per-thread constants of the tile copy: global byte offset inside a tile
-  // and LDS element offset of chunk 0 (chunk i adds i * RPL rows).
   const int ld_row = tid / CPR, ld_col = (tid % CPR) * 8;
   const uint32_t g_off = ld_row * row_bytes + ld_col * 2;
   const int k_st = ld_row * KSTR + ld_col;
   const int v_st = ld_row * VSTR + ld_col;
-  // Transposing-read offset of this lane inside a 16-key slab of V.
   const int gq = lane >> 4;
   const int v_rd = (4 * (gq >> 1) + ((lane & 15) >> 2)) * VSTR + 16 * (gq & 1) + 4 * (lane & 3);
   const int k_rd = n * KSTR + hh * 8;
+  __bf16* const Klds = lds;
+  __bf16* const Vlds = lds + 2 * KT;
+
+  auto advance = [&](TilePos& t) {
+    t.t0 += BN;
+    if (t.t0 >= G.runs[t.r].n_tok) {
+      t.t0 = 0;
+      ++t.r;
+      while (t.r < G.n_runs && G.runs[t.r].n_tok == 0) ++t.r;
+    }
+  };
+  TilePos first{0, 0};
+  {
+    int kk = k;
+    while (kk >= (G.runs[first.r].n_tok + BN - 1) / BN) {
+      kk -= (G.runs[first.r].n_tok + BN - 1) / BN;
+      ++first.r;
+    }
+    first.t0 = kk * BN;
+  }
 
   bf16x8 pk[NLD], pv[NLD];
-  // Issue the loads of the tile starting at token t0 of run r (zero past the run's end).
-  auto issue = [&](int r, int t0) {
-    const int nv = min(G.runs[r].n_tok - t0, BN);
+  auto load = [&](const void* run_base, TilePos t, bf16x8* dst) {
+    const int nv = min(G.runs[t.r].n_tok - t.t0, BN);
     const uint32_t bytes = static_cast<uint32_t>(nv - 1) * row_bytes + D * 2;
-    const int64_t base = static_cast<int64_t>(t0) * ld + hoff;
-    const auto rk = make_rsrc(static_cast<const __bf16*>(G.runs[r].k) + base, bytes);
-    const auto rv = make_rsrc(static_cast<const __bf16*>(G.runs[r].v) + base, bytes);
+    const auto rs = make_rsrc(static_cast<const __bf16*>(run_base) + static_cast<int64_t>(t.t0) * ld + hoff, bytes);
 #pragma unroll
-    for (int i = 0; i < NLD; ++i) {
-      const uint32_t off = g_off + i * RPL * row_bytes;
-      pk[i] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rk, off, 0, 0));
-      pv[i] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rv, off, 0, 0));
+    for (int i = 0; i < NLD; ++i)
+      dst[i] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rs, g_off + i * RPL * row_bytes, 0, 0));
+  };
+  auto store_k = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < NLD; ++i)
+      *reinterpret_cast<bf16x8*>(Klds + buf * KT + k_st + i * RPL * KSTR) = pk[i];
+  };
+  auto store_v = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < NLD; ++i)
+      *reinterpret_cast<bf16x8*>(Vlds + buf * VT + v_st + i * RPL * VSTR) = pv[i];
+  };
+
+  // Matrix-core step: O += P V from V buffer vb (if pv_on), S = K Q^T from K
+  // buffer kb (if s_on).  Operands go through a two-stage register pipeline
+  // (the LDS reads of stage i + 1 are issued before the MFMAs of stage i);
+  // scheduling barriers keep the compiler from hoisting every read up front.
+  auto read_v = [&](const __bf16* Vb, int stage, bf16x8* va) {
+    const int kb = stage >> 1, cc = stage & 1;
+    const __bf16* vrow = Vb + (kb * 32 + cc * 16) * VSTR;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vrow + db * 32));
+      const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vrow + 8 * VSTR + db * 32));
+      va[db] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
     }
   };
-  auto commit = [&](auto bufc) {
-    constexpr int buf = decltype(bufc)::value;
+  auto read_k = [&](const __bf16* Kb, int ks, bf16x8* ka) {
 #pragma unroll
-    for (int i = 0; i < NLD; ++i) {
-      *reinterpret_cast<bf16x8*>(&lds[buf * KT + k_st + i * RPL * KSTR]) = pk[i];
-      *reinterpret_cast<bf16x8*>(&lds[2 * KT + buf * VT + v_st + i * RPL * VSTR]) = pv[i];
+    for (int kb = 0; kb < BN / 32; ++kb)
+      ka[kb] = *reinterpret_cast<const bf16x8*>(Kb + kb * 32 * KSTR + ks * 16);
+  };
+  auto mstep = [&](auto pv_c, auto s_c, int vb, int kb_) {
+    constexpr bool kPV = decltype(pv_c)::value, kS = decltype(s_c)::value;
+    const __bf16* Vb = Vlds + vb * VT + v_rd;
+    const __bf16* Kb = Klds + kb_ * KT + k_rd;
+    constexpr int NV = 2 * (BN / 32);  // P V stages: (key block, 16-key half)
+    if constexpr (kPV) {
+      bf16x8 va[2][DB];
+      read_v(Vb, 0, va[0]);
+#pragma unroll
+      for (int st = 0; st < NV; ++st) {
+        __builtin_amdgcn_sched_barrier(0);
+        if (st + 1 < NV) read_v(Vb, st + 1, va[(st + 1) & 1]);
+        const int kb = st >> 1, cc = st & 1;
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[st & 1][db], pb[kb][cc], o[db], 0, 0, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if constexpr (kS) {
+      bf16x8 ka[2][BN / 32];
+      read_k(Kb, 0, ka[0]);
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        __builtin_amdgcn_sched_barrier(0);
+        if (ks + 1 < KS) read_k(Kb, ks + 1, ka[(ks + 1) & 1]);
+#pragma unroll
+        for (int kb = 0; kb < BN / 32; ++kb)
+          s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[ks & 1][kb], qf[ks], ks == 0 ? f32x16{} : s[kb], 0, 0, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
 
-  // One 64-key tile from LDS buffer `buf`: S^T = K Q^T, online softmax, O^T += V^T P^T.
-  auto compute = [&](auto bufc, int nvalid) {
-    constexpr int buf = decltype(bufc)::value;
-    const __bf16* Kb = lds + buf * KT;
-    const __bf16* Vb = lds + 2 * KT + buf * VT;
-    f32x16 s[BN / 32];
-#pragma unroll
-    for (int kb = 0; kb < BN / 32; ++kb) {
-      const bf16x8 ka0 = *reinterpret_cast<const bf16x8*>(Kb + k_rd + kb * 32 * KSTR);
-      s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka0, qf[0], f32x16{}, 0, 0, 0);
-#pragma unroll
-      for (int ks = 1; ks < KS; ++ks) {
-        const bf16x8 ka = *reinterpret_cast<const bf16x8*>(Kb + k_rd + kb * 32 * KSTR + ks * 16);
-        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[ks], s[kb], 0, 0, 0);
-      }
-    }
+  // Softmax step on S (keys >= nvalid of this tile masked): lazy rescale of
+  // O and l, P = exp2(S c - m) packed to bf16 as the B operand of the next P V.
+  auto sstep = [&](int nvalid) {
     if (nvalid < BN) {
 #pragma unroll
       for (int kb = 0; kb < BN / 32; ++kb)
@@ -180,8 +331,7 @@ void fwd_bf16_kernel(FwdArgs a) {
     for (int kb = 1; kb < BN / 32; ++kb)
 #pragma unroll
       for (int e = 0; e < 16; e += 2) mx = fmaxf(fmaxf(mx, s[kb][e]), s[kb][e + 1]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float mt = mx * c;
+    const float mt = halfwave_max(mx) * c;
     if (__any(mt > m_run + kRescaleLog2)) {
       const float m_new = fmaxf(m_run, mt);
       const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
@@ -191,7 +341,6 @@ void fwd_bf16_kernel(FwdArgs a) {
       for (int db = 0; db < DB; ++db) o[db] *= alpha;
     }
     const float mneg = -m_run;
-    bf16x8 pb[BN / 32][2];
 #pragma unroll
     for (int kb = 0; kb < BN / 32; ++kb)
 #pragma unroll
@@ -203,71 +352,222 @@ void fwd_bf16_kernel(FwdArgs a) {
         pb[kb][e >> 3][e & 7] = pair[0];
         pb[kb][e >> 3][(e & 7) + 1] = pair[1];
       }
-#pragma unroll
-    for (int kb = 0; kb < BN / 32; ++kb)
-#pragma unroll
-      for (int cc = 0; cc < 2; ++cc) {
-        const __bf16* vrow = Vb + v_rd + (kb * 32 + cc * 16) * VSTR;
-#pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vrow + db * 32));
-          const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vrow + 8 * VSTR + db * 32));
-          const bf16x8 va = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[kb][cc], o[db], 0, 0, 0);
-        }
-      }
   };
 
-  // Walk the runs tile by tile; the loop body is unrolled over the two LDS
-  // buffers so that every LDS address is a per-thread constant plus an
-  // immediate.
-  int r = 0, t0 = 0;
-  while (r < G.n_runs && G.runs[r].n_tok == 0) ++r;
-  auto advance = [&](int& rr, int& tt) {
-    tt += BN;
-    if (tt >= G.runs[rr].n_tok) {
-      tt = 0;
-      ++rr;
-      while (rr < G.n_runs && G.runs[rr].n_tok == 0) ++rr;
-    }
-  };
-  if (r < G.n_runs) {
-    issue(r, 0);
-    commit(std::integral_constant<int, 0>{});
-  }
+  // Prologue: K_0 and V_0 loaded, K_0 stored.
+  TilePos kpos = first, vpos = first, spos = first;
+  load(G.runs[kpos.r].k, kpos, pk);
+  load(G.runs[vpos.r].v, vpos, pv);
+  store_k(0);
+  advance(kpos);
   __syncthreads();
-  auto step = [&](auto bufc) -> bool {
-    constexpr int buf = decltype(bufc)::value;
-    const int nvalid = min(BN, G.runs[r].n_tok - t0);
-    int rn = r, tn = t0;
-    advance(rn, tn);
-    const bool has_next = rn < G.n_runs;
-    if (has_next) issue(rn, tn);
-    compute(bufc, nvalid);
-    if (has_next) commit(std::integral_constant<int, buf ^ 1>{});
-    __syncthreads();
-    r = rn;
-    t0 = tn;
-    return has_next;
-  };
-  if (r < G.n_runs) {
-    while (step(std::integral_constant<int, 0>{}) && step(std::integral_constant<int, 1>{})) {
+
+  // Global loads and LDS stores of phase 2j (even) and 2j + 1 (odd), done by
+  // every wave: K_{j+1} is loaded in phase 2j and stored at the end of phase
+  // 2j + 1; V_{j+1} is loaded in phase 2j + 1 and stored at the end of 2j + 2.
+  auto even_begin = [&](int j) {
+    if (j + 1 < nt) {
+      load(G.runs[kpos.r].k, kpos, pk);
+      advance(kpos);
     }
+  };
+  auto even_end = [&](int j) {
+    if (j < nt) store_v(j & 1);
+    __syncthreads();
+  };
+  auto odd_begin = [&](int j) {
+    if (j + 1 < nt) {
+      advance(vpos);
+      load(G.runs[vpos.r].v, vpos, pv);
+    }
+  };
+  auto odd_end = [&](int j) {
+    if (j + 1 < nt) store_k((j + 1) & 1);
+    __syncthreads();
+  };
+  auto soft = [&]() {
+    sstep(min(BN, G.runs[spos.r].n_tok - spos.t0));
+    advance(spos);
+  };
+  using T_ = std::true_type;
+  using F_ = std::false_type;
+  // Matrix-core step with high issue priority, softmax with normal priority.
+  auto mphase = [&](auto pv_c, auto s_c, int j) {
+    __builtin_amdgcn_s_setprio(2);
+    mstep(pv_c, s_c, (j - 1) & 1, j & 1);
+    __builtin_amdgcn_s_setprio(0);
+  };
+  if (grp == 0) {
+    // phase 2j: M(j); phase 2j + 1: softmax(j)
+    even_begin(0);
+    mphase(F_{}, T_{}, 0);
+    even_end(0);
+    odd_begin(0);
+    soft();
+    odd_end(0);
+    for (int j = 1; j < nt; ++j) {
+      even_begin(j);
+      mphase(T_{}, T_{}, j);
+      even_end(j);
+      odd_begin(j);
+      soft();
+      odd_end(j);
+    }
+    even_begin(nt);
+    mphase(T_{}, F_{}, nt);
+    even_end(nt);
+    odd_begin(nt);
+    odd_end(nt);
+  } else {
+    // phase 2j: softmax(j - 1); phase 2j + 1: M(j)
+    even_begin(0);
+    even_end(0);
+    odd_begin(0);
+    mphase(F_{}, T_{}, 0);
+    odd_end(0);
+    for (int j = 1; j < nt; ++j) {
+      even_begin(j);
+      soft();
+      even_end(j);
+      odd_begin(j);
+      mphase(T_{}, T_{}, j);
+      odd_end(j);
+    }
+    even_begin(nt);
+    soft();
+    even_end(nt);
+    odd_begin(nt);
+    mphase(T_{}, F_{}, nt);
+    odd_end(nt);
   }
 
-  const float l_tot = l_part + __shfl_xor(l_part, 32);
-  const float inv = 1.0f / l_tot;
-  if (q_ok) {
-    __bf16* op = static_cast<__bf16*>(a.out) + static_cast<int64_t>(q_row) * ld + hoff + 4 * hh;
+  const float l_tot = halfwave_sum(l_part);
+  if (whole) {
+    if (q_ok) {
+      const float inv = 1.0f / l_tot;
+      __bf16* op = static_cast<__bf16*>(a.out) + static_cast<int64_t>(q_row) * ld + hoff + 4 * hh;
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          bf16x4 v;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) v[i] = static_cast<__bf16>(o[db][4 * jj + i] * inv);
+          *reinterpret_cast<bf16x4*>(op + db * 32 + 8 * jj) = v;
+        }
+    }
+  } else {
+    float* ro = a.partial + static_cast<int64_t>(rec) * partial_record_floats(D);
+    const int ql = wave * 32 + n;
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        bf16x4 v;
+      for (int jj = 0; jj < 4; ++jj) {
+        f32x4 v;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) v[i] = static_cast<__bf16>(o[db][4 * j + i] * inv);
-        *reinterpret_cast<bf16x4*>(op + db * 32 + 8 * j) = v;
+        for (int i = 0; i < 4; ++i) v[i] = o[db][4 * jj + i];
+        *reinterpret_cast<f32x4*>(ro + ql * D + db * 32 + 8 * jj + 4 * hh) = v;
       }
+    if (hh == 0) {
+      ro[BM * D + ql] = m_run;
+      ro[BM * D + BM + ql] = l_tot;
+    }
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void fwd_bf16_kernel(FwdArgs a) {
+  using P = FwdTile<D>;
+  // [K buf0 | K buf1 | V buf0 | V buf1]; every offset fits a ds instruction's immediate.
+  __shared__ __attribute__((aligned(16))) __bf16 lds[2 * P::KT + 2 * P::VT];
+  const int rho = range_of_block(blockIdx.x, a.n_ranges);
+  for (int r = 0; r < a.dp_rounds; ++r) {
+    const int64_t i = static_cast<int64_t>(r) * a.n_ranges + rho;
+    int g = 0;
+    while (g + 1 < a.n_groups && i >= a.groups[g + 1].block_begin) ++g;
+    const FwdGroupArgs& G = a.groups[g];
+    attend_piece<D>(a, G, static_cast<int>(i - G.block_begin), 0, G.tiles_per_item, true, 0, lds);
+  }
+  const int64_t S = range_begin(a, rho), E = range_begin(a, rho + 1);
+  for (int64_t t = S; t < E;) {
+    const Loc L = locate(a, t);
+    const FwdGroupArgs& G = a.groups[L.g];
+    const int64_t piece_end = min(E, L.item_begin + G.tiles_per_item);
+    const int nt = static_cast<int>(piece_end - t);
+    const bool whole = L.k == 0 && nt == G.tiles_per_item;
+    attend_piece<D>(a, G, L.item, L.k, nt, whole, t == S ? 2 * rho : 2 * rho + 1, lds);
+    t = piece_end;
+  }
+}
+
+// Merge the pieces of items split across ranges: block b looks at the
+// boundary between ranges b and b + 1 and, if it is the first boundary inside
+// an item, combines all of that item's pieces in range order.
+template <int D>
+__global__ __launch_bounds__(kFwdThreads) void combine_kernel(FwdArgs a) {
+  constexpr int BM = kFwdBM;
+  const int b = blockIdx.x + 1;
+  const int64_t Sb = range_begin(a, b);
+  if (Sb >= a.total_tiles) return;
+  const Loc L = locate(a, Sb);
+  if (L.k == 0) return;
+  const int64_t T = L.item_begin;
+  if (range_begin(a, b - 1) > T) return;
+  const FwdGroupArgs& G = a.groups[L.g];
+  const int64_t Tend = T + G.tiles_per_item;
+  int j_end = b;
+  while (j_end + 1 < a.n_ranges && range_begin(a, j_end + 1) < Tend) ++j_end;
+  const int head = L.item / G.n_qtiles;
+  const int qtile = L.item - head * G.n_qtiles;
+  const int64_t rec_len = partial_record_floats(D);
+  // Each thread owns NE float4 outputs; pieces are merged in range order
+  // with a running max, like the online softmax itself.
+  constexpr int NE = BM * D / 4 / kFwdThreads;
+  f32x4 acc[NE];
+  float m[NE], l[NE];
+#pragma unroll
+  for (int it = 0; it < NE; ++it) {
+    acc[it] = f32x4{};
+    m[it] = -INFINITY;
+    l[it] = 0.f;
+  }
+  for (int j = b - 1; j <= j_end; ++j) {
+    const int64_t rj = range_begin(a, j);
+    if (rj == range_begin(a, j + 1)) continue;  // empty range: no piece
+    const float* ro = a.partial + (T <= rj ? 2 * j : 2 * j + 1) * rec_len;
+    // issue every load of this piece before using any of them
+    f32x4 ov[NE];
+    float mv[NE], lv[NE];
+#pragma unroll
+    for (int it = 0; it < NE; ++it) {
+      const int e = threadIdx.x + it * kFwdThreads;
+      const int ql = e / (D / 4), d4 = e % (D / 4);
+      ov[it] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(ro + ql * D + 4 * d4));
+      mv[it] = ro[BM * D + ql];
+      lv[it] = ro[BM * D + BM + ql];
+    }
+#pragma unroll
+    for (int it = 0; it < NE; ++it) {
+      const float mn = fmaxf(m[it], mv[it]);
+      const float so = __builtin_amdgcn_exp2f(m[it] - mn), sj = __builtin_amdgcn_exp2f(mv[it] - mn);
+      acc[it] = acc[it] * so + sj * ov[it];
+      l[it] = l[it] * so + sj * lv[it];
+      m[it] = mn;
+    }
+  }
+#pragma unroll
+  for (int it = 0; it < NE; ++it) {
+    const int e = threadIdx.x + it * kFwdThreads;
+    const int ql = e / (D / 4), d4 = e % (D / 4);
+    const int q_row = G.q_begin + qtile * BM + ql;
+    if (q_row >= G.q_end) continue;
+    const float inv = 1.0f / l[it];
+    bf16x4 v;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = static_cast<__bf16>(acc[it][i] * inv);
+    *reinterpret_cast<bf16x4*>(static_cast<__bf16*>(a.out) + static_cast<int64_t>(q_row) * a.ld +
+                               static_cast<int64_t>(head) * D + 4 * d4) = v;
   }
 }
 
@@ -318,19 +618,38 @@ __global__ __launch_bounds__(kFwdF32BM) void fwd_f32_kernel(FwdArgs a) {
 }  // namespace
 
 hipError_t launch_forward(const FwdArgs& a, int head_dim, bool bf16, hipStream_t stream) {
-  if (a.n_blocks <= 0) return hipSuccess;
   if (bf16) {
+    if (a.n_ranges <= 0) return hipSuccess;
     if (head_dim == 128)
-      hipLaunchKernelGGL(fwd_bf16_kernel<128>, dim3(a.n_blocks), dim3(kFwdThreads), 0, stream, a);
+      hipLaunchKernelGGL(fwd_bf16_kernel<128>, dim3(a.n_ranges), dim3(kFwdThreads), 0, stream, a);
     else
-      hipLaunchKernelGGL(fwd_bf16_kernel<64>, dim3(a.n_blocks), dim3(kFwdThreads), 0, stream, a);
-  } else {
+      hipLaunchKernelGGL(fwd_bf16_kernel<64>, dim3(a.n_ranges), dim3(kFwdThreads), 0, stream, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || a.n_ranges < 2) return e;
     if (head_dim == 128)
-      hipLaunchKernelGGL(fwd_f32_kernel<128>, dim3(a.n_blocks), dim3(kFwdF32BM), 0, stream, a);
+      hipLaunchKernelGGL(combine_kernel<128>, dim3(a.n_ranges - 1), dim3(kFwdThreads), 0, stream, a);
     else
-      hipLaunchKernelGGL(fwd_f32_kernel<64>, dim3(a.n_blocks), dim3(kFwdF32BM), 0, stream, a);
+      hipLaunchKernelGGL(combine_kernel<64>, dim3(a.n_ranges - 1), dim3(kFwdThreads), 0, stream, a);
+    return hipGetLastError();
   }
+  if (a.n_blocks <= 0) return hipSuccess;
+  if (head_dim == 128)
+    hipLaunchKernelGGL(fwd_f32_kernel<128>, dim3(a.n_blocks), dim3(kFwdF32BM), 0, stream, a);
+  else
+    hipLaunchKernelGGL(fwd_f32_kernel<64>, dim3(a.n_blocks), dim3(kFwdF32BM), 0, stream, a);
   return hipGetLastError();
+}
+
+int forward_blocks_per_cu(int head_dim) {
+  int n = 0;
+  const hipError_t e = head_dim == 128
+      ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fwd_bf16_kernel<128>, kFwdThreads, 0)
+      : hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fwd_bf16_kernel<64>, kFwdThreads, 0);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return 0;
+  }
+  return n;
 }
 
 }  // namespace mssa

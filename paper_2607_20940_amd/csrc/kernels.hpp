@@ -10,7 +10,11 @@ namespace mssa {
 // Average-pool jobs; grid = (n_blocks, 2): y = 0 pools K, y = 1 pools V.
 hipError_t launch_pool(const PoolArgs& a, int n_blocks, bool bf16, hipStream_t stream);
 
-// Attention forward over the groups of `a` (a.n_blocks logical blocks).
+// Attention forward over the groups of `a`.  bf16: a.n_ranges persistent
+// blocks followed by the combine of split items; fp32: a.n_blocks blocks.
 hipError_t launch_forward(const FwdArgs& a, int head_dim, bool bf16, hipStream_t stream);
+
+// Resident blocks per CU of the bf16 attention kernel (0 if unknown).
+int forward_blocks_per_cu(int head_dim);
 
 }  // namespace mssa

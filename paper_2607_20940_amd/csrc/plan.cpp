@@ -8,6 +8,8 @@
 // in the order sink, history (oldest first), window (state 1..T).
 #include "plan.hpp"
 
+#include "kernel_args.hpp"
+
 #include <algorithm>
 #include <cmath>
 #include <limits>
@@ -21,7 +23,7 @@ int32_t ceil_div(int32_t a, int32_t b) { return (a + b - 1) / b; }
 
 }  // namespace
 
-mssa_status build_plan(const mssa_plan_desc& d, Plan& p, std::string& err) {
+mssa_status build_plan(const mssa_plan_desc& d, int slots, int ranges_override, Plan& p, std::string& err) {
   const int32_t T = d.num_states;
   if (T < 1 || T > MSSA_MAX_STATES) {
     err = "num_states must be in [1, " + std::to_string(MSSA_MAX_STATES) + "]";
@@ -199,6 +201,51 @@ mssa_status build_plan(const mssa_plan_desc& d, Plan& p, std::string& err) {
       ws += bytes;
     }
     for (SegRow& r : rows) p.segs.push_back(r);
+  }
+  // Persistent attention schedule: items (group, head, query tile) in launch
+  // order, each a sequence of 64-key tiles over the group's runs.
+  for (int g = 0; g < G; ++g) p.order.push_back(g);
+  std::stable_sort(p.order.begin(), p.order.end(),
+                   [&](int x, int y) { return p.groups[x].n_kv > p.groups[y].n_kv; });
+  p.tiles_per_item.assign(G, 0);
+  p.tile_begin.assign(G, 0);
+  p.total_tiles = 0;
+  int64_t n_items = 0, t_max = 0;
+  std::vector<int64_t> item_first(G, 0);
+  for (int g : p.order) {
+    int64_t tiles = 0;
+    for (const Run& r : p.runs[g]) tiles += (r.n_tok + kFwdBN - 1) / kFwdBN;
+    p.tiles_per_item[g] = static_cast<int32_t>(tiles);
+    p.tile_begin[g] = p.total_tiles;
+    item_first[g] = n_items;
+    const int64_t items =
+        static_cast<int64_t>((p.groups[g].q_end - p.groups[g].q_begin + kFwdBM - 1) / kFwdBM) * d.num_heads;
+    n_items += items;
+    p.total_tiles += items * tiles;
+    t_max = std::max(t_max, tiles);
+  }
+  if (slots <= 0) slots = 512;
+  int64_t ranges = ranges_override > 0 ? ranges_override : std::min<int64_t>(slots, n_items);
+  ranges = std::max<int64_t>(1, std::min<int64_t>(ranges, p.total_tiles));
+  p.n_ranges = static_cast<int32_t>(ranges);
+  // Whole-item rounds: as many as fit without any block exceeding its even
+  // share total_tiles / ranges; the rest is split into per-block tail ranges
+  // sized to make every block's total equal.
+  p.dp_rounds = static_cast<int32_t>(
+      std::min<int64_t>(n_items / ranges, (p.total_tiles / ranges) / std::max<int64_t>(1, t_max)));
+  {
+    const int64_t i = static_cast<int64_t>(p.dp_rounds) * ranges;  // first tail item
+    int gl = p.order.front();
+    for (int g : p.order)
+      if (i >= item_first[g]) gl = g;
+    p.tail_begin = p.tile_begin[gl] + (i - item_first[gl]) * p.tiles_per_item[gl];
+  }
+  p.partial_off = 0;
+  p.partial_bytes = 0;
+  if (d.dtype == MSSA_BF16 && p.n_ranges > 1) {
+    p.partial_off = ws;
+    p.partial_bytes = align256(2 * static_cast<int64_t>(p.n_ranges) * partial_record_floats(d.head_dim) * 4);
+    ws += p.partial_bytes;
   }
   p.workspace_bytes = ws;
 

@@ -72,11 +72,24 @@ struct Plan {
   int64_t workspace_bytes;
   int64_t pairs_per_head;
   int64_t pool_bytes_alg;
+  // Persistent attention schedule (bf16): groups in launch order (longest
+  // context first), 64-key tiles per item, first tile of each group in the
+  // linear tile space, and the number of equal tile ranges (one per block).
+  std::vector<int> order;
+  std::vector<int32_t> tiles_per_item;   // per group
+  std::vector<int64_t> tile_begin;       // per group
+  int64_t total_tiles;
+  int32_t n_ranges;
+  int32_t dp_rounds;    // rounds of whole items (one per block) before the tail
+  int64_t tail_begin;   // first tile of the tail ranges
+  int64_t partial_off, partial_bytes;    // partial records in the workspace
 };
 
-// Validates `d` and fills `p`.  Returns MSSA_OK or an error status with a
-// message in `err`.
-mssa_status build_plan(const mssa_plan_desc& d, Plan& p, std::string& err);
+// Validates `d` and fills `p`.  `slots` is the number of attention blocks
+// the device keeps resident at once (<= 0: 512, two per CU of an MI355X);
+// `ranges_override` > 0 forces the number of tile ranges instead.  Returns
+// MSSA_OK or an error status with a message in `err`.
+mssa_status build_plan(const mssa_plan_desc& d, int slots, int ranges_override, Plan& p, std::string& err);
 
 // Flat int64 export of GRID / QGRP / SEG / TOTAL (layout in libmssa.h).
 std::vector<int64_t> export_tables(const Plan& p);

@@ -80,6 +80,16 @@ def test_bf16_large_logits(mult):
     _full_check(desc, "bf16", seed + 200, 1.0, f"large_logits_x{mult:g}")
 
 
+@pytest.mark.parametrize("ranges", [1, 2, 3, 7, 97, 1000])
+@pytest.mark.parametrize("name", ["ragged_3level_d128", "ragged_3level_d64", "tiny_runs"])
+def test_bf16_forced_tile_ranges(monkeypatch, name, ranges):
+    """Items split across 1..many persistent tile ranges (partial records
+    merged by the combine kernel) give the same result."""
+    monkeypatch.setenv("MSSA_FWD_RANGES", str(ranges))
+    desc, seed = SMALL[name]
+    _full_check(desc, "bf16", seed + 300, 1.0, f"{name}_ranges{ranges}")
+
+
 def test_zero_output_fails_guard():
     """The comparison rejects an all-zero output."""
     desc, seed = SMALL["paper_schedule_small"]
