@@ -160,6 +160,28 @@ mssa_status mssa_forward(mssa_plan plan, const void* q_win, const void* k_sink,
                          const void* k_win, const void* v_win, const void* workspace,
                          int64_t workspace_bytes, void* out, void* stream);
 
+/* Streaming cache roll (Sec. 3.1, Eq. 2; Alg. 1 KV-cache update): after a
+ * rolling pass the head state (window state 1, which must be at native
+ * scale: scales[0] == 1) is emitted, and its F native frames of K and V
+ * become the newest history frames.  They are copied from the first
+ * F * grid_h * grid_w tokens of k_win / v_win into a caller-owned ring of
+ * ring_cap_frames native frames ([ring_cap_frames * grid_h * grid_w, H, D],
+ * plan dtype).  The ring holds *ring_count valid frames: while it is not
+ * full they are slots [0, count) and the frames are appended at slot count;
+ * once full, the oldest frames (starting at slot *ring_head) are overwritten
+ * and *ring_head advances.  The valid frames are therefore always slots
+ * [0, count), which a plan with hist_frames == count reads as its history
+ * (attention is invariant to the order of its context frames).
+ *   k_win, v_win     [n_q, H, D] device, this pass's window K/V
+ *   k_ring, v_ring   device ring buffers (must not overlap k_win / v_win)
+ *   ring_head, ring_count  host in/out; 0 <= count <= cap, 0 <= head < cap,
+ *                    head == 0 unless count == cap
+ * Enqueues device-to-device copies on `stream`; MSSA_ERR_UNSUPPORTED if
+ * scales[0] != 1 or ring_cap_frames < frames_per_state. */
+mssa_status mssa_hist_append(mssa_plan plan, const void* k_win, const void* v_win, void* k_ring,
+                             void* v_ring, int32_t ring_cap_frames, int32_t* ring_head,
+                             int32_t* ring_count, void* stream);
+
 /* Name of a status code (static string). */
 const char* mssa_status_string(mssa_status s);
 

@@ -241,6 +241,53 @@ mssa_status mssa_forward(mssa_plan plan, const void* q_win, const void* k_sink, 
                       "attention kernel launch");
 }
 
+mssa_status mssa_hist_append(mssa_plan plan, const void* k_win, const void* v_win, void* k_ring, void* v_ring,
+                             int32_t ring_cap_frames, int32_t* ring_head, int32_t* ring_count, void* stream) {
+  if (!plan || !k_win || !v_win || !k_ring || !v_ring || !ring_head || !ring_count)
+    return fail(MSSA_ERR_INVALID_ARG, "null argument");
+  const mssa::Plan& p = plan->p;
+  const int32_t F = p.desc.frames_per_state;
+  if (p.desc.scales[0] != 1)
+    return fail(MSSA_ERR_UNSUPPORTED, "the emitted head state must be at native scale (scales[0] == 1)");
+  if (ring_cap_frames < F) return fail(MSSA_ERR_UNSUPPORTED, "ring_cap_frames < frames_per_state");
+  const int32_t head = *ring_head, count = *ring_count;
+  if (count < 0 || count > ring_cap_frames || head < 0 || head >= ring_cap_frames ||
+      (head != 0 && count != ring_cap_frames))
+    return fail(MSSA_ERR_INVALID_ARG, "inconsistent ring_head / ring_count");
+  const size_t frame_bytes = static_cast<size_t>(p.tok1 * p.ld * p.elem_bytes);
+  const char* kw = static_cast<const char*>(k_win);
+  const char* vw = static_cast<const char*>(v_win);
+  char* kr = static_cast<char*>(k_ring);
+  char* vr = static_cast<char*>(v_ring);
+  const size_t ring_bytes = frame_bytes * ring_cap_frames;
+  const size_t win_bytes = frame_bytes * F;
+  auto overlap = [](const char* a, size_t na, const char* b, size_t nb) { return a < b + nb && b < a + na; };
+  if (overlap(kr, ring_bytes, kw, win_bytes) || overlap(kr, ring_bytes, vw, win_bytes) ||
+      overlap(vr, ring_bytes, kw, win_bytes) || overlap(vr, ring_bytes, vw, win_bytes) ||
+      overlap(kr, ring_bytes, vr, ring_bytes))
+    return fail(MSSA_ERR_INVALID_ARG, "ring buffers overlap each other or the window");
+  int32_t h = head, c = count;
+  for (int32_t f = 0; f < F; ++f) {
+    int32_t slot;
+    if (c < ring_cap_frames) {
+      slot = c++;
+    } else {
+      slot = h;
+      h = (h + 1) % ring_cap_frames;
+    }
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    mssa_status s = check_device(hipMemcpyAsync(kr + slot * frame_bytes, kw + f * frame_bytes, frame_bytes,
+                                                hipMemcpyDeviceToDevice, st), "history append (K)");
+    if (s != MSSA_OK) return s;
+    s = check_device(hipMemcpyAsync(vr + slot * frame_bytes, vw + f * frame_bytes, frame_bytes,
+                                    hipMemcpyDeviceToDevice, st), "history append (V)");
+    if (s != MSSA_OK) return s;
+  }
+  *ring_head = h;
+  *ring_count = c;
+  return MSSA_OK;
+}
+
 const char* mssa_status_string(mssa_status s) {
   switch (s) {
     case MSSA_OK: return "MSSA_OK";

@@ -54,3 +54,24 @@ def make_inputs(shapes, seed, amplitude=1.0, dtype="bf16"):
         x = (rng.standard_normal(shape) * amplitude).astype(np.float32)
         out[name] = f32_to_bf16_bits(x) if dtype == "bf16" else x
     return out
+
+
+def make_inputs_device(shapes, seed, amplitude=1.0, dtype="bf16", names=DRAW_ORDER, device="cuda"):
+    """Device-side variant for workloads too large to draw on the host:
+    torch's generator on `device` seeded with `seed` draws N(0,1) float32
+    tensors in the order of `names`, scaled by the amplitude and rounded to
+    bf16 (round-to-nearest-even) or kept float32.  The values are defined by
+    this function (the oracle reads them back from the device)."""
+    import torch
+
+    gen = torch.Generator(device=device)
+    gen.manual_seed(int(seed))
+    out = {}
+    for name in names:
+        shape = tuple(shapes.get(name, (0,)))
+        if int(np.prod(shape)) == 0:
+            out[name] = None
+            continue
+        x = torch.randn(shape, generator=gen, device=device, dtype=torch.float32) * amplitude
+        out[name] = x.to(torch.bfloat16) if dtype == "bf16" else x
+    return out

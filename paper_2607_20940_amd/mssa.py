@@ -21,7 +21,8 @@ MSSA_BF16, MSSA_F32 = 0, 1
 
 # Every symbol include/libmssa.h declares.
 EXPORTS = ("mssa_plan_create", "mssa_plan_destroy", "mssa_plan_query", "mssa_plan_tables",
-           "mssa_pool_kv", "mssa_forward", "mssa_status_string", "mssa_last_error")
+           "mssa_pool_kv", "mssa_forward", "mssa_hist_append", "mssa_status_string",
+           "mssa_last_error")
 
 
 class mssa_plan_desc(ctypes.Structure):
@@ -64,12 +65,14 @@ def _load():
     lib.mssa_plan_tables.argtypes = [P, ctypes.POINTER(I64), I64, ctypes.POINTER(I64)]
     lib.mssa_pool_kv.argtypes = [P, V, V, V, V, V, I64, V]
     lib.mssa_forward.argtypes = [P, V, V, V, V, V, V, V, V, I64, V, V]
+    lib.mssa_hist_append.argtypes = [P, V, V, V, V, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32),
+                                     ctypes.POINTER(ctypes.c_int32), V]
     lib.mssa_status_string.argtypes = [ctypes.c_int]
     lib.mssa_status_string.restype = ctypes.c_char_p
     lib.mssa_last_error.argtypes = []
     lib.mssa_last_error.restype = ctypes.c_char_p
     for name in ("mssa_plan_create", "mssa_plan_query", "mssa_plan_tables", "mssa_pool_kv",
-                 "mssa_forward"):
+                 "mssa_forward", "mssa_hist_append"):
         getattr(lib, name).restype = ctypes.c_int
     runtimes = _loaded_hip_runtimes()
     if len(runtimes) > 1:
@@ -219,3 +222,21 @@ def mssa_forward(plan, q_win, k_sink, v_sink, k_hist, v_hist, k_win, v_win, work
     _check(lib.mssa_forward(plan.handle, _ptr(q_win), _ptr(k_sink), _ptr(v_sink), _ptr(k_hist),
                             _ptr(v_hist), _ptr(k_win), _ptr(v_win), _ptr(workspace), wb,
                             _ptr(out), _stream(stream)), "mssa_forward")
+
+
+class Ring:
+    """Host-side head/count of a history ring used with mssa_hist_append."""
+
+    def __init__(self, cap_frames, count=0, head=0):
+        self.cap = int(cap_frames)
+        self.count = int(count)
+        self.head = int(head)
+
+
+def mssa_hist_append(plan, k_win, v_win, k_ring, v_ring, ring, stream=None):
+    head = ctypes.c_int32(ring.head)
+    count = ctypes.c_int32(ring.count)
+    _check(lib.mssa_hist_append(plan.handle, _ptr(k_win), _ptr(v_win), _ptr(k_ring), _ptr(v_ring),
+                                ring.cap, ctypes.byref(head), ctypes.byref(count), _stream(stream)),
+           "mssa_hist_append")
+    ring.head, ring.count = head.value, count.value

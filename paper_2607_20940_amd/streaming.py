@@ -1,0 +1,100 @@
+"""Rolling-window streaming of stacked MSSA layers (Ms. Forcing, Sec. 3.1
+Eq. 2 and Alg. 1's per-pass KV-cache update) driven through the C ABI.
+
+Each layer keeps its sink K/V and a history ring of native frames.  A layer
+pass is: mssa_pool_kv (history and fine window frames resampled), then
+mssa_forward, then mssa_hist_append (the head state's native frames become
+the newest history frames, FIFO-capped).  The ring's valid frames are always
+slots [0, count), read as a plan whose hist_frames equals count; one plan per
+history length is kept.  This module only sequences library calls and owns
+device buffers (torch allocations); all arithmetic runs in the library.
+"""
+
+from . import mssa
+from .workloads import input_shapes
+
+
+class StreamingMSSA:
+    def __init__(self, layer_desc, layers, hist_cap_frames, dtype="bf16", device="cuda"):
+        import torch
+
+        self.desc = dict(layer_desc)
+        self.layers = int(layers)
+        self.cap = int(hist_cap_frames)
+        self.dtype = dtype
+        self.device = device
+        self.tdtype = torch.bfloat16 if dtype == "bf16" else torch.float32
+        self._plans = {}
+        base = self.plan(0)
+        info = base.info()
+        self.n_q = info["n_q"]
+        self.tok1 = int(layer_desc["grid_h"]) * int(layer_desc["grid_w"])
+        nh, d = int(layer_desc["num_heads"]), int(layer_desc["head_dim"])
+        ws = max(self.plan(h).info()["workspace_bytes"] for h in range(self.cap + 1))
+        self.workspace = torch.empty(max(256, ws), dtype=torch.uint8, device=device)
+        shape = (self.cap * self.tok1, nh, d)
+        self.k_ring = [torch.zeros(shape, dtype=self.tdtype, device=device) for _ in range(self.layers)]
+        self.v_ring = [torch.zeros(shape, dtype=self.tdtype, device=device) for _ in range(self.layers)]
+        self.ring = [mssa.Ring(self.cap) for _ in range(self.layers)]
+        self.k_sink = [None] * self.layers
+        self.v_sink = [None] * self.layers
+
+    def plan(self, hist_frames):
+        if hist_frames not in self._plans:
+            self._plans[hist_frames] = mssa.mssa_plan_create(
+                dict(self.desc, hist_frames=hist_frames, dtype=self.dtype))
+        return self._plans[hist_frames]
+
+    def shapes(self, hist_frames):
+        info = self.plan(hist_frames).info()
+        return input_shapes(self.desc, info["n_q"], info["n_sink_tok"], info["n_hist_tok"])
+
+    def init_layer(self, layer, k_sink, v_sink, k_hist, v_hist):
+        """Sink K/V and the initial history (oldest first) of one layer."""
+        self.k_sink[layer], self.v_sink[layer] = k_sink, v_sink
+        n = 0 if k_hist is None else k_hist.shape[0] // self.tok1
+        if n > self.cap:
+            raise ValueError("initial history longer than the ring")
+        if n:
+            self.k_ring[layer][: n * self.tok1].copy_(k_hist)
+            self.v_ring[layer][: n * self.tok1].copy_(v_hist)
+        self.ring[layer] = mssa.Ring(self.cap, count=n, head=0)
+
+    def layer_pass(self, layer, q_win, k_win, v_win, out, stream=None):
+        ring = self.ring[layer]
+        plan = self.plan(ring.count)
+        nh = ring.count * self.tok1
+        kh = self.k_ring[layer][:nh] if nh else None
+        vh = self.v_ring[layer][:nh] if nh else None
+        mssa.mssa_pool_kv(plan, kh, vh, k_win, v_win, self.workspace, stream=stream)
+        mssa.mssa_forward(plan, q_win, self.k_sink[layer], self.v_sink[layer], kh, vh, k_win, v_win,
+                          self.workspace, out, stream=stream)
+        mssa.mssa_hist_append(plan, k_win, v_win, self.k_ring[layer], self.v_ring[layer], ring,
+                              stream=stream)
+
+
+def init_inputs(stream_w, layer, shapes, device="cuda"):
+    """Sink and initial history of one layer (seeded init_seed_base + layer)."""
+    from .inputs import make_inputs_device
+
+    return make_inputs_device(shapes, stream_w["init_seed_base"] + layer, stream_w["amplitude"],
+                              stream_w["dtype"], names=("k_sink", "v_sink", "k_hist", "v_hist"),
+                              device=device)
+
+
+def window_inputs(stream_w, pass_index, layers, shapes, device="cuda"):
+    """Window Q/K/V of every layer for one pass: one generator seeded
+    seed_base + pass_index draws q, k, v of layer 0, then layer 1, ..."""
+    import torch
+
+    gen = torch.Generator(device=device)
+    gen.manual_seed(int(stream_w["seed_base"] + pass_index))
+    tdt = torch.bfloat16 if stream_w["dtype"] == "bf16" else torch.float32
+    out = []
+    for _ in range(layers):
+        t = {}
+        for name in ("q_win", "k_win", "v_win"):
+            x = torch.randn(shapes[name], generator=gen, device=device, dtype=torch.float32)
+            t[name] = (x * stream_w["amplitude"]).to(tdt)
+        out.append(t)
+    return out
