@@ -101,6 +101,69 @@ def cpu_baseline(w, x, info, budget_s):
     }
 
 
+def bench_streaming(args):
+    """Steady-state streaming: stacked layers over rolling passes (pool +
+    forward + history append per layer and pass); window inputs of a pass
+    are generated on the device before that pass is timed."""
+    import torch
+
+    from paper_2607_20940_amd.streaming import StreamingMSSA, init_inputs, window_inputs
+    from paper_2607_20940_amd.workloads import STREAMING
+
+    w = STREAMING
+    layers = args.layers or w["layers"]
+    passes = args.passes or w["passes"]
+    desc = w["layer"]
+    F = desc["frames_per_state"]
+    st = StreamingMSSA(desc, layers, w["hist_cap_frames"], dtype=w["dtype"])
+    init_shapes = st.shapes(w["hist_start_frames"])
+    for L in range(layers):
+        x = init_inputs(w, L, init_shapes)
+        st.init_layer(L, x["k_sink"], x["v_sink"], x["k_hist"], x["v_hist"])
+    win_shapes = st.shapes(0)
+    outs = [torch.empty(win_shapes["q_win"], dtype=torch.bfloat16, device="cuda") for _ in range(layers)]
+    stream = torch.cuda.current_stream()
+    pass_ms, pass_flops = [], []
+    for p in range(passes):
+        wins = window_inputs(w, p, layers, win_shapes)
+        flops = sum(st.plan(st.ring[L].count).info()["flops_alg"] for L in range(layers))
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for L in range(layers):
+            st.layer_pass(L, wins[L]["q_win"], wins[L]["k_win"], wins[L]["v_win"], outs[L])
+        e1.record(stream)
+        torch.cuda.synchronize()
+        pass_ms.append(e0.elapsed_time(e1))
+        pass_flops.append(flops)
+        if p % 8 == 0 or p == passes - 1:
+            log(f"pass {p}: {pass_ms[-1]:.2f} ms, history {st.ring[0].count} frames")
+    steady = list(range(min(5, passes - 1), passes))
+    tot_ms = sum(pass_ms)
+    st_ms = sum(pass_ms[i] for i in steady)
+    result = {
+        "metric": "MSSA attention ms per emitted latent frame (stacked layers, rolling passes)",
+        "value": round(st_ms / (len(steady) * F), 4),
+        "unit": "ms/frame",
+        "n_gpus": 1,
+        "steps": passes,
+        "warmup": 0,
+        "ms_per_step": round(tot_ms / passes, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w["dtype"],
+        "data": "synthetic",
+        "config": {"workload": "streaming_wan13b", "layers": layers, "passes": passes,
+                   "hist_frames": f"{w['hist_start_frames']}->{w['hist_cap_frames']} FIFO",
+                   "frames_per_state": F},
+        "all_passes_ms_per_frame": round(tot_ms / (passes * F), 4),
+        "steady_state_passes": [steady[0], steady[-1]],
+        "effective_tflops_steady": round(sum(pass_flops[i] for i in steady) / (st_ms * 1e-3) / 1e12, 2),
+    }
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -111,6 +174,8 @@ def main():
                     help="distinct device copies of the inputs rotated between steps")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--layers", type=int, default=0, help="streaming: layers (default 30)")
+    ap.add_argument("--passes", type=int, default=0, help="streaming: rolling passes (default 64)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -118,6 +183,10 @@ def main():
         print(f"bench.py runs on one GPU only: MSSA here is a single-GPU kernel path with no "
               f"collectives (asked for --gpus {args.gpus}, WORLD_SIZE={world}).", file=sys.stderr)
         sys.exit(2)
+
+    if args.workload == "streaming":
+        bench_streaming(args)
+        return
 
     import torch
 
