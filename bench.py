@@ -302,7 +302,7 @@ def main():
                  "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                  "frac": None if pool_gbps is None else round(pool_gbps / PEAK_HBM_GBPS, 4),
                  "bytes_alg": info["pool_bytes_alg"]},
-        "roofline": {"kernel": "mssa_forward (fwd_bf16_kernel)" if dtype == "bf16" else "fwd_f32_kernel",
+        "roofline": {"kernel": "mssa_forward (fwd_bf16_kernel + combine_kernel)" if dtype == "bf16" else "mssa_forward (fwd_f32_kernel)",
                      "bound": "mfma", "achieved": round(fwd_tflops, 2), "peak": peak,
                      "unit": "TFLOP/s", "frac": round(fwd_tflops / peak, 4),
                      "traffic": read_traffic(args.workload)},
