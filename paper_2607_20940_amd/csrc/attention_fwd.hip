@@ -3,9 +3,10 @@
 // context runs of that scale (sink | history at the query scale | window at
 // max(query scale, own scale)).
 //
-// bf16 path (gfx950 matrix cores).  One block = 4 waves = 128 queries of one
-// (query scale, head); each wave owns 32 queries.  The block walks the
-// scale's runs in 64-key tiles staged through LDS.  Per tile and wave:
+// bf16 path (gfx950 matrix cores).  A persistent block of 8 waves attends
+// 256 queries of one (query scale, head) at a time; each wave owns 32
+// queries.  The block walks the scale's runs in 64-key tiles staged through
+// LDS.  Per tile and wave:
 //   S^T = K Q^T   with v_mfma_f32_32x32x16_bf16 (A = K rows from LDS,
 //                 B = the wave's Q fragment held in registers), so each lane
 //                 holds 16 keys of ONE query: the softmax row reductions are
@@ -16,6 +17,8 @@
 //                 laid out as the B operand (their key order defines the
 //                 contraction order), and V^T comes from row-major V in LDS
 //                 through the gfx950 transposing LDS read ds_read_b64_tr_b16.
+// The two halves of the block alternate matrix-core and softmax phases so
+// that every SIMD always has one wave feeding its matrix core.
 // Keys past the end of a run are zero-filled in LDS and masked to -inf.
 //
 // fp32 path: one lane per query, plain fp32 FMA dot products and an online
@@ -134,11 +137,6 @@ struct FwdTile {
   static_assert(NLD * RPL == BN, "tile load must divide evenly");
 };
 
-// Position of a 64-key tile inside an item's run list.
-struct TilePos {
-  int r, t0;
-};
-
 // Value of lane l ^ 32.  v_permlane32_swap exchanges the upper half of its
 // first operand with the lower half of its second; whether the compiler gives
 // the two operands one register or two, lane l < 32 finds lane l + 32 in the
@@ -221,29 +219,50 @@ __device__ __forceinline__ void attend_piece(const FwdArgs& a, const FwdGroupArg
   __bf16* const Klds = lds;
   __bf16* const Vlds = lds + 2 * KT;
 
-  auto advance = [&](TilePos& t) {
-    t.t0 += BN;
-    if (t.t0 >= G.runs[t.r].n_tok) {
-      t.t0 = 0;
-      ++t.r;
-      while (t.r < G.n_runs && G.runs[t.r].n_tok == 0) ++t.r;
+  // Tile streams over the item's context runs.  A stream points at its
+  // current tile (head offset applied) and counts the tokens of the run from
+  // there on, so stepping to the next tile is a pointer add and a subtract;
+  // only a step past the end of a run (a few times per item) reads the run
+  // table again, skipping empty runs.
+  struct Stream {
+    const __bf16* p;  // first token of the current tile
+    int left;         // tokens of the current run from p on (> 0 while live)
+    int r;            // current run
+  };
+  const int64_t tile_step = static_cast<int64_t>(BN) * ld;
+  auto run_base = [&](auto is_v, int r) {
+    return static_cast<const __bf16*>(decltype(is_v)::value ? G.runs[r].v : G.runs[r].k) + hoff;
+  };
+  auto stream_at = [&](auto is_v, int j) {  // j: tile index within the item
+    int r = 0;
+    while (j >= (G.runs[r].n_tok + BN - 1) / BN) {
+      j -= (G.runs[r].n_tok + BN - 1) / BN;
+      ++r;
+    }
+    return Stream{run_base(is_v, r) + j * tile_step, G.runs[r].n_tok - j * BN, r};
+  };
+  auto step = [&](auto is_v, Stream& st) {
+    st.left -= BN;
+    st.p += tile_step;
+    if (st.left <= 0) {
+      do {
+        ++st.r;
+      } while (st.r < G.n_runs && G.runs[st.r].n_tok == 0);
+      if (st.r < G.n_runs) {
+        st.p = run_base(is_v, st.r);
+        st.left = G.runs[st.r].n_tok;
+      }
     }
   };
-  TilePos first{0, 0};
-  {
-    int kk = k;
-    while (kk >= (G.runs[first.r].n_tok + BN - 1) / BN) {
-      kk -= (G.runs[first.r].n_tok + BN - 1) / BN;
-      ++first.r;
-    }
-    first.t0 = kk * BN;
-  }
+  using KSel = std::false_type;
+  using VSel = std::true_type;
 
   bf16x8 pk[NLD], pv[NLD];
-  auto load = [&](const void* run_base, TilePos t, bf16x8* dst) {
-    const int nv = min(G.runs[t.r].n_tok - t.t0, BN);
-    const uint32_t bytes = static_cast<uint32_t>(nv - 1) * row_bytes + D * 2;
-    const auto rs = make_rsrc(static_cast<const __bf16*>(run_base) + static_cast<int64_t>(t.t0) * ld + hoff, bytes);
+  // The stream's current tile into registers; rows past the run's end read as
+  // zeros through the buffer range check.
+  auto load = [&](const Stream& st, bf16x8* dst) {
+    const uint32_t bytes = static_cast<uint32_t>(min(st.left, BN) - 1) * row_bytes + D * 2;
+    const auto rs = make_rsrc(st.p, bytes);
 #pragma unroll
     for (int i = 0; i < NLD; ++i)
       dst[i] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rs, g_off + i * RPL * row_bytes, 0, 0));
@@ -259,57 +278,60 @@ __device__ __forceinline__ void attend_piece(const FwdArgs& a, const FwdGroupArg
       *reinterpret_cast<bf16x8*>(Vlds + buf * VT + v_st + i * RPL * VSTR) = pv[i];
   };
 
-  // Matrix-core step: O += P V from V buffer vb (if pv_on), S = K Q^T from K
-  // buffer kb (if s_on).  Operands go through a two-stage register pipeline
-  // (the LDS reads of stage i + 1 are issued before the MFMAs of stage i);
-  // scheduling barriers keep the compiler from hoisting every read up front.
-  auto read_v = [&](const __bf16* Vb, int stage, bf16x8* va) {
-    const int kb = stage >> 1, cc = stage & 1;
-    const __bf16* vrow = Vb + (kb * 32 + cc * 16) * VSTR;
-#pragma unroll
-    for (int db = 0; db < DB; ++db) {
-      const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vrow + db * 32));
-      const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vrow + 8 * VSTR + db * 32));
-      va[db] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-    }
-  };
-  auto read_k = [&](const __bf16* Kb, int ks, bf16x8* ka) {
-#pragma unroll
-    for (int kb = 0; kb < BN / 32; ++kb)
-      ka[kb] = *reinterpret_cast<const bf16x8*>(Kb + kb * 32 * KSTR + ks * 16);
-  };
+  // Matrix-core step: O += P V from V buffer vb (if pv_c), then S = K Q^T from
+  // K buffer kb_ (if s_c), as one stream of MFMAs whose LDS operands (V^T
+  // through transposing reads, K row-major) run kLead operands ahead in a
+  // register ring, so LDS latency hides behind kLead MFMAs.  Scheduling group
+  // barriers fix the interleave: the compiler would otherwise hoist every read
+  // to the top (more registers) or sink each next to its MFMA (no overlap).
   auto mstep = [&](auto pv_c, auto s_c, int vb, int kb_) {
     constexpr bool kPV = decltype(pv_c)::value, kS = decltype(s_c)::value;
+    constexpr int NPV = kPV ? 2 * (BN / 32) * DB : 0;  // (key block, 16-key half, d block)
+    constexpr int NS = kS ? KS * (BN / 32) : 0;        // (d slice, key block)
+    constexpr int N = NPV + NS;
+    constexpr int kLead = 8;
     const __bf16* Vb = Vlds + vb * VT + v_rd;
     const __bf16* Kb = Klds + kb_ * KT + k_rd;
-    constexpr int NV = 2 * (BN / 32);  // P V stages: (key block, 16-key half)
-    if constexpr (kPV) {
-      bf16x8 va[2][DB];
-      read_v(Vb, 0, va[0]);
-#pragma unroll
-      for (int st = 0; st < NV; ++st) {
-        __builtin_amdgcn_sched_barrier(0);
-        if (st + 1 < NV) read_v(Vb, st + 1, va[(st + 1) & 1]);
-        const int kb = st >> 1, cc = st & 1;
-#pragma unroll
-        for (int db = 0; db < DB; ++db)
-          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[st & 1][db], pb[kb][cc], o[db], 0, 0, 0);
+    auto operand = [&](int i) -> bf16x8 {
+      if (i < NPV) {
+        const int st = i / DB, db = i % DB, kb = st >> 1, cc = st & 1;
+        const __bf16* vrow = Vb + (kb * 32 + cc * 16) * VSTR + db * 32;
+        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)vrow);
+        const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vrow + 8 * VSTR));
+        return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
       }
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    if constexpr (kS) {
-      bf16x8 ka[2][BN / 32];
-      read_k(Kb, 0, ka[0]);
+      const int j = i - NPV, ks = j / (BN / 32), kb = j % (BN / 32);
+      return *reinterpret_cast<const bf16x8*>(Kb + kb * 32 * KSTR + ks * 16);
+    };
+    bf16x8 ring[kLead];
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        __builtin_amdgcn_sched_barrier(0);
-        if (ks + 1 < KS) read_k(Kb, ks + 1, ka[(ks + 1) & 1]);
+    for (int i = 0; i < kLead; ++i)
+      if (i < N) ring[i] = operand(i);
 #pragma unroll
-        for (int kb = 0; kb < BN / 32; ++kb)
-          s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[ks & 1][kb], qf[ks], ks == 0 ? f32x16{} : s[kb], 0, 0, 0);
+    for (int i = 0; i < N; ++i) {
+      const bf16x8 a = ring[i % kLead];
+      if (i < NPV) {
+        const int st = i / DB, db = i % DB, kb = st >> 1, cc = st & 1;
+        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[kb][cc], o[db], 0, 0, 0);
+      } else {
+        const int j = i - NPV, ks = j / (BN / 32), kb = j % (BN / 32);
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], ks == 0 ? f32x16{} : s[kb], 0, 0, 0);
       }
-      __builtin_amdgcn_sched_barrier(0);
+      if (i + kLead < N) ring[i % kLead] = operand(i + kLead);
     }
+    // A V operand is two LDS reads, a K operand one.
+    auto read_group = [&](int i) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      if (i < NPV) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    };
+#pragma unroll
+    for (int i = 0; i < (N < kLead ? N : kLead); ++i) read_group(i);
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      if (i + kLead < N) read_group(i + kLead);
+    }
+    __builtin_amdgcn_sched_barrier(0);
   };
 
   // Softmax step on S (keys >= nvalid of this tile masked): lazy rescale of
@@ -352,14 +374,22 @@ __device__ __forceinline__ void attend_piece(const FwdArgs& a, const FwdGroupArg
         pb[kb][e >> 3][e & 7] = pair[0];
         pb[kb][e >> 3][(e & 7) + 1] = pair[1];
       }
+    // P and the row sum are pure register values, so the compiler is free to
+    // sink their exponentials past the phase barrier into the next
+    // matrix-core step, which would load that step with this one's VALU work.
+    // Empty asm with read-write register operands pins them here.
+#pragma unroll
+    for (int kb = 0; kb < BN / 32; ++kb)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) asm volatile("" : "+v"(pb[kb][h]));
+    asm volatile("" : "+v"(l_part));
   };
 
   // Prologue: K_0 and V_0 loaded, K_0 stored.
-  TilePos kpos = first, vpos = first, spos = first;
-  load(G.runs[kpos.r].k, kpos, pk);
-  load(G.runs[vpos.r].v, vpos, pv);
+  Stream ks = stream_at(KSel{}, k), vs = stream_at(VSel{}, k), ss = stream_at(KSel{}, k);
+  load(ks, pk);
+  load(vs, pv);
   store_k(0);
-  advance(kpos);
   __syncthreads();
 
   // Global loads and LDS stores of phase 2j (even) and 2j + 1 (odd), done by
@@ -367,8 +397,8 @@ __device__ __forceinline__ void attend_piece(const FwdArgs& a, const FwdGroupArg
   // 2j + 1; V_{j+1} is loaded in phase 2j + 1 and stored at the end of 2j + 2.
   auto even_begin = [&](int j) {
     if (j + 1 < nt) {
-      load(G.runs[kpos.r].k, kpos, pk);
-      advance(kpos);
+      step(KSel{}, ks);
+      load(ks, pk);
     }
   };
   auto even_end = [&](int j) {
@@ -377,8 +407,8 @@ __device__ __forceinline__ void attend_piece(const FwdArgs& a, const FwdGroupArg
   };
   auto odd_begin = [&](int j) {
     if (j + 1 < nt) {
-      advance(vpos);
-      load(G.runs[vpos.r].v, vpos, pv);
+      step(VSel{}, vs);
+      load(vs, pv);
     }
   };
   auto odd_end = [&](int j) {
@@ -386,8 +416,8 @@ __device__ __forceinline__ void attend_piece(const FwdArgs& a, const FwdGroupArg
     __syncthreads();
   };
   auto soft = [&]() {
-    sstep(min(BN, G.runs[spos.r].n_tok - spos.t0));
-    advance(spos);
+    sstep(min(ss.left, BN));
+    step(KSel{}, ss);
   };
   using T_ = std::true_type;
   using F_ = std::false_type;
@@ -482,22 +512,38 @@ void fwd_bf16_kernel(FwdArgs a) {
   // [K buf0 | K buf1 | V buf0 | V buf1]; every offset fits a ds instruction's immediate.
   __shared__ __attribute__((aligned(16))) __bf16 lds[2 * P::KT + 2 * P::VT];
   const int rho = range_of_block(blockIdx.x, a.n_ranges);
-  for (int r = 0; r < a.dp_rounds; ++r) {
-    const int64_t i = static_cast<int64_t>(r) * a.n_ranges + rho;
-    int g = 0;
-    while (g + 1 < a.n_groups && i >= a.groups[g + 1].block_begin) ++g;
-    const FwdGroupArgs& G = a.groups[g];
-    attend_piece<D>(a, G, static_cast<int>(i - G.block_begin), 0, G.tiles_per_item, true, 0, lds);
-  }
   const int64_t S = range_begin(a, rho), E = range_begin(a, rho + 1);
-  for (int64_t t = S; t < E;) {
-    const Loc L = locate(a, t);
-    const FwdGroupArgs& G = a.groups[L.g];
-    const int64_t piece_end = min(E, L.item_begin + G.tiles_per_item);
-    const int nt = static_cast<int>(piece_end - t);
-    const bool whole = L.k == 0 && nt == G.tiles_per_item;
-    attend_piece<D>(a, G, L.item, L.k, nt, whole, t == S ? 2 * rho : 2 * rho + 1, lds);
-    t = piece_end;
+  // Whole items of the aligned rounds, then the pieces of the tail range;
+  // one call site keeps a single copy of the attention loop.
+  int round = 0;
+  int64_t t = S;
+  while (true) {
+    int g, item, k, nt, rec;
+    bool whole;
+    if (round < a.dp_rounds) {
+      const int64_t i = static_cast<int64_t>(round) * a.n_ranges + rho;
+      g = 0;
+      while (g + 1 < a.n_groups && i >= a.groups[g + 1].block_begin) ++g;
+      item = static_cast<int>(i - a.groups[g].block_begin);
+      k = 0;
+      nt = a.groups[g].tiles_per_item;
+      whole = true;
+      rec = 0;
+      ++round;
+    } else if (t < E) {
+      const Loc L = locate(a, t);
+      const int64_t piece_end = min(E, L.item_begin + a.groups[L.g].tiles_per_item);
+      g = L.g;
+      item = L.item;
+      k = L.k;
+      nt = static_cast<int>(piece_end - t);
+      whole = L.k == 0 && nt == a.groups[g].tiles_per_item;
+      rec = t == S ? 2 * rho : 2 * rho + 1;
+      t = piece_end;
+    } else {
+      break;
+    }
+    attend_piece<D>(a, a.groups[g], item, k, nt, whole, rec, lds);
   }
 }
 
