@@ -39,7 +39,6 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
-__device__ constexpr bf16x2 kOnes2 = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
 
 // Logical block -> (group, head, query tile).  Groups are stored longest
 // context first; inside a group consecutive blocks share a head.
@@ -363,17 +362,21 @@ __device__ __forceinline__ void attend_piece(const FwdArgs& a, const FwdGroupArg
       for (int db = 0; db < DB; ++db) o[db] *= alpha;
     }
     const float mneg = -m_run;
+    // Row sum in fp32 VALU adds (four independent partial sums): the bf16 dot
+    // instruction would wait on the matrix core that the other wave of this
+    // SIMD keeps busy.
+    float ls[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kb = 0; kb < BN / 32; ++kb)
 #pragma unroll
       for (int e = 0; e < 16; e += 2) {
-        bf16x2 pair;
-        pair[0] = static_cast<__bf16>(__builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][e], c, mneg)));
-        pair[1] = static_cast<__bf16>(__builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][e + 1], c, mneg)));
-        l_part = __builtin_amdgcn_fdot2_f32_bf16(pair, kOnes2, l_part, false);
-        pb[kb][e >> 3][e & 7] = pair[0];
-        pb[kb][e >> 3][(e & 7) + 1] = pair[1];
+        const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][e], c, mneg));
+        const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][e + 1], c, mneg));
+        ls[(e >> 1) & 3] += p0 + p1;
+        pb[kb][e >> 3][e & 7] = static_cast<__bf16>(p0);
+        pb[kb][e >> 3][(e & 7) + 1] = static_cast<__bf16>(p1);
       }
+    l_part += (ls[0] + ls[1]) + (ls[2] + ls[3]);
     // P and the row sum are pure register values, so the compiler is free to
     // sink their exponentials past the phase barrier into the next
     // matrix-core step, which would load that step with this one's VALU work.
@@ -385,34 +388,37 @@ __device__ __forceinline__ void attend_piece(const FwdArgs& a, const FwdGroupArg
     asm volatile("" : "+v"(l_part));
   };
 
-  // Prologue: K_0 and V_0 loaded, K_0 stored.
+  // Prologue: K_0 stored, V_0 and K_1 in flight.
   Stream ks = stream_at(KSel{}, k), vs = stream_at(VSel{}, k), ss = stream_at(KSel{}, k);
   load(ks, pk);
   load(vs, pv);
   store_k(0);
+  if (nt > 1) {
+    step(KSel{}, ks);
+    load(ks, pk);
+  }
   __syncthreads();
 
-  // Global loads and LDS stores of phase 2j (even) and 2j + 1 (odd), done by
-  // every wave: K_{j+1} is loaded in phase 2j and stored at the end of phase
-  // 2j + 1; V_{j+1} is loaded in phase 2j + 1 and stored at the end of 2j + 2.
-  auto even_begin = [&](int j) {
-    if (j + 1 < nt) {
-      step(KSel{}, ks);
-      load(ks, pk);
-    }
-  };
+  // Global loads and LDS stores, done by every wave at the end of its phase
+  // (the issue of the loads overlaps the wait at the barrier, and the data
+  // has the whole next phase to arrive): phase 2j ends by storing V_j and
+  // loading V_{j+1}; phase 2j + 1 ends by storing K_{j+1} and loading K_{j+2}.
+  auto even_begin = [&](int) {};
   auto even_end = [&](int j) {
     if (j < nt) store_v(j & 1);
-    __syncthreads();
-  };
-  auto odd_begin = [&](int j) {
     if (j + 1 < nt) {
       step(VSel{}, vs);
       load(vs, pv);
     }
+    __syncthreads();
   };
+  auto odd_begin = [&](int) {};
   auto odd_end = [&](int j) {
     if (j + 1 < nt) store_k((j + 1) & 1);
+    if (j + 2 < nt) {
+      step(KSel{}, ks);
+      load(ks, pk);
+    }
     __syncthreads();
   };
   auto soft = [&]() {
