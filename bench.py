@@ -115,7 +115,7 @@ def bench_streaming(args):
     passes = args.passes or w["passes"]
     desc = w["layer"]
     F = desc["frames_per_state"]
-    st = StreamingMSSA(desc, layers, w["hist_cap_frames"], dtype=w["dtype"])
+    st = StreamingMSSA(desc, layers, w["hist_cap_frames"], dtype=w["dtype"], pooled_ring=args.pooled_ring)
     init_shapes = st.shapes(w["hist_start_frames"])
     for L in range(layers):
         x = init_inputs(w, L, init_shapes)
@@ -156,7 +156,8 @@ def bench_streaming(args):
         "data": "synthetic",
         "config": {"workload": "streaming_wan13b", "layers": layers, "passes": passes,
                    "hist_frames": f"{w['hist_start_frames']}->{w['hist_cap_frames']} FIFO",
-                   "frames_per_state": F},
+                   "frames_per_state": F,
+                   "history_pooling": "pooled_ring" if args.pooled_ring else "per_pass"},
         "all_passes_ms_per_frame": round(tot_ms / (passes * F), 4),
         "steady_state_passes": [steady[0], steady[-1]],
         "effective_tflops_steady": round(sum(pass_flops[i] for i in steady) / (st_ms * 1e-3) / 1e12, 2),
@@ -176,6 +177,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--layers", type=int, default=0, help="streaming: layers (default 30)")
     ap.add_argument("--passes", type=int, default=0, help="streaming: rolling passes (default 64)")
+    ap.add_argument("--pooled-ring", action="store_true",
+                    help="streaming: keep pooled history rings instead of re-pooling history each pass")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="only run a plain device copy of this many MiB (5 times), the reference "
                          "for scaling HBM byte counters")

@@ -71,7 +71,15 @@ typedef struct {
   int32_t head_dim;                 /* 64 or 128 */
   int32_t dtype;                    /* mssa_dtype of every tensor */
   float softmax_scale;              /* <= 0 selects 1/sqrt(head_dim) */
+  int32_t flags;                    /* MSSA_PLAN_* bits, 0 for the plain path */
 } mssa_plan_desc;
+
+/* Plan flag: the history pooled to every query scale s > 1 lives in
+ * caller-owned pooled-history rings (one K and one V ring per such scale)
+ * that the cache roll keeps up to date, instead of being pooled from native
+ * history by every mssa_pool_kv.  Such a plan pools only window frames in
+ * mssa_pool_kv and is run with mssa_forward_ring / mssa_hist_append_ring. */
+#define MSSA_PLAN_POOLED_HIST_RING 1
 
 /* Sizes derived by the plan.  Group g is the g-th distinct query scale in
  * window token order; its queries are the contiguous range
@@ -181,6 +189,46 @@ mssa_status mssa_forward(mssa_plan plan, const void* q_win, const void* k_sink,
 mssa_status mssa_hist_append(mssa_plan plan, const void* k_win, const void* v_win, void* k_ring,
                              void* v_ring, int32_t ring_cap_frames, int32_t* ring_head,
                              int32_t* ring_count, void* stream);
+
+/* Streaming with incrementally pooled history (Sec. 3.1, Eq. 2 cache roll;
+ * Eq. 4 history at the query scale), for plans created with
+ * MSSA_PLAN_POOLED_HIST_RING.  For query group g (mssa_plan_info order) with
+ * scale s = group_scale[g] > 1, the pooled-history ring of K (V) is a
+ * caller-owned device buffer of ring_cap_frames slots of tok_s tokens
+ * ([ring_cap_frames * tok_s, H, D], plan dtype, tok_s the tokens of a frame
+ * at scale s); slot f holds the native ring's slot f pooled to s.  Arrays
+ * k_*_pooled / v_*_pooled have one entry per query group; entries of groups
+ * with scale 1 are ignored and may be NULL.  The history the plan reads is
+ * slots [0, hist_frames), as for the native ring.  Pooled frames equal, bit
+ * for bit, what mssa_pool_kv computes from the native frames; the attention
+ * outputs agree with the plain path up to the kernel's rounding (the
+ * pooled history is a key run of its own, so key tiles fall differently). */
+
+/* Pool native ring slots [0, hist_frames) to every query scale s > 1 into
+ * the pooled rings (once, to start from an existing native history).
+ * MSSA_ERR_UNSUPPORTED for a plan without the flag. */
+mssa_status mssa_pool_hist_ring(mssa_plan plan, const void* k_ring, const void* v_ring, void* const* k_ring_pooled,
+                                void* const* v_ring_pooled, void* stream);
+
+/* mssa_forward for a MSSA_PLAN_POOLED_HIST_RING plan: group g with scale > 1
+ * reads its history from k_hist_pooled[g] / v_hist_pooled[g]; everything else
+ * (and workspace, which holds this pass's pooled window frames) as in
+ * mssa_forward.  MSSA_ERR_UNSUPPORTED for a plan without the flag. */
+mssa_status mssa_forward_ring(mssa_plan plan, const void* q_win, const void* k_sink, const void* v_sink,
+                              const void* k_hist, const void* v_hist, const void* const* k_hist_pooled,
+                              const void* const* v_hist_pooled, const void* k_win, const void* v_win,
+                              const void* workspace, int64_t workspace_bytes, void* out, void* stream);
+
+/* mssa_hist_append for a MSSA_PLAN_POOLED_HIST_RING plan: the head state's F
+ * native frames go to the native ring as there, and the same frames pooled
+ * to each scale s > 1, which this pass's mssa_pool_kv left in `workspace`,
+ * go to the same slots of the pooled rings.  Enqueues device-to-device
+ * copies on `stream` (after this pass's mssa_forward, which reads the
+ * rings).  MSSA_ERR_UNSUPPORTED for a plan without the flag. */
+mssa_status mssa_hist_append_ring(mssa_plan plan, const void* k_win, const void* v_win, const void* workspace,
+                                  int64_t workspace_bytes, void* k_ring, void* v_ring, void* const* k_ring_pooled,
+                                  void* const* v_ring_pooled, int32_t ring_cap_frames, int32_t* ring_head,
+                                  int32_t* ring_count, void* stream);
 
 /* Name of a status code (static string). */
 const char* mssa_status_string(mssa_status s);

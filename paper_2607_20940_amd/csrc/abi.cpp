@@ -8,6 +8,7 @@
 #include <cstring>
 #include <new>
 #include <string>
+#include <vector>
 
 #include "../../include/libmssa.h"
 #include "kernels.hpp"
@@ -51,6 +52,189 @@ int ranges_override() {
 mssa_status check_device(hipError_t e, const char* what) {
   if (e == hipSuccess) return MSSA_OK;
   return fail(MSSA_ERR_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+// Launch pool jobs (source and destination pointers filled in), at most
+// kMaxPoolJobs per launch.
+mssa_status launch_pool_jobs(const mssa::Plan& p, std::vector<mssa::PoolJobArgs>& jobs, void* stream) {
+  mssa::PoolArgs a{};
+  a.ld = p.ld;
+  a.chunks_per_tok = static_cast<int32_t>(p.ld * p.elem_bytes / 16);
+  size_t j0 = 0;
+  while (j0 < jobs.size()) {
+    const size_t nj = std::min<size_t>(mssa::kMaxPoolJobs, jobs.size() - j0);
+    int64_t blocks = 0;
+    for (size_t i = 0; i < nj; ++i) {
+      mssa::PoolJobArgs& A = a.jobs[i];
+      A = jobs[j0 + i];
+      A.block_begin = static_cast<int32_t>(blocks);
+      const int64_t work = static_cast<int64_t>(A.n_frames) * A.dst_gh * A.dst_gw * a.chunks_per_tok;
+      blocks += (work + mssa::kPoolThreads - 1) / mssa::kPoolThreads;
+    }
+    if (blocks > 0x7fffffff) return fail(MSSA_ERR_UNSUPPORTED, "pool grid too large");
+    a.n_jobs = static_cast<int32_t>(nj);
+    const mssa_status s = check_device(
+        mssa::launch_pool(a, static_cast<int>(blocks), p.desc.dtype == MSSA_BF16, static_cast<hipStream_t>(stream)),
+        "pool kernel launch");
+    if (s != MSSA_OK) return s;
+    j0 += nj;
+  }
+  return MSSA_OK;
+}
+
+// Ring slots (FIFO once full) that F appended frames take, with the head and
+// count after them; false for an inconsistent head / count.
+bool ring_slots(int32_t cap, int32_t F, int32_t* head, int32_t* count, std::vector<int32_t>& slots) {
+  const int32_t h0 = *head, c0 = *count;
+  if (c0 < 0 || c0 > cap || h0 < 0 || h0 >= cap || (h0 != 0 && c0 != cap)) return false;
+  int32_t h = h0, c = c0;
+  slots.clear();
+  for (int32_t f = 0; f < F; ++f) {
+    if (c < cap) {
+      slots.push_back(c++);
+    } else {
+      slots.push_back(h);
+      h = (h + 1) % cap;
+    }
+  }
+  *head = h;
+  *count = c;
+  return true;
+}
+
+// Token count of one frame at scale s.
+int64_t frame_tokens(const mssa::Plan& p, int32_t s) {
+  const int64_t gh = (p.desc.grid_h + s - 1) / s, gw = (p.desc.grid_w + s - 1) / s;
+  return gh * gw;
+}
+
+// Validation and slot assignment shared by both appends; enqueues the native
+// frame copies.  On success *ring_head / *ring_count are advanced and slots
+// holds the ring slot of each appended frame.
+mssa_status append_native(const mssa::Plan& p, const void* k_win, const void* v_win, void* k_ring, void* v_ring,
+                          int32_t ring_cap_frames, int32_t* ring_head, int32_t* ring_count,
+                          std::vector<int32_t>& slots, void* stream) {
+  if (!k_win || !v_win || !k_ring || !v_ring || !ring_head || !ring_count)
+    return fail(MSSA_ERR_INVALID_ARG, "null argument");
+  const int32_t F = p.desc.frames_per_state;
+  if (p.desc.scales[0] != 1)
+    return fail(MSSA_ERR_UNSUPPORTED, "the emitted head state must be at native scale (scales[0] == 1)");
+  if (ring_cap_frames < F) return fail(MSSA_ERR_UNSUPPORTED, "ring_cap_frames < frames_per_state");
+  int32_t head = *ring_head, count = *ring_count;
+  if (!ring_slots(ring_cap_frames, F, &head, &count, slots))
+    return fail(MSSA_ERR_INVALID_ARG, "inconsistent ring_head / ring_count");
+  const size_t frame_bytes = static_cast<size_t>(p.tok1 * p.ld * p.elem_bytes);
+  const char* kw = static_cast<const char*>(k_win);
+  const char* vw = static_cast<const char*>(v_win);
+  char* kr = static_cast<char*>(k_ring);
+  char* vr = static_cast<char*>(v_ring);
+  const size_t ring_bytes = frame_bytes * ring_cap_frames;
+  const size_t win_bytes = frame_bytes * F;
+  auto overlap = [](const char* x, size_t nx, const char* y, size_t ny) { return x < y + ny && y < x + nx; };
+  if (overlap(kr, ring_bytes, kw, win_bytes) || overlap(kr, ring_bytes, vw, win_bytes) ||
+      overlap(vr, ring_bytes, kw, win_bytes) || overlap(vr, ring_bytes, vw, win_bytes) ||
+      overlap(kr, ring_bytes, vr, ring_bytes))
+    return fail(MSSA_ERR_INVALID_ARG, "ring buffers overlap each other or the window");
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  for (int32_t f = 0; f < F; ++f) {
+    const size_t slot = static_cast<size_t>(slots[f]);
+    mssa_status s = check_device(hipMemcpyAsync(kr + slot * frame_bytes, kw + f * frame_bytes, frame_bytes,
+                                                hipMemcpyDeviceToDevice, st), "history append (K)");
+    if (s != MSSA_OK) return s;
+    s = check_device(hipMemcpyAsync(vr + slot * frame_bytes, vw + f * frame_bytes, frame_bytes,
+                                    hipMemcpyDeviceToDevice, st), "history append (V)");
+    if (s != MSSA_OK) return s;
+  }
+  *ring_head = head;
+  *ring_count = count;
+  return MSSA_OK;
+}
+
+// mssa_forward / mssa_forward_ring: validate, pack the kernel arguments and
+// launch.  k_hist_pooled / v_hist_pooled (ring plans only) give each group's
+// pooled-history ring.
+mssa_status forward_impl(const mssa::Plan& p, const void* q_win, const void* k_sink, const void* v_sink,
+                         const void* k_hist, const void* v_hist, const void* const* k_hist_pooled,
+                         const void* const* v_hist_pooled, const void* k_win, const void* v_win,
+                         const void* workspace, int64_t workspace_bytes, void* out, void* stream) {
+  if (!q_win || !k_win || !v_win || !out)
+    return fail(MSSA_ERR_INVALID_ARG, "q_win, k_win, v_win and out must be non-null");
+  if (p.n_sink_tok > 0 && (!k_sink || !v_sink))
+    return fail(MSSA_ERR_INVALID_ARG, "k_sink and v_sink must be non-null when sink_frames > 0");
+  if (p.n_hist_tok > 0 && (!k_hist || !v_hist))
+    return fail(MSSA_ERR_INVALID_ARG, "k_hist and v_hist must be non-null when hist_frames > 0");
+  if (p.workspace_bytes > 0 && (!workspace || workspace_bytes < p.workspace_bytes))
+    return fail(MSSA_ERR_WORKSPACE, "workspace smaller than mssa_plan_info.workspace_bytes");
+  for (const void* t : {q_win, k_sink, v_sink, k_hist, v_hist, k_win, v_win, static_cast<const void*>(out)})
+    if (t && !aligned16(t)) return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
+  if (out == q_win || out == k_win || out == v_win)
+    return fail(MSSA_ERR_INVALID_ARG, "out must not alias an input");
+  if (p.hist_ring && p.n_hist_tok > 0) {
+    if (!k_hist_pooled || !v_hist_pooled)
+      return fail(MSSA_ERR_INVALID_ARG, "k_hist_pooled and v_hist_pooled must be non-null");
+    for (size_t g = 0; g < p.groups.size(); ++g) {
+      if (p.groups[g].scale == 1) continue;
+      const void* kp = k_hist_pooled[g];
+      const void* vp = v_hist_pooled[g];
+      if (!kp || !vp) return fail(MSSA_ERR_INVALID_ARG, "null pooled-history ring for a coarse query scale");
+      if (!aligned16(kp) || !aligned16(vp)) return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
+    }
+  }
+
+  const bool bf16 = p.desc.dtype == MSSA_BF16;
+  const int bm = bf16 ? mssa::kFwdBM : mssa::kFwdF32BM;
+  const int64_t row_bytes = p.ld * p.elem_bytes;
+  mssa::FwdArgs a{};
+  a.q = q_win;
+  a.out = out;
+  a.ld = p.ld;
+  a.num_heads = p.desc.num_heads;
+  a.scale = p.softmax_scale;
+  a.scale_log2e = p.softmax_scale * 1.4426950408889634f;
+  a.n_ranges = p.n_ranges;
+  a.total_tiles = p.total_tiles;
+  a.tail_begin = p.tail_begin;
+  a.dp_rounds = p.dp_rounds;
+  const char* ws = static_cast<const char*>(workspace);
+  a.partial = p.partial_bytes > 0 ? reinterpret_cast<float*>(const_cast<char*>(ws) + p.partial_off) : nullptr;
+  int64_t blocks = 0;
+  int gi = 0;
+  for (int g : p.order) {
+    const mssa::QGroup& Q = p.groups[g];
+    mssa::FwdGroupArgs& A = a.groups[gi++];
+    A.q_begin = Q.q_begin;
+    A.q_end = Q.q_end;
+    A.n_qtiles = (Q.q_end - Q.q_begin + bm - 1) / bm;
+    A.block_begin = static_cast<int32_t>(blocks);
+    A.tiles_per_item = p.tiles_per_item[g];
+    A.tile_begin = p.tile_begin[g];
+    if (p.runs[g].size() > static_cast<size_t>(mssa::kMaxRuns))
+      return fail(MSSA_ERR_UNSUPPORTED, "too many context runs for one query scale");
+    A.n_runs = static_cast<int32_t>(p.runs[g].size());
+    for (size_t r = 0; r < p.runs[g].size(); ++r) {
+      const mssa::Run& R = p.runs[g][r];
+      const char *kb = nullptr, *vb = nullptr;
+      switch (R.buffer) {
+        case mssa::kBufSink: kb = static_cast<const char*>(k_sink); vb = static_cast<const char*>(v_sink); break;
+        case mssa::kBufHist: kb = static_cast<const char*>(k_hist); vb = static_cast<const char*>(v_hist); break;
+        case mssa::kBufWin: kb = static_cast<const char*>(k_win); vb = static_cast<const char*>(v_win); break;
+        case mssa::kBufHistPooled:
+          kb = static_cast<const char*>(k_hist_pooled[g]);
+          vb = static_cast<const char*>(v_hist_pooled[g]);
+          break;
+        default: kb = ws + p.pooled_k_off[g]; vb = ws + p.pooled_v_off[g]; break;
+      }
+      A.runs[r].k = kb + R.tok_offset * row_bytes;
+      A.runs[r].v = vb + R.tok_offset * row_bytes;
+      A.runs[r].n_tok = static_cast<int32_t>(R.n_tok);
+    }
+    blocks += static_cast<int64_t>(A.n_qtiles) * p.desc.num_heads;
+  }
+  if (blocks > 0x7fffffff) return fail(MSSA_ERR_UNSUPPORTED, "attention grid too large");
+  a.n_groups = gi;
+  a.n_blocks = static_cast<int32_t>(blocks);
+  return check_device(mssa::launch_forward(a, p.desc.head_dim, bf16, static_cast<hipStream_t>(stream)),
+                      "attention kernel launch");
 }
 
 }  // namespace
@@ -122,8 +306,10 @@ mssa_status mssa_pool_kv(mssa_plan plan, const void* k_hist, const void* v_hist,
   const mssa::Plan& p = plan->p;
   if (p.pool_jobs.empty()) return MSSA_OK;
   if (!k_win || !v_win) return fail(MSSA_ERR_INVALID_ARG, "k_win and v_win must be non-null");
-  if (p.n_hist_tok > 0 && (!k_hist || !v_hist))
-    return fail(MSSA_ERR_INVALID_ARG, "k_hist and v_hist must be non-null when hist_frames > 0");
+  bool reads_hist = false;
+  for (const mssa::PoolJob& J : p.pool_jobs) reads_hist |= J.buffer == mssa::kBufHist;
+  if (reads_hist && (!k_hist || !v_hist))
+    return fail(MSSA_ERR_INVALID_ARG, "k_hist and v_hist must be non-null when history is pooled");
   if (!workspace || workspace_bytes < p.workspace_bytes)
     return fail(MSSA_ERR_WORKSPACE, "workspace smaller than mssa_plan_info.workspace_bytes");
   if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
@@ -131,161 +317,141 @@ mssa_status mssa_pool_kv(mssa_plan plan, const void* k_hist, const void* v_hist,
   if (!aligned16(k_win) || !aligned16(v_win) || (k_hist && !aligned16(k_hist)) || (v_hist && !aligned16(v_hist)))
     return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
 
-  const int64_t eb = p.elem_bytes;
-  const int64_t row_bytes = p.ld * eb;
-  mssa::PoolArgs a{};
-  a.ld = p.ld;
-  a.chunks_per_tok = static_cast<int32_t>(row_bytes / 16);
+  const int64_t row_bytes = p.ld * p.elem_bytes;
   auto* ws = static_cast<char*>(workspace);
-  size_t j0 = 0;
-  while (j0 < p.pool_jobs.size()) {
-    const size_t nj = std::min<size_t>(mssa::kMaxPoolJobs, p.pool_jobs.size() - j0);
-    int64_t blocks = 0;
-    for (size_t i = 0; i < nj; ++i) {
-      const mssa::PoolJob& J = p.pool_jobs[j0 + i];
-      mssa::PoolJobArgs& A = a.jobs[i];
-      const char* sk = static_cast<const char*>(J.buffer == mssa::kBufHist ? k_hist : k_win);
-      const char* sv = static_cast<const char*>(J.buffer == mssa::kBufHist ? v_hist : v_win);
-      A.src_k = sk + J.src_tok * row_bytes;
-      A.src_v = sv + J.src_tok * row_bytes;
-      A.dst_k = ws + p.pooled_k_off[J.group] + J.dst_tok * row_bytes;
-      A.dst_v = ws + p.pooled_v_off[J.group] + J.dst_tok * row_bytes;
-      A.src_gh = J.src_gh;
-      A.src_gw = J.src_gw;
-      A.dst_gh = J.dst_gh;
-      A.dst_gw = J.dst_gw;
-      A.factor = J.factor;
-      A.n_frames = J.n_frames;
-      A.block_begin = static_cast<int32_t>(blocks);
-      const int64_t work = static_cast<int64_t>(J.n_frames) * J.dst_gh * J.dst_gw * a.chunks_per_tok;
-      blocks += (work + mssa::kPoolThreads - 1) / mssa::kPoolThreads;
-    }
-    if (blocks > 0x7fffffff) return fail(MSSA_ERR_UNSUPPORTED, "pool grid too large");
-    a.n_jobs = static_cast<int32_t>(nj);
-    const mssa_status s = check_device(
-        mssa::launch_pool(a, static_cast<int>(blocks), p.desc.dtype == MSSA_BF16, static_cast<hipStream_t>(stream)),
-        "pool kernel launch");
-    if (s != MSSA_OK) return s;
-    j0 += nj;
+  std::vector<mssa::PoolJobArgs> jobs;
+  for (const mssa::PoolJob& J : p.pool_jobs) {
+    mssa::PoolJobArgs A{};
+    const char* sk = static_cast<const char*>(J.buffer == mssa::kBufHist ? k_hist : k_win);
+    const char* sv = static_cast<const char*>(J.buffer == mssa::kBufHist ? v_hist : v_win);
+    A.src_k = sk + J.src_tok * row_bytes;
+    A.src_v = sv + J.src_tok * row_bytes;
+    A.dst_k = ws + p.pooled_k_off[J.group] + J.dst_tok * row_bytes;
+    A.dst_v = ws + p.pooled_v_off[J.group] + J.dst_tok * row_bytes;
+    A.src_gh = J.src_gh;
+    A.src_gw = J.src_gw;
+    A.dst_gh = J.dst_gh;
+    A.dst_gw = J.dst_gw;
+    A.factor = J.factor;
+    A.n_frames = J.n_frames;
+    jobs.push_back(A);
   }
-  return MSSA_OK;
+  return launch_pool_jobs(p, jobs, stream);
 }
 
 mssa_status mssa_forward(mssa_plan plan, const void* q_win, const void* k_sink, const void* v_sink,
                          const void* k_hist, const void* v_hist, const void* k_win, const void* v_win,
                          const void* workspace, int64_t workspace_bytes, void* out, void* stream) {
   if (!plan) return fail(MSSA_ERR_INVALID_ARG, "plan must be non-null");
-  const mssa::Plan& p = plan->p;
-  if (!q_win || !k_win || !v_win || !out)
-    return fail(MSSA_ERR_INVALID_ARG, "q_win, k_win, v_win and out must be non-null");
-  if (p.n_sink_tok > 0 && (!k_sink || !v_sink))
-    return fail(MSSA_ERR_INVALID_ARG, "k_sink and v_sink must be non-null when sink_frames > 0");
-  if (p.n_hist_tok > 0 && (!k_hist || !v_hist))
-    return fail(MSSA_ERR_INVALID_ARG, "k_hist and v_hist must be non-null when hist_frames > 0");
-  if (p.workspace_bytes > 0 && (!workspace || workspace_bytes < p.workspace_bytes))
-    return fail(MSSA_ERR_WORKSPACE, "workspace smaller than mssa_plan_info.workspace_bytes");
-  for (const void* t : {q_win, k_sink, v_sink, k_hist, v_hist, k_win, v_win, static_cast<const void*>(out)})
-    if (t && !aligned16(t)) return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
-  if (out == q_win || out == k_win || out == v_win)
-    return fail(MSSA_ERR_INVALID_ARG, "out must not alias an input");
+  if (plan->p.hist_ring)
+    return fail(MSSA_ERR_UNSUPPORTED, "plan has MSSA_PLAN_POOLED_HIST_RING: use mssa_forward_ring");
+  return forward_impl(plan->p, q_win, k_sink, v_sink, k_hist, v_hist, nullptr, nullptr, k_win, v_win, workspace,
+                      workspace_bytes, out, stream);
+}
 
-  const bool bf16 = p.desc.dtype == MSSA_BF16;
-  const int bm = bf16 ? mssa::kFwdBM : mssa::kFwdF32BM;
-  const int64_t row_bytes = p.ld * p.elem_bytes;
-  mssa::FwdArgs a{};
-  a.q = q_win;
-  a.out = out;
-  a.ld = p.ld;
-  a.num_heads = p.desc.num_heads;
-  a.scale = p.softmax_scale;
-  a.scale_log2e = p.softmax_scale * 1.4426950408889634f;
-  a.n_ranges = p.n_ranges;
-  a.total_tiles = p.total_tiles;
-  a.tail_begin = p.tail_begin;
-  a.dp_rounds = p.dp_rounds;
-  const char* ws = static_cast<const char*>(workspace);
-  a.partial = p.partial_bytes > 0 ? reinterpret_cast<float*>(const_cast<char*>(ws) + p.partial_off) : nullptr;
-  int64_t blocks = 0;
-  int gi = 0;
-  for (int g : p.order) {
-    const mssa::QGroup& Q = p.groups[g];
-    mssa::FwdGroupArgs& A = a.groups[gi++];
-    A.q_begin = Q.q_begin;
-    A.q_end = Q.q_end;
-    A.n_qtiles = (Q.q_end - Q.q_begin + bm - 1) / bm;
-    A.block_begin = static_cast<int32_t>(blocks);
-    A.tiles_per_item = p.tiles_per_item[g];
-    A.tile_begin = p.tile_begin[g];
-    if (p.runs[g].size() > static_cast<size_t>(mssa::kMaxRuns))
-      return fail(MSSA_ERR_UNSUPPORTED, "too many context runs for one query scale");
-    A.n_runs = static_cast<int32_t>(p.runs[g].size());
-    for (size_t r = 0; r < p.runs[g].size(); ++r) {
-      const mssa::Run& R = p.runs[g][r];
-      const char *kb = nullptr, *vb = nullptr;
-      switch (R.buffer) {
-        case mssa::kBufSink: kb = static_cast<const char*>(k_sink); vb = static_cast<const char*>(v_sink); break;
-        case mssa::kBufHist: kb = static_cast<const char*>(k_hist); vb = static_cast<const char*>(v_hist); break;
-        case mssa::kBufWin: kb = static_cast<const char*>(k_win); vb = static_cast<const char*>(v_win); break;
-        default: kb = ws + p.pooled_k_off[g]; vb = ws + p.pooled_v_off[g]; break;
-      }
-      A.runs[r].k = kb + R.tok_offset * row_bytes;
-      A.runs[r].v = vb + R.tok_offset * row_bytes;
-      A.runs[r].n_tok = static_cast<int32_t>(R.n_tok);
-    }
-    blocks += static_cast<int64_t>(A.n_qtiles) * p.desc.num_heads;
-  }
-  if (blocks > 0x7fffffff) return fail(MSSA_ERR_UNSUPPORTED, "attention grid too large");
-  a.n_groups = gi;
-  a.n_blocks = static_cast<int32_t>(blocks);
-  return check_device(mssa::launch_forward(a, p.desc.head_dim, bf16, static_cast<hipStream_t>(stream)),
-                      "attention kernel launch");
+mssa_status mssa_forward_ring(mssa_plan plan, const void* q_win, const void* k_sink, const void* v_sink,
+                              const void* k_hist, const void* v_hist, const void* const* k_hist_pooled,
+                              const void* const* v_hist_pooled, const void* k_win, const void* v_win,
+                              const void* workspace, int64_t workspace_bytes, void* out, void* stream) {
+  if (!plan) return fail(MSSA_ERR_INVALID_ARG, "plan must be non-null");
+  if (!plan->p.hist_ring)
+    return fail(MSSA_ERR_UNSUPPORTED, "plan lacks MSSA_PLAN_POOLED_HIST_RING: use mssa_forward");
+  return forward_impl(plan->p, q_win, k_sink, v_sink, k_hist, v_hist, k_hist_pooled, v_hist_pooled, k_win, v_win,
+                      workspace, workspace_bytes, out, stream);
 }
 
 mssa_status mssa_hist_append(mssa_plan plan, const void* k_win, const void* v_win, void* k_ring, void* v_ring,
                              int32_t ring_cap_frames, int32_t* ring_head, int32_t* ring_count, void* stream) {
-  if (!plan || !k_win || !v_win || !k_ring || !v_ring || !ring_head || !ring_count)
-    return fail(MSSA_ERR_INVALID_ARG, "null argument");
+  if (!plan) return fail(MSSA_ERR_INVALID_ARG, "null argument");
+  std::vector<int32_t> slots;
+  return append_native(plan->p, k_win, v_win, k_ring, v_ring, ring_cap_frames, ring_head, ring_count, slots,
+                       stream);
+}
+
+mssa_status mssa_hist_append_ring(mssa_plan plan, const void* k_win, const void* v_win, const void* workspace,
+                                  int64_t workspace_bytes, void* k_ring, void* v_ring, void* const* k_ring_pooled,
+                                  void* const* v_ring_pooled, int32_t ring_cap_frames, int32_t* ring_head,
+                                  int32_t* ring_count, void* stream) {
+  if (!plan) return fail(MSSA_ERR_INVALID_ARG, "null argument");
   const mssa::Plan& p = plan->p;
-  const int32_t F = p.desc.frames_per_state;
-  if (p.desc.scales[0] != 1)
-    return fail(MSSA_ERR_UNSUPPORTED, "the emitted head state must be at native scale (scales[0] == 1)");
-  if (ring_cap_frames < F) return fail(MSSA_ERR_UNSUPPORTED, "ring_cap_frames < frames_per_state");
-  const int32_t head = *ring_head, count = *ring_count;
-  if (count < 0 || count > ring_cap_frames || head < 0 || head >= ring_cap_frames ||
-      (head != 0 && count != ring_cap_frames))
-    return fail(MSSA_ERR_INVALID_ARG, "inconsistent ring_head / ring_count");
-  const size_t frame_bytes = static_cast<size_t>(p.tok1 * p.ld * p.elem_bytes);
-  const char* kw = static_cast<const char*>(k_win);
-  const char* vw = static_cast<const char*>(v_win);
-  char* kr = static_cast<char*>(k_ring);
-  char* vr = static_cast<char*>(v_ring);
-  const size_t ring_bytes = frame_bytes * ring_cap_frames;
-  const size_t win_bytes = frame_bytes * F;
-  auto overlap = [](const char* a, size_t na, const char* b, size_t nb) { return a < b + nb && b < a + na; };
-  if (overlap(kr, ring_bytes, kw, win_bytes) || overlap(kr, ring_bytes, vw, win_bytes) ||
-      overlap(vr, ring_bytes, kw, win_bytes) || overlap(vr, ring_bytes, vw, win_bytes) ||
-      overlap(kr, ring_bytes, vr, ring_bytes))
-    return fail(MSSA_ERR_INVALID_ARG, "ring buffers overlap each other or the window");
-  int32_t h = head, c = count;
-  for (int32_t f = 0; f < F; ++f) {
-    int32_t slot;
-    if (c < ring_cap_frames) {
-      slot = c++;
-    } else {
-      slot = h;
-      h = (h + 1) % ring_cap_frames;
-    }
-    const hipStream_t st = static_cast<hipStream_t>(stream);
-    mssa_status s = check_device(hipMemcpyAsync(kr + slot * frame_bytes, kw + f * frame_bytes, frame_bytes,
-                                                hipMemcpyDeviceToDevice, st), "history append (K)");
-    if (s != MSSA_OK) return s;
-    s = check_device(hipMemcpyAsync(vr + slot * frame_bytes, vw + f * frame_bytes, frame_bytes,
-                                    hipMemcpyDeviceToDevice, st), "history append (V)");
-    if (s != MSSA_OK) return s;
+  if (!p.hist_ring)
+    return fail(MSSA_ERR_UNSUPPORTED, "plan lacks MSSA_PLAN_POOLED_HIST_RING: use mssa_hist_append");
+  if (!k_ring_pooled || !v_ring_pooled) return fail(MSSA_ERR_INVALID_ARG, "null pooled ring array");
+  bool coarse = false;
+  for (size_t g = 0; g < p.groups.size(); ++g) {
+    if (p.groups[g].scale == 1) continue;
+    coarse = true;
+    if (!k_ring_pooled[g] || !v_ring_pooled[g])
+      return fail(MSSA_ERR_INVALID_ARG, "null pooled-history ring for a coarse query scale");
   }
-  *ring_head = h;
-  *ring_count = c;
+  if (coarse && (!workspace || workspace_bytes < p.workspace_bytes))
+    return fail(MSSA_ERR_WORKSPACE, "workspace smaller than mssa_plan_info.workspace_bytes");
+  std::vector<int32_t> slots;
+  const mssa_status s0 = append_native(p, k_win, v_win, k_ring, v_ring, ring_cap_frames, ring_head, ring_count,
+                                       slots, stream);
+  if (s0 != MSSA_OK) return s0;
+  // The head state's frames pooled to each coarse scale: window frames
+  // 0 .. F-1 of that group's context, which mssa_pool_kv wrote to the
+  // group's pooled block.
+  const int64_t row_bytes = p.ld * p.elem_bytes;
+  const char* ws = static_cast<const char*>(workspace);
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  for (size_t g = 0; g < p.groups.size(); ++g) {
+    const int32_t sc = p.groups[g].scale;
+    if (sc == 1) continue;
+    const int64_t tok_s = frame_tokens(p, sc);
+    const size_t fbytes = static_cast<size_t>(tok_s * row_bytes);
+    for (const mssa::SegRow& r : p.segs) {
+      if (r.q_scale != sc || r.kind != mssa::kWin || r.frame >= p.desc.frames_per_state) continue;
+      if (r.buffer != mssa::kBufPooled || r.n_tok != tok_s)
+        return fail(MSSA_ERR_UNSUPPORTED, "head frames are not pooled to a coarse scale in this plan");
+      const size_t slot = static_cast<size_t>(slots[r.frame]);
+      mssa_status s = check_device(
+          hipMemcpyAsync(static_cast<char*>(k_ring_pooled[g]) + slot * fbytes,
+                         ws + p.pooled_k_off[g] + r.tok_offset * row_bytes, fbytes, hipMemcpyDeviceToDevice, st),
+          "pooled history append (K)");
+      if (s != MSSA_OK) return s;
+      s = check_device(
+          hipMemcpyAsync(static_cast<char*>(v_ring_pooled[g]) + slot * fbytes,
+                         ws + p.pooled_v_off[g] + r.tok_offset * row_bytes, fbytes, hipMemcpyDeviceToDevice, st),
+          "pooled history append (V)");
+      if (s != MSSA_OK) return s;
+    }
+  }
   return MSSA_OK;
+}
+
+mssa_status mssa_pool_hist_ring(mssa_plan plan, const void* k_ring, const void* v_ring, void* const* k_ring_pooled,
+                                void* const* v_ring_pooled, void* stream) {
+  if (!plan) return fail(MSSA_ERR_INVALID_ARG, "plan must be non-null");
+  const mssa::Plan& p = plan->p;
+  if (!p.hist_ring)
+    return fail(MSSA_ERR_UNSUPPORTED, "plan lacks MSSA_PLAN_POOLED_HIST_RING");
+  if (p.n_hist_tok == 0) return MSSA_OK;
+  if (!k_ring || !v_ring || !k_ring_pooled || !v_ring_pooled) return fail(MSSA_ERR_INVALID_ARG, "null argument");
+  if (!aligned16(k_ring) || !aligned16(v_ring)) return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
+  std::vector<mssa::PoolJobArgs> jobs;
+  for (size_t g = 0; g < p.groups.size(); ++g) {
+    const int32_t sc = p.groups[g].scale;
+    if (sc == 1) continue;
+    if (!k_ring_pooled[g] || !v_ring_pooled[g])
+      return fail(MSSA_ERR_INVALID_ARG, "null pooled-history ring for a coarse query scale");
+    if (!aligned16(k_ring_pooled[g]) || !aligned16(v_ring_pooled[g]))
+      return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
+    mssa::PoolJobArgs A{};
+    A.src_k = k_ring;
+    A.src_v = v_ring;
+    A.dst_k = k_ring_pooled[g];
+    A.dst_v = v_ring_pooled[g];
+    A.src_gh = p.desc.grid_h;
+    A.src_gw = p.desc.grid_w;
+    A.factor = sc;
+    A.dst_gh = (p.desc.grid_h + sc - 1) / sc;
+    A.dst_gw = (p.desc.grid_w + sc - 1) / sc;
+    A.n_frames = p.desc.hist_frames;
+    jobs.push_back(A);
+  }
+  return launch_pool_jobs(p, jobs, stream);
 }
 
 const char* mssa_status_string(mssa_status s) {

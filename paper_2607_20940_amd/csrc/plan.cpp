@@ -49,6 +49,10 @@ mssa_status build_plan(const mssa_plan_desc& d, int slots, int ranges_override, 
     err = "softmax_scale must be finite";
     return MSSA_ERR_INVALID_ARG;
   }
+  if ((d.flags & ~MSSA_PLAN_POOLED_HIST_RING) != 0) {
+    err = "unknown plan flags";
+    return MSSA_ERR_INVALID_ARG;
+  }
   for (int l = 0; l < T; ++l) {
     if (!is_pow2(d.scales[l]) || d.scales[l] > 64) {
       err = "scales must be powers of two in [1, 64]";
@@ -66,6 +70,7 @@ mssa_status build_plan(const mssa_plan_desc& d, int slots, int ranges_override, 
 
   p = Plan{};
   p.desc = d;
+  p.hist_ring = (d.flags & MSSA_PLAN_POOLED_HIST_RING) != 0;
   p.softmax_scale = d.softmax_scale > 0.f ? d.softmax_scale
                                           : 1.0f / std::sqrt(static_cast<float>(d.head_dim));
   const int32_t F = d.frames_per_state;
@@ -132,7 +137,15 @@ mssa_status build_plan(const mssa_plan_desc& d, int slots, int ranges_override, 
       rows.push_back({s, kSink, f, 1, 1, 1, static_cast<int32_t>(p.tok1), 0, kBufSink, f * p.tok1});
     for (int f = 0; f < d.hist_frames; ++f) {
       SegRow r{s, kHist, f, 1, s, s, static_cast<int32_t>(tok_at(s)), 0, kBufHist, f * p.tok1};
-      if (s > 1) { r.buffer = kBufPooled; r.tok_offset = pooled; pooled += r.n_tok; hist_read = true; }
+      if (s > 1 && p.hist_ring) {
+        r.buffer = kBufHistPooled;
+        r.tok_offset = f * r.n_tok;
+      } else if (s > 1) {
+        r.buffer = kBufPooled;
+        r.tok_offset = pooled;
+        pooled += r.n_tok;
+        hist_read = true;
+      }
       rows.push_back(r);
     }
     for (size_t i = 0; i < wf.size(); ++i) {

@@ -14,7 +14,9 @@ namespace mssa {
 enum Kind : int32_t { kSink = 0, kHist = 1, kWin = 2 };
 
 // Where a run of context tokens lives.
-enum Buffer : int32_t { kBufSink = 0, kBufHist = 1, kBufWin = 2, kBufPooled = 3 };
+// kBufHistPooled: the caller's pooled-history ring of the group (plans with
+// MSSA_PLAN_POOLED_HIST_RING), frame f at token f * tok_s.
+enum Buffer : int32_t { kBufSink = 0, kBufHist = 1, kBufWin = 2, kBufPooled = 3, kBufHistPooled = 4 };
 
 struct GridRow {
   int32_t scale, gh, gw, tok;
@@ -57,6 +59,7 @@ struct PoolJob {
 
 struct Plan {
   mssa_plan_desc desc;
+  bool hist_ring;  // MSSA_PLAN_POOLED_HIST_RING
   float softmax_scale;
   int64_t tok1;  // native tokens per frame
   int64_t n_q, n_sink_tok, n_hist_tok;

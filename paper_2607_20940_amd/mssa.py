@@ -18,11 +18,12 @@ MSSA_MAX_STATES = 8
 MSSA_OK, MSSA_ERR_INVALID_ARG, MSSA_ERR_UNSUPPORTED = 0, 1, 2
 MSSA_ERR_WORKSPACE, MSSA_ERR_DEVICE, MSSA_ERR_NO_MEMORY = 3, 4, 5
 MSSA_BF16, MSSA_F32 = 0, 1
+MSSA_PLAN_POOLED_HIST_RING = 1
 
 # Every symbol include/libmssa.h declares.
 EXPORTS = ("mssa_plan_create", "mssa_plan_destroy", "mssa_plan_query", "mssa_plan_tables",
-           "mssa_pool_kv", "mssa_forward", "mssa_hist_append", "mssa_status_string",
-           "mssa_last_error")
+           "mssa_pool_kv", "mssa_forward", "mssa_hist_append", "mssa_pool_hist_ring",
+           "mssa_forward_ring", "mssa_hist_append_ring", "mssa_status_string", "mssa_last_error")
 
 
 class mssa_plan_desc(ctypes.Structure):
@@ -31,7 +32,7 @@ class mssa_plan_desc(ctypes.Structure):
                 ("frames_per_state", ctypes.c_int32), ("sink_frames", ctypes.c_int32),
                 ("hist_frames", ctypes.c_int32), ("num_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("dtype", ctypes.c_int32),
-                ("softmax_scale", ctypes.c_float)]
+                ("softmax_scale", ctypes.c_float), ("flags", ctypes.c_int32)]
 
 
 _I32S = ctypes.c_int32 * MSSA_MAX_STATES
@@ -67,12 +68,18 @@ def _load():
     lib.mssa_forward.argtypes = [P, V, V, V, V, V, V, V, V, I64, V, V]
     lib.mssa_hist_append.argtypes = [P, V, V, V, V, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32),
                                      ctypes.POINTER(ctypes.c_int32), V]
+    PP = ctypes.POINTER(ctypes.c_void_p)
+    lib.mssa_pool_hist_ring.argtypes = [P, V, V, PP, PP, V]
+    lib.mssa_forward_ring.argtypes = [P, V, V, V, V, V, PP, PP, V, V, V, I64, V, V]
+    lib.mssa_hist_append_ring.argtypes = [P, V, V, V, I64, V, V, PP, PP, ctypes.c_int32,
+                                          ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32), V]
     lib.mssa_status_string.argtypes = [ctypes.c_int]
     lib.mssa_status_string.restype = ctypes.c_char_p
     lib.mssa_last_error.argtypes = []
     lib.mssa_last_error.restype = ctypes.c_char_p
     for name in ("mssa_plan_create", "mssa_plan_query", "mssa_plan_tables", "mssa_pool_kv",
-                 "mssa_forward", "mssa_hist_append"):
+                 "mssa_forward", "mssa_hist_append", "mssa_pool_hist_ring", "mssa_forward_ring",
+                 "mssa_hist_append_ring"):
         getattr(lib, name).restype = ctypes.c_int
     runtimes = _loaded_hip_runtimes()
     if len(runtimes) > 1:
@@ -168,6 +175,7 @@ def make_desc(desc):
     dt = desc.get("dtype", "bf16")
     d.dtype = MSSA_BF16 if dt in ("bf16", MSSA_BF16) else MSSA_F32 if dt in ("f32", MSSA_F32) else int(dt)
     d.softmax_scale = float(desc.get("softmax_scale", 0.0) or 0.0)
+    d.flags = int(desc.get("flags", 0) or 0)
     return d
 
 
@@ -239,4 +247,38 @@ def mssa_hist_append(plan, k_win, v_win, k_ring, v_ring, ring, stream=None):
     _check(lib.mssa_hist_append(plan.handle, _ptr(k_win), _ptr(v_win), _ptr(k_ring), _ptr(v_ring),
                                 ring.cap, ctypes.byref(head), ctypes.byref(count), _stream(stream)),
            "mssa_hist_append")
+    ring.head, ring.count = head.value, count.value
+
+
+def _ptr_array(xs):
+    """Per-group pointer array (None entries -> NULL)."""
+    arr = (ctypes.c_void_p * max(1, len(xs)))()
+    for i, x in enumerate(xs):
+        arr[i] = _ptr(x)
+    return arr
+
+
+def mssa_pool_hist_ring(plan, k_ring, v_ring, k_ring_pooled, v_ring_pooled, stream=None):
+    _check(lib.mssa_pool_hist_ring(plan.handle, _ptr(k_ring), _ptr(v_ring), _ptr_array(k_ring_pooled),
+                                   _ptr_array(v_ring_pooled), _stream(stream)), "mssa_pool_hist_ring")
+
+
+def mssa_forward_ring(plan, q_win, k_sink, v_sink, k_hist, v_hist, k_hist_pooled, v_hist_pooled, k_win,
+                      v_win, workspace, out, workspace_bytes=None, stream=None):
+    wb = _nbytes(workspace) if workspace_bytes is None else int(workspace_bytes)
+    _check(lib.mssa_forward_ring(plan.handle, _ptr(q_win), _ptr(k_sink), _ptr(v_sink), _ptr(k_hist),
+                                 _ptr(v_hist), _ptr_array(k_hist_pooled), _ptr_array(v_hist_pooled),
+                                 _ptr(k_win), _ptr(v_win), _ptr(workspace), wb, _ptr(out),
+                                 _stream(stream)), "mssa_forward_ring")
+
+
+def mssa_hist_append_ring(plan, k_win, v_win, workspace, k_ring, v_ring, k_ring_pooled, v_ring_pooled, ring,
+                          workspace_bytes=None, stream=None):
+    wb = _nbytes(workspace) if workspace_bytes is None else int(workspace_bytes)
+    head = ctypes.c_int32(ring.head)
+    count = ctypes.c_int32(ring.count)
+    _check(lib.mssa_hist_append_ring(plan.handle, _ptr(k_win), _ptr(v_win), _ptr(workspace), wb,
+                                     _ptr(k_ring), _ptr(v_ring), _ptr_array(k_ring_pooled),
+                                     _ptr_array(v_ring_pooled), ring.cap, ctypes.byref(head),
+                                     ctypes.byref(count), _stream(stream)), "mssa_hist_append_ring")
     ring.head, ring.count = head.value, count.value

@@ -6,8 +6,19 @@ pass is: mssa_pool_kv (history and fine window frames resampled), then
 mssa_forward, then mssa_hist_append (the head state's native frames become
 the newest history frames, FIFO-capped).  The ring's valid frames are always
 slots [0, count), read as a plan whose hist_frames equals count; one plan per
-history length is kept.  This module only sequences library calls and owns
-device buffers (torch allocations); all arithmetic runs in the library.
+history length is kept.
+
+With pooled_ring=True each layer also keeps, for every coarser query scale,
+a ring of the history already pooled to that scale: mssa_pool_kv then pools
+only window frames, mssa_forward_ring reads those rings, and
+mssa_hist_append_ring moves the head state's pooled frames (computed by this
+pass's mssa_pool_kv) into them, so history is never pooled again.  The
+pooled rings hold exactly the bytes re-pooling would give; outputs agree
+with the plain path up to the attention kernel's rounding (key tiles fall
+differently around the separate pooled-history run).
+
+This module only sequences library calls and owns device buffers (torch
+allocations); all arithmetic runs in the library.
 """
 
 from . import mssa
@@ -15,10 +26,11 @@ from .workloads import input_shapes
 
 
 class StreamingMSSA:
-    def __init__(self, layer_desc, layers, hist_cap_frames, dtype="bf16", device="cuda"):
+    def __init__(self, layer_desc, layers, hist_cap_frames, dtype="bf16", device="cuda", pooled_ring=False):
         import torch
 
-        self.desc = dict(layer_desc)
+        self.pooled_ring = bool(pooled_ring)
+        self.desc = dict(layer_desc, flags=mssa.MSSA_PLAN_POOLED_HIST_RING if pooled_ring else 0)
         self.layers = int(layers)
         self.cap = int(hist_cap_frames)
         self.dtype = dtype
@@ -38,6 +50,19 @@ class StreamingMSSA:
         self.ring = [mssa.Ring(self.cap) for _ in range(self.layers)]
         self.k_sink = [None] * self.layers
         self.v_sink = [None] * self.layers
+        # Pooled-history rings [layer][group] (None for groups at scale 1).
+        self.k_pool = [[None] * info["n_groups"] for _ in range(self.layers)]
+        self.v_pool = [[None] * info["n_groups"] for _ in range(self.layers)]
+        if self.pooled_ring:
+            gh, gw = int(layer_desc["grid_h"]), int(layer_desc["grid_w"])
+            for g, sc in enumerate(info["group_scale"]):
+                if sc == 1:
+                    continue
+                tok_s = -(-gh // sc) * -(-gw // sc)
+                pshape = (self.cap * tok_s, nh, d)
+                for layer in range(self.layers):
+                    self.k_pool[layer][g] = torch.zeros(pshape, dtype=self.tdtype, device=device)
+                    self.v_pool[layer][g] = torch.zeros(pshape, dtype=self.tdtype, device=device)
 
     def plan(self, hist_frames):
         if hist_frames not in self._plans:
@@ -59,6 +84,9 @@ class StreamingMSSA:
             self.k_ring[layer][: n * self.tok1].copy_(k_hist)
             self.v_ring[layer][: n * self.tok1].copy_(v_hist)
         self.ring[layer] = mssa.Ring(self.cap, count=n, head=0)
+        if self.pooled_ring and n:
+            mssa.mssa_pool_hist_ring(self.plan(n), self.k_ring[layer], self.v_ring[layer],
+                                     self.k_pool[layer], self.v_pool[layer])
 
     def layer_pass(self, layer, q_win, k_win, v_win, out, stream=None):
         ring = self.ring[layer]
@@ -67,10 +95,18 @@ class StreamingMSSA:
         kh = self.k_ring[layer][:nh] if nh else None
         vh = self.v_ring[layer][:nh] if nh else None
         mssa.mssa_pool_kv(plan, kh, vh, k_win, v_win, self.workspace, stream=stream)
-        mssa.mssa_forward(plan, q_win, self.k_sink[layer], self.v_sink[layer], kh, vh, k_win, v_win,
-                          self.workspace, out, stream=stream)
-        mssa.mssa_hist_append(plan, k_win, v_win, self.k_ring[layer], self.v_ring[layer], ring,
-                              stream=stream)
+        if self.pooled_ring:
+            mssa.mssa_forward_ring(plan, q_win, self.k_sink[layer], self.v_sink[layer], kh, vh,
+                                   self.k_pool[layer], self.v_pool[layer], k_win, v_win, self.workspace,
+                                   out, stream=stream)
+            mssa.mssa_hist_append_ring(plan, k_win, v_win, self.workspace, self.k_ring[layer],
+                                       self.v_ring[layer], self.k_pool[layer], self.v_pool[layer], ring,
+                                       stream=stream)
+        else:
+            mssa.mssa_forward(plan, q_win, self.k_sink[layer], self.v_sink[layer], kh, vh, k_win, v_win,
+                              self.workspace, out, stream=stream)
+            mssa.mssa_hist_append(plan, k_win, v_win, self.k_ring[layer], self.v_ring[layer], ring,
+                                  stream=stream)
 
 
 def init_inputs(stream_w, layer, shapes, device="cuda"):

@@ -156,3 +156,72 @@ def test_table_buffer_too_small():
     buf = (ctypes.c_int64 * 4)()
     st_ = mssa.lib.mssa_plan_tables(plan.handle, buf, 4, ctypes.byref(need))
     assert st_ == mssa.MSSA_ERR_INVALID_ARG and need.value > 4
+
+
+RING = mssa.MSSA_PLAN_POOLED_HIST_RING
+
+
+@pytest.mark.parametrize("name", ["wan13b_layer", "wan13b_longhist", "wan14b_720p"])
+def test_pooled_hist_ring_plan_same_context(name):
+    """A plan whose pooled history lives in the caller's rings has the same
+    context tables (the same Eq. 4 construction) and pools only window
+    frames: its workspace and pool traffic drop by the history's share."""
+    desc = WORKLOADS[name]["desc"]
+    plain, ring = _plan(desc), _plan(desc, flags=RING)
+    a, b = plain.tables(), ring.tables()
+    for key in ("GRID", "QGRP", "SEG", "TOTAL"):
+        assert np.array_equal(a[key], b[key]), key
+    ia, ib = plain.info(), ring.info()
+    assert ib["flops_alg"] == ia["flops_alg"]
+    nh, d = desc["num_heads"], desc["head_dim"]
+    tok1 = desc["grid_h"] * desc["grid_w"]
+    ld_bytes = nh * d * 2
+    hist_pooled = 0
+    for s in ia["group_scale"]:
+        if s > 1:
+            hist_pooled += desc["hist_frames"] * (-(-desc["grid_h"] // s)) * (-(-desc["grid_w"] // s))
+    assert ia["pool_bytes_alg"] - ib["pool_bytes_alg"] == 2 * (desc["hist_frames"] * tok1 + hist_pooled) * ld_bytes
+    for g, s in enumerate(ia["group_scale"]):
+        hp = desc["hist_frames"] * (-(-desc["grid_h"] // s)) * (-(-desc["grid_w"] // s)) if s > 1 else 0
+        assert ib["pooled_tokens"][g] == ia["pooled_tokens"][g] - hp
+    assert ib["workspace_bytes"] < ia["workspace_bytes"]
+
+
+def test_pooled_hist_ring_calls_checked():
+    """Ring entry points refuse plans without the flag and the plain ones
+    refuse ring plans, before anything is enqueued; unknown flags are
+    rejected at plan creation."""
+    desc = WORKLOADS["wan13b_layer"]["desc"]
+    with pytest.raises(mssa.MssaError) as e:
+        _plan(desc, flags=2)
+    assert e.value.status == mssa.MSSA_ERR_INVALID_ARG
+    plain, ring = _plan(desc), _plan(desc, flags=RING)
+    fake = 1 << 20
+    ws = ring.info()["workspace_bytes"]
+    pools = [None, fake]  # group 0 is scale 1, group 1 scale 2
+    with pytest.raises(mssa.MssaError) as e:
+        mssa.mssa_forward(ring, fake, fake, fake, fake, fake, fake, fake, fake, fake + 4096,
+                          workspace_bytes=ws, stream=0)
+    assert e.value.status == mssa.MSSA_ERR_UNSUPPORTED
+    with pytest.raises(mssa.MssaError) as e:
+        mssa.mssa_forward_ring(plain, fake, fake, fake, fake, fake, pools, pools, fake, fake, fake,
+                               fake + 4096, workspace_bytes=ws, stream=0)
+    assert e.value.status == mssa.MSSA_ERR_UNSUPPORTED
+    with pytest.raises(mssa.MssaError) as e:
+        mssa.mssa_forward_ring(ring, fake, fake, fake, fake, fake, [None, None], pools, fake, fake, fake,
+                               fake + 4096, workspace_bytes=ws, stream=0)
+    assert e.value.status == mssa.MSSA_ERR_INVALID_ARG
+    with pytest.raises(mssa.MssaError) as e:
+        mssa.mssa_hist_append_ring(plain, fake, fake, fake, fake, fake, pools, pools, mssa.Ring(21),
+                                   workspace_bytes=ws, stream=0)
+    assert e.value.status == mssa.MSSA_ERR_UNSUPPORTED
+    with pytest.raises(mssa.MssaError) as e:
+        mssa.mssa_hist_append_ring(ring, fake, fake, fake, fake, fake, [None, None], pools,
+                                   mssa.Ring(21), workspace_bytes=ws, stream=0)
+    assert e.value.status == mssa.MSSA_ERR_INVALID_ARG
+    with pytest.raises(mssa.MssaError) as e:
+        mssa.mssa_pool_hist_ring(plain, fake, fake, pools, pools, stream=0)
+    assert e.value.status == mssa.MSSA_ERR_UNSUPPORTED
+    with pytest.raises(mssa.MssaError) as e:
+        mssa.mssa_pool_hist_ring(ring, fake, fake, [None, None], pools, stream=0)
+    assert e.value.status == mssa.MSSA_ERR_INVALID_ARG

@@ -21,10 +21,11 @@ def _f64(t):
     return None if t is None else t.float().cpu().numpy().astype(np.float64)
 
 
-def _run(stream_w, layers, passes, check):
+def _run(stream_w, layers, passes, check, pooled_ring=False):
     desc = stream_w["layer"]
     F = desc["frames_per_state"]
-    st = StreamingMSSA(desc, layers, stream_w["hist_cap_frames"], dtype=stream_w["dtype"])
+    st = StreamingMSSA(desc, layers, stream_w["hist_cap_frames"], dtype=stream_w["dtype"],
+                       pooled_ring=pooled_ring)
     tok1 = st.tok1
     hist = {}
     init_shapes = st.shapes(stream_w["hist_start_frames"])
@@ -104,3 +105,72 @@ def test_streaming_wan13b_shape_sampled():
     st, n = _run(STREAMING, layers=2, passes=8, check=check)
     assert n == 3
     assert st.ring[0].count == 21 and st.ring[0].head == 9  # 6 + 8*3 = 30 frames -> 9 evicted
+
+
+SMALL = dict(STREAMING, layer=dict(num_states=3, scales=[1, 1, 2], grid_h=6, grid_w=8,
+                                   frames_per_state=2, sink_frames=1, hist_frames=0,
+                                   num_heads=2, head_dim=128),
+             hist_start_frames=2, hist_cap_frames=6, seed_base=40, init_seed_base=7000)
+
+
+def test_streaming_pooled_ring_small_every_output():
+    """The pooled-history-ring path against the oracle: every output of two
+    small layers through the ring's fill and wrap-arounds."""
+    st, n = _run(SMALL, layers=2, passes=7, check=lambda p, L: (None, None), pooled_ring=True)
+    assert n == 14
+    assert [r.head for r in st.ring] == [4, 4]
+
+
+@pytest.mark.parametrize("layer", [
+    SMALL["layer"],
+    # two coarse query scales, ragged at scale 4 (6x10 -> 2x3 cells of 3x3..)
+    dict(num_states=4, scales=[1, 2, 4, 4], grid_h=6, grid_w=10, frames_per_state=1, sink_frames=1,
+         hist_frames=0, num_heads=2, head_dim=64),
+])
+def test_streaming_pooled_ring_equals_plain(layer):
+    """Pooled history kept incrementally (pooled once, then appended from each
+    pass's own pooled window frames) holds exactly the bytes that pooling the
+    current native ring gives, through the ring's wrap-around; outputs agree
+    with the plain path up to the attention kernel's rounding (the history
+    is a run of its own there, so the key tiles fall differently)."""
+    from paper_2607_20940_amd import mssa
+    from gpu_common import errors
+
+    w = dict(SMALL, layer=layer, hist_cap_frames=5)
+    F = layer["frames_per_state"]
+    plain = StreamingMSSA(layer, 2, w["hist_cap_frames"], dtype="bf16")
+    ring = StreamingMSSA(layer, 2, w["hist_cap_frames"], dtype="bf16", pooled_ring=True)
+    shapes = plain.shapes(w["hist_start_frames"])
+    for L in range(2):
+        x = init_inputs(w, L, shapes)
+        plain.init_layer(L, x["k_sink"], x["v_sink"], x["k_hist"], x["v_hist"])
+        ring.init_layer(L, x["k_sink"], x["v_sink"], x["k_hist"], x["v_hist"])
+    win_shapes = plain.shapes(0)
+    for p in range(8):
+        wins = window_inputs(w, p, 2, win_shapes)
+        for L in range(2):
+            a = torch.empty_like(wins[L]["q_win"])
+            b = torch.empty_like(wins[L]["q_win"])
+            plain.layer_pass(L, wins[L]["q_win"], wins[L]["k_win"], wins[L]["v_win"], a)
+            ring.layer_pass(L, wins[L]["q_win"], wins[L]["k_win"], wins[L]["v_win"], b)
+            torch.cuda.synchronize()
+            rg = ring.ring[L]
+            print(f"[stream-ring] pass {p} layer {L} hist {rg.count} head {rg.head}", flush=True)
+            assert rg.count == plain.ring[L].count and rg.head == plain.ring[L].head
+            e = errors(b.float().cpu().numpy().astype(np.float64), a.float().cpu().numpy().astype(np.float64))
+            assert e["max_abs"] <= 1e-2 * float(a.float().abs().max()), (p, L, e)
+            # the incrementally kept pooled rings == the native ring pooled afresh
+            plan = ring.plan(rg.count)
+            fresh_k = [None if t is None else torch.zeros_like(t) for t in ring.k_pool[L]]
+            fresh_v = [None if t is None else torch.zeros_like(t) for t in ring.v_pool[L]]
+            mssa.mssa_pool_hist_ring(plan, ring.k_ring[L], ring.v_ring[L], fresh_k, fresh_v)
+            torch.cuda.synchronize()
+            for g, t in enumerate(ring.k_pool[L]):
+                if t is None:
+                    continue
+                n = rg.count * t.shape[0] // w["hist_cap_frames"]
+                assert torch.equal(t[:n].view(torch.int16), fresh_k[g][:n].view(torch.int16)), (p, L, g)
+                assert torch.equal(ring.v_pool[L][g][:n].view(torch.int16),
+                                   fresh_v[g][:n].view(torch.int16)), (p, L, g)
+    assert plain.ring[0].count == w["hist_cap_frames"]
+    assert (w["hist_start_frames"] + 8 * F) > w["hist_cap_frames"]
