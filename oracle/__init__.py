@@ -8,6 +8,6 @@ from .mssa_oracle import (  # noqa: F401
     KIND_HIST, KIND_SINK, KIND_WIN, algorithmic_flops, attention,
     brute_force_attention, context, context_rows, frame_tokens, grid,
     mssa_attention, num_hist_tokens, num_sink_tokens, num_window_tokens,
-    pool_frame, pooled_kv, query_groups, scales_in_use, softmax_scale, tables,
+    pool_frame, pooled_kv, query_groups, resample_mode, scales_in_use, softmax_scale, tables,
     window_frames,
 )

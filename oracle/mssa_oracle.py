@@ -27,7 +27,11 @@ What is computed (Ms. Forcing, Sec. 4.1):
 * "Subsample" is read as a 2-D spatial average pool over each f x f block of
   the frame's own grid, f = max(1, s / p_b), averaging only the cells that
   exist on a ragged edge (Sec. 3.2 uses the 2 x 2 block mean as the
-  coarse-token proxy).
+  coarse-token proxy).  The literal strided reading of Eq. 4 (and of the
+  stride-2 probe of Sec. 3.2) is the variant resample="stride": each f x f
+  block is represented by its first (top-left) cell, i.e. rows and columns
+  0, f, 2f, ... of the frame's grid, which on a ragged grid also gives the
+  ceil(gh/f) x ceil(gw/f) grid.
 * Attention: softmax(scale * q k^T) v over the whole context, per head, no
   mask inside the context, no bias for pooled tokens.
 
@@ -37,7 +41,8 @@ arithmetic is float64 on the exact input values the GPU receives.
 A descriptor is a mapping with the keys
     num_states, scales, grid_h, grid_w, frames_per_state, sink_frames,
     hist_frames, num_heads, head_dim, softmax_scale (optional, <= 0 or absent
-    means 1/sqrt(head_dim)).
+    means 1/sqrt(head_dim)), resample (optional, "mean" (default) or
+    "stride").
 Tensors are token-major arrays [tokens, heads, head_dim].
 """
 
@@ -57,6 +62,15 @@ def _ceil_div(a, b):
 
 def _scales(desc):
     return [int(s) for s in desc["scales"][: int(desc["num_states"])]]
+
+
+def resample_mode(desc):
+    """How a frame is brought to a coarser scale: "mean" (block average) or
+    "stride" (first cell of each block)."""
+    m = desc.get("resample", "mean")
+    if m not in ("mean", "stride"):
+        raise ValueError("resample must be 'mean' or 'stride'")
+    return m
 
 
 def softmax_scale(desc):
@@ -162,9 +176,11 @@ def tables(desc):
     }
 
 
-def pool_frame(x, gh, gw, f):
-    """Average pool of one frame's tokens x [gh*gw, ...] over f x f blocks of
-    its grid; a block on a ragged edge averages only the cells it holds."""
+def pool_frame(x, gh, gw, f, mode="mean"):
+    """Resample one frame's tokens x [gh*gw, ...] over f x f blocks of its
+    grid.  mode "mean": block average, a block on a ragged edge averaging only
+    the cells it holds.  mode "stride": the block's first cell (grid row f*Y,
+    column f*X), which always exists."""
     x = np.asarray(x, dtype=np.float64)
     if f == 1:
         return x.copy()
@@ -173,8 +189,11 @@ def pool_frame(x, gh, gw, f):
     out = np.empty((oh, ow) + x.shape[1:], dtype=np.float64)
     for Y in range(oh):
         for X in range(ow):
-            block = img[f * Y: f * Y + f, f * X: f * X + f]
-            out[Y, X] = block.reshape(-1, *x.shape[1:]).mean(axis=0)
+            if mode == "stride":
+                out[Y, X] = img[f * Y, f * X]
+            else:
+                block = img[f * Y: f * Y + f, f * X: f * X + f]
+                out[Y, X] = block.reshape(-1, *x.shape[1:]).mean(axis=0)
     return out.reshape(oh * ow, *x.shape[1:])
 
 
@@ -187,6 +206,7 @@ def context(desc, s, x_sink, x_hist, x_win):
     """Concatenated K (or V) context for queries at scale s, float64, in
     the canonical row order of context_rows()."""
     parts = []
+    mode = resample_mode(desc)
     n1 = frame_tokens(desc, 1)
     gh1, gw1 = grid(desc, 1)
     wf = {w: (p, first, n) for (w, _, p, first, n) in window_frames(desc)}
@@ -194,11 +214,11 @@ def context(desc, s, x_sink, x_hist, x_win):
         if kind == KIND_SINK:
             parts.append(np.asarray(x_sink[frame * n1: (frame + 1) * n1], dtype=np.float64))
         elif kind == KIND_HIST:
-            parts.append(pool_frame(hist_frame(desc, x_hist, frame), gh1, gw1, fac))
+            parts.append(pool_frame(hist_frame(desc, x_hist, frame), gh1, gw1, fac, mode))
         else:
             p, first, nsrc = wf[frame]
             gh, gw = grid(desc, p)
-            parts.append(pool_frame(x_win[first: first + nsrc], gh, gw, fac))
+            parts.append(pool_frame(x_win[first: first + nsrc], gh, gw, fac, mode))
     return np.concatenate(parts, axis=0)
 
 
@@ -224,6 +244,7 @@ def pooled_kv(desc, x_hist, x_win):
     float64 tokens: history frames and window frames resampled to each query
     scale coarser than their own."""
     out = {}
+    mode = resample_mode(desc)
     n1 = frame_tokens(desc, 1)
     gh1, gw1 = grid(desc, 1)
     for (s, _, _) in query_groups(desc):
@@ -232,11 +253,11 @@ def pooled_kv(desc, x_hist, x_win):
                 continue
             if kind == KIND_HIST:
                 out[(kind, frame, eff)] = pool_frame(
-                    x_hist[frame * n1: (frame + 1) * n1], gh1, gw1, fac)
+                    x_hist[frame * n1: (frame + 1) * n1], gh1, gw1, fac, mode)
             else:
                 p, first, nsrc = {w: (p, f0, nn) for (w, _, p, f0, nn) in window_frames(desc)}[frame]
                 gh, gw = grid(desc, p)
-                out[(kind, frame, eff)] = pool_frame(x_win[first: first + nsrc], gh, gw, fac)
+                out[(kind, frame, eff)] = pool_frame(x_win[first: first + nsrc], gh, gw, fac, mode)
     return out
 
 
@@ -289,6 +310,7 @@ def brute_force_attention(desc, q_win, k_sink, v_sink, k_hist, v_hist, k_win, v_
     Hh = int(desc["hist_frames"])
     nh, d = int(desc["num_heads"]), int(desc["head_dim"])
     sc = softmax_scale(desc)
+    pick_first = resample_mode(desc) == "stride"
 
     def cells(s):
         return (H + s - 1) // s, (W + s - 1) // s
@@ -309,6 +331,8 @@ def brute_force_attention(desc, q_win, k_sink, v_sink, k_hist, v_hist, k_win, v_
         for dy in range(f):
             for dx in range(f):
                 r, c = f * Y + dy, f * X + dx
+                if pick_first and (dy or dx):
+                    continue
                 if r < src_gh and c < src_gw:
                     t = base + r * src_gw + c
                     for j in range(d):

@@ -199,6 +199,72 @@ def test_two_stage_pool_equals_direct_when_divisible():
     assert np.allclose(two, oracle.pool_frame(x, 8, 12, 4), atol=1e-14)
 
 
+# ------------------------------------------------- strided-subsample variant
+
+
+@settings(max_examples=60, deadline=None)
+@given(gh=st.integers(1, 11), gw=st.integers(1, 11), f=st.sampled_from([1, 2, 4, 8]),
+       seed=st.integers(0, 1000))
+def test_stride_pool_is_grid_slicing(gh, gw, f, seed):
+    """Stride f keeps grid rows and columns 0, f, 2f, ...: numpy's img[::f, ::f]."""
+    x = np.random.default_rng(seed).standard_normal((gh * gw, 2, 3))
+    y = oracle.pool_frame(x, gh, gw, f, "stride")
+    ref = x.reshape(gh, gw, 2, 3)[::f, ::f].reshape(-1, 2, 3)
+    assert np.array_equal(y, ref)
+
+
+def test_stride_two_stage_equals_direct_on_every_grid():
+    """Two stride-2 steps are one stride-4 step on any grid, ragged 3 mod 4
+    included (where the block mean's two-stage route differs)."""
+    rng = np.random.default_rng(8)
+    for gh, gw in [(8, 12), (7, 11), (3, 5), (15, 26)]:
+        x = rng.standard_normal((gh * gw, 1, 2))
+        one = oracle.pool_frame(oracle.pool_frame(x, gh, gw, 2, "stride"), -(-gh // 2), -(-gw // 2), 2, "stride")
+        assert np.array_equal(one, oracle.pool_frame(x, gh, gw, 4, "stride"))
+    x = rng.standard_normal((7 * 11, 1, 2))
+    two = oracle.pool_frame(oracle.pool_frame(x, 7, 11, 2), 4, 6, 2)
+    assert not np.allclose(two, oracle.pool_frame(x, 7, 11, 4))
+
+
+@settings(max_examples=30, deadline=None)
+@given(gh=st.integers(1, 9), gw=st.integers(1, 9), f=st.sampled_from([2, 4]), seed=st.integers(0, 1000))
+def test_stride_equals_mean_on_block_constant_fields(gh, gw, f, seed):
+    """A field constant on every f x f block (ragged edge blocks included)
+    has its block mean equal to its first cell."""
+    oh, ow = -(-gh // f), -(-gw // f)
+    c = np.random.default_rng(seed).standard_normal((oh, ow, 1, 2))
+    x = np.repeat(np.repeat(c, f, axis=0), f, axis=1)[:gh, :gw].reshape(gh * gw, 1, 2)
+    assert np.allclose(oracle.pool_frame(x, gh, gw, f, "stride"), oracle.pool_frame(x, gh, gw, f), atol=1e-14)
+
+
+def test_stride_variant_keeps_tables_and_changes_outputs():
+    """Eq. 5 counts only tokens, so both readings of Subsample give the same
+    plan; the outputs differ once a frame is resampled."""
+    desc = _desc(3, [1, 2, 4], 6, 9, F=2, S=1, Hh=2, nh=1, d=8)
+    sdesc = dict(desc, resample="stride")
+    a, b = oracle.tables(desc), oracle.tables(sdesc)
+    for k in a:
+        assert np.array_equal(a[k], b[k])
+    x = _rand_inputs(desc, 6)
+    assert not np.allclose(_run(desc, x), _run(sdesc, x))
+    with pytest.raises(ValueError):
+        oracle.resample_mode(dict(desc, resample="max"))
+
+
+@settings(max_examples=10, deadline=None)
+@given(H=st.integers(1, 7), W=st.integers(1, 7),
+       sched=st.lists(st.sampled_from([1, 2, 4]), min_size=1, max_size=3).map(sorted),
+       F=st.integers(1, 2), S=st.integers(0, 1), Hh=st.integers(0, 2),
+       seed=st.integers(0, 10000))
+def test_stride_matches_brute_force_tiny(H, W, sched, F, S, Hh, seed):
+    desc = dict(_desc(len(sched), sched, H, W, F=F, S=S, Hh=Hh, nh=2, d=3), resample="stride")
+    x = _rand_inputs(desc, seed)
+    a = _run(desc, x)
+    b = oracle.brute_force_attention(desc, x["q_win"], x["k_sink"], x["v_sink"], x["k_hist"],
+                                     x["v_hist"], x["k_win"], x["v_win"])
+    assert np.allclose(a, b, atol=1e-12, rtol=0)
+
+
 # ---------------------------------------------------------------- attention
 
 
