@@ -81,6 +81,14 @@ typedef struct {
  * mssa_pool_kv and is run with mssa_forward_ring / mssa_hist_append_ring. */
 #define MSSA_PLAN_POOLED_HIST_RING 1
 
+/* Plan flag: resample by stride instead of by block mean (the literal reading
+ * of Eq. 4's Subsample and of the stride-2 probe of Sec. 3.2).  Every pooled
+ * token is the first cell (row f*Y, column f*X) of its f x f block on the
+ * source frame's grid, copied bit for bit.  Grids, context tables and
+ * attention are unchanged; only what mssa_pool_kv / mssa_pool_hist_ring write
+ * differs.  Combines with MSSA_PLAN_POOLED_HIST_RING. */
+#define MSSA_PLAN_STRIDED_SUBSAMPLE 2
+
 /* Sizes derived by the plan.  Group g is the g-th distinct query scale in
  * window token order; its queries are the contiguous range
  * [q_begin[g], q_end[g]) and its context has n_kv[g] tokens per head.

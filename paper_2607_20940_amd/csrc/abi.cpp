@@ -60,6 +60,7 @@ mssa_status launch_pool_jobs(const mssa::Plan& p, std::vector<mssa::PoolJobArgs>
   mssa::PoolArgs a{};
   a.ld = p.ld;
   a.chunks_per_tok = static_cast<int32_t>(p.ld * p.elem_bytes / 16);
+  a.pick_first = p.strided ? 1 : 0;
   size_t j0 = 0;
   while (j0 < jobs.size()) {
     const size_t nj = std::min<size_t>(mssa::kMaxPoolJobs, jobs.size() - j0);

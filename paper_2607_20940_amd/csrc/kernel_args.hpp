@@ -76,6 +76,8 @@ struct PoolArgs {
   int64_t ld;               // elements between tokens
   int32_t chunks_per_tok;   // 16-byte chunks per token (all heads)
   int32_t n_jobs;
+  int32_t pick_first;       // 1: copy each block's first cell (stride); 0: block mean
+  int32_t pad;
   PoolJobArgs jobs[kMaxPoolJobs];
 };
 

@@ -49,7 +49,7 @@ mssa_status build_plan(const mssa_plan_desc& d, int slots, int ranges_override, 
     err = "softmax_scale must be finite";
     return MSSA_ERR_INVALID_ARG;
   }
-  if ((d.flags & ~MSSA_PLAN_POOLED_HIST_RING) != 0) {
+  if ((d.flags & ~(MSSA_PLAN_POOLED_HIST_RING | MSSA_PLAN_STRIDED_SUBSAMPLE)) != 0) {
     err = "unknown plan flags";
     return MSSA_ERR_INVALID_ARG;
   }
@@ -71,6 +71,7 @@ mssa_status build_plan(const mssa_plan_desc& d, int slots, int ranges_override, 
   p = Plan{};
   p.desc = d;
   p.hist_ring = (d.flags & MSSA_PLAN_POOLED_HIST_RING) != 0;
+  p.strided = (d.flags & MSSA_PLAN_STRIDED_SUBSAMPLE) != 0;
   p.softmax_scale = d.softmax_scale > 0.f ? d.softmax_scale
                                           : 1.0f / std::sqrt(static_cast<float>(d.head_dim));
   const int32_t F = d.frames_per_state;
@@ -262,13 +263,15 @@ mssa_status build_plan(const mssa_plan_desc& d, int slots, int ranges_override, 
   }
   p.workspace_bytes = ws;
 
-  // Algorithmic pool traffic: each pooled source frame read once, each
-  // pooled frame written once, for K and V.
+  // Algorithmic pool traffic, K and V: block mean, each pooled source frame
+  // read once and each pooled frame written once; stride, each pooled token
+  // reads the one source token it copies.
+  int64_t write_tok = 0;
+  for (int64_t t : p.pooled_tokens) write_tok += t;
   int64_t read_tok = hist_read ? p.n_hist_tok : 0;
   for (size_t i = 0; i < wf.size(); ++i)
     if (win_read[i]) read_tok += wf[i].n;
-  int64_t write_tok = 0;
-  for (int64_t t : p.pooled_tokens) write_tok += t;
+  if (p.strided) read_tok = write_tok;
   p.pool_bytes_alg = 2 * (read_tok + write_tok) * p.ld * p.elem_bytes;
   return MSSA_OK;
 }

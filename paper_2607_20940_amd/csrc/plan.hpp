@@ -60,6 +60,7 @@ struct PoolJob {
 struct Plan {
   mssa_plan_desc desc;
   bool hist_ring;  // MSSA_PLAN_POOLED_HIST_RING
+  bool strided;    // MSSA_PLAN_STRIDED_SUBSAMPLE: first cell of each block
   float softmax_scale;
   int64_t tok1;  // native tokens per frame
   int64_t n_q, n_sink_tok, n_hist_tok;

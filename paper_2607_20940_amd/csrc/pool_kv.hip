@@ -1,7 +1,10 @@
 // K/V resampling for MSSA (Ms. Forcing, Sec. 4.1, Eq. 4 "Subsample", read
 // as a 2-D average pool; Sec. 3.2 uses the 2 x 2 block mean as the coarse
 // token).  Each output cell averages the cells of its f x f block that exist
-// on the source frame's grid, per head and channel, for K and V alike.
+// on the source frame's grid, per head and channel, for K and V alike.  The
+// strided variant (Eq. 4 read literally; the stride-2 probe of Sec. 3.2)
+// copies the block's first cell instead: the same loop over a 1 x 1 block,
+// whose sum divided by 1 is the source value exactly.
 //
 // HBM-bound: every source byte is read once per output scale and every
 // pooled byte written once.  One thread produces one 16-byte chunk of one
@@ -49,8 +52,8 @@ __global__ __launch_bounds__(kPoolThreads) void pool_kernel(PoolArgs a) {
   const T* src = static_cast<const T*>(blockIdx.y == 0 ? J.src_k : J.src_v);
   T* dst = static_cast<T*>(blockIdx.y == 0 ? J.dst_k : J.dst_v);
   const int f = J.factor;
-  const int rows = min(f, J.src_gh - f * Y);
-  const int cols = min(f, J.src_gw - f * X);
+  const int rows = a.pick_first ? 1 : min(f, J.src_gh - f * Y);
+  const int cols = a.pick_first ? 1 : min(f, J.src_gw - f * X);
   const T* base = src + (fr * J.src_gh * J.src_gw + static_cast<int64_t>(f * Y) * J.src_gw + f * X) * a.ld +
                   chunk * N;
   float acc[N];

@@ -19,6 +19,7 @@ MSSA_OK, MSSA_ERR_INVALID_ARG, MSSA_ERR_UNSUPPORTED = 0, 1, 2
 MSSA_ERR_WORKSPACE, MSSA_ERR_DEVICE, MSSA_ERR_NO_MEMORY = 3, 4, 5
 MSSA_BF16, MSSA_F32 = 0, 1
 MSSA_PLAN_POOLED_HIST_RING = 1
+MSSA_PLAN_STRIDED_SUBSAMPLE = 2
 
 # Every symbol include/libmssa.h declares.
 EXPORTS = ("mssa_plan_create", "mssa_plan_destroy", "mssa_plan_query", "mssa_plan_tables",
@@ -176,6 +177,11 @@ def make_desc(desc):
     d.dtype = MSSA_BF16 if dt in ("bf16", MSSA_BF16) else MSSA_F32 if dt in ("f32", MSSA_F32) else int(dt)
     d.softmax_scale = float(desc.get("softmax_scale", 0.0) or 0.0)
     d.flags = int(desc.get("flags", 0) or 0)
+    resample = desc.get("resample", "mean")
+    if resample not in ("mean", "stride"):
+        raise ValueError("resample must be 'mean' or 'stride'")
+    if resample == "stride":
+        d.flags |= MSSA_PLAN_STRIDED_SUBSAMPLE
     return d
 
 

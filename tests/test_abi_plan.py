@@ -187,13 +187,34 @@ def test_pooled_hist_ring_plan_same_context(name):
     assert ib["workspace_bytes"] < ia["workspace_bytes"]
 
 
+@pytest.mark.parametrize("name", ["tiny_f32", "wan13b_layer", "wan13b_longhist", "wan14b_720p"])
+def test_strided_plan_same_tables(name):
+    """The strided-subsample plan builds the same Eq. 4 context (tables,
+    workspace, FLOP) as the block-mean plan, equal to the oracle's tables for
+    resample="stride"; its pool reads one source token per pooled token."""
+    desc = WORKLOADS[name]["desc"]
+    mean, stride = _plan(desc), _plan(desc, resample="stride")
+    a, b = mean.tables(), stride.tables()
+    want = oracle.tables(dict(desc, resample="stride"))
+    for key in ("GRID", "QGRP", "SEG", "TOTAL"):
+        assert np.array_equal(a[key], b[key]), key
+        assert np.array_equal(b[key].reshape(want[key].shape), want[key]), key
+    ia, ib = mean.info(), stride.info()
+    for key in ("flops_alg", "workspace_bytes", "pooled_tokens", "n_kv"):
+        assert ia[key] == ib[key], key
+    row = desc["num_heads"] * desc["head_dim"] * 2  # bf16 plan
+    assert ib["pool_bytes_alg"] == 2 * 2 * sum(ib["pooled_tokens"]) * row
+    with pytest.raises(ValueError):
+        _plan(desc, resample="max")
+
+
 def test_pooled_hist_ring_calls_checked():
     """Ring entry points refuse plans without the flag and the plain ones
     refuse ring plans, before anything is enqueued; unknown flags are
     rejected at plan creation."""
     desc = WORKLOADS["wan13b_layer"]["desc"]
     with pytest.raises(mssa.MssaError) as e:
-        _plan(desc, flags=2)
+        _plan(desc, flags=4)
     assert e.value.status == mssa.MSSA_ERR_INVALID_ARG
     plain, ring = _plan(desc), _plan(desc, flags=RING)
     fake = 1 << 20

@@ -199,3 +199,61 @@ def test_full_size_sampled(name):
         assert_close(np.zeros_like(ref), ref, w["dtype"])
     if name == "wan13b_layer":
         _check_pool(r, name)
+
+
+# ------------------------------------------------------------------ strided-subsample variant
+
+
+def _check_pool_exact(r, label):
+    """Strided pooled blocks are copies of source tokens: bit-equal to the
+    oracle's picks of the same input values."""
+    x = r.oracle_inputs()
+    want = {"k": oracle.pooled_kv(r.desc, x["k_hist"], x["k_win"]),
+            "v": oracle.pooled_kv(r.desc, x["v_hist"], x["v_win"])}
+    n = 0
+    for g, s in enumerate(r.info["group_scale"]):
+        if r.info["pooled_tokens"][g] == 0:
+            continue
+        rows = [row for row in oracle.context_rows(r.desc, s) if row[0] != oracle.KIND_SINK and row[4] > 1]
+        for which in ("k", "v"):
+            ref = np.concatenate([want[which][(row[0], row[1], row[3])] for row in rows])
+            got = r.pooled(g, which)
+            assert got.shape == ref.shape
+            assert np.array_equal(got, ref), f"{label}: strided pooled {which} of group {g} differs"
+            n += got.size
+    assert n > 0
+    print(f"[parity] {label} strided pool bit-exact over {n} values", flush=True)
+
+
+@pytest.mark.parametrize("name", ["ragged_3level_d128", "ragged_3level_d64", "paper_schedule_small",
+                                  "eight_states", "tiny_runs"])
+def test_stride_small_full(name):
+    desc, seed = SMALL[name]
+    r = _full_check(dict(desc, resample="stride"), "bf16", seed, AMP, f"stride_{name}")
+    _check_pool_exact(r, f"stride_{name}")
+
+
+def test_stride_f32():
+    r = _full_check(dict(_desc(3, [1, 2, 4], 7, 11, F=2, S=1, Hh=2, nh=2, d=64), resample="stride"),
+                    "f32", 22, 1.0, "stride_f32")
+    _check_pool_exact(r, "stride_f32")
+
+
+def test_stride_full_size_sampled():
+    """Long history with ragged 4x resampling (30x52 -> 8x13), strided."""
+    w = WORKLOADS["wan13b_longhist"]
+    desc = dict(w["desc"], resample="stride")
+    r = GpuRun(desc, w["dtype"], w["seed"], w["amplitude"])
+    r.run()
+    rng = np.random.default_rng(321)
+    rows = _sample_rows(r.info, rng)
+    heads = [0, 5, 11]
+    ref = r.oracle(heads=heads, q_index=rows)[rows]
+    e = assert_close(r.output()[rows][:, heads], ref, w["dtype"], "stride_wan13b_longhist")
+    print(f"[parity] stride wan13b_longhist rows={len(rows)} {e}", flush=True)
+    _check_pool_exact(r, "stride_wan13b_longhist")
+    # the variant is not the block mean: the outputs differ measurably
+    m = dict(w["desc"])
+    rm = GpuRun(m, w["dtype"], w["seed"], w["amplitude"])
+    rm.run()
+    assert not np.array_equal(rm.output()[rows], r.output()[rows])

@@ -121,11 +121,22 @@ def test_streaming_pooled_ring_small_every_output():
     assert [r.head for r in st.ring] == [4, 4]
 
 
+def test_streaming_pooled_ring_stride_every_output():
+    """Strided subsampling through the pooled-ring path, every output against
+    the oracle's stride reading."""
+    w = dict(SMALL, layer=dict(SMALL["layer"], resample="stride"))
+    st, n = _run(w, layers=2, passes=7, check=lambda p, L: (None, None), pooled_ring=True)
+    assert n == 14
+
+
 @pytest.mark.parametrize("layer", [
     SMALL["layer"],
     # two coarse query scales, ragged at scale 4 (6x10 -> 2x3 cells of 3x3..)
     dict(num_states=4, scales=[1, 2, 4, 4], grid_h=6, grid_w=10, frames_per_state=1, sink_frames=1,
          hist_frames=0, num_heads=2, head_dim=64),
+    # the same with strided subsampling
+    dict(num_states=4, scales=[1, 2, 4, 4], grid_h=6, grid_w=10, frames_per_state=1, sink_frames=1,
+         hist_frames=0, num_heads=2, head_dim=64, resample="stride"),
 ])
 def test_streaming_pooled_ring_equals_plain(layer):
     """Pooled history kept incrementally (pooled once, then appended from each
