@@ -11,3 +11,4 @@ from .mssa_oracle import (  # noqa: F401
     pool_frame, pooled_kv, query_groups, resample_mode, scales_in_use, softmax_scale, tables,
     window_frames,
 )
+from .mssa_backward import attention_backward, mssa_backward, pool_frame_adjoint  # noqa: F401,E402
