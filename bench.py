@@ -165,6 +165,84 @@ def bench_streaming(args):
     print(json.dumps(result), flush=True)
 
 
+def bench_training(args):
+    """One training step of one layer's MSSA: mssa_pool_kv, mssa_forward_lse
+    and mssa_backward (all seven input gradients) on one workspace.  The
+    backward's algorithmic work is 2.5x the forward's (the products
+    P^T dO, dO V^T, dS K and dS^T Q besides Q K^T), the usual count; the dQ
+    kernel's recomputation of Q K^T and dO V^T is overhead, not work."""
+    import torch
+
+    from paper_2607_20940_amd import mssa
+    from paper_2607_20940_amd.inputs import make_grad_output, make_inputs
+    from paper_2607_20940_amd.workloads import WORKLOADS, input_shapes
+
+    w = dict(WORKLOADS[args.workload], name=args.workload)
+    desc, dtype = w["desc"], w["dtype"]
+    plan = mssa.mssa_plan_create(dict(desc, dtype=dtype))
+    info = plan.info()
+    shapes = input_shapes(desc, info["n_q"], info["n_sink_tok"], info["n_hist_tok"])
+    x = make_inputs(shapes, w["seed"], w["amplitude"], dtype)
+    go = make_grad_output(shapes["q_win"], w["seed"] + 7919, 1.0, dtype)
+
+    def dev(a):
+        if a is None:
+            return None
+        if dtype == "bf16":
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
+        return torch.from_numpy(a).cuda()
+
+    d = {k: dev(v) for k, v in x.items()}
+    g_out = dev(go)
+    ws = torch.empty(mssa.mssa_backward_workspace_size(plan), dtype=torch.uint8, device="cuda")
+    out = torch.empty_like(d["q_win"])
+    lse = torch.empty(desc["num_heads"] * info["n_q"], dtype=torch.float32, device="cuda")
+    grads = {k: (None if v is None else torch.empty_like(v)) for k, v in d.items()}
+    names = ("q_win", "k_sink", "v_sink", "k_hist", "v_hist", "k_win", "v_win")
+    stream = torch.cuda.current_stream()
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        mssa.mssa_pool_kv(plan, d["k_hist"], d["v_hist"], d["k_win"], d["v_win"], ws)
+        mssa.mssa_forward_lse(plan, d["q_win"], d["k_sink"], d["v_sink"], d["k_hist"], d["v_hist"],
+                              d["k_win"], d["v_win"], ws, out, lse)
+        if ev is not None:
+            ev[1].record(stream)
+        mssa.mssa_backward(plan, *(d[k] for k in names), out, lse, g_out, ws, *(grads[k] for k in names))
+        if ev is not None:
+            ev[2].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    for e in evs:
+        step(e)
+    torch.cuda.synchronize()
+    fwd_ms = np.array([e[0].elapsed_time(e[1]) for e in evs])
+    bwd_ms = np.array([e[1].elapsed_time(e[2]) for e in evs])
+    step_ms = fwd_ms + bwd_ms
+    F = info["flops_alg"]
+    result = {
+        "metric": "MSSA training step (pool + forward + backward) effective TFLOP/s (1 GPU)",
+        "value": round(3.5 * F / (step_ms.mean() * 1e-3) / 1e12, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(float(step_ms.mean()), 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": dtype, "data": "synthetic",
+        "config": {"workload": args.workload, "flops_alg_forward": F, "flops_alg_backward": 2.5 * F},
+        "forward_pool_ms": round(float(fwd_ms.mean()), 4),
+        "backward_ms": round(float(bwd_ms.mean()), 4),
+        "backward_ms_p10_p90": [round(float(np.percentile(bwd_ms, 10)), 4),
+                                round(float(np.percentile(bwd_ms, 90)), 4)],
+        "backward_tflops": round(2.5 * F / (bwd_ms.mean() * 1e-3) / 1e12, 2),
+        "backward_pct_of_bf16_peak": round(100 * 2.5 * F / (bwd_ms.mean() * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 2),
+    }
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -177,6 +255,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--layers", type=int, default=0, help="streaming: layers (default 30)")
     ap.add_argument("--passes", type=int, default=0, help="streaming: rolling passes (default 64)")
+    ap.add_argument("--training", action="store_true",
+                    help="time pool + forward (with lse) + backward of one layer instead")
     ap.add_argument("--pooled-ring", action="store_true",
                     help="streaming: keep pooled history rings instead of re-pooling history each pass")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
@@ -192,6 +272,9 @@ def main():
 
     if args.workload == "streaming":
         bench_streaming(args)
+        return
+    if args.training:
+        bench_training(args)
         return
     if args.copy_calibration_mb:
         import torch

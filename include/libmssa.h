@@ -176,6 +176,55 @@ mssa_status mssa_forward(mssa_plan plan, const void* q_win, const void* k_sink,
                          const void* k_win, const void* v_win, const void* workspace,
                          int64_t workspace_bytes, void* out, void* stream);
 
+/* ----------------------------------------------------------------- training
+ * The window is trained through its attention (Sec. 3.1; Alg. 1 updates the
+ * model by gradient steps on the rolling window), so the backward of Eq. 4:
+ * per head and query scale s, with P = softmax(softmax_scale q k_s^T) and dO
+ * the gradient of the output,
+ *   dV_s = P^T dO,  dS = P * (dO V_s^T - rowsum(dO * out)),
+ *   dQ = softmax_scale dS K_s,  dK_s = softmax_scale dS^T Q,
+ * and each context row's gradient goes back to the sink, history or window
+ * token(s) it was made from (block mean: g / c to each of the block's c
+ * cells; strided plans: g to the block's first cell), summed over the query
+ * scales whose contexts hold it.  Plans with MSSA_PLAN_POOLED_HIST_RING are
+ * not supported (MSSA_ERR_UNSUPPORTED). */
+
+/* mssa_forward that also writes lse [H, n_q] (fp32, device, head-major):
+ * lse[h * n_q + i] = log sum_j exp(softmax_scale q_i . k_j) over query i's
+ * context, natural log.  Same arguments and errors as mssa_forward; lse must
+ * be non-null and 16-byte aligned. */
+mssa_status mssa_forward_lse(mssa_plan plan, const void* q_win, const void* k_sink,
+                             const void* v_sink, const void* k_hist, const void* v_hist,
+                             const void* k_win, const void* v_win, const void* workspace,
+                             int64_t workspace_bytes, void* out, float* lse, void* stream);
+
+/* Bytes of device workspace mssa_backward needs (>= workspace_bytes: the
+ * pooled K/V sit at the same offsets as for mssa_forward, followed by the
+ * backward's own fp32 buffers). */
+mssa_status mssa_backward_workspace_size(mssa_plan plan, int64_t* bytes);
+
+/* Gradients of MSSA with respect to all seven inputs.
+ *   q_win .. v_win   the forward's inputs (as for mssa_forward)
+ *   out, lse         the forward's output and mssa_forward_lse's lse
+ *   d_out            [n_q, H, D] device, gradient of the output
+ *   workspace        device, >= mssa_backward_workspace_size bytes,
+ *                    256-byte aligned, whose pooled K/V are what
+ *                    mssa_pool_kv wrote for these inputs (the forward's
+ *                    workspace can be reused as is)
+ *   dq_win .. dv_win device outputs shaped like the inputs, plan dtype,
+ *                    written (not accumulated); dk_sink / dv_sink may be
+ *                    NULL iff sink_frames == 0, dk_hist / dv_hist iff
+ *                    hist_frames == 0; no gradient may alias an input.
+ * bf16 plans use bf16 matrix cores with fp32 accumulation (probabilities
+ * and dS rounded to bf16 as matrix operands); fp32 plans compute in fp32.
+ * Enqueues on `stream`; deterministic (fixed summation orders, no atomics).
+ * MSSA_ERR_WORKSPACE for a small workspace. */
+mssa_status mssa_backward(mssa_plan plan, const void* q_win, const void* k_sink, const void* v_sink,
+                          const void* k_hist, const void* v_hist, const void* k_win, const void* v_win,
+                          const void* out, const float* lse, const void* d_out, void* workspace,
+                          int64_t workspace_bytes, void* dq_win, void* dk_sink, void* dv_sink, void* dk_hist,
+                          void* dv_hist, void* dk_win, void* dv_win, void* stream);
+
 /* Streaming cache roll (Sec. 3.1, Eq. 2; Alg. 1 KV-cache update): after a
  * rolling pass the head state (window state 1, which must be at native
  * scale: scales[0] == 1) is emitted, and its F native frames of K and V

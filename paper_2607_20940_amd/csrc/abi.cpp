@@ -154,10 +154,37 @@ mssa_status append_native(const mssa::Plan& p, const void* k_win, const void* v_
 // mssa_forward / mssa_forward_ring: validate, pack the kernel arguments and
 // launch.  k_hist_pooled / v_hist_pooled (ring plans only) give each group's
 // pooled-history ring.
+// Device addresses of the first token (head 0) of run R of group g, K and V.
+struct KvSources {
+  const void *k_sink, *v_sink, *k_hist, *v_hist;
+  const void* const* k_hist_pooled;
+  const void* const* v_hist_pooled;
+  const void *k_win, *v_win;
+  const char* ws;
+};
+
+void run_pointers(const mssa::Plan& p, int g, const mssa::Run& R, const KvSources& s, const void** kp,
+                  const void** vp) {
+  const int64_t row_bytes = p.ld * p.elem_bytes;
+  const char *kb = nullptr, *vb = nullptr;
+  switch (R.buffer) {
+    case mssa::kBufSink: kb = static_cast<const char*>(s.k_sink); vb = static_cast<const char*>(s.v_sink); break;
+    case mssa::kBufHist: kb = static_cast<const char*>(s.k_hist); vb = static_cast<const char*>(s.v_hist); break;
+    case mssa::kBufWin: kb = static_cast<const char*>(s.k_win); vb = static_cast<const char*>(s.v_win); break;
+    case mssa::kBufHistPooled:
+      kb = static_cast<const char*>(s.k_hist_pooled[g]);
+      vb = static_cast<const char*>(s.v_hist_pooled[g]);
+      break;
+    default: kb = s.ws + p.pooled_k_off[g]; vb = s.ws + p.pooled_v_off[g]; break;
+  }
+  *kp = kb + R.tok_offset * row_bytes;
+  *vp = vb + R.tok_offset * row_bytes;
+}
+
 mssa_status forward_impl(const mssa::Plan& p, const void* q_win, const void* k_sink, const void* v_sink,
                          const void* k_hist, const void* v_hist, const void* const* k_hist_pooled,
                          const void* const* v_hist_pooled, const void* k_win, const void* v_win,
-                         const void* workspace, int64_t workspace_bytes, void* out, void* stream) {
+                         const void* workspace, int64_t workspace_bytes, void* out, float* lse, void* stream) {
   if (!q_win || !k_win || !v_win || !out)
     return fail(MSSA_ERR_INVALID_ARG, "q_win, k_win, v_win and out must be non-null");
   if (p.n_sink_tok > 0 && (!k_sink || !v_sink))
@@ -170,6 +197,7 @@ mssa_status forward_impl(const mssa::Plan& p, const void* q_win, const void* k_s
     if (t && !aligned16(t)) return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
   if (out == q_win || out == k_win || out == v_win)
     return fail(MSSA_ERR_INVALID_ARG, "out must not alias an input");
+  if (lse && !aligned16(lse)) return fail(MSSA_ERR_INVALID_ARG, "lse must be 16-byte aligned");
   if (p.hist_ring && p.n_hist_tok > 0) {
     if (!k_hist_pooled || !v_hist_pooled)
       return fail(MSSA_ERR_INVALID_ARG, "k_hist_pooled and v_hist_pooled must be non-null");
@@ -184,10 +212,11 @@ mssa_status forward_impl(const mssa::Plan& p, const void* q_win, const void* k_s
 
   const bool bf16 = p.desc.dtype == MSSA_BF16;
   const int bm = bf16 ? mssa::kFwdBM : mssa::kFwdF32BM;
-  const int64_t row_bytes = p.ld * p.elem_bytes;
   mssa::FwdArgs a{};
   a.q = q_win;
   a.out = out;
+  a.lse = lse;
+  a.n_q = static_cast<int32_t>(p.n_q);
   a.ld = p.ld;
   a.num_heads = p.desc.num_heads;
   a.scale = p.softmax_scale;
@@ -212,22 +241,10 @@ mssa_status forward_impl(const mssa::Plan& p, const void* q_win, const void* k_s
     if (p.runs[g].size() > static_cast<size_t>(mssa::kMaxRuns))
       return fail(MSSA_ERR_UNSUPPORTED, "too many context runs for one query scale");
     A.n_runs = static_cast<int32_t>(p.runs[g].size());
+    const KvSources src{k_sink, v_sink, k_hist, v_hist, k_hist_pooled, v_hist_pooled, k_win, v_win, ws};
     for (size_t r = 0; r < p.runs[g].size(); ++r) {
-      const mssa::Run& R = p.runs[g][r];
-      const char *kb = nullptr, *vb = nullptr;
-      switch (R.buffer) {
-        case mssa::kBufSink: kb = static_cast<const char*>(k_sink); vb = static_cast<const char*>(v_sink); break;
-        case mssa::kBufHist: kb = static_cast<const char*>(k_hist); vb = static_cast<const char*>(v_hist); break;
-        case mssa::kBufWin: kb = static_cast<const char*>(k_win); vb = static_cast<const char*>(v_win); break;
-        case mssa::kBufHistPooled:
-          kb = static_cast<const char*>(k_hist_pooled[g]);
-          vb = static_cast<const char*>(v_hist_pooled[g]);
-          break;
-        default: kb = ws + p.pooled_k_off[g]; vb = ws + p.pooled_v_off[g]; break;
-      }
-      A.runs[r].k = kb + R.tok_offset * row_bytes;
-      A.runs[r].v = vb + R.tok_offset * row_bytes;
-      A.runs[r].n_tok = static_cast<int32_t>(R.n_tok);
+      run_pointers(p, g, p.runs[g][r], src, &A.runs[r].k, &A.runs[r].v);
+      A.runs[r].n_tok = static_cast<int32_t>(p.runs[g][r].n_tok);
     }
     blocks += static_cast<int64_t>(A.n_qtiles) * p.desc.num_heads;
   }
@@ -347,7 +364,7 @@ mssa_status mssa_forward(mssa_plan plan, const void* q_win, const void* k_sink, 
   if (plan->p.hist_ring)
     return fail(MSSA_ERR_UNSUPPORTED, "plan has MSSA_PLAN_POOLED_HIST_RING: use mssa_forward_ring");
   return forward_impl(plan->p, q_win, k_sink, v_sink, k_hist, v_hist, nullptr, nullptr, k_win, v_win, workspace,
-                      workspace_bytes, out, stream);
+                      workspace_bytes, out, nullptr, stream);
 }
 
 mssa_status mssa_forward_ring(mssa_plan plan, const void* q_win, const void* k_sink, const void* v_sink,
@@ -358,7 +375,153 @@ mssa_status mssa_forward_ring(mssa_plan plan, const void* q_win, const void* k_s
   if (!plan->p.hist_ring)
     return fail(MSSA_ERR_UNSUPPORTED, "plan lacks MSSA_PLAN_POOLED_HIST_RING: use mssa_forward");
   return forward_impl(plan->p, q_win, k_sink, v_sink, k_hist, v_hist, k_hist_pooled, v_hist_pooled, k_win, v_win,
-                      workspace, workspace_bytes, out, stream);
+                      workspace, workspace_bytes, out, nullptr, stream);
+}
+
+mssa_status mssa_forward_lse(mssa_plan plan, const void* q_win, const void* k_sink, const void* v_sink,
+                             const void* k_hist, const void* v_hist, const void* k_win, const void* v_win,
+                             const void* workspace, int64_t workspace_bytes, void* out, float* lse, void* stream) {
+  if (!plan) return fail(MSSA_ERR_INVALID_ARG, "plan must be non-null");
+  if (plan->p.hist_ring)
+    return fail(MSSA_ERR_UNSUPPORTED, "mssa_forward_lse takes plans without MSSA_PLAN_POOLED_HIST_RING");
+  if (!lse) return fail(MSSA_ERR_INVALID_ARG, "lse must be non-null");
+  return forward_impl(plan->p, q_win, k_sink, v_sink, k_hist, v_hist, nullptr, nullptr, k_win, v_win, workspace,
+                      workspace_bytes, out, lse, stream);
+}
+
+mssa_status mssa_backward_workspace_size(mssa_plan plan, int64_t* bytes) {
+  if (!plan || !bytes) return fail(MSSA_ERR_INVALID_ARG, "plan and bytes must be non-null");
+  *bytes = plan->p.bwd_workspace_bytes;
+  return MSSA_OK;
+}
+
+mssa_status mssa_backward(mssa_plan plan, const void* q_win, const void* k_sink, const void* v_sink,
+                          const void* k_hist, const void* v_hist, const void* k_win, const void* v_win,
+                          const void* out, const float* lse, const void* d_out, void* workspace,
+                          int64_t workspace_bytes, void* dq_win, void* dk_sink, void* dv_sink, void* dk_hist,
+                          void* dv_hist, void* dk_win, void* dv_win, void* stream) {
+  if (!plan) return fail(MSSA_ERR_INVALID_ARG, "plan must be non-null");
+  const mssa::Plan& p = plan->p;
+  if (p.hist_ring)
+    return fail(MSSA_ERR_UNSUPPORTED, "mssa_backward takes plans without MSSA_PLAN_POOLED_HIST_RING");
+  if (!q_win || !k_win || !v_win || !out || !lse || !d_out || !dq_win || !dk_win || !dv_win)
+    return fail(MSSA_ERR_INVALID_ARG, "window tensors, out, lse, d_out and their gradients must be non-null");
+  if (p.n_sink_tok > 0 && (!k_sink || !v_sink || !dk_sink || !dv_sink))
+    return fail(MSSA_ERR_INVALID_ARG, "sink tensors and their gradients must be non-null when sink_frames > 0");
+  if (p.n_hist_tok > 0 && (!k_hist || !v_hist || !dk_hist || !dv_hist))
+    return fail(MSSA_ERR_INVALID_ARG, "history tensors and their gradients must be non-null when hist_frames > 0");
+  if (!workspace || workspace_bytes < p.bwd_workspace_bytes)
+    return fail(MSSA_ERR_WORKSPACE, "workspace smaller than mssa_backward_workspace_size");
+  if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
+    return fail(MSSA_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+  const void* ins[] = {q_win, k_sink, v_sink, k_hist, v_hist, k_win, v_win, out, lse, d_out};
+  const void* grads[] = {dq_win, dk_sink, dv_sink, dk_hist, dv_hist, dk_win, dv_win};
+  for (const void* t : ins)
+    if (t && !aligned16(t)) return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
+  for (const void* t : grads) {
+    if (!t) continue;
+    if (!aligned16(t)) return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
+    for (const void* u : ins)
+      if (t == u) return fail(MSSA_ERR_INVALID_ARG, "gradients must not alias an input");
+  }
+  const int G = static_cast<int>(p.groups.size());
+  if (G > mssa::kMaxGroups) return fail(MSSA_ERR_UNSUPPORTED, "too many query scales");
+  if (p.scatter_jobs.size() > static_cast<size_t>(mssa::kMaxScatterJobs))
+    return fail(MSSA_ERR_UNSUPPORTED, "too many source frame runs");
+
+  const bool bf16 = p.desc.dtype == MSSA_BF16;
+  const int hd = p.desc.head_dim, nh = p.desc.num_heads;
+  auto hs = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(workspace);
+  float* dsum = reinterpret_cast<float*>(ws + p.bwd_dsum_off);
+
+  mssa::DotArgs da{};
+  da.out = out;
+  da.d_out = d_out;
+  da.dsum = dsum;
+  da.ld = p.ld;
+  da.n_q = static_cast<int32_t>(p.n_q);
+  da.num_heads = nh;
+  da.head_dim = hd;
+  mssa_status s = check_device(mssa::launch_bwd_dot(da, bf16, hs), "backward rowsum launch");
+  if (s != MSSA_OK) return s;
+
+  mssa::BwdArgs a{};
+  a.q = q_win;
+  a.d_out = d_out;
+  a.lse = lse;
+  a.dsum = dsum;
+  a.dq = dq_win;
+  a.ld = p.ld;
+  a.n_q = static_cast<int32_t>(p.n_q);
+  a.num_heads = nh;
+  a.n_groups = G;
+  a.scale = p.softmax_scale;
+  a.scale_log2e = p.softmax_scale * 1.4426950408889634f;
+  const int qb = bf16 ? mssa::kBwdQ : mssa::kBwdF32, kb = bf16 ? mssa::kBwdK : mssa::kBwdF32;
+  const KvSources src{k_sink, v_sink, k_hist, v_hist, nullptr, nullptr, k_win, v_win, ws};
+  int64_t dq_blocks = 0, kv_blocks = 0;
+  int gi = 0;
+  for (int g : p.order) {
+    mssa::BwdGroupArgs& A = a.groups[gi++];
+    const mssa::QGroup& Q = p.groups[g];
+    A.q_begin = Q.q_begin;
+    A.q_end = Q.q_end;
+    A.n_kv = static_cast<int32_t>(Q.n_kv);
+    if (p.runs[g].size() > static_cast<size_t>(mssa::kMaxRuns))
+      return fail(MSSA_ERR_UNSUPPORTED, "too many context runs for one query scale");
+    A.n_runs = static_cast<int32_t>(p.runs[g].size());
+    for (size_t r = 0; r < p.runs[g].size(); ++r) {
+      run_pointers(p, g, p.runs[g][r], src, &A.runs[r].k, &A.runs[r].v);
+      A.runs[r].n_tok = static_cast<int32_t>(p.runs[g][r].n_tok);
+    }
+    A.dk_ctx = reinterpret_cast<float*>(ws + p.bwd_dk_off[g]);
+    A.dv_ctx = reinterpret_cast<float*>(ws + p.bwd_dv_off[g]);
+    A.n_qblocks = (Q.q_end - Q.q_begin + qb - 1) / qb;
+    A.n_kblocks = static_cast<int32_t>((Q.n_kv + kb - 1) / kb);
+    A.dq_block_begin = static_cast<int32_t>(dq_blocks);
+    A.kv_block_begin = static_cast<int32_t>(kv_blocks);
+    dq_blocks += static_cast<int64_t>(A.n_qblocks) * nh;
+    kv_blocks += static_cast<int64_t>(A.n_kblocks) * nh;
+  }
+  if (dq_blocks > 0x7fffffff || kv_blocks > 0x7fffffff) return fail(MSSA_ERR_UNSUPPORTED, "backward grid too large");
+  s = check_device(mssa::launch_bwd(a, static_cast<int>(dq_blocks), static_cast<int>(kv_blocks), hd, bf16, hs),
+                   "backward attention launch");
+  if (s != MSSA_OK) return s;
+
+  mssa::ScatterArgs sa{};
+  for (int g = 0; g < G; ++g) {
+    sa.ctx_k[g] = reinterpret_cast<const float*>(ws + p.bwd_dk_off[g]);
+    sa.ctx_v[g] = reinterpret_cast<const float*>(ws + p.bwd_dv_off[g]);
+  }
+  sa.ld = p.ld;
+  sa.chunks_per_tok = static_cast<int32_t>(p.ld * p.elem_bytes / 16);
+  sa.n_groups = G;
+  sa.pick_first = p.strided ? 1 : 0;
+  const int64_t row_bytes = p.ld * p.elem_bytes;
+  int64_t blocks = 0;
+  int nj = 0;
+  for (const mssa::ScatterJob& J : p.scatter_jobs) {
+    mssa::ScatterJobArgs& A = sa.jobs[nj++];
+    char* dk = static_cast<char*>(J.buffer == mssa::kBufSink ? dk_sink : J.buffer == mssa::kBufHist ? dk_hist : dk_win);
+    char* dv = static_cast<char*>(J.buffer == mssa::kBufSink ? dv_sink : J.buffer == mssa::kBufHist ? dv_hist : dv_win);
+    A.dst_k = dk + J.src_tok * row_bytes;
+    A.dst_v = dv + J.src_tok * row_bytes;
+    A.n_frames = J.n_frames;
+    A.gh = J.gh;
+    A.gw = J.gw;
+    A.block_begin = static_cast<int32_t>(blocks);
+    for (int g = 0; g < G; ++g) {
+      A.g[g].ctx_begin = J.ctx_begin[g];
+      A.g[g].frame_stride = J.frame_stride[g];
+      A.g[g].factor = J.factor[g];
+    }
+    const int64_t work = static_cast<int64_t>(J.n_frames) * J.gh * J.gw * sa.chunks_per_tok;
+    blocks += (work + mssa::kPoolThreads - 1) / mssa::kPoolThreads;
+  }
+  sa.n_jobs = nj;
+  if (blocks > 0x7fffffff) return fail(MSSA_ERR_UNSUPPORTED, "scatter grid too large");
+  return check_device(mssa::launch_scatter(sa, static_cast<int>(blocks), bf16, hs), "backward scatter launch");
 }
 
 mssa_status mssa_hist_append(mssa_plan plan, const void* k_win, const void* v_win, void* k_ring, void* v_ring,

@@ -1,0 +1,590 @@
+// Multi-scale self-attention backward: the chain rule through Eq. 4 of Ms.
+// Forcing (Sec. 4.1), whose rolling-window training (Sec. 3.1, Alg. 1)
+// differentiates the attention of every window state.  For each head and
+// query scale s, with P = softmax(scale q k_s^T) over the context of s and dO
+// the gradient of the output:
+//   dV_s = P^T dO,  dS = P * (dO V_s^T - rowsum(dO * O)),
+//   dQ = scale dS K_s,  dK_s = scale dS^T Q.
+// The statistics come from the forward: the log of each row's softmax
+// denominator (lse) and rowsum(dO * O) (dot_kernel).  Context gradients are
+// kept per query scale in fp32; scatter_kernel then sums, for every sink,
+// history and window token, the gradients of the context rows made from it
+// (the adjoint of the resampling: the block mean hands g / c to each of its c
+// cells, the strided pick g to the block's first cell).  Fixed summation
+// orders and no atomics: the result is the same bits on every run.
+//
+// bf16 path (gfx950 matrix cores, v_mfma_f32_32x32x16_bf16, fp32
+// accumulation), two kernels so that no gradient needs atomics:
+//   dq_kernel    a wave owns 32 queries and walks the context in 64-key
+//                stages through LDS: S^T = K Q^T and dP^T = V dO^T (A = K, V
+//                rows from LDS, B = the wave's Q and dO fragments in
+//                registers), so each lane holds 16 keys of ONE query and its
+//                lse / rowsum are scalars; dS^T packed to bf16 is already the
+//                B operand of dQ^T += K^T dS^T, with K^T read from LDS by the
+//                transposing read ds_read_b64_tr_b16.
+//   dkdv_kernel  a wave owns 32 context keys (K, V fragments in registers)
+//                and walks the scale's queries in 64-query stages: S = Q K^T,
+//                dP = dO V^T (lane = key), then dV^T += dO^T P and
+//                dK^T += Q^T dS with dO^T, Q^T from transposing reads.
+// Rows past the end of a context or query range are zero-filled; their
+// probabilities are forced to zero.
+//
+// fp32 path (correctness path for fp32 plans): one lane per query (dQ) or
+// per context key (dK, dV), plain fp32 arithmetic with expf.
+#include <hip/hip_runtime.h>
+
+#include "kernels.hpp"
+
+namespace mssa {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+// Blocks are dispatched round-robin over the 8 XCDs; give each XCD a
+// contiguous eighth of the logical blocks so that its L2 serves few heads.
+__device__ inline int xcd_remap(int b, int n) {
+  const int q = n / 8, r = n % 8, x = b % 8, j = b / 8;
+  return (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + j;
+}
+
+// Context token j of group G -> its K (or V) row, head 0; nullptr past the end.
+template <typename T>
+__device__ inline const T* ctx_row(const BwdGroupArgs& G, int j, bool v, int64_t ld) {
+  if (j >= G.n_kv) return nullptr;
+  int r = 0;
+  while (r + 1 < G.n_runs && j >= G.runs[r].n_tok) {
+    j -= G.runs[r].n_tok;
+    ++r;
+  }
+  return static_cast<const T*>(v ? G.runs[r].v : G.runs[r].k) + static_cast<int64_t>(j) * ld;
+}
+
+// Operand reads shared by both bf16 kernels.  Row layout (stride D + 8): a
+// 32-row block is read as the A operand of a 32x32x16 MFMA, lane n taking row
+// n and the 8 columns of its half-wave.  Transposing layout (stride D + 32):
+// the A operand X^T[d][row] of a 32-wide d block db and 16 rows, in the row
+// order in which a 32x32 accumulator's lane holds its 16 values, so that the
+// accumulator packed to bf16 is the matching B operand.
+template <int D>
+struct Lay {
+  static constexpr int KS = D / 16, DB = D / 32, CPR = D / 8;
+  static constexpr int ASTR = D + 8, TSTR = D + 32;
+  static constexpr int RPL = kBwdThreads / CPR;  // rows per pass of the block's loads
+};
+
+__device__ inline int tr_offset(int lane, int tstr) {
+  const int gq = lane >> 4;
+  return (4 * (gq >> 1) + ((lane & 15) >> 2)) * tstr + 16 * (gq & 1) + 4 * (lane & 3);
+}
+
+__device__ inline bf16x8 tr_read(const __bf16* p, int tstr) {
+  const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)p);
+  const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p + 8 * tstr));
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+// ------------------------------------------------------------------ rowsum(dO * O)
+
+template <typename T>
+__global__ __launch_bounds__(kDotThreads) void dot_kernel(DotArgs a) {
+  constexpr int N = 16 / sizeof(T);
+  typedef T vecT __attribute__((ext_vector_type(N)));
+  const int64_t r = static_cast<int64_t>(blockIdx.x) * kDotThreads + threadIdx.x;
+  if (r >= static_cast<int64_t>(a.n_q) * a.num_heads) return;
+  const int q = static_cast<int>(r / a.num_heads), h = static_cast<int>(r % a.num_heads);
+  const int64_t off = static_cast<int64_t>(q) * a.ld + static_cast<int64_t>(h) * a.head_dim;
+  const T* o = static_cast<const T*>(a.out) + off;
+  const T* g = static_cast<const T*>(a.d_out) + off;
+  float acc = 0.f;
+  for (int d = 0; d < a.head_dim; d += N) {
+    const vecT ov = *reinterpret_cast<const vecT*>(o + d);
+    const vecT gv = *reinterpret_cast<const vecT*>(g + d);
+#pragma unroll
+    for (int e = 0; e < N; ++e) acc = __builtin_fmaf(static_cast<float>(ov[e]), static_cast<float>(gv[e]), acc);
+  }
+  a.dsum[static_cast<int64_t>(h) * a.n_q + q] = acc;
+}
+
+// ------------------------------------------------------------------ bf16: dQ
+
+template <int D>
+__global__ __launch_bounds__(kBwdThreads) void dq_kernel(BwdArgs a) {
+  using L = Lay<D>;
+  constexpr int KS = L::KS, DB = L::DB, CPR = L::CPR, ASTR = L::ASTR, TSTR = L::TSTR, RPL = L::RPL;
+  constexpr int BN = kBwdKS, NLD = BN / RPL;
+  constexpr int KA = BN * ASTR, KT = BN * TSTR, STAGE = 2 * KA + KT;  // K rows | V rows | K transposing
+  static_assert(NLD * RPL == BN, "stage load must divide evenly");
+  __shared__ __attribute__((aligned(16))) __bf16 lds[2 * STAGE];
+
+  int n_blocks = 0;
+  for (int g = 0; g < a.n_groups; ++g) n_blocks += a.groups[g].n_qblocks * a.num_heads;
+  const int b = xcd_remap(blockIdx.x, n_blocks);
+  int g = 0;
+  while (g + 1 < a.n_groups && b >= a.groups[g + 1].dq_block_begin) ++g;
+  const BwdGroupArgs& G = a.groups[g];
+  const int idx = b - G.dq_block_begin;
+  const int head = idx / G.n_qblocks, qt = idx % G.n_qblocks;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n = lane & 31, hh = lane >> 5;
+  const int q_row = G.q_begin + qt * kBwdQ + wave * 32 + n;
+  const bool q_ok = q_row < G.q_end;
+  const int64_t ld = a.ld, hoff = static_cast<int64_t>(head) * D;
+  const float c = a.scale_log2e;
+
+  // B operands: this lane's query, 8 channels of its half-wave per k step.
+  bf16x8 qf[KS], gf[KS];
+  {
+    const int64_t off = static_cast<int64_t>(q_ok ? q_row : G.q_begin) * ld + hoff + hh * 8;
+    const __bf16* qp = static_cast<const __bf16*>(a.q) + off;
+    const __bf16* gp = static_cast<const __bf16*>(a.d_out) + off;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      qf[ks] = q_ok ? *reinterpret_cast<const bf16x8*>(qp + ks * 16) : bf16x8{};
+      gf[ks] = q_ok ? *reinterpret_cast<const bf16x8*>(gp + ks * 16) : bf16x8{};
+    }
+  }
+  const int64_t stat = static_cast<int64_t>(head) * a.n_q + (q_ok ? q_row : G.q_begin);
+  const float lse2 = q_ok ? a.lse[stat] * kLog2e : 0.f;
+  const float dsum = q_ok ? a.dsum[stat] : 0.f;
+
+  f32x16 acc[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) acc[db] = f32x16{};
+
+  const int ld_row = tid / CPR, ld_col = (tid % CPR) * 8;
+  bf16x8 pk[NLD], pv[NLD];
+  auto load_stage = [&](int j0) {
+#pragma unroll
+    for (int i = 0; i < NLD; ++i) {
+      const int j = j0 + ld_row + i * RPL;
+      const __bf16* kp = ctx_row<__bf16>(G, j, false, ld);
+      const __bf16* vp = ctx_row<__bf16>(G, j, true, ld);
+      pk[i] = kp ? *reinterpret_cast<const bf16x8*>(kp + hoff + ld_col) : bf16x8{};
+      pv[i] = vp ? *reinterpret_cast<const bf16x8*>(vp + hoff + ld_col) : bf16x8{};
+    }
+  };
+  auto store_stage = [&](int buf) {
+    __bf16* base = lds + buf * STAGE;
+#pragma unroll
+    for (int i = 0; i < NLD; ++i) {
+      const int row = ld_row + i * RPL;
+      *reinterpret_cast<bf16x8*>(base + row * ASTR + ld_col) = pk[i];
+      *reinterpret_cast<bf16x8*>(base + KA + row * ASTR + ld_col) = pv[i];
+      *reinterpret_cast<bf16x8*>(base + 2 * KA + row * TSTR + ld_col) = pk[i];
+    }
+  };
+  const int t_rd = tr_offset(lane, TSTR);
+
+  auto compute = [&](int buf, int nvalid) {
+    const __bf16* Ka = lds + buf * STAGE;
+    const __bf16* Va = Ka + KA;
+    const __bf16* Kt = Ka + 2 * KA + t_rd;
+    f32x16 s[BN / 32], dp[BN / 32];
+#pragma unroll
+    for (int kb = 0; kb < BN / 32; ++kb)
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const bf16x8 ak = *reinterpret_cast<const bf16x8*>(Ka + (kb * 32 + n) * ASTR + hh * 8 + ks * 16);
+        const bf16x8 av = *reinterpret_cast<const bf16x8*>(Va + (kb * 32 + n) * ASTR + hh * 8 + ks * 16);
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ak, qf[ks], ks == 0 ? f32x16{} : s[kb], 0, 0, 0);
+        dp[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, gf[ks], ks == 0 ? f32x16{} : dp[kb], 0, 0, 0);
+      }
+    // dS^T = P^T * (dP^T - rowsum), element e of block kb is key kb*32 + 8(e/4) + 4hh + e%4.
+    bf16x8 dsb[BN / 32][2];
+#pragma unroll
+    for (int kb = 0; kb < BN / 32; ++kb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int key = kb * 32 + 8 * (e >> 2) + 4 * hh + (e & 3);
+        const float p = key < nvalid ? __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][e], c, -lse2)) : 0.f;
+        dsb[kb][e >> 3][e & 7] = static_cast<__bf16>(p * (dp[kb][e] - dsum));
+      }
+#pragma unroll
+    for (int kb = 0; kb < BN / 32; ++kb)
+#pragma unroll
+      for (int cc = 0; cc < 2; ++cc)
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+          const bf16x8 at = tr_read(Kt + (kb * 32 + cc * 16) * TSTR + db * 32, TSTR);
+          acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(at, dsb[kb][cc], acc[db], 0, 0, 0);
+        }
+  };
+
+  const int nst = (G.n_kv + BN - 1) / BN;
+  load_stage(0);
+  store_stage(0);
+  __syncthreads();
+  for (int st = 0; st < nst; ++st) {
+    if (st + 1 < nst) load_stage((st + 1) * BN);
+    compute(st & 1, min(BN, G.n_kv - st * BN));
+    if (st + 1 < nst) store_stage((st + 1) & 1);
+    __syncthreads();
+  }
+
+  if (q_ok) {
+    __bf16* op = static_cast<__bf16*>(a.dq) + static_cast<int64_t>(q_row) * ld + hoff + 4 * hh;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        bf16x4 v;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] = static_cast<__bf16>(acc[db][4 * jj + i] * a.scale);
+        *reinterpret_cast<bf16x4*>(op + db * 32 + 8 * jj) = v;
+      }
+  }
+}
+
+// ------------------------------------------------------------------ bf16: dK, dV
+
+template <int D>
+__global__ __launch_bounds__(kBwdThreads) void dkdv_kernel(BwdArgs a) {
+  using L = Lay<D>;
+  constexpr int KS = L::KS, DB = L::DB, CPR = L::CPR, ASTR = L::ASTR, TSTR = L::TSTR, RPL = L::RPL;
+  constexpr int BQ = kBwdQS, NLD = BQ / RPL;
+  // Q rows | dO rows | Q transposing | dO transposing | lse2, rowsum (fp32)
+  constexpr int QA = BQ * ASTR, QT = BQ * TSTR, STAGE = 2 * QA + 2 * QT + 4 * BQ;
+  static_assert(NLD * RPL == BQ, "stage load must divide evenly");
+  __shared__ __attribute__((aligned(16))) __bf16 lds[2 * STAGE];
+
+  int n_blocks = 0;
+  for (int g = 0; g < a.n_groups; ++g) n_blocks += a.groups[g].n_kblocks * a.num_heads;
+  const int b = xcd_remap(blockIdx.x, n_blocks);
+  int g = 0;
+  while (g + 1 < a.n_groups && b >= a.groups[g + 1].kv_block_begin) ++g;
+  const BwdGroupArgs& G = a.groups[g];
+  const int idx = b - G.kv_block_begin;
+  const int head = idx / G.n_kblocks, kt = idx % G.n_kblocks;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n = lane & 31, hh = lane >> 5;
+  const int key = kt * kBwdK + wave * 32 + n;
+  const bool k_ok = key < G.n_kv;
+  const int64_t ld = a.ld, hoff = static_cast<int64_t>(head) * D;
+  const float c = a.scale_log2e;
+
+  // B operands: this lane's key, 8 channels of its half-wave per k step.
+  bf16x8 kf[KS], vf[KS];
+  {
+    const __bf16* kp = ctx_row<__bf16>(G, key, false, ld);
+    const __bf16* vp = ctx_row<__bf16>(G, key, true, ld);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      kf[ks] = kp ? *reinterpret_cast<const bf16x8*>(kp + hoff + hh * 8 + ks * 16) : bf16x8{};
+      vf[ks] = vp ? *reinterpret_cast<const bf16x8*>(vp + hoff + hh * 8 + ks * 16) : bf16x8{};
+    }
+  }
+  f32x16 dk[DB], dv[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) {
+    dk[db] = f32x16{};
+    dv[db] = f32x16{};
+  }
+
+  const int ld_row = tid / CPR, ld_col = (tid % CPR) * 8;
+  bf16x8 pq[NLD], pg[NLD];
+  float pstat = 0.f;
+  auto load_stage = [&](int q0) {
+#pragma unroll
+    for (int i = 0; i < NLD; ++i) {
+      const int q = q0 + ld_row + i * RPL;
+      const int64_t off = static_cast<int64_t>(q) * ld + hoff + ld_col;
+      const bool ok = q < G.q_end;
+      pq[i] = ok ? *reinterpret_cast<const bf16x8*>(static_cast<const __bf16*>(a.q) + off) : bf16x8{};
+      pg[i] = ok ? *reinterpret_cast<const bf16x8*>(static_cast<const __bf16*>(a.d_out) + off) : bf16x8{};
+    }
+    // threads 0..BQ-1: lse in log2 units (+inf past the end: probability 0);
+    // threads BQ..2BQ-1: rowsum (0 past the end)
+    if (tid < 2 * BQ) {
+      const int q = q0 + (tid % BQ);
+      const bool ok = q < G.q_end;
+      const int64_t s = static_cast<int64_t>(head) * a.n_q + q;
+      pstat = tid < BQ ? (ok ? a.lse[s] * kLog2e : INFINITY) : (ok ? a.dsum[s] : 0.f);
+    }
+  };
+  auto store_stage = [&](int buf) {
+    __bf16* base = lds + buf * STAGE;
+#pragma unroll
+    for (int i = 0; i < NLD; ++i) {
+      const int row = ld_row + i * RPL;
+      *reinterpret_cast<bf16x8*>(base + row * ASTR + ld_col) = pq[i];
+      *reinterpret_cast<bf16x8*>(base + QA + row * ASTR + ld_col) = pg[i];
+      *reinterpret_cast<bf16x8*>(base + 2 * QA + row * TSTR + ld_col) = pq[i];
+      *reinterpret_cast<bf16x8*>(base + 2 * QA + QT + row * TSTR + ld_col) = pg[i];
+    }
+    if (tid < 2 * BQ) reinterpret_cast<float*>(base + 2 * QA + 2 * QT)[tid] = pstat;
+  };
+  const int t_rd = tr_offset(lane, TSTR);
+
+  auto compute = [&](int buf) {
+    const __bf16* Qa = lds + buf * STAGE;
+    const __bf16* Ga = Qa + QA;
+    const __bf16* Qt = Qa + 2 * QA + t_rd;
+    const __bf16* Gt = Qa + 2 * QA + QT + t_rd;
+    const float* lse2 = reinterpret_cast<const float*>(Qa + 2 * QA + 2 * QT);
+    const float* rsum = lse2 + BQ;
+    bf16x8 pb[BQ / 32][2], dsb[BQ / 32][2];
+#pragma unroll
+    for (int qb = 0; qb < BQ / 32; ++qb) {
+      f32x16 s, dp;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const bf16x8 aq = *reinterpret_cast<const bf16x8*>(Qa + (qb * 32 + n) * ASTR + hh * 8 + ks * 16);
+        const bf16x8 ag = *reinterpret_cast<const bf16x8*>(Ga + (qb * 32 + n) * ASTR + hh * 8 + ks * 16);
+        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(aq, kf[ks], ks == 0 ? f32x16{} : s, 0, 0, 0);
+        dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ag, vf[ks], ks == 0 ? f32x16{} : dp, 0, 0, 0);
+      }
+      // element e holds query qb*32 + 8(e/4) + 4hh + e%4 of this lane's key
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const f32x4 l4 = *reinterpret_cast<const f32x4*>(lse2 + qb * 32 + 8 * j + 4 * hh);
+        const f32x4 r4 = *reinterpret_cast<const f32x4*>(rsum + qb * 32 + 8 * j + 4 * hh);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int e = 4 * j + i;
+          const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e], c, -l4[i]));
+          pb[qb][e >> 3][e & 7] = static_cast<__bf16>(p);
+          dsb[qb][e >> 3][e & 7] = static_cast<__bf16>(p * (dp[e] - r4[i]));
+        }
+      }
+    }
+#pragma unroll
+    for (int qb = 0; qb < BQ / 32; ++qb)
+#pragma unroll
+      for (int cc = 0; cc < 2; ++cc)
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+          const int off = (qb * 32 + cc * 16) * TSTR + db * 32;
+          const bf16x8 ag = tr_read(Gt + off, TSTR);
+          const bf16x8 aq = tr_read(Qt + off, TSTR);
+          dv[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ag, pb[qb][cc], dv[db], 0, 0, 0);
+          dk[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(aq, dsb[qb][cc], dk[db], 0, 0, 0);
+        }
+  };
+
+  const int nst = (G.q_end - G.q_begin + BQ - 1) / BQ;
+  load_stage(G.q_begin);
+  store_stage(0);
+  __syncthreads();
+  for (int st = 0; st < nst; ++st) {
+    if (st + 1 < nst) load_stage(G.q_begin + (st + 1) * BQ);
+    compute(st & 1);
+    if (st + 1 < nst) store_stage((st + 1) & 1);
+    __syncthreads();
+  }
+
+  if (k_ok) {
+    const int64_t off = static_cast<int64_t>(key) * ld + hoff + 4 * hh;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        f32x4 vk, vv;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          vk[i] = dk[db][4 * jj + i] * a.scale;
+          vv[i] = dv[db][4 * jj + i];
+        }
+        *reinterpret_cast<f32x4*>(G.dk_ctx + off + db * 32 + 8 * jj) = vk;
+        *reinterpret_cast<f32x4*>(G.dv_ctx + off + db * 32 + 8 * jj) = vv;
+      }
+  }
+}
+
+// ------------------------------------------------------------------ fp32 path
+
+template <int D>
+__global__ __launch_bounds__(kBwdF32) void dq_f32_kernel(BwdArgs a) {
+  int g = 0;
+  while (g + 1 < a.n_groups && static_cast<int>(blockIdx.x) >= a.groups[g + 1].dq_block_begin) ++g;
+  const BwdGroupArgs& G = a.groups[g];
+  const int idx = blockIdx.x - G.dq_block_begin;
+  const int head = idx / G.n_qblocks, qt = idx % G.n_qblocks;
+  const int q_row = G.q_begin + qt * kBwdF32 + threadIdx.x;
+  if (q_row >= G.q_end) return;
+  const int64_t ld = a.ld, hoff = static_cast<int64_t>(head) * D;
+  const float* qp = static_cast<const float*>(a.q) + static_cast<int64_t>(q_row) * ld + hoff;
+  const float* gp = static_cast<const float*>(a.d_out) + static_cast<int64_t>(q_row) * ld + hoff;
+  const int64_t stat = static_cast<int64_t>(head) * a.n_q + q_row;
+  const float lse = a.lse[stat], dsum = a.dsum[stat];
+  float acc[D];
+#pragma unroll
+  for (int d = 0; d < D; ++d) acc[d] = 0.f;
+  for (int j = 0; j < G.n_kv; ++j) {
+    const float* kp = ctx_row<float>(G, j, false, ld) + hoff;
+    const float* vp = ctx_row<float>(G, j, true, ld) + hoff;
+    float s = 0.f, dp = 0.f;
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+      s = __builtin_fmaf(qp[d], kp[d], s);
+      dp = __builtin_fmaf(gp[d], vp[d], dp);
+    }
+    const float ds = expf(s * a.scale - lse) * (dp - dsum);
+#pragma unroll
+    for (int d = 0; d < D; ++d) acc[d] = __builtin_fmaf(ds, kp[d], acc[d]);
+  }
+  float* op = static_cast<float*>(a.dq) + static_cast<int64_t>(q_row) * ld + hoff;
+#pragma unroll
+  for (int d = 0; d < D; ++d) op[d] = acc[d] * a.scale;
+}
+
+template <int D>
+__global__ __launch_bounds__(kBwdF32) void dkdv_f32_kernel(BwdArgs a) {
+  int g = 0;
+  while (g + 1 < a.n_groups && static_cast<int>(blockIdx.x) >= a.groups[g + 1].kv_block_begin) ++g;
+  const BwdGroupArgs& G = a.groups[g];
+  const int idx = blockIdx.x - G.kv_block_begin;
+  const int head = idx / G.n_kblocks, kt = idx % G.n_kblocks;
+  const int key = kt * kBwdF32 + threadIdx.x;
+  if (key >= G.n_kv) return;
+  const int64_t ld = a.ld, hoff = static_cast<int64_t>(head) * D;
+  const float* kp = ctx_row<float>(G, key, false, ld) + hoff;
+  const float* vp = ctx_row<float>(G, key, true, ld) + hoff;
+  float dk[D], dv[D];
+#pragma unroll
+  for (int d = 0; d < D; ++d) {
+    dk[d] = 0.f;
+    dv[d] = 0.f;
+  }
+  for (int q = G.q_begin; q < G.q_end; ++q) {
+    const float* qp = static_cast<const float*>(a.q) + static_cast<int64_t>(q) * ld + hoff;
+    const float* gp = static_cast<const float*>(a.d_out) + static_cast<int64_t>(q) * ld + hoff;
+    const int64_t stat = static_cast<int64_t>(head) * a.n_q + q;
+    float s = 0.f, dp = 0.f;
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+      s = __builtin_fmaf(qp[d], kp[d], s);
+      dp = __builtin_fmaf(gp[d], vp[d], dp);
+    }
+    const float p = expf(s * a.scale - a.lse[stat]);
+    const float ds = p * (dp - a.dsum[stat]);
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+      dv[d] = __builtin_fmaf(p, gp[d], dv[d]);
+      dk[d] = __builtin_fmaf(ds, qp[d], dk[d]);
+    }
+  }
+  float* dkp = G.dk_ctx + static_cast<int64_t>(key) * ld + hoff;
+  float* dvp = G.dv_ctx + static_cast<int64_t>(key) * ld + hoff;
+#pragma unroll
+  for (int d = 0; d < D; ++d) {
+    dkp[d] = dk[d] * a.scale;
+    dvp[d] = dv[d];
+  }
+}
+
+// ------------------------------------------------------------------ scatter to the sources
+
+// One thread per 16-byte output chunk of a source token; it adds, in group
+// order, the context gradient of the row each group made from this token.
+template <typename T>
+__global__ __launch_bounds__(kPoolThreads) void scatter_kernel(ScatterArgs a) {
+  constexpr int N = 16 / sizeof(T);
+  typedef T vecT __attribute__((ext_vector_type(N)));
+  const int b = blockIdx.x;
+  int jn = 0;
+  while (jn + 1 < a.n_jobs && b >= a.jobs[jn + 1].block_begin) ++jn;
+  const ScatterJobArgs& J = a.jobs[jn];
+  const int64_t cpt = a.chunks_per_tok;
+  const int64_t ftok = static_cast<int64_t>(J.gh) * J.gw;
+  const int64_t idx = static_cast<int64_t>(b - J.block_begin) * kPoolThreads + threadIdx.x;
+  if (idx >= J.n_frames * ftok * cpt) return;
+  const int64_t chunk = idx % cpt;
+  const int64_t t = idx / cpt;
+  const int x = static_cast<int>(t % J.gw);
+  const int y = static_cast<int>((t / J.gw) % J.gh);
+  const int64_t fr = t / ftok;
+  const bool is_v = blockIdx.y != 0;
+  float acc[N];
+#pragma unroll
+  for (int e = 0; e < N; ++e) acc[e] = 0.f;
+  for (int g = 0; g < a.n_groups; ++g) {
+    const ScatterGroupArgs& S = J.g[g];
+    const int f = S.factor;
+    if (a.pick_first && f > 1 && ((y % f) != 0 || (x % f) != 0)) continue;
+    const int Y = y / f, X = x / f;
+    const int ow = (J.gw + f - 1) / f;
+    const float cnt = a.pick_first ? 1.f : static_cast<float>(min(f, J.gh - f * Y) * min(f, J.gw - f * X));
+    const float* src = (is_v ? a.ctx_v[g] : a.ctx_k[g]) +
+                       (S.ctx_begin + fr * S.frame_stride + static_cast<int64_t>(Y) * ow + X) * a.ld + chunk * N;
+#pragma unroll
+    for (int e = 0; e < N; e += 4) {
+      const f32x4 v = *reinterpret_cast<const f32x4*>(src + e);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc[e + i] += v[i] / cnt;
+    }
+  }
+  vecT o;
+#pragma unroll
+  for (int e = 0; e < N; ++e) o[e] = static_cast<T>(acc[e]);
+  T* dst = static_cast<T*>(is_v ? J.dst_v : J.dst_k);
+  *reinterpret_cast<vecT*>(dst + (fr * ftok + static_cast<int64_t>(y) * J.gw + x) * a.ld + chunk * N) = o;
+}
+
+}  // namespace
+
+hipError_t launch_bwd_dot(const DotArgs& a, bool bf16, hipStream_t stream) {
+  const int64_t rows = static_cast<int64_t>(a.n_q) * a.num_heads;
+  if (rows == 0) return hipSuccess;
+  const int blocks = static_cast<int>((rows + kDotThreads - 1) / kDotThreads);
+  if (bf16)
+    hipLaunchKernelGGL(dot_kernel<__bf16>, dim3(blocks), dim3(kDotThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL(dot_kernel<float>, dim3(blocks), dim3(kDotThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd(const BwdArgs& a, int dq_blocks, int kv_blocks, int head_dim, bool bf16,
+                      hipStream_t stream) {
+  if (dq_blocks > 0) {
+    if (bf16) {
+      if (head_dim == 128)
+        hipLaunchKernelGGL(dq_kernel<128>, dim3(dq_blocks), dim3(kBwdThreads), 0, stream, a);
+      else
+        hipLaunchKernelGGL(dq_kernel<64>, dim3(dq_blocks), dim3(kBwdThreads), 0, stream, a);
+    } else {
+      if (head_dim == 128)
+        hipLaunchKernelGGL(dq_f32_kernel<128>, dim3(dq_blocks), dim3(kBwdF32), 0, stream, a);
+      else
+        hipLaunchKernelGGL(dq_f32_kernel<64>, dim3(dq_blocks), dim3(kBwdF32), 0, stream, a);
+    }
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (kv_blocks > 0) {
+    if (bf16) {
+      if (head_dim == 128)
+        hipLaunchKernelGGL(dkdv_kernel<128>, dim3(kv_blocks), dim3(kBwdThreads), 0, stream, a);
+      else
+        hipLaunchKernelGGL(dkdv_kernel<64>, dim3(kv_blocks), dim3(kBwdThreads), 0, stream, a);
+    } else {
+      if (head_dim == 128)
+        hipLaunchKernelGGL(dkdv_f32_kernel<128>, dim3(kv_blocks), dim3(kBwdF32), 0, stream, a);
+      else
+        hipLaunchKernelGGL(dkdv_f32_kernel<64>, dim3(kv_blocks), dim3(kBwdF32), 0, stream, a);
+    }
+    return hipGetLastError();
+  }
+  return hipSuccess;
+}
+
+hipError_t launch_scatter(const ScatterArgs& a, int n_blocks, bool bf16, hipStream_t stream) {
+  if (n_blocks <= 0) return hipSuccess;
+  const dim3 grid(n_blocks, 2), block(kPoolThreads);
+  if (bf16)
+    hipLaunchKernelGGL(scatter_kernel<__bf16>, grid, block, 0, stream, a);
+  else
+    hipLaunchKernelGGL(scatter_kernel<float>, grid, block, 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace mssa

@@ -23,6 +23,10 @@
 //
 // fp32 path: one lane per query, plain fp32 FMA dot products and an online
 // softmax with expf; used for fp32 plans (correctness path).
+//
+// Optionally (a.lse non-null) every path also writes, per head and query, the
+// natural log of the softmax denominator, log sum_j exp(scale q k_j): the
+// statistic the backward pass recomputes the probabilities from.
 #include <hip/hip_runtime.h>
 
 #include <type_traits>
@@ -59,6 +63,7 @@ __device__ inline Work decode(const FwdArgs& a, int L) {
 // so exponentials stay <= 2^8 and most tiles skip the O rescale.  The final
 // O / l is unchanged; only rounding differs.
 constexpr float kRescaleLog2 = 8.0f;
+constexpr float kLn2 = 0.6931471805599453f;
 
 // ---------------------------------------------------------------------------
 // Persistent schedule.  An item is one (query scale, head, 128-query tile); its
@@ -479,6 +484,8 @@ __device__ __forceinline__ void attend_piece(const FwdArgs& a, const FwdGroupArg
 
   const float l_tot = halfwave_sum(l_part);
   if (whole) {
+    if (a.lse && q_ok && hh == 0)
+      a.lse[static_cast<int64_t>(head) * a.n_q + q_row] = (m_run + log2f(l_tot)) * kLn2;
     if (q_ok) {
       const float inv = 1.0f / l_tot;
       __bf16* op = static_cast<__bf16*>(a.out) + static_cast<int64_t>(q_row) * ld + hoff + 4 * hh;
@@ -615,6 +622,8 @@ __global__ __launch_bounds__(kFwdThreads) void combine_kernel(FwdArgs a) {
     const int q_row = G.q_begin + qtile * BM + ql;
     if (q_row >= G.q_end) continue;
     const float inv = 1.0f / l[it];
+    if (a.lse && d4 == 0)
+      a.lse[static_cast<int64_t>(head) * a.n_q + q_row] = (m[it] + log2f(l[it])) * kLn2;
     bf16x4 v;
 #pragma unroll
     for (int i = 0; i < 4; ++i) v[i] = static_cast<__bf16>(acc[it][i] * inv);
@@ -665,6 +674,7 @@ __global__ __launch_bounds__(kFwdF32BM) void fwd_f32_kernel(FwdArgs a) {
   float* op = static_cast<float*>(a.out) + static_cast<int64_t>(q_row) * ld + hoff;
 #pragma unroll
   for (int d = 0; d < D; ++d) op[d] = o[d] / l;
+  if (a.lse) a.lse[static_cast<int64_t>(w.head) * a.n_q + q_row] = m + logf(l);
 }
 
 }  // namespace

@@ -52,12 +52,98 @@ struct FwdArgs {
   int32_t dp_rounds;        // bf16 kernel: rounds of whole items before the tail ranges
   int32_t pad2;
   float* partial;           // bf16 kernel: 2 * n_ranges partial records
+  float* lse;               // optional [heads, n_q]: log of the softmax denominator (natural log)
+  int32_t n_q;
+  int32_t pad3;
   FwdGroupArgs groups[kMaxGroups];  // in launch order (longest context first)
 };
 
 // One partial record: unnormalised O [BM][D] (fp32), running max m [BM] and
 // row sum l [BM] of one piece of an item that spans several tile ranges.
 constexpr int64_t partial_record_floats(int head_dim) { return static_cast<int64_t>(kFwdBM) * (head_dim + 2); }
+
+// ---------------------------------------------------------------- backward
+
+// bf16 backward kernels: 4 waves, 32 queries (dQ kernel) or 32 keys (dK/dV
+// kernel) per wave; the other operand streams through LDS in stages.
+constexpr int kBwdThreads = 256;
+constexpr int kBwdQ = 128;     // dQ kernel: queries per block
+constexpr int kBwdKS = 64;     // dQ kernel: keys per LDS stage
+constexpr int kBwdK = 128;     // dK/dV kernel: keys per block
+constexpr int kBwdQS = 64;     // dK/dV kernel: queries per LDS stage
+constexpr int kBwdF32 = 64;    // fp32 kernels: one query or key per lane
+constexpr int kDotThreads = 256;
+constexpr int kMaxScatterJobs = 10;
+
+struct BwdGroupArgs {
+  int32_t q_begin, q_end;     // query token range of this scale
+  int32_t n_kv;               // context tokens
+  int32_t n_runs;
+  int32_t dq_block_begin;     // first block of the group in the dQ grid (head-major inside)
+  int32_t kv_block_begin;     // first block of the group in the dK/dV grid
+  int32_t n_qblocks;          // dQ blocks per head
+  int32_t n_kblocks;          // dK/dV blocks per head
+  FwdRunArgs runs[kMaxRuns];  // context runs (K, V source tokens), context order
+  float* dk_ctx;              // [n_kv, heads * head_dim] fp32 context gradients
+  float* dv_ctx;
+};
+
+struct BwdArgs {
+  const void* q;
+  const void* d_out;
+  const float* lse;         // [heads, n_q] from the forward
+  const float* dsum;        // [heads, n_q]: rowsum(d_out * out)
+  void* dq;
+  int64_t ld;               // elements between tokens: heads * head_dim
+  int32_t n_q;
+  int32_t num_heads;
+  int32_t n_groups;
+  float scale;              // softmax scale
+  float scale_log2e;
+  int32_t pad;
+  BwdGroupArgs groups[kMaxGroups];  // longest query range first
+};
+
+struct DotArgs {
+  const void* out;
+  const void* d_out;
+  float* dsum;              // [heads, n_q]
+  int64_t ld;
+  int32_t n_q;
+  int32_t num_heads;
+  int32_t head_dim;
+  int32_t pad;
+};
+
+// One run of source frames (sink, history, or window frames of one scale)
+// whose gradient gathers from every query scale's context gradient: frame f
+// of the job sits in group g's context at token ctx_begin + f * frame_stride,
+// resampled by factor.
+struct ScatterGroupArgs {
+  int64_t ctx_begin;
+  int32_t frame_stride;
+  int32_t factor;
+};
+
+struct ScatterJobArgs {
+  void* dst_k;              // gradient of the job's first source token (head 0, channel 0)
+  void* dst_v;
+  int32_t n_frames;
+  int32_t gh, gw;           // source grid
+  int32_t block_begin;
+  ScatterGroupArgs g[kMaxGroups];
+};
+
+struct ScatterArgs {
+  const float* ctx_k[kMaxGroups];
+  const float* ctx_v[kMaxGroups];
+  int64_t ld;
+  int32_t chunks_per_tok;   // output chunks per token: 8 elements (bf16) or 4 (fp32)
+  int32_t n_jobs;
+  int32_t n_groups;
+  int32_t pick_first;       // strided resampling: only each block's first cell
+  ScatterJobArgs jobs[kMaxScatterJobs];
+};
 
 struct PoolJobArgs {
   const void* src_k;        // first source token of the job (head 0, ch 0)

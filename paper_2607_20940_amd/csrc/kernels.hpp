@@ -14,6 +14,18 @@ hipError_t launch_pool(const PoolArgs& a, int n_blocks, bool bf16, hipStream_t s
 // blocks followed by the combine of split items; fp32: a.n_blocks blocks.
 hipError_t launch_forward(const FwdArgs& a, int head_dim, bool bf16, hipStream_t stream);
 
+// Backward: rowsum(d_out * out) per head and query.
+hipError_t launch_bwd_dot(const DotArgs& a, bool bf16, hipStream_t stream);
+
+// Backward: dQ kernel (dq_blocks blocks), then dK/dV context gradients
+// (kv_blocks blocks).
+hipError_t launch_bwd(const BwdArgs& a, int dq_blocks, int kv_blocks, int head_dim, bool bf16,
+                      hipStream_t stream);
+
+// Backward: context gradients to the sink, history and window tokens; grid
+// (n_blocks, 2): y = 0 for K, y = 1 for V.
+hipError_t launch_scatter(const ScatterArgs& a, int n_blocks, bool bf16, hipStream_t stream);
+
 // Resident blocks per CU of the bf16 attention kernel (0 if unknown).
 int forward_blocks_per_cu(int head_dim);
 

@@ -263,6 +263,60 @@ mssa_status build_plan(const mssa_plan_desc& d, int slots, int ranges_override, 
   }
   p.workspace_bytes = ws;
 
+  // Backward workspace and the scatter of context gradients to the sources.
+  ws = align256(ws);
+  p.bwd_dsum_off = ws;
+  ws += align256(static_cast<int64_t>(d.num_heads) * p.n_q * 4);
+  p.bwd_dk_off.assign(G, 0);
+  p.bwd_dv_off.assign(G, 0);
+  for (int g = 0; g < G; ++g) {
+    const int64_t bytes = align256(p.groups[g].n_kv * p.ld * 4);
+    p.bwd_dk_off[g] = ws;
+    ws += bytes;
+    p.bwd_dv_off[g] = ws;
+    ws += bytes;
+  }
+  p.bwd_workspace_bytes = ws;
+  auto seg_of = [&](int g, int32_t kind, int32_t frame) -> const SegRow& {
+    for (const SegRow& r : p.segs)
+      if (r.q_scale == p.groups[g].scale && r.kind == kind && r.frame == frame) return r;
+    return p.segs.front();  // unreachable: every source frame is in every context
+  };
+  bool scatter_ok = true;
+  auto add_job = [&](int32_t buffer, int32_t kind, int32_t frame0, int64_t src_tok, int32_t n_frames,
+                     int32_t src_scale) {
+    ScatterJob j;
+    j.buffer = buffer;
+    j.src_tok = src_tok;
+    j.n_frames = n_frames;
+    j.gh = ceil_div(d.grid_h, src_scale);
+    j.gw = ceil_div(d.grid_w, src_scale);
+    for (int g = 0; g < G; ++g) {
+      const SegRow& r = seg_of(g, kind, frame0);
+      j.ctx_begin.push_back(r.kv_begin);
+      j.frame_stride.push_back(r.n_tok);
+      j.factor.push_back(r.factor);
+      // a resampled frame has ceil(gh / f) x ceil(gw / f) tokens, and the
+      // job's frames lie inside the context
+      scatter_ok &= r.kind == kind && r.frame == frame0 &&
+                    static_cast<int64_t>(ceil_div(j.gh, r.factor)) * ceil_div(j.gw, r.factor) == r.n_tok &&
+                    r.kv_begin + static_cast<int64_t>(n_frames) * r.n_tok <= p.groups[g].n_kv;
+    }
+    p.scatter_jobs.push_back(j);
+  };
+  if (d.sink_frames > 0) add_job(kBufSink, kSink, 0, 0, d.sink_frames, 1);
+  if (d.hist_frames > 0) add_job(kBufHist, kHist, 0, 0, d.hist_frames, 1);
+  for (size_t i = 0; i < wf.size();) {
+    size_t e = i;
+    while (e < wf.size() && wf[e].p == wf[i].p) ++e;
+    add_job(kBufWin, kWin, wf[i].w, wf[i].first, static_cast<int32_t>(e - i), wf[i].p);
+    i = e;
+  }
+  if (!scatter_ok) {
+    err = "internal: inconsistent gradient scatter tables";
+    return MSSA_ERR_UNSUPPORTED;
+  }
+
   // Algorithmic pool traffic, K and V: block mean, each pooled source frame
   // read once and each pooled frame written once; stride, each pooled token
   // reads the one source token it copies.

@@ -57,6 +57,17 @@ struct PoolJob {
   int64_t dst_tok;
 };
 
+// Source frames whose gradients gather from the context gradients of every
+// query scale (the adjoint of building the contexts): sink frames, history
+// frames, or consecutive window frames of one scale.
+struct ScatterJob {
+  int32_t buffer;                 // kBufSink, kBufHist or kBufWin
+  int64_t src_tok;                // first token in that buffer
+  int32_t n_frames, gh, gw;
+  std::vector<int64_t> ctx_begin; // per group: context token of the job's first frame
+  std::vector<int32_t> frame_stride, factor;  // per group
+};
+
 struct Plan {
   mssa_plan_desc desc;
   bool hist_ring;  // MSSA_PLAN_POOLED_HIST_RING
@@ -87,6 +98,12 @@ struct Plan {
   int32_t dp_rounds;    // rounds of whole items (one per block) before the tail
   int64_t tail_begin;   // first tile of the tail ranges
   int64_t partial_off, partial_bytes;    // partial records in the workspace
+  // Backward workspace: the forward's, then rowsum(dO * O) [heads, n_q]
+  // fp32, then per group the fp32 context gradients of K and V.
+  int64_t bwd_dsum_off;
+  std::vector<int64_t> bwd_dk_off, bwd_dv_off;  // bytes, per group
+  int64_t bwd_workspace_bytes;
+  std::vector<ScatterJob> scatter_jobs;
 };
 
 // Validates `d` and fills `p`.  `slots` is the number of attention blocks

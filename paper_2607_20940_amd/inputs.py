@@ -56,6 +56,13 @@ def make_inputs(shapes, seed, amplitude=1.0, dtype="bf16"):
     return out
 
 
+def make_grad_output(shape, seed, amplitude=1.0, dtype="bf16"):
+    """Seeded gradient of the attention output (same recipe as the inputs:
+    N(0, 1) draws times the amplitude, rounded once to the dtype)."""
+    x = (np.random.default_rng(seed).standard_normal(tuple(shape)) * amplitude).astype(np.float32)
+    return f32_to_bf16_bits(x) if dtype == "bf16" else x
+
+
 def make_inputs_device(shapes, seed, amplitude=1.0, dtype="bf16", names=DRAW_ORDER, device="cuda"):
     """Device-side variant for workloads too large to draw on the host:
     torch's generator on `device` seeded with `seed` draws N(0,1) float32

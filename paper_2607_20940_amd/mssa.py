@@ -24,7 +24,8 @@ MSSA_PLAN_STRIDED_SUBSAMPLE = 2
 # Every symbol include/libmssa.h declares.
 EXPORTS = ("mssa_plan_create", "mssa_plan_destroy", "mssa_plan_query", "mssa_plan_tables",
            "mssa_pool_kv", "mssa_forward", "mssa_hist_append", "mssa_pool_hist_ring",
-           "mssa_forward_ring", "mssa_hist_append_ring", "mssa_status_string", "mssa_last_error")
+           "mssa_forward_ring", "mssa_hist_append_ring", "mssa_forward_lse", "mssa_backward_workspace_size",
+           "mssa_backward", "mssa_status_string", "mssa_last_error")
 
 
 class mssa_plan_desc(ctypes.Structure):
@@ -74,6 +75,9 @@ def _load():
     lib.mssa_forward_ring.argtypes = [P, V, V, V, V, V, PP, PP, V, V, V, I64, V, V]
     lib.mssa_hist_append_ring.argtypes = [P, V, V, V, I64, V, V, PP, PP, ctypes.c_int32,
                                           ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32), V]
+    lib.mssa_forward_lse.argtypes = [P, V, V, V, V, V, V, V, V, I64, V, V, V]
+    lib.mssa_backward_workspace_size.argtypes = [P, ctypes.POINTER(I64)]
+    lib.mssa_backward.argtypes = [P, V, V, V, V, V, V, V, V, V, V, V, I64, V, V, V, V, V, V, V, V]
     lib.mssa_status_string.argtypes = [ctypes.c_int]
     lib.mssa_status_string.restype = ctypes.c_char_p
     lib.mssa_last_error.argtypes = []
@@ -236,6 +240,31 @@ def mssa_forward(plan, q_win, k_sink, v_sink, k_hist, v_hist, k_win, v_win, work
     _check(lib.mssa_forward(plan.handle, _ptr(q_win), _ptr(k_sink), _ptr(v_sink), _ptr(k_hist),
                             _ptr(v_hist), _ptr(k_win), _ptr(v_win), _ptr(workspace), wb,
                             _ptr(out), _stream(stream)), "mssa_forward")
+
+
+def mssa_forward_lse(plan, q_win, k_sink, v_sink, k_hist, v_hist, k_win, v_win, workspace, out, lse,
+                     workspace_bytes=None, stream=None):
+    wb = _nbytes(workspace) if workspace_bytes is None else int(workspace_bytes)
+    _check(lib.mssa_forward_lse(plan.handle, _ptr(q_win), _ptr(k_sink), _ptr(v_sink), _ptr(k_hist),
+                                _ptr(v_hist), _ptr(k_win), _ptr(v_win), _ptr(workspace), wb,
+                                _ptr(out), _ptr(lse), _stream(stream)), "mssa_forward_lse")
+
+
+def mssa_backward_workspace_size(plan):
+    n = ctypes.c_int64()
+    _check(lib.mssa_backward_workspace_size(plan.handle, ctypes.byref(n)), "mssa_backward_workspace_size")
+    return n.value
+
+
+def mssa_backward(plan, q_win, k_sink, v_sink, k_hist, v_hist, k_win, v_win, out, lse, d_out, workspace,
+                  dq_win, dk_sink, dv_sink, dk_hist, dv_hist, dk_win, dv_win, workspace_bytes=None,
+                  stream=None):
+    wb = _nbytes(workspace) if workspace_bytes is None else int(workspace_bytes)
+    _check(lib.mssa_backward(plan.handle, _ptr(q_win), _ptr(k_sink), _ptr(v_sink), _ptr(k_hist),
+                             _ptr(v_hist), _ptr(k_win), _ptr(v_win), _ptr(out), _ptr(lse), _ptr(d_out),
+                             _ptr(workspace), wb, _ptr(dq_win), _ptr(dk_sink), _ptr(dv_sink),
+                             _ptr(dk_hist), _ptr(dv_hist), _ptr(dk_win), _ptr(dv_win), _stream(stream)),
+           "mssa_backward")
 
 
 class Ring:

@@ -246,3 +246,22 @@ def test_pooled_hist_ring_calls_checked():
     with pytest.raises(mssa.MssaError) as e:
         mssa.mssa_pool_hist_ring(ring, fake, fake, [None, None], pools, stream=0)
     assert e.value.status == mssa.MSSA_ERR_INVALID_ARG
+
+
+def test_backward_calls_checked():
+    """Bad calls are rejected before anything is enqueued."""
+    desc = dict(num_states=2, scales=[1, 2], grid_h=12, grid_w=8, frames_per_state=2, sink_frames=0,
+                hist_frames=2, num_heads=2, head_dim=128)
+    plan = mssa.mssa_plan_create(dict(desc, dtype="bf16"))
+    fake = 1 << 20
+    with pytest.raises(mssa.MssaError) as e:
+        mssa.mssa_backward(plan, fake, None, None, fake, fake, fake, fake, fake, fake, fake, fake,
+                           fake + 4096, None, None, fake + 8192, fake + 8192, fake + 8192, fake + 8192,
+                           workspace_bytes=16, stream=0)
+    assert e.value.status == mssa.MSSA_ERR_WORKSPACE
+    wsz = mssa.mssa_backward_workspace_size(plan)
+    with pytest.raises(mssa.MssaError) as e:
+        mssa.mssa_backward(plan, fake, None, None, fake, fake, fake, fake, fake, fake, fake, fake,
+                           fake, None, None, fake + 8192, fake + 8192, fake + 8192, fake + 8192,
+                           workspace_bytes=wsz, stream=0)
+    assert e.value.status == mssa.MSSA_ERR_INVALID_ARG  # dq aliases q

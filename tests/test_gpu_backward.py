@@ -1,0 +1,208 @@
+"""GPU parity of the MSSA backward (through the C ABI) against the fp64
+backward oracle: pool -> forward with lse -> backward on one workspace, every
+gradient compared with the oracle's on the same seeded inputs.
+
+Tolerances (relative to each gradient tensor, as for the forward's relative
+guard): bf16 plans round the probabilities and dS to bf16 as matrix-core
+operands (relative error 2^-9 per term) and the gradients once more on
+output, so the rms error stays a few 1e-3 of the tensor's rms; the bound is
+1e-2 rms and 5e-2 of the tensor's max for the worst element.  fp32 plans
+compute in fp32: 1e-5 rms, 1e-4 max."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_20940_amd import mssa
+from paper_2607_20940_amd.inputs import make_grad_output, make_inputs, to_f64
+from paper_2607_20940_amd.workloads import WORKLOADS, input_shapes
+
+from gpu_common import errors, from_device, to_device
+
+pytestmark = pytest.mark.gpu
+
+NAMES = ("q_win", "k_sink", "v_sink", "k_hist", "v_hist", "k_win", "v_win")
+GRAD_TOL = {"f32": dict(rel_rms=1e-5, rel_max=1e-4), "bf16": dict(rel_rms=1e-2, rel_max=5e-2)}
+AMP = 1.0 / np.sqrt(128.0)
+
+
+def _desc(T, scales, H, W, F=1, S=1, Hh=1, nh=1, d=128, **kw):
+    return dict(num_states=T, scales=list(scales), grid_h=H, grid_w=W, frames_per_state=F,
+                sink_frames=S, hist_frames=Hh, num_heads=nh, head_dim=d, **kw)
+
+
+class BwdRun:
+    """Plan, seeded inputs and output gradient, one training pass on cuda:0."""
+
+    def __init__(self, desc, dtype, seed, amp, gamp=1.0):
+        self.desc, self.dtype = dict(desc), dtype
+        self.plan = mssa.mssa_plan_create(dict(desc, dtype=dtype))
+        self.info = self.plan.info()
+        shapes = input_shapes(desc, self.info["n_q"], self.info["n_sink_tok"], self.info["n_hist_tok"])
+        self.x = make_inputs(shapes, seed, amp, dtype)
+        self.go = make_grad_output(shapes["q_win"], seed + 7919, gamp, dtype)
+        self.d = {k: to_device(v, dtype) for k, v in self.x.items()}
+        self.d_out = to_device(self.go, dtype)
+        wsz = mssa.mssa_backward_workspace_size(self.plan)
+        assert wsz >= self.info["workspace_bytes"]
+        self.ws = torch.empty(max(256, wsz), dtype=torch.uint8, device="cuda")
+        self.out = torch.empty_like(self.d["q_win"])
+        self.lse = torch.empty(desc["num_heads"] * self.info["n_q"], dtype=torch.float32, device="cuda")
+
+    def run(self):
+        d = self.d
+        mssa.mssa_pool_kv(self.plan, d["k_hist"], d["v_hist"], d["k_win"], d["v_win"], self.ws)
+        mssa.mssa_forward_lse(self.plan, d["q_win"], d["k_sink"], d["v_sink"], d["k_hist"], d["v_hist"],
+                              d["k_win"], d["v_win"], self.ws, self.out, self.lse)
+        g = {k: (None if d[k] is None else torch.empty_like(d[k])) for k in NAMES}
+        mssa.mssa_backward(self.plan, d["q_win"], d["k_sink"], d["v_sink"], d["k_hist"], d["v_hist"],
+                           d["k_win"], d["v_win"], self.out, self.lse, self.d_out, self.ws,
+                           g["q_win"], g["k_sink"], g["v_sink"], g["k_hist"], g["v_hist"], g["k_win"],
+                           g["v_win"])
+        torch.cuda.synchronize()
+        self.g = g
+        return g
+
+    def grads(self):
+        return {k: (None if t is None else from_device(t, self.dtype)) for k, t in self.g.items()}
+
+    def x64(self):
+        return {k: (None if v is None else to_f64(v, self.dtype)) for k, v in self.x.items()}
+
+    def oracle(self, heads=None):
+        x = self.x64()
+        return oracle.mssa_backward(self.desc, *(x[k] for k in NAMES), to_f64(self.go, self.dtype),
+                                    heads=heads)
+
+    def oracle_lse(self):
+        """log sum exp of the scaled scores over each query's context (from
+        the forward oracle's contexts), [heads, n_q]."""
+        x = self.x64()
+        nh = self.desc["num_heads"]
+        sc = oracle.softmax_scale(self.desc)
+        out = np.empty((nh, self.info["n_q"]))
+        for (s, qb, qe) in oracle.query_groups(self.desc):
+            for h in range(nh):
+                hd = lambda a: None if a is None else a[:, h]  # noqa: E731
+                kc = oracle.context(self.desc, s, hd(x["k_sink"]), hd(x["k_hist"]), hd(x["k_win"]))
+                z = sc * (x["q_win"][qb:qe, h] @ kc.T)
+                m = z.max(axis=1)
+                out[h, qb:qe] = m + np.log(np.exp(z - m[:, None]).sum(axis=1))
+        return out
+
+
+def _assert_grads(got, ref, dtype, label, heads=None):
+    tol = GRAD_TOL[dtype]
+    res = {}
+    for k in NAMES:
+        gk = "d" + k
+        if got[k] is None:
+            assert ref[gk].size == 0, (label, k)
+            continue
+        a, b = got[k], ref[gk]
+        if heads is not None:
+            a, b = a[:, heads], b[:, heads]
+        assert np.isfinite(a).all(), f"{label}: non-finite {gk}"
+        assert np.abs(b).max() > 0, f"{label}: degenerate reference {gk}"
+        e = errors(a, b)
+        bad = {t: (e[t], tol[t]) for t in tol if not e[t] <= tol[t]}
+        assert not bad, f"{label}: {gk} errors above tolerance {bad}"
+        res[gk] = (round(e["rel_rms"], 6), round(e["rel_max"], 6))
+    return res
+
+
+def _check(desc, dtype, seed, amp, label, gamp=1.0):
+    print(f"[bwd] {label} desc={desc} dtype={dtype} seed={seed}", flush=True)
+    r = BwdRun(desc, dtype, seed, amp, gamp)
+    got = r.run()
+    res = _assert_grads(r.grads(), r.oracle(), dtype, label)
+    lse = r.lse.cpu().numpy().astype(np.float64).reshape(desc["num_heads"], -1)
+    lerr = np.abs(lse - r.oracle_lse()).max()
+    assert lerr <= (1e-5 if dtype == "f32" else 1e-3), f"{label}: lse off by {lerr}"
+    print(f"[bwd] {label} ok lse_err={lerr:.2e} {res}", flush=True)
+    return r, got
+
+
+SMALL = {
+    "ragged_3level_d128": (_desc(4, [1, 1, 2, 4], 10, 13, F=2, S=1, Hh=3, nh=3), 7),
+    "ragged_3level_d64": (_desc(4, [1, 1, 2, 4], 10, 13, F=2, S=1, Hh=3, nh=3, d=64), 8),
+    "paper_schedule_small": (_desc(5, [1, 1, 2, 2, 2], 6, 10, F=3, S=1, Hh=2, nh=2), 9),
+    "no_history": (_desc(3, [1, 2, 2], 9, 9, F=2, S=2, Hh=0, nh=2), 10),
+    "no_sink": (_desc(2, [1, 2], 12, 8, F=2, S=0, Hh=2, nh=2), 11),
+    "single_state_native": (_desc(1, [1], 11, 17, F=3, S=1, Hh=1, nh=2), 12),
+    "all_coarse_equal": (_desc(3, [2, 2, 2], 9, 14, F=1, S=1, Hh=2, nh=1), 13),
+    "tiny_runs": (_desc(3, [1, 2, 4], 2, 3, F=1, S=1, Hh=1, nh=1), 14),
+    "eight_states": (_desc(8, [1, 1, 2, 2, 4, 4, 8, 8], 16, 16, F=1, S=1, Hh=1, nh=1, d=64), 15),
+    "stride_ragged": (_desc(4, [1, 1, 2, 4], 10, 13, F=2, S=1, Hh=3, nh=2, resample="stride"), 16),
+    "stride_all_coarse": (_desc(3, [2, 2, 4], 9, 14, F=1, S=1, Hh=2, nh=1, d=64, resample="stride"), 17),
+}
+
+
+@pytest.mark.parametrize("name", sorted(SMALL))
+def test_backward_bf16_small(name):
+    desc, seed = SMALL[name]
+    _check(desc, "bf16", seed, AMP, name)
+
+
+@pytest.mark.parametrize("name", ["ragged_3level_d128", "paper_schedule_small", "stride_ragged"])
+def test_backward_bf16_unit_logits(name):
+    """N(0, 1) inputs: logits of unit spread, a far from uniform softmax."""
+    desc, seed = SMALL[name]
+    _check(desc, "bf16", seed + 100, 1.0, name + "_unit")
+
+
+def test_backward_f32_tiny_workload():
+    w = WORKLOADS["tiny_f32"]
+    _check(w["desc"], "f32", w["seed"], w["amplitude"], "tiny_f32")
+
+
+@pytest.mark.parametrize("resample", ["mean", "stride"])
+def test_backward_f32_ragged_d128(resample):
+    _check(_desc(3, [1, 2, 4], 7, 11, F=2, S=1, Hh=2, nh=2, resample=resample), "f32", 21, 1.0,
+           f"f32_d128_{resample}")
+
+
+def test_backward_deterministic():
+    desc, seed = SMALL["ragged_3level_d128"]
+    r = BwdRun(desc, "bf16", seed, 1.0)
+    a = {k: (None if t is None else t.clone()) for k, t in r.run().items()}
+    b = r.run()
+    for k in NAMES:
+        if a[k] is not None:
+            assert torch.equal(a[k].view(torch.int16), b[k].view(torch.int16)), k
+
+
+def test_backward_zero_gradients_fail_guard():
+    desc, seed = SMALL["paper_schedule_small"]
+    r = BwdRun(desc, "bf16", seed, AMP)
+    r.run()
+    ref = r.oracle()
+    zero = {k: (None if v is None else np.zeros_like(v)) for k, v in r.grads().items()}
+    with pytest.raises(AssertionError):
+        _assert_grads(zero, ref, "bf16", "zeros")
+
+
+def test_backward_full_size_one_head_and_sum_rules():
+    """The 1.3B-shaped layer (12 x 128, 30 x 52, 6 history frames) in the
+    launch configuration of the benchmark: every gradient of one head against
+    the oracle, and for all heads the two sum rules (sum of dV over every
+    source token equals the sum of dO; sum of dK is zero)."""
+    w = WORKLOADS["wan13b_layer"]
+    print("[bwd] full-size wan13b_layer", flush=True)
+    r = BwdRun(w["desc"], w["dtype"], w["seed"], w["amplitude"])
+    r.run()
+    got = r.grads()
+    head = 7
+    res = _assert_grads(got, r.oracle(heads=[head]), "bf16", "wan13b_layer", heads=[head])
+    print(f"[bwd] wan13b_layer head {head} {res}", flush=True)
+    go = to_f64(r.go, "bf16")
+    dv = sum(got[k].sum(axis=0) for k in ("v_sink", "v_hist", "v_win"))
+    dk = sum(got[k].sum(axis=0) for k in ("k_sink", "k_hist", "k_win"))
+    want = go.sum(axis=0)
+    scale_v = np.abs(got["v_win"]).sum(axis=0).max()
+    scale_k = np.abs(got["k_win"]).sum(axis=0).max()
+    assert np.abs(dv - want).max() <= 1e-2 * scale_v, np.abs(dv - want).max()
+    assert np.abs(dk).max() <= 1e-2 * scale_k, np.abs(dk).max()
+    print(f"[bwd] sum rules: dV {np.abs(dv - want).max():.3e} (scale {scale_v:.3e}), "
+          f"dK {np.abs(dk).max():.3e} (scale {scale_k:.3e})", flush=True)
