@@ -26,6 +26,10 @@
 //                and walks the scale's queries in 64-query stages: S = Q K^T,
 //                dP = dO V^T (lane = key), then dV^T += dO^T P and
 //                dK^T += Q^T dS with dO^T, Q^T from transposing reads.
+// The dQ kernel keeps its LDS operand reads several MFMAs ahead and overlaps
+// one key block's softmax with the next block's MFMAs; in the dK/dV kernel
+// (K, V, dK and dV per wave fill the register file) the same scheme measured
+// slower than the plain loop, which is kept.
 // Rows past the end of a context or query range are zero-filled; their
 // probabilities are forced to zero.
 //
@@ -111,6 +115,46 @@ __global__ __launch_bounds__(kDotThreads) void dot_kernel(DotArgs a) {
   a.dsum[static_cast<int64_t>(h) * a.n_q + q] = acc;
 }
 
+// ------------------------------------------------------------------ bf16 kernels
+
+// Buffer resource (gfx9 layout) over `bytes` bytes from `base`: loads past
+// the end return zeros, which zero-fills ragged stage tiles without selects.
+__device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0),
+                                           static_cast<int>(bytes), 0x00020000);
+}
+
+// N MFMAs whose A operands come from LDS: operand i is read by rd(i) (NRD LDS
+// instructions) L operands ahead of its MFMA mf(i, a), so LDS latency hides
+// behind L MFMAs.  VALU (TRANS) vector (transcendental) instructions of the
+// same region, e.g. the softmax of the previous 32-row block, are placed
+// after each MFMA so they issue while the matrix core is busy.  Scheduling
+// group barriers fix this interleave (the compiler would otherwise hoist the
+// reads or sink each next to its MFMA).
+template <int N, int L, int NRD, int VALU, int TRANS, typename Rd, typename Mf>
+__device__ __forceinline__ void mfma_pipe(Rd&& rd, Mf&& mf) {
+  bf16x8 ring[L];
+#pragma unroll
+  for (int i = 0; i < L; ++i)
+    if (i < N) ring[i] = rd(i);
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    const bf16x8 av = ring[i % L];
+    mf(i, av);
+    if (i + L < N) ring[i % L] = rd(i + L);
+  }
+#pragma unroll
+  for (int i = 0; i < (N < L ? N : L); ++i) __builtin_amdgcn_sched_group_barrier(0x100, NRD, 0);
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    if (VALU > 0) __builtin_amdgcn_sched_group_barrier(0x002, VALU, 0);
+    if (TRANS > 0) __builtin_amdgcn_sched_group_barrier(0x400, TRANS, 0);
+    if (i + L < N) __builtin_amdgcn_sched_group_barrier(0x100, NRD, 0);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+}
+
 // ------------------------------------------------------------------ bf16: dQ
 
 template <int D>
@@ -119,7 +163,7 @@ __global__ __launch_bounds__(kBwdThreads) void dq_kernel(BwdArgs a) {
   constexpr int KS = L::KS, DB = L::DB, CPR = L::CPR, ASTR = L::ASTR, TSTR = L::TSTR, RPL = L::RPL;
   constexpr int BN = kBwdKS, NLD = BN / RPL;
   constexpr int KA = BN * ASTR, KT = BN * TSTR, STAGE = 2 * KA + KT;  // K rows | V rows | K transposing
-  static_assert(NLD * RPL == BN, "stage load must divide evenly");
+  static_assert(NLD * RPL == BN && BN == 64, "stage load must divide evenly; two 32-key blocks");
   __shared__ __attribute__((aligned(16))) __bf16 lds[2 * STAGE];
 
   int n_blocks = 0;
@@ -159,16 +203,44 @@ __global__ __launch_bounds__(kBwdThreads) void dq_kernel(BwdArgs a) {
 #pragma unroll
   for (int db = 0; db < DB; ++db) acc[db] = f32x16{};
 
+  // Stage tiles of BN keys inside one run at a time; rows past the run's end
+  // read as zeros and are masked.
+  const int nr = G.n_runs;
+  int nst = 0;
+  for (int r = 0; r < nr; ++r) nst += (G.runs[r].n_tok + BN - 1) / BN;
+  struct Stream {
+    const __bf16* k;
+    const __bf16* v;
+    int left;  // tokens of the current run from k on
+    int r;
+  };
+  const int64_t tile_step = static_cast<int64_t>(BN) * ld;
+  auto seek = [&](Stream& s, int r) {
+    while (r < nr && G.runs[r].n_tok == 0) ++r;
+    s.r = r;
+    if (r < nr) {
+      s.k = static_cast<const __bf16*>(G.runs[r].k) + hoff;
+      s.v = static_cast<const __bf16*>(G.runs[r].v) + hoff;
+      s.left = G.runs[r].n_tok;
+    }
+  };
+  auto step = [&](Stream& s) {
+    s.left -= BN;
+    s.k += tile_step;
+    s.v += tile_step;
+    if (s.left <= 0) seek(s, s.r + 1);
+  };
+  const uint32_t row_bytes = static_cast<uint32_t>(ld) * 2;
   const int ld_row = tid / CPR, ld_col = (tid % CPR) * 8;
+  const uint32_t g_off = ld_row * row_bytes + ld_col * 2;
   bf16x8 pk[NLD], pv[NLD];
-  auto load_stage = [&](int j0) {
+  auto load = [&](const Stream& s) {
+    const uint32_t bytes = static_cast<uint32_t>(min(s.left, BN) - 1) * row_bytes + D * 2;
+    const auto rk = make_rsrc(s.k, bytes), rv = make_rsrc(s.v, bytes);
 #pragma unroll
     for (int i = 0; i < NLD; ++i) {
-      const int j = j0 + ld_row + i * RPL;
-      const __bf16* kp = ctx_row<__bf16>(G, j, false, ld);
-      const __bf16* vp = ctx_row<__bf16>(G, j, true, ld);
-      pk[i] = kp ? *reinterpret_cast<const bf16x8*>(kp + hoff + ld_col) : bf16x8{};
-      pv[i] = vp ? *reinterpret_cast<const bf16x8*>(vp + hoff + ld_col) : bf16x8{};
+      pk[i] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rk, g_off + i * RPL * row_bytes, 0, 0));
+      pv[i] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rv, g_off + i * RPL * row_bytes, 0, 0));
     }
   };
   auto store_stage = [&](int buf) {
@@ -183,48 +255,68 @@ __global__ __launch_bounds__(kBwdThreads) void dq_kernel(BwdArgs a) {
   };
   const int t_rd = tr_offset(lane, TSTR);
 
+  // One stage: S^T, dP^T of key block 0; the same for block 1 with block 0's
+  // softmax interleaved; dQ^T from block 0 with block 1's softmax
+  // interleaved; dQ^T from block 1.
   auto compute = [&](int buf, int nvalid) {
     const __bf16* Ka = lds + buf * STAGE;
     const __bf16* Va = Ka + KA;
     const __bf16* Kt = Ka + 2 * KA + t_rd;
-    f32x16 s[BN / 32], dp[BN / 32];
-#pragma unroll
-    for (int kb = 0; kb < BN / 32; ++kb)
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const bf16x8 ak = *reinterpret_cast<const bf16x8*>(Ka + (kb * 32 + n) * ASTR + hh * 8 + ks * 16);
-        const bf16x8 av = *reinterpret_cast<const bf16x8*>(Va + (kb * 32 + n) * ASTR + hh * 8 + ks * 16);
-        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ak, qf[ks], ks == 0 ? f32x16{} : s[kb], 0, 0, 0);
-        dp[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, gf[ks], ks == 0 ? f32x16{} : dp[kb], 0, 0, 0);
-      }
-    // dS^T = P^T * (dP^T - rowsum), element e of block kb is key kb*32 + 8(e/4) + 4hh + e%4.
-    bf16x8 dsb[BN / 32][2];
-#pragma unroll
-    for (int kb = 0; kb < BN / 32; ++kb)
+    f32x16 s[2], dp[2];
+    bf16x8 dsb[2][2];
+    auto rows = [&](int kb) {
+      return [&, kb](int i) {
+        const __bf16* base = (i & 1) ? Va : Ka;
+        return *reinterpret_cast<const bf16x8*>(base + (kb * 32 + n) * ASTR + hh * 8 + (i >> 1) * 16);
+      };
+    };
+    auto sdp = [&](int kb) {
+      return [&, kb](int i, bf16x8 av) {
+        const int ks = i >> 1;
+        if (i & 1)
+          dp[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, gf[ks], ks == 0 ? f32x16{} : dp[kb], 0, 0, 0);
+        else
+          s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qf[ks], ks == 0 ? f32x16{} : s[kb], 0, 0, 0);
+      };
+    };
+    // dS^T = P^T * (dP^T - rowsum); element e of block kb is key kb*32 + 8(e/4) + 4hh + e%4.
+    auto soft = [&](int kb) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int key = kb * 32 + 8 * (e >> 2) + 4 * hh + (e & 3);
         const float p = key < nvalid ? __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][e], c, -lse2)) : 0.f;
         dsb[kb][e >> 3][e & 7] = static_cast<__bf16>(p * (dp[kb][e] - dsum));
       }
-#pragma unroll
-    for (int kb = 0; kb < BN / 32; ++kb)
-#pragma unroll
-      for (int cc = 0; cc < 2; ++cc)
-#pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          const bf16x8 at = tr_read(Kt + (kb * 32 + cc * 16) * TSTR + db * 32, TSTR);
-          acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(at, dsb[kb][cc], acc[db], 0, 0, 0);
-        }
+    };
+    auto trs = [&](int kb) {
+      return [&, kb](int i) { return tr_read(Kt + (kb * 32 + (i / DB) * 16) * TSTR + (i % DB) * 32, TSTR); };
+    };
+    auto dq = [&](int kb) {
+      return [&, kb](int i, bf16x8 at) {
+        acc[i % DB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(at, dsb[kb][i / DB], acc[i % DB], 0, 0, 0);
+      };
+    };
+    mfma_pipe<2 * KS, 6, 1, 0, 0>(rows(0), sdp(0));
+    soft(0);
+    mfma_pipe<2 * KS, 6, 1, 6, 1>(rows(1), sdp(1));
+    soft(1);
+    mfma_pipe<2 * DB, 4, 2, 12, 2>(trs(0), dq(0));
+    mfma_pipe<2 * DB, 4, 2, 0, 0>(trs(1), dq(1));
   };
 
-  const int nst = (G.n_kv + BN - 1) / BN;
-  load_stage(0);
+  Stream ls, cs;
+  seek(ls, 0);
+  cs = ls;
+  load(ls);
   store_stage(0);
   __syncthreads();
   for (int st = 0; st < nst; ++st) {
-    if (st + 1 < nst) load_stage((st + 1) * BN);
-    compute(st & 1, min(BN, G.n_kv - st * BN));
+    if (st + 1 < nst) {
+      step(ls);
+      load(ls);
+    }
+    compute(st & 1, min(cs.left, BN));
+    step(cs);
     if (st + 1 < nst) store_stage((st + 1) & 1);
     __syncthreads();
   }
