@@ -12,3 +12,4 @@ from .mssa_oracle import (  # noqa: F401
     window_frames,
 )
 from .mssa_backward import attention_backward, mssa_backward, pool_frame_adjoint  # noqa: F401,E402
+from .mssa_tiers import patch_embed, patch_unembed, patchify, qkv_project, unpatchify  # noqa: F401,E402
