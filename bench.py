@@ -243,6 +243,77 @@ def bench_training(args):
     print(json.dumps(result), flush=True)
 
 
+def bench_tiers(args):
+    """The steps on either side of the attention for the 1.3B-shaped window
+    (16 latent channels, patch 2, width 1536 = 12 x 128): tier patch
+    embedding, QKV projection and de-embedding, synthetic weights."""
+    import torch
+
+    from paper_2607_20940_amd import mssa
+    from paper_2607_20940_amd.workloads import WORKLOADS
+
+    desc = WORKLOADS["wan13b_layer"]["desc"]
+    C, patch = 16, 2
+    hidden = desc["num_heads"] * desc["head_dim"]
+    plan = mssa.mssa_plan_create(dict(desc, dtype="bf16"))
+    info = plan.info()
+    nq = info["n_q"]
+    tier = mssa.tier_desc(C, patch, hidden)
+    gen = torch.Generator(device="cuda").manual_seed(7)
+    rnd = lambda *s: (torch.randn(*s, generator=gen, device="cuda") * 0.05).to(torch.bfloat16)  # noqa: E731
+    frames = desc["num_states"] * desc["frames_per_state"]
+    lat = rnd(frames, C, desc["grid_h"] * patch, desc["grid_w"] * patch)
+    kps = [C * (patch * s) ** 2 for s in info["group_scale"]]
+    w_in = [rnd(hidden, kp) for kp in kps]
+    b_in = [rnd(hidden) for _ in kps]
+    w_out = [rnd(kp, hidden) for kp in kps]
+    b_out = [rnd(kp) for kp in kps]
+    w_qkv, b_qkv = rnd(3 * hidden, hidden), rnd(3 * hidden)
+    ws = torch.empty(mssa.mssa_tier_workspace_size(plan, tier), dtype=torch.uint8, device="cuda")
+    tok = torch.empty((nq, hidden), dtype=torch.bfloat16, device="cuda")
+    q, k, v = (torch.empty_like(tok) for _ in range(3))
+    out = torch.empty_like(lat)
+    stream = torch.cuda.current_stream()
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        mssa.mssa_patch_embed(plan, tier, lat, w_in, b_in, ws, tok)
+        if ev is not None:
+            ev[1].record(stream)
+        mssa.mssa_qkv_project(nq, hidden, tok, w_qkv, b_qkv, q, k, v)
+        if ev is not None:
+            ev[2].record(stream)
+        mssa.mssa_patch_unembed(plan, tier, q, w_out, b_out, ws, out)
+        if ev is not None:
+            ev[3].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    for e in evs:
+        step(e)
+    torch.cuda.synchronize()
+    t = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(3)] for e in evs]).mean(axis=0)
+    qkv_flops = 2.0 * nq * hidden * 3 * hidden
+    emb_flops = sum(2.0 * (g1 - g0) * hidden * kp for g0, g1, kp in zip(info["q_begin"], info["q_end"], kps))
+    result = {
+        "metric": "MSP tier steps around MSSA: patch embedding, QKV projection, de-embedding (1 GPU)",
+        "value": round(qkv_flops / (t[1] * 1e-3) / 1e12, 2), "unit": "TFLOP/s (QKV projection)",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(float(t.sum()), 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "wan13b_layer tiers", "latent_channels": C, "patch": patch, "hidden": hidden,
+                   "n_q": nq},
+        "patch_embed_ms": round(float(t[0]), 4), "qkv_ms": round(float(t[1]), 4),
+        "patch_unembed_ms": round(float(t[2]), 4),
+        "qkv_pct_of_bf16_peak": round(100 * qkv_flops / (t[1] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 2),
+        "embed_unembed_tflops": round(2 * emb_flops / ((t[0] + t[2]) * 1e-3) / 1e12, 2),
+    }
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -255,6 +326,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--layers", type=int, default=0, help="streaming: layers (default 30)")
     ap.add_argument("--passes", type=int, default=0, help="streaming: rolling passes (default 64)")
+    ap.add_argument("--tiers", action="store_true",
+                    help="time the tier patch embedding, QKV projection and de-embedding instead")
     ap.add_argument("--training", action="store_true",
                     help="time pool + forward (with lse) + backward of one layer instead")
     ap.add_argument("--pooled-ring", action="store_true",
@@ -275,6 +348,9 @@ def main():
         return
     if args.training:
         bench_training(args)
+        return
+    if args.tiers:
+        bench_tiers(args)
         return
     if args.copy_calibration_mb:
         import torch

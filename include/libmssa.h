@@ -225,6 +225,47 @@ mssa_status mssa_backward(mssa_plan plan, const void* q_win, const void* k_sink,
                           int64_t workspace_bytes, void* dq_win, void* dk_sink, void* dv_sink, void* dk_hist,
                           void* dv_hist, void* dk_win, void* dv_win, void* stream);
 
+/* --------------------------------------------------------------- MSP tiers
+ * The steps on either side of the attention (Sec. 4.1, Multi-Scale
+ * Patchification): window state l is tokenized with patch p * p_l by its
+ * tier's own patch embedding (each (p p_l) x (p p_l) patch of all latent
+ * channels, flattened in (channel, row, column) order, times the tier's
+ * weights, plus bias: a 2-D convolution with kernel = stride = p p_l); the
+ * de-embedding maps tokens back to pixels; the attention's q, k, v are one
+ * linear projection of the tokens.  Patches past a ragged frame edge see
+ * zeros; de-embedded pixels past it are dropped.  bf16 plans only (fp32
+ * accumulation); MSSA_ERR_UNSUPPORTED for fp32 plans or when
+ * C * (p * scale)^2 is not a multiple of 8. */
+typedef struct {
+  int32_t latent_channels;  /* C */
+  int32_t patch;            /* p: native patch size in latent pixels (the plan's grid is in patches) */
+  int32_t hidden;           /* model width (heads x head_dim for the attention), multiple of 8 */
+} mssa_tier_desc;
+
+/* Device workspace bytes of mssa_patch_embed / mssa_patch_unembed. */
+mssa_status mssa_tier_workspace_size(mssa_plan plan, const mssa_tier_desc* tier, int64_t* bytes);
+
+/* latent [T*F, C, grid_h * p, grid_w * p] bf16 (window frames in window
+ * order) -> tokens [n_q, hidden] bf16 in the attention's window token order.
+ * w_embed[g] / b_embed[g]: query group g's tier (mssa_plan_info order, scale
+ * s = group_scale[g]), [hidden, C * (p s)^2] and [hidden] bf16, device. */
+mssa_status mssa_patch_embed(mssa_plan plan, const mssa_tier_desc* tier, const void* latent,
+                             const void* const* w_embed, const void* const* b_embed, void* workspace,
+                             int64_t workspace_bytes, void* tokens, void* stream);
+
+/* tokens [n_q, hidden] -> latent [T*F, C, grid_h * p, grid_w * p] (bf16):
+ * w_out[g] [C * (p s)^2, hidden], b_out[g] [C * (p s)^2]. */
+mssa_status mssa_patch_unembed(mssa_plan plan, const mssa_tier_desc* tier, const void* tokens,
+                               const void* const* w_out, const void* const* b_out, void* workspace,
+                               int64_t workspace_bytes, void* latent, void* stream);
+
+/* q, k, v = x W_qkv^T + b_qkv split in three blocks of `hidden` features:
+ * x [n_tokens, hidden], w_qkv [3 * hidden, hidden], b_qkv [3 * hidden],
+ * q, k, v [n_tokens, hidden] (= [n_tokens, heads, head_dim]), all bf16,
+ * device; outputs must not alias x. */
+mssa_status mssa_qkv_project(int64_t n_tokens, int32_t hidden, const void* x, const void* w_qkv,
+                             const void* b_qkv, void* q, void* k, void* v, void* stream);
+
 /* Streaming cache roll (Sec. 3.1, Eq. 2; Alg. 1 KV-cache update): after a
  * rolling pass the head state (window state 1, which must be at native
  * scale: scales[0] == 1) is emitted, and its F native frames of K and V

@@ -524,6 +524,176 @@ mssa_status mssa_backward(mssa_plan plan, const void* q_win, const void* k_sink,
   return check_device(mssa::launch_scatter(sa, static_cast<int>(blocks), bf16, hs), "backward scatter launch");
 }
 
+// ---------------------------------------------------------------- MSP tiers
+
+namespace {
+
+// Per query group: first window frame, frame count, patch size and patch-row
+// features, and the group's patch rows in the tier workspace.
+struct TierGroup {
+  int64_t frame0, n_frames;
+  int32_t P, kp;
+  int64_t rows_off;
+};
+
+mssa_status tier_layout(const mssa::Plan& p, const mssa_tier_desc* t, std::vector<TierGroup>& out, int64_t* bytes) {
+  if (!t) return fail(MSSA_ERR_INVALID_ARG, "tier must be non-null");
+  if (p.desc.dtype != MSSA_BF16) return fail(MSSA_ERR_UNSUPPORTED, "tier kernels take bf16 plans");
+  if (t->latent_channels < 1 || t->patch < 1 || t->hidden < 8 || t->hidden % 8 != 0)
+    return fail(MSSA_ERR_INVALID_ARG, "latent_channels and patch must be >= 1, hidden a positive multiple of 8");
+  out.clear();
+  int64_t off = 0, frame = 0;
+  for (const mssa::QGroup& g : p.groups) {
+    TierGroup tg{};
+    tg.P = t->patch * g.scale;
+    const int64_t kp = static_cast<int64_t>(t->latent_channels) * tg.P * tg.P;
+    if (kp % 8 != 0 || kp > (1 << 20)) return fail(MSSA_ERR_UNSUPPORTED, "C * (patch * scale)^2 must be a multiple of 8");
+    tg.kp = static_cast<int32_t>(kp);
+    const int64_t tok = static_cast<int64_t>((p.desc.grid_h + g.scale - 1) / g.scale) *
+                        ((p.desc.grid_w + g.scale - 1) / g.scale);
+    tg.n_frames = (g.q_end - g.q_begin) / tok;
+    tg.frame0 = frame;
+    frame += tg.n_frames;
+    tg.rows_off = off;
+    off += (static_cast<int64_t>(g.q_end - g.q_begin) * kp * 2 + 255) / 256 * 256;
+    out.push_back(tg);
+  }
+  *bytes = off;
+  return MSSA_OK;
+}
+
+}  // namespace
+
+mssa_status mssa_tier_workspace_size(mssa_plan plan, const mssa_tier_desc* tier, int64_t* bytes) {
+  if (!plan || !bytes) return fail(MSSA_ERR_INVALID_ARG, "plan and bytes must be non-null");
+  std::vector<TierGroup> tg;
+  return tier_layout(plan->p, tier, tg, bytes);
+}
+
+mssa_status mssa_patch_embed(mssa_plan plan, const mssa_tier_desc* tier, const void* latent,
+                             const void* const* w_embed, const void* const* b_embed, void* workspace,
+                             int64_t workspace_bytes, void* tokens, void* stream) {
+  if (!plan) return fail(MSSA_ERR_INVALID_ARG, "plan must be non-null");
+  const mssa::Plan& p = plan->p;
+  std::vector<TierGroup> tg;
+  int64_t need = 0;
+  mssa_status s = tier_layout(p, tier, tg, &need);
+  if (s != MSSA_OK) return s;
+  if (!latent || !w_embed || !b_embed || !tokens) return fail(MSSA_ERR_INVALID_ARG, "null argument");
+  if (!workspace || workspace_bytes < need) return fail(MSSA_ERR_WORKSPACE, "workspace smaller than mssa_tier_workspace_size");
+  if (!aligned16(latent) || !aligned16(tokens) || !aligned16(workspace))
+    return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
+  for (size_t g = 0; g < tg.size(); ++g)
+    if (!w_embed[g] || !b_embed[g] || !aligned16(w_embed[g])) return fail(MSSA_ERR_INVALID_ARG, "null or misaligned tier weights");
+  auto hs = static_cast<hipStream_t>(stream);
+  const int32_t H = p.desc.grid_h * tier->patch, W = p.desc.grid_w * tier->patch, hid = tier->hidden;
+  for (size_t g = 0; g < tg.size(); ++g) {
+    const TierGroup& t = tg[g];
+    const mssa::QGroup& Q = p.groups[g];
+    mssa::PatchArgs pa{};
+    pa.latent = const_cast<void*>(latent);
+    pa.rows = static_cast<char*>(workspace) + t.rows_off;
+    pa.frame0 = t.frame0;
+    pa.n_frames = t.n_frames;
+    pa.C = tier->latent_channels;
+    pa.H = H;
+    pa.W = W;
+    pa.P = t.P;
+    pa.gh = (H + t.P - 1) / t.P;
+    pa.gw = (W + t.P - 1) / t.P;
+    s = check_device(mssa::launch_patchify(pa, hs), "patchify launch");
+    if (s != MSSA_OK) return s;
+    mssa::GemmArgs ga{};
+    ga.x = pa.rows;
+    ga.w = w_embed[g];
+    ga.bias = b_embed[g];
+    ga.y[0] = static_cast<char*>(tokens) + static_cast<int64_t>(Q.q_begin) * hid * 2;
+    ga.M = Q.q_end - Q.q_begin;
+    ga.N = hid;
+    ga.K = t.kp;
+    ga.split = hid;
+    ga.ldx = t.kp;
+    ga.ldy = hid;
+    s = check_device(mssa::launch_gemm(ga, hs), "patch embedding GEMM launch");
+    if (s != MSSA_OK) return s;
+  }
+  return MSSA_OK;
+}
+
+mssa_status mssa_patch_unembed(mssa_plan plan, const mssa_tier_desc* tier, const void* tokens,
+                               const void* const* w_out, const void* const* b_out, void* workspace,
+                               int64_t workspace_bytes, void* latent, void* stream) {
+  if (!plan) return fail(MSSA_ERR_INVALID_ARG, "plan must be non-null");
+  const mssa::Plan& p = plan->p;
+  std::vector<TierGroup> tg;
+  int64_t need = 0;
+  mssa_status s = tier_layout(p, tier, tg, &need);
+  if (s != MSSA_OK) return s;
+  if (!latent || !w_out || !b_out || !tokens) return fail(MSSA_ERR_INVALID_ARG, "null argument");
+  if (!workspace || workspace_bytes < need) return fail(MSSA_ERR_WORKSPACE, "workspace smaller than mssa_tier_workspace_size");
+  if (!aligned16(latent) || !aligned16(tokens) || !aligned16(workspace))
+    return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
+  for (size_t g = 0; g < tg.size(); ++g)
+    if (!w_out[g] || !b_out[g] || !aligned16(w_out[g])) return fail(MSSA_ERR_INVALID_ARG, "null or misaligned tier weights");
+  auto hs = static_cast<hipStream_t>(stream);
+  const int32_t H = p.desc.grid_h * tier->patch, W = p.desc.grid_w * tier->patch, hid = tier->hidden;
+  for (size_t g = 0; g < tg.size(); ++g) {
+    const TierGroup& t = tg[g];
+    const mssa::QGroup& Q = p.groups[g];
+    mssa::GemmArgs ga{};
+    ga.x = static_cast<const char*>(tokens) + static_cast<int64_t>(Q.q_begin) * hid * 2;
+    ga.w = w_out[g];
+    ga.bias = b_out[g];
+    ga.y[0] = static_cast<char*>(workspace) + t.rows_off;
+    ga.M = Q.q_end - Q.q_begin;
+    ga.N = t.kp;
+    ga.K = hid;
+    ga.split = t.kp;
+    ga.ldx = hid;
+    ga.ldy = t.kp;
+    s = check_device(mssa::launch_gemm(ga, hs), "patch de-embedding GEMM launch");
+    if (s != MSSA_OK) return s;
+    mssa::PatchArgs pa{};
+    pa.latent = latent;
+    pa.rows = ga.y[0];
+    pa.frame0 = t.frame0;
+    pa.n_frames = t.n_frames;
+    pa.C = tier->latent_channels;
+    pa.H = H;
+    pa.W = W;
+    pa.P = t.P;
+    pa.gh = (H + t.P - 1) / t.P;
+    pa.gw = (W + t.P - 1) / t.P;
+    s = check_device(mssa::launch_unpatchify(pa, hs), "unpatchify launch");
+    if (s != MSSA_OK) return s;
+  }
+  return MSSA_OK;
+}
+
+mssa_status mssa_qkv_project(int64_t n_tokens, int32_t hidden, const void* x, const void* w_qkv, const void* b_qkv,
+                             void* q, void* k, void* v, void* stream) {
+  if (n_tokens < 0 || n_tokens > 0x7fffffff || hidden < 8 || hidden % 8 != 0 || hidden > (1 << 20))
+    return fail(MSSA_ERR_INVALID_ARG, "n_tokens must fit int32 and hidden be a positive multiple of 8");
+  if (!x || !w_qkv || !b_qkv || !q || !k || !v) return fail(MSSA_ERR_INVALID_ARG, "null argument");
+  for (const void* t : {x, w_qkv, static_cast<const void*>(q), static_cast<const void*>(k), static_cast<const void*>(v)})
+    if (!aligned16(t)) return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
+  if (q == x || k == x || v == x) return fail(MSSA_ERR_INVALID_ARG, "outputs must not alias x");
+  mssa::GemmArgs ga{};
+  ga.x = x;
+  ga.w = w_qkv;
+  ga.bias = b_qkv;
+  ga.y[0] = q;
+  ga.y[1] = k;
+  ga.y[2] = v;
+  ga.M = static_cast<int32_t>(n_tokens);
+  ga.N = 3 * hidden;
+  ga.K = hidden;
+  ga.split = hidden;
+  ga.ldx = hidden;
+  ga.ldy = hidden;
+  return check_device(mssa::launch_gemm(ga, static_cast<hipStream_t>(stream)), "QKV GEMM launch");
+}
+
 mssa_status mssa_hist_append(mssa_plan plan, const void* k_win, const void* v_win, void* k_ring, void* v_ring,
                              int32_t ring_cap_frames, int32_t* ring_head, int32_t* ring_count, void* stream) {
   if (!plan) return fail(MSSA_ERR_INVALID_ARG, "null argument");

@@ -145,6 +145,33 @@ struct ScatterArgs {
   ScatterJobArgs jobs[kMaxScatterJobs];
 };
 
+// ---------------------------------------------------------------- MSP tiers
+
+constexpr int kTierThreads = 256;
+
+// Patch rows of consecutive latent frames of one tier: frame frame0 + f of
+// `latent` [frames, C, H, W] <-> rows [(f * gh + Y) * gw + X][C * P * P].
+struct PatchArgs {
+  void* latent;
+  void* rows;
+  int64_t frame0;
+  int64_t n_frames;
+  int32_t C, H, W, P;
+  int32_t gh, gw;
+};
+
+// Y = X W^T + b: X [M, K] (row stride ldx), W [N, K] dense, b [N]; output
+// feature j goes to y[j / split] at column j % split (row stride ldy).
+struct GemmArgs {
+  const void* x;
+  const void* w;
+  const void* bias;
+  void* y[3];
+  int32_t M, N, K;
+  int32_t split;
+  int64_t ldx, ldy;
+};
+
 struct PoolJobArgs {
   const void* src_k;        // first source token of the job (head 0, ch 0)
   const void* src_v;

@@ -26,6 +26,11 @@ hipError_t launch_bwd(const BwdArgs& a, int dq_blocks, int kv_blocks, int head_d
 // (n_blocks, 2): y = 0 for K, y = 1 for V.
 hipError_t launch_scatter(const ScatterArgs& a, int n_blocks, bool bf16, hipStream_t stream);
 
+// MSP tiers: patch rows of latent frames, the inverse, and Y = X W^T + b.
+hipError_t launch_patchify(const PatchArgs& a, hipStream_t stream);
+hipError_t launch_unpatchify(const PatchArgs& a, hipStream_t stream);
+hipError_t launch_gemm(const GemmArgs& a, hipStream_t stream);
+
 // Resident blocks per CU of the bf16 attention kernel (0 if unknown).
 int forward_blocks_per_cu(int head_dim);
 

@@ -1,0 +1,194 @@
+// Multi-Scale Patchification tiers (Ms. Forcing, Sec. 4.1): the steps on
+// either side of the attention.  Window state l is tokenized with patch
+// p * p_l by its tier's own patch embedding, a strided 2-D convolution
+// (each patch of every latent channel, flattened in (channel, row, column)
+// order, times the tier's weights, plus bias); the de-embedding maps tokens
+// back to pixels; the attention's q, k, v are one linear projection of the
+// tokens.  Patches past a ragged frame edge see zeros; de-embedded pixels
+// past it are dropped.
+//
+// Kernels:
+//   patchify_kernel    latent [frames, C, H, W] -> the patch rows of one
+//                      query group [tokens, C*P*P] (HBM-bound gather);
+//   gemm_kernel        Y[M, N] = X[M, K] W[N, K]^T + b on the matrix cores
+//                      (bf16 in, fp32 accumulation, bf16 out), 128 x 128
+//                      tiles in 32-deep stages double-buffered in LDS; the
+//                      output columns may be split over up to three tensors
+//                      (q | k | v);
+//   unpatchify_kernel  patch rows [tokens, C*P*P] -> latent pixels.
+#include <hip/hip_runtime.h>
+
+#include "kernels.hpp"
+
+namespace mssa {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+// One thread per 8-feature chunk of one patch row: feature k = (c, dy, dx) of
+// patch (Y, X) of frame f reads pixel (c, Y*P + dy, X*P + dx), zero past the
+// frame's edge.
+__global__ __launch_bounds__(kTierThreads) void patchify_kernel(PatchArgs a) {
+  const int kp = a.C * a.P * a.P;
+  const int cpr = kp / 8;
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * kTierThreads + threadIdx.x;
+  const int64_t gtok = static_cast<int64_t>(a.gh) * a.gw;
+  if (idx >= a.n_frames * gtok * cpr) return;
+  const int chunk = static_cast<int>(idx % cpr);
+  const int64_t t = idx / cpr;
+  const int X = static_cast<int>(t % a.gw);
+  const int Y = static_cast<int>((t / a.gw) % a.gh);
+  const int64_t f = t / gtok;
+  const __bf16* src = static_cast<const __bf16*>(a.latent) + (a.frame0 + f) * a.C * a.H * a.W;
+  bf16x8 v;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int k = chunk * 8 + e;
+    const int c = k / (a.P * a.P), r = k % (a.P * a.P);
+    const int y = Y * a.P + r / a.P, x = X * a.P + r % a.P;
+    v[e] = (y < a.H && x < a.W) ? src[(static_cast<int64_t>(c) * a.H + y) * a.W + x] : static_cast<__bf16>(0.f);
+  }
+  *reinterpret_cast<bf16x8*>(static_cast<__bf16*>(a.rows) + t * kp + chunk * 8) = v;
+}
+
+// One thread per pixel: pixel (c, y, x) of frame f comes from feature
+// (c, y % P, x % P) of patch (y / P, x / P).
+__global__ __launch_bounds__(kTierThreads) void unpatchify_kernel(PatchArgs a) {
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * kTierThreads + threadIdx.x;
+  const int64_t fpix = static_cast<int64_t>(a.C) * a.H * a.W;
+  if (idx >= a.n_frames * fpix) return;
+  const int x = static_cast<int>(idx % a.W);
+  const int y = static_cast<int>((idx / a.W) % a.H);
+  const int c = static_cast<int>((idx / (static_cast<int64_t>(a.W) * a.H)) % a.C);
+  const int64_t f = idx / fpix;
+  const int kp = a.C * a.P * a.P;
+  const int64_t tok = (f * a.gh + y / a.P) * a.gw + x / a.P;
+  const int k = (c * a.P + y % a.P) * a.P + x % a.P;
+  static_cast<__bf16*>(a.latent)[(a.frame0 + f) * fpix + (static_cast<int64_t>(c) * a.H + y) * a.W + x] =
+      static_cast<const __bf16*>(a.rows)[tok * kp + k];
+}
+
+// Y = X W^T + b.  A block owns a 128 x 128 output tile (128 rows of X, 128
+// output features); its 4 waves own 64 x 64 quarters as 2 x 2 matrix-core
+// tiles.  The MFMA computes the transposed tile (A = W rows, B = X rows) so
+// that a lane holds one output row and 16 features in runs of 4 (8-byte
+// stores).  K advances in 32-deep stages; the next stage's global loads are
+// in flight during the current stage's MFMAs.  Rows and features past the
+// matrix edges load as zeros and are not stored.
+constexpr int kGM = 128, kGN = 128, kGK = 32, kGStr = kGK + 8;  // LDS row stride: conflict-free 16-byte reads
+
+__global__ __launch_bounds__(kTierThreads) void gemm_kernel(GemmArgs a) {
+  __shared__ __attribute__((aligned(16))) __bf16 lds[2][2][kGM * kGStr];  // [stage][X | W]
+  const int tiles_m = (a.M + kGM - 1) / kGM;
+  const int tm = blockIdx.x % tiles_m, tn = blockIdx.x / tiles_m;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave & 1, wn = wave >> 1;
+  const int n32 = lane & 31, hh = lane >> 5;
+  const __bf16* X = static_cast<const __bf16*>(a.x);
+  const __bf16* W = static_cast<const __bf16*>(a.w);
+
+  // Stage loads: 128 rows x 4 chunks of 16 bytes per matrix, 2 chunks per thread.
+  const int lr = tid >> 2, lc = (tid & 3) * 8;
+  bf16x8 px[2], pw[2];
+  auto load = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int r = lr + i * 64;
+      const int64_t xm = static_cast<int64_t>(tm) * kGM + r, wn_ = static_cast<int64_t>(tn) * kGN + r;
+      const bool kok = k0 + lc < a.K;
+      px[i] = (kok && xm < a.M) ? *reinterpret_cast<const bf16x8*>(X + xm * a.ldx + k0 + lc) : bf16x8{};
+      pw[i] = (kok && wn_ < a.N) ? *reinterpret_cast<const bf16x8*>(W + wn_ * a.K + k0 + lc) : bf16x8{};
+    }
+  };
+  auto store = [&](int s) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int r = lr + i * 64;
+      *reinterpret_cast<bf16x8*>(&lds[s][0][r * kGStr + lc]) = px[i];
+      *reinterpret_cast<bf16x8*>(&lds[s][1][r * kGStr + lc]) = pw[i];
+    }
+  };
+
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+    for (int cb = 0; cb < 2; ++cb) acc[rb][cb] = f32x16{};
+
+  const int nst = (a.K + kGK - 1) / kGK;
+  load(0);
+  store(0);
+  __syncthreads();
+  for (int st = 0; st < nst; ++st) {
+    if (st + 1 < nst) load((st + 1) * kGK);
+    const __bf16* Xs = lds[st & 1][0];
+    const __bf16* Ws = lds[st & 1][1];
+#pragma unroll
+    for (int ks = 0; ks < kGK / 16; ++ks) {
+      bf16x8 xb[2], wa[2];
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        xb[j] = *reinterpret_cast<const bf16x8*>(Xs + (wm * 64 + j * 32 + n32) * kGStr + ks * 16 + hh * 8);
+        wa[j] = *reinterpret_cast<const bf16x8*>(Ws + (wn * 64 + j * 32 + n32) * kGStr + ks * 16 + hh * 8);
+      }
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb)
+          acc[rb][cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wa[cb], xb[rb], acc[rb][cb], 0, 0, 0);
+    }
+    if (st + 1 < nst) store((st + 1) & 1);
+    __syncthreads();
+  }
+
+  // acc[rb][cb] element e: row (wm*64 + rb*32 + n32), feature
+  // (wn*64 + cb*32 + 8(e/4) + 4hh + e%4) of the tile.
+  const __bf16* B = static_cast<const __bf16*>(a.bias);
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb) {
+    const int64_t row = static_cast<int64_t>(tm) * kGM + wm * 64 + rb * 32 + n32;
+    if (row >= a.M) continue;
+#pragma unroll
+    for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        const int col = tn * kGN + wn * 64 + cb * 32 + 8 * jj + 4 * hh;
+        if (col >= a.N) continue;
+        const int part = col / a.split, pc = col % a.split;  // 4 features never straddle a split (split % 4 == 0)
+        bf16x4 v;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] = static_cast<__bf16>(acc[rb][cb][4 * jj + i] + static_cast<float>(B[col + i]));
+        *reinterpret_cast<bf16x4*>(static_cast<__bf16*>(a.y[part]) + row * a.ldy + pc) = v;
+      }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_patchify(const PatchArgs& a, hipStream_t stream) {
+  const int64_t work = a.n_frames * a.gh * a.gw * (a.C * a.P * a.P / 8);
+  if (work <= 0) return hipSuccess;
+  hipLaunchKernelGGL(patchify_kernel, dim3(static_cast<uint32_t>((work + kTierThreads - 1) / kTierThreads)),
+                     dim3(kTierThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_unpatchify(const PatchArgs& a, hipStream_t stream) {
+  const int64_t work = a.n_frames * a.C * a.H * a.W;
+  if (work <= 0) return hipSuccess;
+  hipLaunchKernelGGL(unpatchify_kernel, dim3(static_cast<uint32_t>((work + kTierThreads - 1) / kTierThreads)),
+                     dim3(kTierThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm(const GemmArgs& a, hipStream_t stream) {
+  if (a.M <= 0 || a.N <= 0) return hipSuccess;
+  const int64_t blocks = static_cast<int64_t>((a.M + kGM - 1) / kGM) * ((a.N + kGN - 1) / kGN);
+  hipLaunchKernelGGL(gemm_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kTierThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace mssa

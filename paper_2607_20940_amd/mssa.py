@@ -25,7 +25,12 @@ MSSA_PLAN_STRIDED_SUBSAMPLE = 2
 EXPORTS = ("mssa_plan_create", "mssa_plan_destroy", "mssa_plan_query", "mssa_plan_tables",
            "mssa_pool_kv", "mssa_forward", "mssa_hist_append", "mssa_pool_hist_ring",
            "mssa_forward_ring", "mssa_hist_append_ring", "mssa_forward_lse", "mssa_backward_workspace_size",
-           "mssa_backward", "mssa_status_string", "mssa_last_error")
+           "mssa_backward", "mssa_tier_workspace_size", "mssa_patch_embed", "mssa_patch_unembed",
+           "mssa_qkv_project", "mssa_status_string", "mssa_last_error")
+
+
+class mssa_tier_desc(ctypes.Structure):
+    _fields_ = [("latent_channels", ctypes.c_int32), ("patch", ctypes.c_int32), ("hidden", ctypes.c_int32)]
 
 
 class mssa_plan_desc(ctypes.Structure):
@@ -78,6 +83,11 @@ def _load():
     lib.mssa_forward_lse.argtypes = [P, V, V, V, V, V, V, V, V, I64, V, V, V]
     lib.mssa_backward_workspace_size.argtypes = [P, ctypes.POINTER(I64)]
     lib.mssa_backward.argtypes = [P, V, V, V, V, V, V, V, V, V, V, V, I64, V, V, V, V, V, V, V, V]
+    TD = ctypes.POINTER(mssa_tier_desc)
+    lib.mssa_tier_workspace_size.argtypes = [P, TD, ctypes.POINTER(I64)]
+    lib.mssa_patch_embed.argtypes = [P, TD, V, PP, PP, V, I64, V, V]
+    lib.mssa_patch_unembed.argtypes = [P, TD, V, PP, PP, V, I64, V, V]
+    lib.mssa_qkv_project.argtypes = [I64, ctypes.c_int32, V, V, V, V, V, V, V]
     lib.mssa_status_string.argtypes = [ctypes.c_int]
     lib.mssa_status_string.restype = ctypes.c_char_p
     lib.mssa_last_error.argtypes = []
@@ -265,6 +275,36 @@ def mssa_backward(plan, q_win, k_sink, v_sink, k_hist, v_hist, k_win, v_win, out
                              _ptr(workspace), wb, _ptr(dq_win), _ptr(dk_sink), _ptr(dv_sink),
                              _ptr(dk_hist), _ptr(dv_hist), _ptr(dk_win), _ptr(dv_win), _stream(stream)),
            "mssa_backward")
+
+
+def tier_desc(latent_channels, patch, hidden):
+    return mssa_tier_desc(int(latent_channels), int(patch), int(hidden))
+
+
+def mssa_tier_workspace_size(plan, tier):
+    n = ctypes.c_int64()
+    _check(lib.mssa_tier_workspace_size(plan.handle, ctypes.byref(tier), ctypes.byref(n)),
+           "mssa_tier_workspace_size")
+    return n.value
+
+
+def mssa_patch_embed(plan, tier, latent, w_embed, b_embed, workspace, tokens, workspace_bytes=None, stream=None):
+    wb = _nbytes(workspace) if workspace_bytes is None else int(workspace_bytes)
+    _check(lib.mssa_patch_embed(plan.handle, ctypes.byref(tier), _ptr(latent), _ptr_array(w_embed),
+                                _ptr_array(b_embed), _ptr(workspace), wb, _ptr(tokens), _stream(stream)),
+           "mssa_patch_embed")
+
+
+def mssa_patch_unembed(plan, tier, tokens, w_out, b_out, workspace, latent, workspace_bytes=None, stream=None):
+    wb = _nbytes(workspace) if workspace_bytes is None else int(workspace_bytes)
+    _check(lib.mssa_patch_unembed(plan.handle, ctypes.byref(tier), _ptr(tokens), _ptr_array(w_out),
+                                  _ptr_array(b_out), _ptr(workspace), wb, _ptr(latent), _stream(stream)),
+           "mssa_patch_unembed")
+
+
+def mssa_qkv_project(n_tokens, hidden, x, w_qkv, b_qkv, q, k, v, stream=None):
+    _check(lib.mssa_qkv_project(int(n_tokens), int(hidden), _ptr(x), _ptr(w_qkv), _ptr(b_qkv), _ptr(q), _ptr(k),
+                                _ptr(v), _stream(stream)), "mssa_qkv_project")
 
 
 class Ring:

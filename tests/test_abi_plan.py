@@ -265,3 +265,34 @@ def test_backward_calls_checked():
                            fake, None, None, fake + 8192, fake + 8192, fake + 8192, fake + 8192,
                            workspace_bytes=wsz, stream=0)
     assert e.value.status == mssa.MSSA_ERR_INVALID_ARG  # dq aliases q
+
+
+def test_tier_calls_checked():
+    """Tier entry points validate before enqueuing anything."""
+    desc = dict(num_states=2, scales=[1, 2], grid_h=6, grid_w=8, frames_per_state=1, sink_frames=1,
+                hist_frames=0, num_heads=2, head_dim=64)
+    plan = mssa.mssa_plan_create(dict(desc, dtype="bf16"))
+    tier = mssa.tier_desc(16, 2, 128)
+    need = mssa.mssa_tier_workspace_size(plan, tier)
+    # patch rows of both tiers: 48 tokens x 64 features + 12 tokens x 256 features, bf16
+    assert need == (48 * 64 * 2 + 255) // 256 * 256 + (12 * 256 * 2 + 255) // 256 * 256
+    f32 = mssa.mssa_plan_create(dict(desc, dtype="f32"))
+    with pytest.raises(mssa.MssaError) as e:
+        mssa.mssa_tier_workspace_size(f32, tier)
+    assert e.value.status == mssa.MSSA_ERR_UNSUPPORTED
+    with pytest.raises(mssa.MssaError) as e:
+        mssa.mssa_tier_workspace_size(plan, mssa.tier_desc(16, 2, 100))
+    assert e.value.status == mssa.MSSA_ERR_INVALID_ARG
+    with pytest.raises(mssa.MssaError) as e:
+        mssa.mssa_tier_workspace_size(plan, mssa.tier_desc(1, 1, 64))  # C p^2 = 1
+    assert e.value.status == mssa.MSSA_ERR_UNSUPPORTED
+    fake = 1 << 20
+    with pytest.raises(mssa.MssaError) as e:
+        mssa.mssa_patch_embed(plan, tier, fake, [fake, fake], [fake, fake], fake, fake, workspace_bytes=16, stream=0)
+    assert e.value.status == mssa.MSSA_ERR_WORKSPACE
+    with pytest.raises(mssa.MssaError) as e:
+        mssa.mssa_qkv_project(10, 128, fake, fake, fake, fake, fake + 4096, fake + 8192, stream=0)
+    assert e.value.status == mssa.MSSA_ERR_INVALID_ARG  # q aliases x
+    with pytest.raises(mssa.MssaError) as e:
+        mssa.mssa_qkv_project(10, 12, fake, fake, fake, fake + 4096, fake + 8192, fake + 12288, stream=0)
+    assert e.value.status == mssa.MSSA_ERR_INVALID_ARG

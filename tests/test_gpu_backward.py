@@ -4,7 +4,7 @@ gradient compared with the oracle's on the same seeded inputs.
 
 Tolerances (relative to each gradient tensor, as for the forward's relative
 guard): bf16 plans round the probabilities and dS to bf16 as matrix-core
-operands (relative error 2^-9 per term) and the gradients once more on
+operands (relative rounding error up to 2^-8 per term) and the gradients once more on
 output, so the rms error stays a few 1e-3 of the tensor's rms; the bound is
 1e-2 rms and 5e-2 of the tensor's max for the worst element.  fp32 plans
 compute in fp32: 1e-5 rms, 1e-4 max."""

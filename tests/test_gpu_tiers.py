@@ -1,0 +1,158 @@
+"""GPU parity of the MSP tier steps (patch embedding, de-embedding, QKV
+projection) through the C ABI against the fp64 tier oracle.
+
+Tolerances: each output is an fp32 sum of exact bf16 products rounded once
+to bf16 (relative error <= 2^-8 per element; measured rms 1.7e-3), so the bound is 4e-3 of the
+reference rms and 8e-3 of its max.  With identity weights (hidden = C P^2)
+every step is a pure gather or scatter of bf16 values and must be exact."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_20940_amd import mssa
+from paper_2607_20940_amd.inputs import bf16_bits_to_f32, f32_to_bf16_bits
+
+from gpu_common import errors
+
+pytestmark = pytest.mark.gpu
+
+
+def _desc(scales, H, W, F=1, nh=1, d=64):
+    return dict(num_states=len(scales), scales=list(scales), grid_h=H, grid_w=W, frames_per_state=F,
+                sink_frames=0, hist_frames=0, num_heads=nh, head_dim=d)
+
+
+def _bf16(rng, shape, scale=1.0):
+    """Seeded draw rounded to bf16: (device tensor, float64 values)."""
+    bits = f32_to_bf16_bits((rng.standard_normal(shape) * scale).astype(np.float32))
+    t = torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).cuda()
+    return t, bf16_bits_to_f32(bits).astype(np.float64)
+
+
+def _f64(t):
+    return t.float().cpu().numpy().astype(np.float64)
+
+
+def _close(got, ref, label):
+    e = errors(got, ref)
+    assert np.isfinite(got).all(), label
+    assert e["rel_rms"] <= 4e-3 and e["rel_max"] <= 8e-3, (label, e)
+    print(f"[tiers] {label} {e}", flush=True)
+
+
+def _weights(rng, plan, desc, C, patch, hidden, out=False):
+    info = plan.info()
+    w, b, wd, bd = [], [], {}, {}
+    for s in info["group_scale"]:
+        kp = C * (patch * s) ** 2
+        shape = (kp, hidden) if out else (hidden, kp)
+        wt, wv = _bf16(rng, shape, 1.0 / np.sqrt(shape[1]))
+        bt, bv = _bf16(rng, (shape[0],), 0.1)
+        w.append(wt)
+        b.append(bt)
+        wd[s], bd[s] = wv, bv
+    return w, b, wd, bd
+
+
+CASES = {
+    "ragged_3tier": (_desc([1, 2, 4], 5, 7, F=2), 16, 2, 128, 1),
+    "paper_schedule_small": (_desc([1, 1, 2, 2, 2], 6, 10, F=3), 16, 2, 256, 2),
+    "odd_channels": (_desc([1, 2], 9, 4, F=1), 2, 2, 64, 3),
+}
+
+
+@pytest.mark.parametrize("name", sorted(CASES))
+def test_patch_embed_and_unembed(name):
+    desc, C, patch, hidden, seed = CASES[name]
+    rng = np.random.default_rng(seed)
+    plan = mssa.mssa_plan_create(dict(desc, dtype="bf16"))
+    tier = mssa.tier_desc(C, patch, hidden)
+    nq = plan.info()["n_q"]
+    T, F = desc["num_states"], desc["frames_per_state"]
+    H, W = desc["grid_h"] * patch, desc["grid_w"] * patch
+    ws = torch.empty(max(256, mssa.mssa_tier_workspace_size(plan, tier)), dtype=torch.uint8, device="cuda")
+    lat, lat64 = _bf16(rng, (T * F, C, H, W))
+    w, b, wd, bd = _weights(rng, plan, desc, C, patch, hidden)
+    tok = torch.empty((nq, hidden), dtype=torch.bfloat16, device="cuda")
+    mssa.mssa_patch_embed(plan, tier, lat, w, b, ws, tok)
+    torch.cuda.synchronize()
+    _close(_f64(tok), oracle.patch_embed(desc, patch, lat64, wd, bd), name + " embed")
+
+    t_in, t64 = _bf16(rng, (nq, hidden))
+    wo, bo, wod, bod = _weights(rng, plan, desc, C, patch, hidden, out=True)
+    out = torch.full((T * F, C, H, W), float("nan"), dtype=torch.bfloat16, device="cuda")
+    mssa.mssa_patch_unembed(plan, tier, t_in, wo, bo, ws, out)
+    torch.cuda.synchronize()
+    _close(_f64(out), oracle.patch_unembed(desc, patch, C, t64, wod, bod), name + " unembed")
+
+
+@pytest.mark.parametrize("H,W", [(6, 10), (5, 7)])
+def test_identity_tiers_are_exact(H, W):
+    """hidden = C P^2 and W = I, b = 0: embedding is the patch gather and
+    de-embedding its inverse, bit for bit (ragged edges: zeros in, dropped out)."""
+    C, patch, s = 16, 2, 2
+    desc = _desc([s, s], H, W, F=2)
+    kp = C * (patch * s) ** 2
+    plan = mssa.mssa_plan_create(dict(desc, dtype="bf16"))
+    tier = mssa.tier_desc(C, patch, kp)
+    rng = np.random.default_rng(5)
+    lat, lat64 = _bf16(rng, (4, C, H * patch, W * patch))
+    eye = [torch.eye(kp, dtype=torch.bfloat16, device="cuda")]
+    zero = [torch.zeros(kp, dtype=torch.bfloat16, device="cuda")]
+    ws = torch.empty(mssa.mssa_tier_workspace_size(plan, tier), dtype=torch.uint8, device="cuda")
+    nq = plan.info()["n_q"]
+    tok = torch.empty((nq, kp), dtype=torch.bfloat16, device="cuda")
+    mssa.mssa_patch_embed(plan, tier, lat, eye, zero, ws, tok)
+    back = torch.empty_like(lat)
+    mssa.mssa_patch_unembed(plan, tier, tok, eye, zero, ws, back)
+    torch.cuda.synchronize()
+    want = np.concatenate([oracle.patchify(lat64[f], patch * s) for f in range(4)])
+    assert np.array_equal(_f64(tok), want)
+    assert torch.equal(back.view(torch.int16), lat.view(torch.int16))
+
+
+@pytest.mark.parametrize("n,heads,d", [(77, 2, 64), (300, 3, 128), (1, 1, 64)])
+def test_qkv_projection_small(n, heads, d):
+    rng = np.random.default_rng(n)
+    hidden = heads * d
+    x, x64 = _bf16(rng, (n, hidden))
+    w, w64 = _bf16(rng, (3 * hidden, hidden), 1.0 / np.sqrt(hidden))
+    b, b64 = _bf16(rng, (3 * hidden,), 0.1)
+    q, k, v = (torch.empty((n, heads, d), dtype=torch.bfloat16, device="cuda") for _ in range(3))
+    mssa.mssa_qkv_project(n, hidden, x, w, b, q, k, v)
+    torch.cuda.synchronize()
+    for got, ref, nm in zip((q, k, v), oracle.qkv_project(x64, w64, b64, heads), "qkv"):
+        _close(_f64(got), ref, f"qkv n={n} {nm}")
+
+
+def test_tiers_wan13b_layer_shapes():
+    """The 1.3B-shaped window (30 x 52 tokens of 2 x 2 patches over 16 latent
+    channels, schedule (p, p, 2p, 2p, 2p), width 1536 = 12 x 128): every
+    embedded token, the de-embedded latent, and sampled rows of q, k, v."""
+    desc = _desc([1, 1, 2, 2, 2], 30, 52, F=3, nh=12, d=128)
+    C, patch, hidden = 16, 2, 1536
+    rng = np.random.default_rng(11)
+    plan = mssa.mssa_plan_create(dict(desc, dtype="bf16"))
+    tier = mssa.tier_desc(C, patch, hidden)
+    nq = plan.info()["n_q"]
+    ws = torch.empty(mssa.mssa_tier_workspace_size(plan, tier), dtype=torch.uint8, device="cuda")
+    lat, lat64 = _bf16(rng, (15, C, 60, 104))
+    w, b, wd, bd = _weights(rng, plan, desc, C, patch, hidden)
+    tok = torch.empty((nq, hidden), dtype=torch.bfloat16, device="cuda")
+    mssa.mssa_patch_embed(plan, tier, lat, w, b, ws, tok)
+    wq, wq64 = _bf16(rng, (3 * hidden, hidden), 1.0 / np.sqrt(hidden))
+    bq, bq64 = _bf16(rng, (3 * hidden,), 0.1)
+    q, k, v = (torch.empty((nq, 12, 128), dtype=torch.bfloat16, device="cuda") for _ in range(3))
+    x, x64 = _bf16(rng, (nq, hidden))
+    mssa.mssa_qkv_project(nq, hidden, x, wq, bq, q, k, v)
+    wo, bo, wod, bod = _weights(rng, plan, desc, C, patch, hidden, out=True)
+    out = torch.empty_like(lat)
+    mssa.mssa_patch_unembed(plan, tier, x, wo, bo, ws, out)
+    torch.cuda.synchronize()
+    _close(_f64(tok), oracle.patch_embed(desc, patch, lat64, wd, bd), "wan13b embed")
+    _close(_f64(out), oracle.patch_unembed(desc, patch, C, x64, wod, bod), "wan13b unembed")
+    rows = np.unique(np.concatenate([[0, 1, 127, 128, 9359, 9360, nq - 1], rng.integers(0, nq, 40)]))
+    for got, ref, nm in zip((q, k, v), oracle.qkv_project(x64[rows], wq64, bq64, 12), "qkv"):
+        _close(_f64(got)[rows], ref, f"wan13b {nm}")
