@@ -17,6 +17,13 @@ pooled rings hold exactly the bytes re-pooling would give; outputs agree
 with the plain path up to the attention kernel's rounding (key tiles fall
 differently around the separate pooled-history run).
 
+graph_pass() runs a whole pass (every layer) over static window buffers as
+one HIP graph: once every ring is full the plan no longer changes and the
+ring head cycles through cap / gcd(cap, F) positions, so one graph per head
+position is captured on first use and replayed after (the library enqueues
+only kernels and device-to-device copies, and allocates nothing).  While the
+rings fill, passes run eagerly.
+
 This module only sequences library calls and owns device buffers (torch
 allocations); all arithmetic runs in the library.
 """
@@ -50,6 +57,9 @@ class StreamingMSSA:
         self.ring = [mssa.Ring(self.cap) for _ in range(self.layers)]
         self.k_sink = [None] * self.layers
         self.v_sink = [None] * self.layers
+        self.F = int(layer_desc["frames_per_state"])
+        self._win = None
+        self._graphs = {}
         # Pooled-history rings [layer][group] (None for groups at scale 1).
         self.k_pool = [[None] * info["n_groups"] for _ in range(self.layers)]
         self.v_pool = [[None] * info["n_groups"] for _ in range(self.layers)]
@@ -87,6 +97,51 @@ class StreamingMSSA:
         if self.pooled_ring and n:
             mssa.mssa_pool_hist_ring(self.plan(n), self.k_ring[layer], self.v_ring[layer],
                                      self.k_pool[layer], self.v_pool[layer])
+
+    def window_buffers(self):
+        """Static per-layer window buffers {q_win, k_win, v_win, out} that
+        graph_pass() reads and writes."""
+        import torch
+
+        if self._win is None:
+            sh = self.shapes(0)
+            self._win = [{k: torch.zeros(sh["q_win"], dtype=self.tdtype, device=self.device)
+                          for k in ("q_win", "k_win", "v_win", "out")} for _ in range(self.layers)]
+        return self._win
+
+    def graph_pass(self):
+        """One pass of every layer over window_buffers(): eager until every
+        ring is full, then the captured graph of the current head position.
+        Returns "eager", "captured" (recorded, then replayed) or "replayed"."""
+        import torch
+
+        bufs = self.window_buffers()
+
+        def run_all():
+            for L in range(self.layers):
+                b = bufs[L]
+                self.layer_pass(L, b["q_win"], b["k_win"], b["v_win"], b["out"])
+
+        heads = {r.head for r in self.ring}
+        if any(r.count != self.cap for r in self.ring) or len(heads) != 1:
+            run_all()
+            return "eager"
+        h = heads.pop()
+        g = self._graphs.get(h)
+        if g is None:
+            # Capturing records the pass without running it and advances the
+            # host-side ring state as the pass would; the replay runs it.
+            torch.cuda.synchronize()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                run_all()
+            self._graphs[h] = g
+            g.replay()
+            return "captured"
+        g.replay()
+        for r in self.ring:  # a full ring overwrites its F oldest slots
+            r.head = (r.head + self.F) % self.cap
+        return "replayed"
 
     def layer_pass(self, layer, q_win, k_win, v_win, out, stream=None):
         ring = self.ring[layer]

@@ -185,3 +185,43 @@ def test_streaming_pooled_ring_equals_plain(layer):
                                    fresh_v[g][:n].view(torch.int16)), (p, L, g)
     assert plain.ring[0].count == w["hist_cap_frames"]
     assert (w["hist_start_frames"] + 8 * F) > w["hist_cap_frames"]
+
+
+@pytest.mark.parametrize("pooled_ring", [False, True])
+def test_graph_pass_equals_eager(pooled_ring):
+    """Whole passes replayed as HIP graphs (one per ring head position) give
+    bit for bit the eager passes' outputs and ring contents, over several
+    cycles of head positions; eager work runs between the replays."""
+    w = dict(SMALL, hist_cap_frames=6)
+    layers = 2
+    eager = StreamingMSSA(w["layer"], layers, w["hist_cap_frames"], dtype="bf16", pooled_ring=pooled_ring)
+    graph = StreamingMSSA(w["layer"], layers, w["hist_cap_frames"], dtype="bf16", pooled_ring=pooled_ring)
+    shapes = eager.shapes(w["hist_start_frames"])
+    for L in range(layers):
+        x = init_inputs(w, L, shapes)
+        eager.init_layer(L, x["k_sink"], x["v_sink"], x["k_hist"], x["v_hist"])
+        graph.init_layer(L, x["k_sink"], x["v_sink"], x["k_hist"], x["v_hist"])
+    win_shapes = eager.shapes(0)
+    bufs = graph.window_buffers()
+    replays = 0
+    for p in range(12):
+        wins = window_inputs(w, p, layers, win_shapes)
+        outs = []
+        for L in range(layers):
+            o = torch.empty_like(wins[L]["q_win"])
+            eager.layer_pass(L, wins[L]["q_win"], wins[L]["k_win"], wins[L]["v_win"], o)
+            outs.append(o)
+            for k in ("q_win", "k_win", "v_win"):
+                bufs[L][k].copy_(wins[L][k])
+        replays += graph.graph_pass() != "eager"
+        torch.cuda.synchronize()
+        print(f"[graph] pass {p} graph={replays} head={graph.ring[0].head} count={graph.ring[0].count}", flush=True)
+        for L in range(layers):
+            assert torch.equal(outs[L].view(torch.int16), bufs[L]["out"].view(torch.int16)), (p, L)
+            assert (eager.ring[L].head, eager.ring[L].count) == (graph.ring[L].head, graph.ring[L].count)
+            assert torch.equal(eager.k_ring[L].view(torch.int16), graph.k_ring[L].view(torch.int16)), (p, L)
+            for g, t in enumerate(eager.v_pool[L]):
+                if t is not None:
+                    assert torch.equal(t.view(torch.int16), graph.v_pool[L][g].view(torch.int16)), (p, L, g)
+    # 2 + 2 frames per pass: full after pass 1; 3 head positions, each replayed several times
+    assert replays == 10 and len(graph._graphs) == 3
