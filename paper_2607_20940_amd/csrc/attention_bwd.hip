@@ -23,9 +23,12 @@
 //                B operand of dQ^T += K^T dS^T, with K^T read from LDS by the
 //                transposing read ds_read_b64_tr_b16.
 //   dkdv_kernel  a wave owns 32 context keys (K, V fragments in registers)
-//                and walks the scale's queries in 64-query stages: S = Q K^T,
+//                and walks the scale's queries in 128-query stages: S = Q K^T,
 //                dP = dO V^T (lane = key), then dV^T += dO^T P and
-//                dK^T += Q^T dS with dO^T, Q^T from transposing reads.
+//                dK^T += Q^T dS with dO^T, Q^T from transposing reads.  One
+//                XOR-swizzled copy of Q and dO in LDS serves both read
+//                patterns without bank conflicts; it arrives by direct
+//                global -> LDS transfers (no staging registers).
 // The dQ kernel keeps its LDS operand reads several MFMAs ahead and overlaps
 // one key block's softmax with the next block's MFMAs; in the dK/dV kernel
 // (K, V, dK and dV per wave fill the register file) the same scheme measured
@@ -337,15 +340,61 @@ __global__ __launch_bounds__(kBwdThreads) void dq_kernel(BwdArgs a) {
 
 // ------------------------------------------------------------------ bf16: dK, dV
 
+// Swizzled LDS rows for the dK/dV kernel's query stages: every row takes 256
+// bytes (128 bf16, the head's D channels and, for D = 64, unused space), and
+// 16-byte chunk c of row r is stored at chunk c ^ f(r & 15),
+// f(r) = ((r & 3) << 2) | (r >> 2).  Sixteen consecutive rows read at one
+// column (the row reads of S = Q K^T and dP = dO V^T) then hit 16 distinct
+// bank groups, and so do the 4 rows x 4 chunks of a transposing read (dV^T
+// += dO^T P, dK^T += Q^T dS): one copy of Q and dO serves both.
+__device__ inline int swz(int row, int col) {
+  const int r = row & 15;
+  return row * 128 + ((((col >> 3) ^ (((r & 3) << 2) | (r >> 2)))) << 3) + (col & 7);
+}
+
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+
+// Direct global -> LDS load (buffer_load_dwordx4 ... lds): lane i's 16 bytes
+// at buffer offset voff land at LDS byte address lds_addr + 16 i (lds_addr
+// wave-uniform); offsets past the buffer's range write zeros.  Counted by
+// vmcnt; issued from inline asm so the compiler does not make every later
+// LDS read wait for it (the kernel waits before the barrier that publishes
+// the stage).  m0 is set here and not used otherwise.
+__device__ inline void dma16(i32x4 rsrc, uint32_t voff, uint32_t lds_addr) {
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :: "s"(lds_addr), "v"(voff), "s"(rsrc) : "memory", "m0");
+#pragma clang diagnostic pop
+}
+
+// s_waitcnt vmcnt(N) alone (gfx9 encoding: expcnt and lgkmcnt at their maxima).
+template <int N>
+__device__ inline void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+__device__ inline i32x4 rsrc_of(const void* base, uint32_t bytes) {
+  const uint64_t b = reinterpret_cast<uint64_t>(base);
+  i32x4 r;
+  r[0] = __builtin_amdgcn_readfirstlane(static_cast<int>(b & 0xffffffffu));
+  r[1] = __builtin_amdgcn_readfirstlane(static_cast<int>((b >> 32) & 0xffffu));
+  r[2] = __builtin_amdgcn_readfirstlane(static_cast<int>(bytes));
+  r[3] = 0x00020000;
+  return r;
+}
+
 template <int D>
 __global__ __launch_bounds__(kBwdThreads) void dkdv_kernel(BwdArgs a) {
   using L = Lay<D>;
-  constexpr int KS = L::KS, DB = L::DB, CPR = L::CPR, ASTR = L::ASTR, TSTR = L::TSTR, RPL = L::RPL;
-  constexpr int BQ = kBwdQS, NLD = BQ / RPL;
-  // Q rows | dO rows | Q transposing | dO transposing | lse2, rowsum (fp32)
-  constexpr int QA = BQ * ASTR, QT = BQ * TSTR, STAGE = 2 * QA + 2 * QT + 4 * BQ;
-  static_assert(NLD * RPL == BQ, "stage load must divide evenly");
-  __shared__ __attribute__((aligned(16))) __bf16 lds[2 * STAGE];
+  constexpr int KS = L::KS, DB = L::DB;
+  constexpr int BQ = kBwdQS, RS = 128;                // queries per stage, LDS row stride (elements)
+  constexpr int QT = BQ * RS * 2;                       // bytes of one swizzled tile
+  constexpr int STB = 2 * QT + 8 * BQ;                  // Q | dO | lse2 | rowsum (fp32)
+  constexpr int NDMA = QT / 1024 / (kBwdThreads / 64);  // 1 KB transfers per wave, tile and tensor
+  static_assert(NDMA * 1024 * (kBwdThreads / 64) == QT && BQ % 32 == 0 && BQ <= 128, "stage shape");
+  __shared__ __attribute__((aligned(16))) char lds[2 * STB];
 
   int n_blocks = 0;
   for (int g = 0; g < a.n_groups; ++g) n_blocks += a.groups[g].n_kblocks * a.num_heads;
@@ -382,20 +431,38 @@ __global__ __launch_bounds__(kBwdThreads) void dkdv_kernel(BwdArgs a) {
     dv[db] = f32x16{};
   }
 
-  const int ld_row = tid / CPR, ld_col = (tid % CPR) * 8;
-  bf16x8 pq[NLD], pg[NLD];
-  float pstat = 0.f;
-  auto load_stage = [&](int q0) {
+  // Per-lane global offsets of this wave's transfers (the same every stage):
+  // LDS byte p = tile + 1024 (wave NDMA + i) + 16 lane holds row p / 256,
+  // physical chunk (p / 16) % 16, i.e. logical chunk phys ^ f(row); chunks
+  // past the head's D channels point past the buffer (zero fill).
+  const uint32_t row_bytes = static_cast<uint32_t>(ld) * 2;
+  uint32_t voff[NDMA];
 #pragma unroll
-    for (int i = 0; i < NLD; ++i) {
-      const int q = q0 + ld_row + i * RPL;
-      const int64_t off = static_cast<int64_t>(q) * ld + hoff + ld_col;
-      const bool ok = q < G.q_end;
-      pq[i] = ok ? *reinterpret_cast<const bf16x8*>(static_cast<const __bf16*>(a.q) + off) : bf16x8{};
-      pg[i] = ok ? *reinterpret_cast<const bf16x8*>(static_cast<const __bf16*>(a.d_out) + off) : bf16x8{};
+  for (int i = 0; i < NDMA; ++i) {
+    const int p = (wave * NDMA + i) * 1024 + 16 * lane;
+    const int row = p >> 8, phys = (p >> 4) & 15, r = row & 15;
+    const int lc = phys ^ (((r & 3) << 2) | (r >> 2));
+    voff[i] = lc < D / 8 ? row * row_bytes + lc * 16 : 0x7ffffff0u;
+  }
+  const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds));
+  // Stage queries [q0, q0 + BQ) into LDS buffer buf: Q and dO tiles by
+  // direct transfers (NDMA each per wave); lse (in log2 units, +inf past the
+  // end) and rowsum (0 past the end) through a register of threads 0..2BQ-1,
+  // stored by store_stats once the stage has arrived.
+  float pstat = 0.f;
+  auto issue = [&](int q0, int buf) {
+    const int nv = min(BQ, G.q_end - q0);
+    const uint32_t bytes = static_cast<uint32_t>(nv - 1) * row_bytes + D * 2;
+    const int64_t off = static_cast<int64_t>(q0) * ld + hoff;
+    const i32x4 rq = rsrc_of(static_cast<const __bf16*>(a.q) + off, bytes);
+    const i32x4 rg = rsrc_of(static_cast<const __bf16*>(a.d_out) + off, bytes);
+    const uint32_t base = lds0 + buf * STB;
+#pragma unroll
+    for (int i = 0; i < NDMA; ++i) {
+      const uint32_t dst = __builtin_amdgcn_readfirstlane(base + (wave * NDMA + i) * 1024);
+      dma16(rq, voff[i], dst);
+      dma16(rg, voff[i], dst + QT);
     }
-    // threads 0..BQ-1: lse in log2 units (+inf past the end: probability 0);
-    // threads BQ..2BQ-1: rowsum (0 past the end)
     if (tid < 2 * BQ) {
       const int q = q0 + (tid % BQ);
       const bool ok = q < G.q_end;
@@ -403,74 +470,69 @@ __global__ __launch_bounds__(kBwdThreads) void dkdv_kernel(BwdArgs a) {
       pstat = tid < BQ ? (ok ? a.lse[s] * kLog2e : INFINITY) : (ok ? a.dsum[s] : 0.f);
     }
   };
-  auto store_stage = [&](int buf) {
-    __bf16* base = lds + buf * STAGE;
-#pragma unroll
-    for (int i = 0; i < NLD; ++i) {
-      const int row = ld_row + i * RPL;
-      *reinterpret_cast<bf16x8*>(base + row * ASTR + ld_col) = pq[i];
-      *reinterpret_cast<bf16x8*>(base + QA + row * ASTR + ld_col) = pg[i];
-      *reinterpret_cast<bf16x8*>(base + 2 * QA + row * TSTR + ld_col) = pq[i];
-      *reinterpret_cast<bf16x8*>(base + 2 * QA + QT + row * TSTR + ld_col) = pg[i];
-    }
-    if (tid < 2 * BQ) reinterpret_cast<float*>(base + 2 * QA + 2 * QT)[tid] = pstat;
+  auto store_stats = [&](int buf) {
+    if (tid < 2 * BQ) reinterpret_cast<float*>(lds + buf * STB + 2 * QT)[tid] = pstat;
   };
-  const int t_rd = tr_offset(lane, TSTR);
+  const int t_lane = 4 * (lane >> 5) + ((lane & 15) >> 2);  // row of this lane's transposing read
+  const int t_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
 
   auto compute = [&](int buf) {
-    const __bf16* Qa = lds + buf * STAGE;
-    const __bf16* Ga = Qa + QA;
-    const __bf16* Qt = Qa + 2 * QA + t_rd;
-    const __bf16* Gt = Qa + 2 * QA + QT + t_rd;
-    const float* lse2 = reinterpret_cast<const float*>(Qa + 2 * QA + 2 * QT);
-    const float* rsum = lse2 + BQ;
-    bf16x8 pb[BQ / 32][2], dsb[BQ / 32][2];
+    const __bf16* Qs = reinterpret_cast<const __bf16*>(lds + buf * STB);
+    const __bf16* Gs = reinterpret_cast<const __bf16*>(lds + buf * STB + QT);
+    const float* lse_s = reinterpret_cast<const float*>(lds + buf * STB + 2 * QT);
+    const float* rsum_s = lse_s + BQ;
 #pragma unroll
     for (int qb = 0; qb < BQ / 32; ++qb) {
       f32x16 s, dp;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        const bf16x8 aq = *reinterpret_cast<const bf16x8*>(Qa + (qb * 32 + n) * ASTR + hh * 8 + ks * 16);
-        const bf16x8 ag = *reinterpret_cast<const bf16x8*>(Ga + (qb * 32 + n) * ASTR + hh * 8 + ks * 16);
+        const int o = swz(qb * 32 + n, hh * 8 + ks * 16);
+        const bf16x8 aq = *reinterpret_cast<const bf16x8*>(Qs + o);
+        const bf16x8 ag = *reinterpret_cast<const bf16x8*>(Gs + o);
         s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(aq, kf[ks], ks == 0 ? f32x16{} : s, 0, 0, 0);
         dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ag, vf[ks], ks == 0 ? f32x16{} : dp, 0, 0, 0);
       }
       // element e holds query qb*32 + 8(e/4) + 4hh + e%4 of this lane's key
+      bf16x8 pb[2], dsb[2];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const f32x4 l4 = *reinterpret_cast<const f32x4*>(lse2 + qb * 32 + 8 * j + 4 * hh);
-        const f32x4 r4 = *reinterpret_cast<const f32x4*>(rsum + qb * 32 + 8 * j + 4 * hh);
+        const f32x4 l4 = *reinterpret_cast<const f32x4*>(lse_s + qb * 32 + 8 * j + 4 * hh);
+        const f32x4 r4 = *reinterpret_cast<const f32x4*>(rsum_s + qb * 32 + 8 * j + 4 * hh);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int e = 4 * j + i;
           const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e], c, -l4[i]));
-          pb[qb][e >> 3][e & 7] = static_cast<__bf16>(p);
-          dsb[qb][e >> 3][e & 7] = static_cast<__bf16>(p * (dp[e] - r4[i]));
+          pb[e >> 3][e & 7] = static_cast<__bf16>(p);
+          dsb[e >> 3][e & 7] = static_cast<__bf16>(p * (dp[e] - r4[i]));
         }
       }
-    }
-#pragma unroll
-    for (int qb = 0; qb < BQ / 32; ++qb)
 #pragma unroll
       for (int cc = 0; cc < 2; ++cc)
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
-          const int off = (qb * 32 + cc * 16) * TSTR + db * 32;
-          const bf16x8 ag = tr_read(Gt + off, TSTR);
-          const bf16x8 aq = tr_read(Qt + off, TSTR);
-          dv[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ag, pb[qb][cc], dv[db], 0, 0, 0);
-          dk[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(aq, dsb[qb][cc], dk[db], 0, 0, 0);
+          const int r0 = qb * 32 + cc * 16 + t_lane, c0 = db * 32 + t_col;
+          const bf16x4 glo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(Gs + swz(r0, c0)));
+          const bf16x4 ghi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(Gs + swz(r0 + 8, c0)));
+          const bf16x4 qlo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(Qs + swz(r0, c0)));
+          const bf16x4 qhi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(Qs + swz(r0 + 8, c0)));
+          dv[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_shufflevector(glo, ghi, 0, 1, 2, 3, 4, 5, 6, 7),
+                                                           pb[cc], dv[db], 0, 0, 0);
+          dk[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_shufflevector(qlo, qhi, 0, 1, 2, 3, 4, 5, 6, 7),
+                                                           dsb[cc], dk[db], 0, 0, 0);
         }
+    }
   };
 
   const int nst = (G.q_end - G.q_begin + BQ - 1) / BQ;
-  load_stage(G.q_begin);
-  store_stage(0);
+  issue(G.q_begin, 0);
+  wait_vmcnt<0>();
+  store_stats(0);
   __syncthreads();
   for (int st = 0; st < nst; ++st) {
-    if (st + 1 < nst) load_stage(G.q_begin + (st + 1) * BQ);
+    if (st + 1 < nst) issue(G.q_begin + (st + 1) * BQ, (st + 1) & 1);
     compute(st & 1);
-    if (st + 1 < nst) store_stage((st + 1) & 1);
+    wait_vmcnt<0>();
+    if (st + 1 < nst) store_stats((st + 1) & 1);
     __syncthreads();
   }
 

@@ -70,7 +70,7 @@ constexpr int kBwdThreads = 256;
 constexpr int kBwdQ = 128;     // dQ kernel: queries per block
 constexpr int kBwdKS = 64;     // dQ kernel: keys per LDS stage
 constexpr int kBwdK = 128;     // dK/dV kernel: keys per block
-constexpr int kBwdQS = 64;     // dK/dV kernel: queries per LDS stage
+constexpr int kBwdQS = 128;    // dK/dV kernel: queries per LDS stage
 constexpr int kBwdF32 = 64;    // fp32 kernels: one query or key per lane
 constexpr int kDotThreads = 256;
 constexpr int kMaxScatterJobs = 10;
