@@ -15,10 +15,12 @@
 //
 // bf16 path (gfx950 matrix cores, v_mfma_f32_32x32x16_bf16, fp32
 // accumulation), two kernels so that no gradient needs atomics:
-//   dq_kernel    a wave owns 32 queries and walks the context in 64-key
-//                stages through LDS: S^T = K Q^T and dP^T = V dO^T (A = K, V
-//                rows from LDS, B = the wave's Q and dO fragments in
-//                registers), so each lane holds 16 keys of ONE query and its
+//   dq_kernel    a wave owns 32 queries and walks the context in 128-key
+//                stages through LDS (one swizzled copy each of K and V,
+//                loaded by direct transfers, as below): S^T = K Q^T and
+//                dP^T = V dO^T (A = K, V rows from LDS, B = the wave's Q and
+//                dO fragments in registers), so each lane holds 16 keys of
+//                ONE query and its
 //                lse / rowsum are scalars; dS^T packed to bf16 is already the
 //                B operand of dQ^T += K^T dS^T, with K^T read from LDS by the
 //                transposing read ds_read_b64_tr_b16.
@@ -158,189 +160,7 @@ __device__ __forceinline__ void mfma_pipe(Rd&& rd, Mf&& mf) {
   __builtin_amdgcn_sched_barrier(0);
 }
 
-// ------------------------------------------------------------------ bf16: dQ
-
-template <int D>
-__global__ __launch_bounds__(kBwdThreads) void dq_kernel(BwdArgs a) {
-  using L = Lay<D>;
-  constexpr int KS = L::KS, DB = L::DB, CPR = L::CPR, ASTR = L::ASTR, TSTR = L::TSTR, RPL = L::RPL;
-  constexpr int BN = kBwdKS, NLD = BN / RPL;
-  constexpr int KA = BN * ASTR, KT = BN * TSTR, STAGE = 2 * KA + KT;  // K rows | V rows | K transposing
-  static_assert(NLD * RPL == BN && BN == 64, "stage load must divide evenly; two 32-key blocks");
-  __shared__ __attribute__((aligned(16))) __bf16 lds[2 * STAGE];
-
-  int n_blocks = 0;
-  for (int g = 0; g < a.n_groups; ++g) n_blocks += a.groups[g].n_qblocks * a.num_heads;
-  const int b = xcd_remap(blockIdx.x, n_blocks);
-  int g = 0;
-  while (g + 1 < a.n_groups && b >= a.groups[g + 1].dq_block_begin) ++g;
-  const BwdGroupArgs& G = a.groups[g];
-  const int idx = b - G.dq_block_begin;
-  const int head = idx / G.n_qblocks, qt = idx % G.n_qblocks;
-
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int n = lane & 31, hh = lane >> 5;
-  const int q_row = G.q_begin + qt * kBwdQ + wave * 32 + n;
-  const bool q_ok = q_row < G.q_end;
-  const int64_t ld = a.ld, hoff = static_cast<int64_t>(head) * D;
-  const float c = a.scale_log2e;
-
-  // B operands: this lane's query, 8 channels of its half-wave per k step.
-  bf16x8 qf[KS], gf[KS];
-  {
-    const int64_t off = static_cast<int64_t>(q_ok ? q_row : G.q_begin) * ld + hoff + hh * 8;
-    const __bf16* qp = static_cast<const __bf16*>(a.q) + off;
-    const __bf16* gp = static_cast<const __bf16*>(a.d_out) + off;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      qf[ks] = q_ok ? *reinterpret_cast<const bf16x8*>(qp + ks * 16) : bf16x8{};
-      gf[ks] = q_ok ? *reinterpret_cast<const bf16x8*>(gp + ks * 16) : bf16x8{};
-    }
-  }
-  const int64_t stat = static_cast<int64_t>(head) * a.n_q + (q_ok ? q_row : G.q_begin);
-  const float lse2 = q_ok ? a.lse[stat] * kLog2e : 0.f;
-  const float dsum = q_ok ? a.dsum[stat] : 0.f;
-
-  f32x16 acc[DB];
-#pragma unroll
-  for (int db = 0; db < DB; ++db) acc[db] = f32x16{};
-
-  // Stage tiles of BN keys inside one run at a time; rows past the run's end
-  // read as zeros and are masked.
-  const int nr = G.n_runs;
-  int nst = 0;
-  for (int r = 0; r < nr; ++r) nst += (G.runs[r].n_tok + BN - 1) / BN;
-  struct Stream {
-    const __bf16* k;
-    const __bf16* v;
-    int left;  // tokens of the current run from k on
-    int r;
-  };
-  const int64_t tile_step = static_cast<int64_t>(BN) * ld;
-  auto seek = [&](Stream& s, int r) {
-    while (r < nr && G.runs[r].n_tok == 0) ++r;
-    s.r = r;
-    if (r < nr) {
-      s.k = static_cast<const __bf16*>(G.runs[r].k) + hoff;
-      s.v = static_cast<const __bf16*>(G.runs[r].v) + hoff;
-      s.left = G.runs[r].n_tok;
-    }
-  };
-  auto step = [&](Stream& s) {
-    s.left -= BN;
-    s.k += tile_step;
-    s.v += tile_step;
-    if (s.left <= 0) seek(s, s.r + 1);
-  };
-  const uint32_t row_bytes = static_cast<uint32_t>(ld) * 2;
-  const int ld_row = tid / CPR, ld_col = (tid % CPR) * 8;
-  const uint32_t g_off = ld_row * row_bytes + ld_col * 2;
-  bf16x8 pk[NLD], pv[NLD];
-  auto load = [&](const Stream& s) {
-    const uint32_t bytes = static_cast<uint32_t>(min(s.left, BN) - 1) * row_bytes + D * 2;
-    const auto rk = make_rsrc(s.k, bytes), rv = make_rsrc(s.v, bytes);
-#pragma unroll
-    for (int i = 0; i < NLD; ++i) {
-      pk[i] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rk, g_off + i * RPL * row_bytes, 0, 0));
-      pv[i] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rv, g_off + i * RPL * row_bytes, 0, 0));
-    }
-  };
-  auto store_stage = [&](int buf) {
-    __bf16* base = lds + buf * STAGE;
-#pragma unroll
-    for (int i = 0; i < NLD; ++i) {
-      const int row = ld_row + i * RPL;
-      *reinterpret_cast<bf16x8*>(base + row * ASTR + ld_col) = pk[i];
-      *reinterpret_cast<bf16x8*>(base + KA + row * ASTR + ld_col) = pv[i];
-      *reinterpret_cast<bf16x8*>(base + 2 * KA + row * TSTR + ld_col) = pk[i];
-    }
-  };
-  const int t_rd = tr_offset(lane, TSTR);
-
-  // One stage: S^T, dP^T of key block 0; the same for block 1 with block 0's
-  // softmax interleaved; dQ^T from block 0 with block 1's softmax
-  // interleaved; dQ^T from block 1.
-  auto compute = [&](int buf, int nvalid) {
-    const __bf16* Ka = lds + buf * STAGE;
-    const __bf16* Va = Ka + KA;
-    const __bf16* Kt = Ka + 2 * KA + t_rd;
-    f32x16 s[2], dp[2];
-    bf16x8 dsb[2][2];
-    auto rows = [&](int kb) {
-      return [&, kb](int i) {
-        const __bf16* base = (i & 1) ? Va : Ka;
-        return *reinterpret_cast<const bf16x8*>(base + (kb * 32 + n) * ASTR + hh * 8 + (i >> 1) * 16);
-      };
-    };
-    auto sdp = [&](int kb) {
-      return [&, kb](int i, bf16x8 av) {
-        const int ks = i >> 1;
-        if (i & 1)
-          dp[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, gf[ks], ks == 0 ? f32x16{} : dp[kb], 0, 0, 0);
-        else
-          s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qf[ks], ks == 0 ? f32x16{} : s[kb], 0, 0, 0);
-      };
-    };
-    // dS^T = P^T * (dP^T - rowsum); element e of block kb is key kb*32 + 8(e/4) + 4hh + e%4.
-    auto soft = [&](int kb) {
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int key = kb * 32 + 8 * (e >> 2) + 4 * hh + (e & 3);
-        const float p = key < nvalid ? __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][e], c, -lse2)) : 0.f;
-        dsb[kb][e >> 3][e & 7] = static_cast<__bf16>(p * (dp[kb][e] - dsum));
-      }
-    };
-    auto trs = [&](int kb) {
-      return [&, kb](int i) { return tr_read(Kt + (kb * 32 + (i / DB) * 16) * TSTR + (i % DB) * 32, TSTR); };
-    };
-    auto dq = [&](int kb) {
-      return [&, kb](int i, bf16x8 at) {
-        acc[i % DB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(at, dsb[kb][i / DB], acc[i % DB], 0, 0, 0);
-      };
-    };
-    mfma_pipe<2 * KS, 6, 1, 0, 0>(rows(0), sdp(0));
-    soft(0);
-    mfma_pipe<2 * KS, 6, 1, 6, 1>(rows(1), sdp(1));
-    soft(1);
-    mfma_pipe<2 * DB, 4, 2, 12, 2>(trs(0), dq(0));
-    mfma_pipe<2 * DB, 4, 2, 0, 0>(trs(1), dq(1));
-  };
-
-  Stream ls, cs;
-  seek(ls, 0);
-  cs = ls;
-  load(ls);
-  store_stage(0);
-  __syncthreads();
-  for (int st = 0; st < nst; ++st) {
-    if (st + 1 < nst) {
-      step(ls);
-      load(ls);
-    }
-    compute(st & 1, min(cs.left, BN));
-    step(cs);
-    if (st + 1 < nst) store_stage((st + 1) & 1);
-    __syncthreads();
-  }
-
-  if (q_ok) {
-    __bf16* op = static_cast<__bf16*>(a.dq) + static_cast<int64_t>(q_row) * ld + hoff + 4 * hh;
-#pragma unroll
-    for (int db = 0; db < DB; ++db)
-#pragma unroll
-      for (int jj = 0; jj < 4; ++jj) {
-        bf16x4 v;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) v[i] = static_cast<__bf16>(acc[db][4 * jj + i] * a.scale);
-        *reinterpret_cast<bf16x4*>(op + db * 32 + 8 * jj) = v;
-      }
-  }
-}
-
-// ------------------------------------------------------------------ bf16: dK, dV
-
-// Swizzled LDS rows for the dK/dV kernel's query stages: every row takes 256
+// Swizzled LDS rows for the stages of both bf16 kernels: every row takes 256
 // bytes (128 bf16, the head's D channels and, for D = 64, unused space), and
 // 16-byte chunk c of row r is stored at chunk c ^ f(r & 15),
 // f(r) = ((r & 3) << 2) | (r >> 2).  Sixteen consecutive rows read at one
@@ -384,6 +204,198 @@ __device__ inline i32x4 rsrc_of(const void* base, uint32_t bytes) {
   r[3] = 0x00020000;
   return r;
 }
+
+// ------------------------------------------------------------------ bf16: dQ
+
+template <int D>
+__global__ __launch_bounds__(kBwdThreads) void dq_kernel(BwdArgs a) {
+  using L = Lay<D>;
+  constexpr int KS = L::KS, DB = L::DB;
+  constexpr int BN = kBwdKS, NKB = BN / 32;             // keys per stage, 32-key blocks
+  constexpr int KT = BN * 128 * 2;                      // bytes of one swizzled tile
+  constexpr int STB = 2 * KT;                           // K | V
+  constexpr int NDMA = KT / 1024 / (kBwdThreads / 64);  // 1 KB transfers per wave, tile and tensor
+  static_assert(NDMA * 1024 * (kBwdThreads / 64) == KT && BN % 32 == 0 && BN <= 128, "stage shape");
+  __shared__ __attribute__((aligned(16))) char lds[2 * STB];
+
+  int n_blocks = 0;
+  for (int g = 0; g < a.n_groups; ++g) n_blocks += a.groups[g].n_qblocks * a.num_heads;
+  const int b = xcd_remap(blockIdx.x, n_blocks);
+  int g = 0;
+  while (g + 1 < a.n_groups && b >= a.groups[g + 1].dq_block_begin) ++g;
+  const BwdGroupArgs& G = a.groups[g];
+  const int idx = b - G.dq_block_begin;
+  const int head = idx / G.n_qblocks, qt = idx % G.n_qblocks;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n = lane & 31, hh = lane >> 5;
+  const int q_row = G.q_begin + qt * kBwdQ + wave * 32 + n;
+  const bool q_ok = q_row < G.q_end;
+  const int64_t ld = a.ld, hoff = static_cast<int64_t>(head) * D;
+  const float c = a.scale_log2e;
+
+  // B operands: this lane's query, 8 channels of its half-wave per k step.
+  bf16x8 qf[KS], gf[KS];
+  {
+    const int64_t off = static_cast<int64_t>(q_ok ? q_row : G.q_begin) * ld + hoff + hh * 8;
+    const __bf16* qp = static_cast<const __bf16*>(a.q) + off;
+    const __bf16* gp = static_cast<const __bf16*>(a.d_out) + off;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      qf[ks] = q_ok ? *reinterpret_cast<const bf16x8*>(qp + ks * 16) : bf16x8{};
+      gf[ks] = q_ok ? *reinterpret_cast<const bf16x8*>(gp + ks * 16) : bf16x8{};
+    }
+  }
+  const int64_t stat = static_cast<int64_t>(head) * a.n_q + (q_ok ? q_row : G.q_begin);
+  const float lse2 = q_ok ? a.lse[stat] * kLog2e : 0.f;
+  const float dsum = q_ok ? a.dsum[stat] : 0.f;
+
+  f32x16 acc[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) acc[db] = f32x16{};
+
+  // Stage tiles of BN keys inside one run at a time; rows past the run's end
+  // arrive as zeros and are masked.
+  const int nr = G.n_runs;
+  int nst = 0;
+  for (int r = 0; r < nr; ++r) nst += (G.runs[r].n_tok + BN - 1) / BN;
+  struct Stream {
+    const __bf16* k;
+    const __bf16* v;
+    int left;  // tokens of the current run from k on
+    int r;
+  };
+  const int64_t tile_step = static_cast<int64_t>(BN) * ld;
+  auto seek = [&](Stream& s, int r) {
+    while (r < nr && G.runs[r].n_tok == 0) ++r;
+    s.r = r;
+    if (r < nr) {
+      s.k = static_cast<const __bf16*>(G.runs[r].k) + hoff;
+      s.v = static_cast<const __bf16*>(G.runs[r].v) + hoff;
+      s.left = G.runs[r].n_tok;
+    }
+  };
+  auto step = [&](Stream& s) {
+    s.left -= BN;
+    s.k += tile_step;
+    s.v += tile_step;
+    if (s.left <= 0) seek(s, s.r + 1);
+  };
+
+  // Per-lane global offsets of this wave's transfers, the same every stage
+  // (see the dK/dV kernel): logical chunk of the fixed LDS slot, zero past D.
+  const uint32_t row_bytes = static_cast<uint32_t>(ld) * 2;
+  uint32_t voff[NDMA];
+#pragma unroll
+  for (int i = 0; i < NDMA; ++i) {
+    const int p = (wave * NDMA + i) * 1024 + 16 * lane;
+    const int row = p >> 8, phys = (p >> 4) & 15, r = row & 15;
+    const int lc = phys ^ (((r & 3) << 2) | (r >> 2));
+    voff[i] = lc < D / 8 ? row * row_bytes + lc * 16 : 0x7ffffff0u;
+  }
+  const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds));
+  auto issue = [&](const Stream& s, int buf) {
+    const uint32_t bytes = static_cast<uint32_t>(min(s.left, BN) - 1) * row_bytes + D * 2;
+    const i32x4 rk = rsrc_of(s.k, bytes), rv = rsrc_of(s.v, bytes);
+    const uint32_t base = lds0 + buf * STB;
+#pragma unroll
+    for (int i = 0; i < NDMA; ++i) {
+      const uint32_t dst = __builtin_amdgcn_readfirstlane(base + (wave * NDMA + i) * 1024);
+      dma16(rk, voff[i], dst);
+      dma16(rv, voff[i], dst + KT);
+    }
+  };
+  const int t_lane = 4 * (lane >> 5) + ((lane & 15) >> 2);  // row of this lane's transposing read
+  const int t_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+
+  // One stage, 32-key blocks kb: S^T, dP^T of block kb with block kb - 1's
+  // softmax interleaved, then dQ^T from block kb - 1.
+  auto compute = [&](int buf, int nvalid) {
+    const __bf16* Ks = reinterpret_cast<const __bf16*>(lds + buf * STB);
+    const __bf16* Vs = reinterpret_cast<const __bf16*>(lds + buf * STB + KT);
+    f32x16 s[NKB], dp[NKB];
+    bf16x8 dsb[NKB][2];
+    auto rows = [&](int kb) {
+      return [&, kb](int i) {
+        const int o = swz(kb * 32 + n, hh * 8 + (i >> 1) * 16);
+        return *reinterpret_cast<const bf16x8*>(((i & 1) ? Vs : Ks) + o);
+      };
+    };
+    auto sdp = [&](int kb) {
+      return [&, kb](int i, bf16x8 av) {
+        const int ks = i >> 1;
+        if (i & 1)
+          dp[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, gf[ks], ks == 0 ? f32x16{} : dp[kb], 0, 0, 0);
+        else
+          s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qf[ks], ks == 0 ? f32x16{} : s[kb], 0, 0, 0);
+      };
+    };
+    // dS^T = P^T * (dP^T - rowsum); element e of block kb is key kb*32 + 8(e/4) + 4hh + e%4.
+    auto soft = [&](int kb) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int key = kb * 32 + 8 * (e >> 2) + 4 * hh + (e & 3);
+        const float p = key < nvalid ? __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][e], c, -lse2)) : 0.f;
+        dsb[kb][e >> 3][e & 7] = static_cast<__bf16>(p * (dp[kb][e] - dsum));
+      }
+    };
+    auto trs = [&](int kb) {
+      return [&, kb](int i) {
+        const int r0 = kb * 32 + (i / DB) * 16 + t_lane, c0 = (i % DB) * 32 + t_col;
+        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(Ks + swz(r0, c0)));
+        const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(Ks + swz(r0 + 8, c0)));
+        return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+      };
+    };
+    auto dq = [&](int kb) {
+      return [&, kb](int i, bf16x8 at) {
+        acc[i % DB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(at, dsb[kb][i / DB], acc[i % DB], 0, 0, 0);
+      };
+    };
+    mfma_pipe<2 * KS, 6, 1, 0, 0>(rows(0), sdp(0));
+#pragma unroll
+    for (int kb = 1; kb < NKB; ++kb) {
+      soft(kb - 1);
+      mfma_pipe<2 * KS, 6, 1, 6, 1>(rows(kb), sdp(kb));
+      mfma_pipe<2 * DB, 4, 2, 0, 0>(trs(kb - 1), dq(kb - 1));
+    }
+    soft(NKB - 1);
+    mfma_pipe<2 * DB, 4, 2, 0, 0>(trs(NKB - 1), dq(NKB - 1));
+  };
+
+  Stream ls, cs;
+  seek(ls, 0);
+  cs = ls;
+  issue(ls, 0);
+  wait_vmcnt<0>();
+  __syncthreads();
+  for (int st = 0; st < nst; ++st) {
+    if (st + 1 < nst) {
+      step(ls);
+      issue(ls, (st + 1) & 1);
+    }
+    compute(st & 1, min(cs.left, BN));
+    step(cs);
+    wait_vmcnt<0>();
+    __syncthreads();
+  }
+
+  if (q_ok) {
+    __bf16* op = static_cast<__bf16*>(a.dq) + static_cast<int64_t>(q_row) * ld + hoff + 4 * hh;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        bf16x4 v;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] = static_cast<__bf16>(acc[db][4 * jj + i] * a.scale);
+        *reinterpret_cast<bf16x4*>(op + db * 32 + 8 * jj) = v;
+      }
+  }
+}
+
+// ------------------------------------------------------------------ bf16: dK, dV
 
 template <int D>
 __global__ __launch_bounds__(kBwdThreads) void dkdv_kernel(BwdArgs a) {

@@ -68,7 +68,7 @@ constexpr int64_t partial_record_floats(int head_dim) { return static_cast<int64
 // kernel) per wave; the other operand streams through LDS in stages.
 constexpr int kBwdThreads = 256;
 constexpr int kBwdQ = 128;     // dQ kernel: queries per block
-constexpr int kBwdKS = 64;     // dQ kernel: keys per LDS stage
+constexpr int kBwdKS = 128;    // dQ kernel: keys per LDS stage
 constexpr int kBwdK = 128;     // dK/dV kernel: keys per block
 constexpr int kBwdQS = 128;    // dK/dV kernel: queries per LDS stage
 constexpr int kBwdF32 = 64;    // fp32 kernels: one query or key per lane
