@@ -43,6 +43,7 @@
 #include <hip/hip_runtime.h>
 
 #include "kernels.hpp"
+#include "lds_stage.hpp"
 
 namespace mssa {
 namespace {
@@ -74,29 +75,16 @@ __device__ inline const T* ctx_row(const BwdGroupArgs& G, int j, bool v, int64_t
   return static_cast<const T*>(v ? G.runs[r].v : G.runs[r].k) + static_cast<int64_t>(j) * ld;
 }
 
-// Operand reads shared by both bf16 kernels.  Row layout (stride D + 8): a
-// 32-row block is read as the A operand of a 32x32x16 MFMA, lane n taking row
-// n and the 8 columns of its half-wave.  Transposing layout (stride D + 32):
-// the A operand X^T[d][row] of a 32-wide d block db and 16 rows, in the row
-// order in which a 32x32 accumulator's lane holds its 16 values, so that the
-// accumulator packed to bf16 is the matching B operand.
+// Operand shapes of both bf16 kernels: a 32-row block is read as the A
+// operand of a 32x32x16 MFMA (lane n takes row n and the 8 columns of its
+// half-wave), or, through the transposing read, as X^T[d][row] of a 32-wide d
+// block and 16 rows in the row order in which a 32x32 accumulator's lane holds
+// its 16 values, so that the accumulator packed to bf16 is the matching B
+// operand.
 template <int D>
 struct Lay {
-  static constexpr int KS = D / 16, DB = D / 32, CPR = D / 8;
-  static constexpr int ASTR = D + 8, TSTR = D + 32;
-  static constexpr int RPL = kBwdThreads / CPR;  // rows per pass of the block's loads
+  static constexpr int KS = D / 16, DB = D / 32;
 };
-
-__device__ inline int tr_offset(int lane, int tstr) {
-  const int gq = lane >> 4;
-  return (4 * (gq >> 1) + ((lane & 15) >> 2)) * tstr + 16 * (gq & 1) + 4 * (lane & 3);
-}
-
-__device__ inline bf16x8 tr_read(const __bf16* p, int tstr) {
-  const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)p);
-  const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p + 8 * tstr));
-  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-}
 
 // ------------------------------------------------------------------ rowsum(dO * O)
 
@@ -121,13 +109,6 @@ __global__ __launch_bounds__(kDotThreads) void dot_kernel(DotArgs a) {
 }
 
 // ------------------------------------------------------------------ bf16 kernels
-
-// Buffer resource (gfx9 layout) over `bytes` bytes from `base`: loads past
-// the end return zeros, which zero-fills ragged stage tiles without selects.
-__device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0),
-                                           static_cast<int>(bytes), 0x00020000);
-}
 
 // N MFMAs whose A operands come from LDS: operand i is read by rd(i) (NRD LDS
 // instructions) L operands ahead of its MFMA mf(i, a), so LDS latency hides
@@ -160,50 +141,10 @@ __device__ __forceinline__ void mfma_pipe(Rd&& rd, Mf&& mf) {
   __builtin_amdgcn_sched_barrier(0);
 }
 
-// Swizzled LDS rows for the stages of both bf16 kernels: every row takes 256
-// bytes (128 bf16, the head's D channels and, for D = 64, unused space), and
-// 16-byte chunk c of row r is stored at chunk c ^ f(r & 15),
-// f(r) = ((r & 3) << 2) | (r >> 2).  Sixteen consecutive rows read at one
-// column (the row reads of S = Q K^T and dP = dO V^T) then hit 16 distinct
-// bank groups, and so do the 4 rows x 4 chunks of a transposing read (dV^T
-// += dO^T P, dK^T += Q^T dS): one copy of Q and dO serves both.
-__device__ inline int swz(int row, int col) {
-  const int r = row & 15;
-  return row * 128 + ((((col >> 3) ^ (((r & 3) << 2) | (r >> 2)))) << 3) + (col & 7);
-}
-
-typedef int i32x4 __attribute__((ext_vector_type(4)));
-
-// Direct global -> LDS load (buffer_load_dwordx4 ... lds): lane i's 16 bytes
-// at buffer offset voff land at LDS byte address lds_addr + 16 i (lds_addr
-// wave-uniform); offsets past the buffer's range write zeros.  Counted by
-// vmcnt; issued from inline asm so the compiler does not make every later
-// LDS read wait for it (the kernel waits before the barrier that publishes
-// the stage).  m0 is set here and not used otherwise.
-__device__ inline void dma16(i32x4 rsrc, uint32_t voff, uint32_t lds_addr) {
-#pragma clang diagnostic push
-#pragma clang diagnostic ignored "-Winline-asm"
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
-               :: "s"(lds_addr), "v"(voff), "s"(rsrc) : "memory", "m0");
-#pragma clang diagnostic pop
-}
-
-// s_waitcnt vmcnt(N) alone (gfx9 encoding: expcnt and lgkmcnt at their maxima).
-template <int N>
-__device__ inline void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
-}
-
-__device__ inline i32x4 rsrc_of(const void* base, uint32_t bytes) {
-  const uint64_t b = reinterpret_cast<uint64_t>(base);
-  i32x4 r;
-  r[0] = __builtin_amdgcn_readfirstlane(static_cast<int>(b & 0xffffffffu));
-  r[1] = __builtin_amdgcn_readfirstlane(static_cast<int>((b >> 32) & 0xffffu));
-  r[2] = __builtin_amdgcn_readfirstlane(static_cast<int>(bytes));
-  r[3] = 0x00020000;
-  return r;
-}
+// Stage rows: one copy per tensor in the 256-byte swizzled layout of
+// lds_stage.hpp (row reads and transposing reads both conflict-free), filled
+// by direct transfers.
+__device__ inline int swz(int row, int col) { return swz256(row, col); }
 
 // ------------------------------------------------------------------ bf16: dQ
 
@@ -290,9 +231,9 @@ __global__ __launch_bounds__(kBwdThreads) void dq_kernel(BwdArgs a) {
 #pragma unroll
   for (int i = 0; i < NDMA; ++i) {
     const int p = (wave * NDMA + i) * 1024 + 16 * lane;
-    const int row = p >> 8, phys = (p >> 4) & 15, r = row & 15;
-    const int lc = phys ^ (((r & 3) << 2) | (r >> 2));
-    voff[i] = lc < D / 8 ? row * row_bytes + lc * 16 : 0x7ffffff0u;
+    const int row = p >> 8, phys = (p >> 4) & 15;
+    const int lc = unswz256(row, phys);
+    voff[i] = lc < D / 8 ? row * row_bytes + lc * 16 : kPastEnd;
   }
   const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds));
   auto issue = [&](const Stream& s, int buf) {
@@ -452,9 +393,9 @@ __global__ __launch_bounds__(kBwdThreads) void dkdv_kernel(BwdArgs a) {
 #pragma unroll
   for (int i = 0; i < NDMA; ++i) {
     const int p = (wave * NDMA + i) * 1024 + 16 * lane;
-    const int row = p >> 8, phys = (p >> 4) & 15, r = row & 15;
-    const int lc = phys ^ (((r & 3) << 2) | (r >> 2));
-    voff[i] = lc < D / 8 ? row * row_bytes + lc * 16 : 0x7ffffff0u;
+    const int row = p >> 8, phys = (p >> 4) & 15;
+    const int lc = unswz256(row, phys);
+    voff[i] = lc < D / 8 ? row * row_bytes + lc * 16 : kPastEnd;
   }
   const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds));
   // Stage queries [q0, q0 + BQ) into LDS buffer buf: Q and dO tiles by

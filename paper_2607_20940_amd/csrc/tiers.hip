@@ -14,11 +14,14 @@
 //                      (bf16 in, fp32 accumulation, bf16 out), 128 x 128
 //                      tiles in 32-deep stages double-buffered in LDS; the
 //                      output columns may be split over up to three tensors
-//                      (q | k | v);
+//                      (q | k | v); gemm_dma_kernel is the same product for
+//                      K a multiple of 64 with 64-deep stages filled by
+//                      direct global -> LDS transfers;
 //   unpatchify_kernel  patch rows [tokens, C*P*P] -> latent pixels.
 #include <hip/hip_runtime.h>
 
 #include "kernels.hpp"
+#include "lds_stage.hpp"
 
 namespace mssa {
 namespace {
@@ -166,6 +169,104 @@ __global__ __launch_bounds__(kTierThreads) void gemm_kernel(GemmArgs a) {
   }
 }
 
+// The same product for K a multiple of 64: 64-deep stages of 128-byte rows in
+// the swizzled layout of lds_stage.hpp, filled by direct global -> LDS
+// transfers (no staging registers), 64 KB of LDS so that two blocks share a
+// CU (two waves per SIMD); 16 MFMAs per wave between barriers.
+constexpr int kG2K = 64, kG2Tile = kGM * kG2K * 2;  // bytes of one 128 x 64 operand tile
+
+__global__ __launch_bounds__(kTierThreads, 2) void gemm_dma_kernel(GemmArgs a) {
+  constexpr int NDMA = kG2Tile / 1024 / (kTierThreads / 64);
+  static_assert(NDMA * 1024 * (kTierThreads / 64) == kG2Tile, "tile must split into 1 KB transfers per wave");
+  __shared__ __attribute__((aligned(16))) char lds[2][2][kG2Tile];  // [stage][X | W]
+  const int tiles_m = (a.M + kGM - 1) / kGM;
+  const int tm = blockIdx.x % tiles_m, tn = blockIdx.x / tiles_m;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave & 1, wn = wave >> 1;
+  const int n32 = lane & 31, hh = lane >> 5;
+
+  // Per-lane offsets of this wave's transfers inside a stage (row p / 128 of
+  // the tile, logical chunk of the physical slot): the same for every stage
+  // of both operands up to the row stride.
+  const uint32_t xrb = static_cast<uint32_t>(a.ldx) * 2, wrb = static_cast<uint32_t>(a.K) * 2;
+  uint32_t xo[NDMA], wo[NDMA];
+#pragma unroll
+  for (int i = 0; i < NDMA; ++i) {
+    const int p = (wave * NDMA + i) * 1024 + 16 * lane;
+    const int row = p >> 7, lc = unswz128(row, (p >> 4) & 7);
+    xo[i] = row * xrb + lc * 16;
+    wo[i] = row * wrb + lc * 16;
+  }
+  const int mrows = min(kGM, a.M - tm * kGM), nrows = min(kGN, a.N - tn * kGN);
+  const __bf16* X = static_cast<const __bf16*>(a.x) + static_cast<int64_t>(tm) * kGM * a.ldx;
+  const __bf16* W = static_cast<const __bf16*>(a.w) + static_cast<int64_t>(tn) * kGN * a.K;
+  const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(&lds[0][0][0]));
+  auto issue = [&](int k0, int s) {
+    // rows past the matrix edge fall past the range: zeros
+    const i32x4 rx = rsrc_of(X + k0, static_cast<uint32_t>(mrows - 1) * xrb + kG2K * 2);
+    const i32x4 rw = rsrc_of(W + k0, static_cast<uint32_t>(nrows - 1) * wrb + kG2K * 2);
+    const uint32_t base = lds0 + s * 2 * kG2Tile;
+#pragma unroll
+    for (int i = 0; i < NDMA; ++i) {
+      const uint32_t dst = __builtin_amdgcn_readfirstlane(base + (wave * NDMA + i) * 1024);
+      dma16(rx, xo[i], dst);
+      dma16(rw, wo[i], dst + kG2Tile);
+    }
+  };
+
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+    for (int cb = 0; cb < 2; ++cb) acc[rb][cb] = f32x16{};
+
+  const int nst = a.K / kG2K;
+  issue(0, 0);
+  wait_vmcnt<0>();
+  __syncthreads();
+  for (int st = 0; st < nst; ++st) {
+    if (st + 1 < nst) issue((st + 1) * kG2K, (st + 1) & 1);
+    const __bf16* Xs = reinterpret_cast<const __bf16*>(lds[st & 1][0]);
+    const __bf16* Ws = reinterpret_cast<const __bf16*>(lds[st & 1][1]);
+#pragma unroll
+    for (int ks = 0; ks < kG2K / 16; ++ks) {
+      bf16x8 xb[2], wa[2];
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        xb[j] = *reinterpret_cast<const bf16x8*>(Xs + swz128(wm * 64 + j * 32 + n32, ks * 16 + hh * 8));
+        wa[j] = *reinterpret_cast<const bf16x8*>(Ws + swz128(wn * 64 + j * 32 + n32, ks * 16 + hh * 8));
+      }
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb)
+          acc[rb][cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wa[cb], xb[rb], acc[rb][cb], 0, 0, 0);
+    }
+    wait_vmcnt<0>();
+    __syncthreads();
+  }
+
+  const __bf16* B = static_cast<const __bf16*>(a.bias);
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb) {
+    const int64_t row = static_cast<int64_t>(tm) * kGM + wm * 64 + rb * 32 + n32;
+    if (row >= a.M) continue;
+#pragma unroll
+    for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        const int col = tn * kGN + wn * 64 + cb * 32 + 8 * jj + 4 * hh;
+        if (col >= a.N) continue;
+        const int part = col / a.split, pc = col % a.split;
+        bf16x4 v;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] = static_cast<__bf16>(acc[rb][cb][4 * jj + i] + static_cast<float>(B[col + i]));
+        *reinterpret_cast<bf16x4*>(static_cast<__bf16*>(a.y[part]) + row * a.ldy + pc) = v;
+      }
+  }
+}
+
 }  // namespace
 
 hipError_t launch_patchify(const PatchArgs& a, hipStream_t stream) {
@@ -187,7 +288,10 @@ hipError_t launch_unpatchify(const PatchArgs& a, hipStream_t stream) {
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t stream) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
   const int64_t blocks = static_cast<int64_t>((a.M + kGM - 1) / kGM) * ((a.N + kGN - 1) / kGN);
-  hipLaunchKernelGGL(gemm_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kTierThreads), 0, stream, a);
+  if (a.K % kG2K == 0)
+    hipLaunchKernelGGL(gemm_dma_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kTierThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL(gemm_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kTierThreads), 0, stream, a);
   return hipGetLastError();
 }
 
