@@ -166,7 +166,8 @@ class Plan:
 
     def __del__(self):
         h, self._h = getattr(self, "_h", None), None
-        if h:
+        # at interpreter exit the module globals may already be gone
+        if h and lib is not None:
             lib.mssa_plan_destroy(h)
 
     def info(self):
