@@ -90,11 +90,22 @@ def cpu_baseline(w, x, info, budget_s):
         log(f"cpu oracle head {h}: {t_total:.1f} s cumulative")
         if t_total >= budget_s:
             break
+    cpu_model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    cpu_model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
     return {
         "value": flops_per_head * done / t_total / 1e12,
         "unit": "TFLOP/s",
         "cores": threads,
         "kind": "oracle",
+        "cpu_model": cpu_model,
+        "nproc": os.cpu_count(),
         "sample": f"{done} of {nh} heads of {w['name']} (pool + attention, all {info['n_q']} queries), "
                   f"fp64 numpy, {t_total:.1f} s",
         "ms_per_pass_extrapolated": 1e3 * t_total / done * nh,
@@ -474,6 +485,7 @@ def main():
         },
         "pct_of_bf16_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
         "forward_ms": round(float(fwd_ms.mean()), 4),
+        "forward_ms_median": round(float(np.median(fwd_ms)), 4),
         "forward_ms_p10_p90": [round(float(np.percentile(fwd_ms, 10)), 4),
                                round(float(np.percentile(fwd_ms, 90)), 4)],
         "pool_ms": round(float(pool_ms.mean()), 4),

@@ -206,3 +206,36 @@ def test_backward_full_size_one_head_and_sum_rules():
     assert np.abs(dk).max() <= 1e-2 * scale_k, np.abs(dk).max()
     print(f"[bwd] sum rules: dV {np.abs(dv - want).max():.3e} (scale {scale_v:.3e}), "
           f"dK {np.abs(dk).max():.3e} (scale {scale_k:.3e})", flush=True)
+
+
+def test_backward_long_history_one_head():
+    """21 history frames and the three-level schedule with ragged 4x pooling
+    (30 x 52 -> 8 x 13): one head's gradients in full against the oracle."""
+    w = WORKLOADS["wan13b_longhist"]
+    print("[bwd] full-size wan13b_longhist", flush=True)
+    r = BwdRun(w["desc"], w["dtype"], w["seed"], w["amplitude"])
+    r.run()
+    res = _assert_grads(r.grads(), r.oracle(heads=[3]), "bf16", "wan13b_longhist", heads=[3])
+    print(f"[bwd] wan13b_longhist head 3 {res}", flush=True)
+
+
+def test_backward_720p_sum_rules():
+    """The 14B-shaped 720p layer (40 heads, 45 x 80, ragged at 2x and 4x): for
+    every head, the sum of dV over all source tokens equals the sum of dO and
+    the sum of dK is zero, up to the gradients' rounding."""
+    w = WORKLOADS["wan14b_720p"]
+    print("[bwd] full-size wan14b_720p sum rules", flush=True)
+    r = BwdRun(w["desc"], w["dtype"], w["seed"], w["amplitude"])
+    r.run()
+    got = r.grads()
+    for k in NAMES:
+        assert np.isfinite(got[k]).all(), k
+    go = to_f64(r.go, "bf16")
+    dv = sum(got[k].sum(axis=0) for k in ("v_sink", "v_hist", "v_win"))
+    dk = sum(got[k].sum(axis=0) for k in ("k_sink", "k_hist", "k_win"))
+    scale_v = np.abs(got["v_win"]).sum(axis=0).max()
+    scale_k = np.abs(got["k_win"]).sum(axis=0).max()
+    assert np.abs(dv - go.sum(axis=0)).max() <= 1e-2 * scale_v
+    assert np.abs(dk).max() <= 1e-2 * scale_k
+    print(f"[bwd] 720p sum rules: dV {np.abs(dv - go.sum(axis=0)).max():.3e} (scale {scale_v:.3e}), "
+          f"dK {np.abs(dk).max():.3e} (scale {scale_k:.3e})", flush=True)
