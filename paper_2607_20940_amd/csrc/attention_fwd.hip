@@ -32,6 +32,7 @@
 #include <type_traits>
 
 #include "kernels.hpp"
+#include "lds_stage.hpp"
 
 namespace mssa {
 namespace {
@@ -63,6 +64,7 @@ __device__ inline Work decode(const FwdArgs& a, int L) {
 // so exponentials stay <= 2^8 and most tiles skip the O rescale.  The final
 // O / l is unchanged; only rounding differs.
 constexpr float kRescaleLog2 = 8.0f;
+constexpr float kRescaleSum = 256.0f;  // 2^kRescaleLog2
 constexpr float kLn2 = 0.6931471805599453f;
 
 // ---------------------------------------------------------------------------
@@ -119,26 +121,20 @@ __device__ inline Loc locate(const FwdArgs& a, int64_t t) {
   return {g, item, k, G.tile_begin + static_cast<int64_t>(item) * G.tiles_per_item};
 }
 
-// Buffer resource (gfx9 layout) over `bytes` bytes from `base`: loads past
-// the end return zeros, which is how ragged K/V tiles are zero-filled without
-// per-element selects.
-__device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0),
-                                           static_cast<int>(bytes), 0x00020000);
-}
-
 template <int D>
 struct FwdTile {
   static constexpr int BM = kFwdBM, BN = kFwdBN;
   static constexpr int KS = D / 16;    // 16-wide k-steps of q k^T
   static constexpr int DB = D / 32;    // 32-row blocks of O^T
-  static constexpr int CPR = D / 8;    // 16-byte chunks per K/V row
-  static constexpr int RPL = kFwdThreads / CPR;  // rows covered by one pass of the block
-  static constexpr int KSTR = D + 8;   // K row stride: 16 consecutive rows hit disjoint banks
-  static constexpr int VSTR = D + 32;  // V row stride: transposing reads of 32 lanes hit disjoint banks
-  static constexpr int NLD = BN / RPL; // 16-byte chunks per thread per tile and tensor
-  static constexpr int KT = BN * KSTR, VT = BN * VSTR;  // elements per LDS tile
-  static_assert(NLD * RPL == BN, "tile load must divide evenly");
+  // K and V tiles: 256-byte rows (the channels of one head, zero past D) in
+  // the XOR-swizzled layout of lds_stage.hpp, so that the K row reads and
+  // the transposing V reads are both conflict-free; filled by direct
+  // global -> LDS transfers of 1 KB (four rows) per wave instruction.
+  static constexpr int KT = BN * 128, VT = BN * 128;  // elements per LDS tile
+  static constexpr int NDMA = BN * 256 / 1024 / 4;    // transfers per wave of a group, per tile
+  static constexpr int kLead = 8;                     // operands read ahead of their MFMA
+  static constexpr int LDS_BYTES = 2 * (2 * KT + 2 * VT);
+  static_assert(NDMA == 4, "transfer addressing assumes 16 rows per wave");
 };
 
 // Value of lane l ^ 32.  v_permlane32_swap exchanges the upper half of its
@@ -164,16 +160,22 @@ __device__ inline float halfwave_sum(float v) { return v + other_half(v); }
 // are separated by block barriers; in phase 2j group 0 runs its matrix-core
 // step M(j) = {O += P_{j-1} V_{j-1}; S_j = K_j Q^T} while group 1 runs its
 // softmax step on S_{j-1}, and in phase 2j + 1 the roles swap.  Each SIMD
-// thus has one wave issuing MFMAs while the other issues VALU work.  K_j is
-// loaded from global memory during phase 2j - 2 and stored to LDS at the end
-// of phase 2j - 1; V_j is loaded during phase 2j - 1 and stored at the end of
-// phase 2j; two LDS buffers each suffice.
+// thus has one wave issuing MFMAs while the other issues VALU work.
+//
+// Tile traffic is by direct transfers: at the start of phase 2j group 0
+// issues K_{j+1} (waited for at the end of phase 2j + 1) and group 1 issues
+// V_j (waited for at the end of phase 2j, its softmax phase).  The first
+// kLead operands of a matrix-core step (V^T of the previous tile) are read
+// from LDS at the end of the wave's softmax phase, before the barrier, so
+// the step starts with its operands in registers.  K_{j+1} goes to the
+// buffer of K_{j-1} (last read in phase 2j - 1), V_j to that of V_{j-2}
+// (last read in phase 2j - 1, prefetched in phase 2j - 2 at the latest).
 template <int D>
 __device__ __forceinline__ void attend_piece(const FwdArgs& a, const FwdGroupArgs& G, int item, int k,
-                                             int nt, bool whole, int rec, __bf16* lds) {
+                                             int nt, bool whole, int rec, char* lds) {
   using P = FwdTile<D>;
-  constexpr int BM = P::BM, BN = P::BN, KS = P::KS, DB = P::DB, CPR = P::CPR, RPL = P::RPL;
-  constexpr int KSTR = P::KSTR, VSTR = P::VSTR, NLD = P::NLD, KT = P::KT, VT = P::VT;
+  constexpr int BM = P::BM, BN = P::BN, KS = P::KS, DB = P::DB, NDMA = P::NDMA, kLead = P::kLead;
+  constexpr int KT = P::KT, VT = P::VT;
 
   const int head = item / G.n_qtiles;
   const int qtile = item - head * G.n_qtiles;
@@ -212,16 +214,32 @@ __device__ __forceinline__ void attend_piece(const FwdArgs& a, const FwdGroupArg
   float l_part = 0.f;       // this lane's share of the row sum
   f32x16 s[BN / 32];
   bf16x8 pb[BN / 32][2];
+  bf16x8 ring[kLead];       // LDS operands of the matrix-core step, kLead ahead
 
-  const int ld_row = tid / CPR, ld_col = (tid % CPR) * 8;
-  const uint32_t g_off = ld_row * row_bytes + ld_col * 2;
-  const int k_st = ld_row * KSTR + ld_col;
-  const int v_st = ld_row * VSTR + ld_col;
-  const int gq = lane >> 4;
-  const int v_rd = (4 * (gq >> 1) + ((lane & 15) >> 2)) * VSTR + 16 * (gq & 1) + 4 * (lane & 3);
-  const int k_rd = n * KSTR + hh * 8;
-  __bf16* const Klds = lds;
-  __bf16* const Vlds = lds + 2 * KT;
+  // Operand addresses in the swizzled tiles (elements).  K row reads: row
+  // 32 kb + n, columns 16 ks + 8 hh, at 32 kb * 128 + (k_rd ^ 16 ks).
+  // Transposing V reads: rows R + t_row (+ 8 for the upper half), columns
+  // 32 db + t_col with R a multiple of 16, at R * 128 + v_rd[db][half]: the
+  // swizzle of a row depends only on its index mod 16.
+  const int k_rd = swz256(n, hh * 8);
+  const int t_row = 4 * (lane >> 5) + ((lane & 15) >> 2);
+  const int t_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  int v_rd[DB][2];
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int h = 0; h < 2; ++h) v_rd[db][h] = swz256(t_row + 8 * h, db * 32 + t_col);
+  __bf16* const Klds = reinterpret_cast<__bf16*>(lds);
+  __bf16* const Vlds = Klds + 2 * KT;
+
+  // This wave's tile transfers: transfer i fills LDS bytes
+  // ((wave & 3) * NDMA + i) * 1024 + 16 lane, i.e. row (wave & 3) * 16 + 4 i +
+  // lane / 16, physical chunk lane % 16, whose logical chunk is
+  // lane % 16 ^ 4 (lane / 16) ^ i (the swizzle of rows 4 i .. 4 i + 3 mod 16).
+  // The lane's global offset is then t_off ^ 16 i plus the scalar 4 i rows
+  // (row_bytes is a multiple of 128, so the chunk bits do not carry).
+  const int t_lc = (lane & 15) ^ ((lane >> 4) << 2);
+  const uint32_t t_off = ((wave & 3) * 16 + (lane >> 4)) * row_bytes + t_lc * 16;
 
   // Tile streams over the item's context runs.  A stream points at its
   // current tile (head offset applied) and counts the tokens of the run from
@@ -234,10 +252,10 @@ __device__ __forceinline__ void attend_piece(const FwdArgs& a, const FwdGroupArg
     int r;            // current run
   };
   const int64_t tile_step = static_cast<int64_t>(BN) * ld;
-  auto run_base = [&](auto is_v, int r) {
-    return static_cast<const __bf16*>(decltype(is_v)::value ? G.runs[r].v : G.runs[r].k) + hoff;
+  auto run_base = [&](bool is_v, int r) {
+    return static_cast<const __bf16*>(is_v ? G.runs[r].v : G.runs[r].k) + hoff;
   };
-  auto stream_at = [&](auto is_v, int j) {  // j: tile index within the item
+  auto stream_at = [&](bool is_v, int j) {  // j: tile index within the item
     int r = 0;
     while (j >= (G.runs[r].n_tok + BN - 1) / BN) {
       j -= (G.runs[r].n_tok + BN - 1) / BN;
@@ -245,7 +263,7 @@ __device__ __forceinline__ void attend_piece(const FwdArgs& a, const FwdGroupArg
     }
     return Stream{run_base(is_v, r) + j * tile_step, G.runs[r].n_tok - j * BN, r};
   };
-  auto step = [&](auto is_v, Stream& st) {
+  auto step = [&](bool is_v, Stream& st) {
     st.left -= BN;
     st.p += tile_step;
     if (st.left <= 0) {
@@ -258,78 +276,77 @@ __device__ __forceinline__ void attend_piece(const FwdArgs& a, const FwdGroupArg
       }
     }
   };
-  using KSel = std::false_type;
-  using VSel = std::true_type;
 
-  bf16x8 pk[NLD], pv[NLD];
-  // The stream's current tile into registers; rows past the run's end read as
-  // zeros through the buffer range check.
-  auto load = [&](const Stream& st, bf16x8* dst) {
+  // Direct transfers of the stream's current tile into K (is_v false) or V
+  // buffer buf; rows past the run's end arrive as zeros through the buffer
+  // range check.  Waited for (vmcnt) before the barrier that publishes it.
+  const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds));
+  auto issue = [&](const Stream& st, bool is_v, int buf) {
     const uint32_t bytes = static_cast<uint32_t>(min(st.left, BN) - 1) * row_bytes + D * 2;
-    const auto rs = make_rsrc(st.p, bytes);
+    const i32x4 rs = rsrc_of(st.p, bytes);
+    const uint32_t base = lds0 + (is_v ? 2 * KT * 2 : 0) + buf * KT * 2 + (wave & 3) * NDMA * 1024;
 #pragma unroll
-    for (int i = 0; i < NLD; ++i)
-      dst[i] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rs, g_off + i * RPL * row_bytes, 0, 0));
+    for (int i = 0; i < NDMA; ++i) {
+      // chunks past D (head_dim 64) read past the range: zeros
+      const uint32_t vo = (D / 8 >= 16 || (t_lc ^ i) < D / 8) ? (t_off ^ (i * 16)) : kPastEnd;
+      dma16_soff(rs, vo, i * 4 * row_bytes, __builtin_amdgcn_readfirstlane(base + i * 1024));
+    }
   };
-  auto store_k = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < NLD; ++i)
-      *reinterpret_cast<bf16x8*>(Klds + buf * KT + k_st + i * RPL * KSTR) = pk[i];
+
+  // Operands of a matrix-core step, in MFMA order: with pv_c the V^T
+  // operands of O += P V (key block kb, 16-key half cc, column block db;
+  // two transposing reads each), then with s_c the K operands of S = K Q^T
+  // (k-step ks, key block kb; one row read each).
+  auto operand = [&](auto pv_c, int i, int vb, int kb_) -> bf16x8 {
+    constexpr int NPV = decltype(pv_c)::value ? 2 * (BN / 32) * DB : 0;
+    if (i < NPV) {
+      const int st = i / DB, db = i % DB, kb = st >> 1, cc = st & 1;
+      const __bf16* vrow = Vlds + vb * VT + (kb * 32 + cc * 16) * 128;
+      const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vrow + v_rd[db][0]));
+      const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vrow + v_rd[db][1]));
+      return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+    }
+    const int j = i - NPV, ks = j / (BN / 32), kb = j % (BN / 32);
+    return *reinterpret_cast<const bf16x8*>(Klds + kb_ * KT + kb * 32 * 128 + (k_rd ^ (ks * 16)));
   };
-  auto store_v = [&](int buf) {
+  // The first kLead operands of a step into the ring (a step has at least
+  // kLead operands: 2 (BN / 32) DB V^T operands, or KS (BN / 32) K operands).
+  auto prefill = [&](auto pv_c, int vb, int kb_) {
+    constexpr int N = (decltype(pv_c)::value ? 2 * (BN / 32) * DB : KS * (BN / 32));
+    static_assert(N >= kLead, "ring longer than a step");
 #pragma unroll
-    for (int i = 0; i < NLD; ++i)
-      *reinterpret_cast<bf16x8*>(Vlds + buf * VT + v_st + i * RPL * VSTR) = pv[i];
+    for (int i = 0; i < kLead; ++i)
+      if (i < N) ring[i] = operand(pv_c, i, vb, kb_);
   };
 
   // Matrix-core step: O += P V from V buffer vb (if pv_c), then S = K Q^T from
-  // K buffer kb_ (if s_c), as one stream of MFMAs whose LDS operands (V^T
-  // through transposing reads, K row-major) run kLead operands ahead in a
-  // register ring, so LDS latency hides behind kLead MFMAs.  Scheduling group
-  // barriers fix the interleave: the compiler would otherwise hoist every read
-  // to the top (more registers) or sink each next to its MFMA (no overlap).
+  // K buffer kb_ (if s_c), as one stream of MFMAs whose LDS operands run
+  // kLead operands ahead in the register ring (filled before the step).
+  // Scheduling group barriers fix the interleave: the compiler would
+  // otherwise hoist every read to the top (more registers) or sink each next
+  // to its MFMA (no overlap).
   auto mstep = [&](auto pv_c, auto s_c, int vb, int kb_) {
     constexpr bool kPV = decltype(pv_c)::value, kS = decltype(s_c)::value;
     constexpr int NPV = kPV ? 2 * (BN / 32) * DB : 0;  // (key block, 16-key half, d block)
     constexpr int NS = kS ? KS * (BN / 32) : 0;        // (d slice, key block)
     constexpr int N = NPV + NS;
-    constexpr int kLead = 8;
-    const __bf16* Vb = Vlds + vb * VT + v_rd;
-    const __bf16* Kb = Klds + kb_ * KT + k_rd;
-    auto operand = [&](int i) -> bf16x8 {
-      if (i < NPV) {
-        const int st = i / DB, db = i % DB, kb = st >> 1, cc = st & 1;
-        const __bf16* vrow = Vb + (kb * 32 + cc * 16) * VSTR + db * 32;
-        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)vrow);
-        const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vrow + 8 * VSTR));
-        return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-      }
-      const int j = i - NPV, ks = j / (BN / 32), kb = j % (BN / 32);
-      return *reinterpret_cast<const bf16x8*>(Kb + kb * 32 * KSTR + ks * 16);
-    };
-    bf16x8 ring[kLead];
-#pragma unroll
-    for (int i = 0; i < kLead; ++i)
-      if (i < N) ring[i] = operand(i);
 #pragma unroll
     for (int i = 0; i < N; ++i) {
-      const bf16x8 a = ring[i % kLead];
+      const bf16x8 av = ring[i % kLead];
       if (i < NPV) {
         const int st = i / DB, db = i % DB, kb = st >> 1, cc = st & 1;
-        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[kb][cc], o[db], 0, 0, 0);
+        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[kb][cc], o[db], 0, 0, 0);
       } else {
         const int j = i - NPV, ks = j / (BN / 32), kb = j % (BN / 32);
-        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], ks == 0 ? f32x16{} : s[kb], 0, 0, 0);
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qf[ks], ks == 0 ? f32x16{} : s[kb], 0, 0, 0);
       }
-      if (i + kLead < N) ring[i % kLead] = operand(i + kLead);
+      if (i + kLead < N) ring[i % kLead] = operand(pv_c, i + kLead, vb, kb_);
     }
     // A V operand is two LDS reads, a K operand one.
     auto read_group = [&](int i) {
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       if (i < NPV) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     };
-#pragma unroll
-    for (int i = 0; i < (N < kLead ? N : kLead); ++i) read_group(i);
 #pragma unroll
     for (int i = 0; i < N; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
@@ -338,8 +355,14 @@ __device__ __forceinline__ void attend_piece(const FwdArgs& a, const FwdGroupArg
     __builtin_amdgcn_sched_barrier(0);
   };
 
-  // Softmax step on S (keys >= nvalid of this tile masked): lazy rescale of
-  // O and l, P = exp2(S c - m) packed to bf16 as the B operand of the next P V.
+  // Softmax step on S (keys >= nvalid of this tile masked): P = exp2(S c - m)
+  // packed to bf16 as the B operand of the next P V, with m the running max.
+  // Lazy rescaling without a per-tile max: P is first computed against the
+  // current m; if every lane's sum over its 32 keys stays <= 2^kRescaleLog2,
+  // so does every P and nothing else is needed.  Otherwise (the first tile,
+  // where m is -inf, or scores well above m) the tile max is taken, m is
+  // raised if the max exceeds it by more than kRescaleLog2 (O and l scaled
+  // down), and P is recomputed.  Either way P <= 2^kRescaleLog2.
   auto sstep = [&](int nvalid) {
     if (nvalid < BN) {
 #pragma unroll
@@ -350,38 +373,45 @@ __device__ __forceinline__ void attend_piece(const FwdArgs& a, const FwdGroupArg
           if (key >= nvalid) s[kb][e] = -INFINITY;
         }
     }
-    float mx = fmaxf(s[0][0], s[0][1]);
-#pragma unroll
-    for (int e = 2; e < 16; e += 2) mx = fmaxf(fmaxf(mx, s[0][e]), s[0][e + 1]);
-#pragma unroll
-    for (int kb = 1; kb < BN / 32; ++kb)
-#pragma unroll
-      for (int e = 0; e < 16; e += 2) mx = fmaxf(fmaxf(mx, s[kb][e]), s[kb][e + 1]);
-    const float mt = halfwave_max(mx) * c;
-    if (__any(mt > m_run + kRescaleLog2)) {
-      const float m_new = fmaxf(m_run, mt);
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      m_run = m_new;
-      l_part *= alpha;
-#pragma unroll
-      for (int db = 0; db < DB; ++db) o[db] *= alpha;
-    }
-    const float mneg = -m_run;
     // Row sum in fp32 VALU adds (four independent partial sums): the bf16 dot
     // instruction would wait on the matrix core that the other wave of this
     // SIMD keeps busy.
-    float ls[4] = {0.f, 0.f, 0.f, 0.f};
+    auto exps = [&]() {
+      const float mneg = -m_run;
+      float ls[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int kb = 0; kb < BN / 32; ++kb)
+      for (int kb = 0; kb < BN / 32; ++kb)
 #pragma unroll
-      for (int e = 0; e < 16; e += 2) {
-        const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][e], c, mneg));
-        const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][e + 1], c, mneg));
-        ls[(e >> 1) & 3] += p0 + p1;
-        pb[kb][e >> 3][e & 7] = static_cast<__bf16>(p0);
-        pb[kb][e >> 3][(e & 7) + 1] = static_cast<__bf16>(p1);
+        for (int e = 0; e < 16; e += 2) {
+          const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][e], c, mneg));
+          const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][e + 1], c, mneg));
+          ls[(e >> 1) & 3] += p0 + p1;
+          pb[kb][e >> 3][e & 7] = static_cast<__bf16>(p0);
+          pb[kb][e >> 3][(e & 7) + 1] = static_cast<__bf16>(p1);
+        }
+      return (ls[0] + ls[1]) + (ls[2] + ls[3]);
+    };
+    float lt = exps();
+    if (__any(!(lt <= kRescaleSum))) {  // also true for inf / NaN sums
+      float mx = fmaxf(s[0][0], s[0][1]);
+#pragma unroll
+      for (int e = 2; e < 16; e += 2) mx = fmaxf(fmaxf(mx, s[0][e]), s[0][e + 1]);
+#pragma unroll
+      for (int kb = 1; kb < BN / 32; ++kb)
+#pragma unroll
+        for (int e = 0; e < 16; e += 2) mx = fmaxf(fmaxf(mx, s[kb][e]), s[kb][e + 1]);
+      const float mt = halfwave_max(mx) * c;
+      if (__any(mt > m_run + kRescaleLog2)) {
+        const float m_new = fmaxf(m_run, mt);
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+        m_run = m_new;
+        l_part *= alpha;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) o[db] *= alpha;
       }
-    l_part += (ls[0] + ls[1]) + (ls[2] + ls[3]);
+      lt = exps();
+    }
+    l_part += lt;
     // P and the row sum are pure register values, so the compiler is free to
     // sink their exponentials past the phase barrier into the next
     // matrix-core step, which would load that step with this one's VALU work.
@@ -393,93 +423,104 @@ __device__ __forceinline__ void attend_piece(const FwdArgs& a, const FwdGroupArg
     asm volatile("" : "+v"(l_part));
   };
 
-  // Prologue: K_0 stored, V_0 and K_1 in flight.
-  Stream ks = stream_at(KSel{}, k), vs = stream_at(VSel{}, k), ss = stream_at(KSel{}, k);
-  load(ks, pk);
-  load(vs, pv);
-  store_k(0);
-  if (nt > 1) {
-    step(KSel{}, ks);
-    load(ks, pk);
-  }
+  Stream ts = stream_at(grp != 0, k);  // group 0: K tiles, group 1: V tiles
+  Stream ss = stream_at(false, k);     // tile lengths for the softmax masks
+  if (grp == 0) issue(ts, false, 0);
+  wait_vmcnt<0>();
   __syncthreads();
-
-  // Global loads and LDS stores, done by every wave at the end of its phase
-  // (the issue of the loads overlaps the wait at the barrier, and the data
-  // has the whole next phase to arrive): phase 2j ends by storing V_j and
-  // loading V_{j+1}; phase 2j + 1 ends by storing K_{j+1} and loading K_{j+2}.
-  auto even_begin = [&](int) {};
-  auto even_end = [&](int j) {
-    if (j < nt) store_v(j & 1);
-    if (j + 1 < nt) {
-      step(VSel{}, vs);
-      load(vs, pv);
+  // Transfer of tile t (if it exists) of the group's tensor into buffer
+  // t & 1 = buf: K_t for group 0, V_t for group 1.
+  auto transfer = [&](int t, int buf) {
+    if (t < nt) {
+      if (t > 0 || grp == 0) step(grp != 0, ts);
+      issue(ts, grp != 0, buf);
     }
-    __syncthreads();
-  };
-  auto odd_begin = [&](int) {};
-  auto odd_end = [&](int j) {
-    if (j + 1 < nt) store_k((j + 1) & 1);
-    if (j + 2 < nt) {
-      step(KSel{}, ks);
-      load(ks, pk);
-    }
-    __syncthreads();
-  };
-  auto soft = [&]() {
-    sstep(min(ss.left, BN));
-    step(KSel{}, ss);
   };
   using T_ = std::true_type;
   using F_ = std::false_type;
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
   // Matrix-core step with high issue priority, softmax with normal priority.
-  auto mphase = [&](auto pv_c, auto s_c, int j) {
+  auto mphase = [&](auto pv_c, auto s_c, int vb, int kb_) {
     __builtin_amdgcn_s_setprio(2);
-    mstep(pv_c, s_c, (j - 1) & 1, j & 1);
+    mstep(pv_c, s_c, vb, kb_);
     __builtin_amdgcn_s_setprio(0);
   };
+  auto soft = [&]() {
+    sstep(min(ss.left, BN));
+    step(false, ss);
+  };
+  // The tile loops are unrolled by two so that every LDS buffer index is a
+  // compile-time constant (par = j & 1) and operand addresses are immediates.
   if (grp == 0) {
-    // phase 2j: M(j); phase 2j + 1: softmax(j)
-    even_begin(0);
-    mphase(F_{}, T_{}, 0);
-    even_end(0);
-    odd_begin(0);
+    // phase 2j: K_{j+1} issued, M(j); phase 2j + 1: softmax(j), then the
+    // first operands of M(j + 1) (V_j, published at the end of phase 2j).
+    transfer(1, 1);
+    prefill(F_{}, 0, 0);
+    mphase(F_{}, T_{}, 0, 0);
+    __syncthreads();
     soft();
-    odd_end(0);
-    for (int j = 1; j < nt; ++j) {
-      even_begin(j);
-      mphase(T_{}, T_{}, j);
-      even_end(j);
-      odd_begin(j);
+    prefill(T_{}, 0, 1);
+    wait_vmcnt<0>();
+    __syncthreads();
+    auto iter = [&](int j, auto par) {
+      constexpr int p = decltype(par)::value;
+      transfer(j + 1, p ^ 1);
+      mphase(T_{}, T_{}, p ^ 1, p);
+      __syncthreads();
       soft();
-      odd_end(j);
+      prefill(T_{}, p, p ^ 1);
+      wait_vmcnt<0>();
+      __syncthreads();
+    };
+    int j = 1;
+    for (; j + 1 < nt; j += 2) {
+      iter(j, I1{});
+      iter(j + 1, I0{});
     }
-    even_begin(nt);
-    mphase(T_{}, F_{}, nt);
-    even_end(nt);
-    odd_begin(nt);
-    odd_end(nt);
+    if (j < nt) iter(j, I1{});
+    if (nt & 1)
+      mphase(T_{}, F_{}, 0, 1);
+    else
+      mphase(T_{}, F_{}, 1, 0);
+    __syncthreads();
+    __syncthreads();
   } else {
-    // phase 2j: softmax(j - 1); phase 2j + 1: M(j)
-    even_begin(0);
-    even_end(0);
-    odd_begin(0);
-    mphase(F_{}, T_{}, 0);
-    odd_end(0);
-    for (int j = 1; j < nt; ++j) {
-      even_begin(j);
+    // phase 2j: V_j issued, softmax(j - 1), wait for V_j, the first operands
+    // of M(j) (V_{j-1}); phase 2j + 1: M(j).
+    transfer(0, 0);
+    prefill(F_{}, 0, 0);
+    wait_vmcnt<0>();
+    __syncthreads();
+    mphase(F_{}, T_{}, 0, 0);
+    __syncthreads();
+    auto iter = [&](int j, auto par) {
+      constexpr int p = decltype(par)::value;
+      transfer(j, p);
       soft();
-      even_end(j);
-      odd_begin(j);
-      mphase(T_{}, T_{}, j);
-      odd_end(j);
+      prefill(T_{}, p ^ 1, p);
+      wait_vmcnt<0>();
+      __syncthreads();
+      mphase(T_{}, T_{}, p ^ 1, p);
+      __syncthreads();
+    };
+    int j = 1;
+    for (; j + 1 < nt; j += 2) {
+      iter(j, I1{});
+      iter(j + 1, I0{});
     }
-    even_begin(nt);
+    if (j < nt) iter(j, I1{});
     soft();
-    even_end(nt);
-    odd_begin(nt);
-    mphase(T_{}, F_{}, nt);
-    odd_end(nt);
+    if (nt & 1) {
+      prefill(T_{}, 0, 0);
+      __syncthreads();
+      mphase(T_{}, F_{}, 0, 1);
+    } else {
+      prefill(T_{}, 1, 0);
+      __syncthreads();
+      mphase(T_{}, F_{}, 1, 0);
+    }
+    __syncthreads();
   }
 
   const float l_tot = halfwave_sum(l_part);
@@ -522,8 +563,8 @@ template <int D>
 __global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void fwd_bf16_kernel(FwdArgs a) {
   using P = FwdTile<D>;
-  // [K buf0 | K buf1 | V buf0 | V buf1]; every offset fits a ds instruction's immediate.
-  __shared__ __attribute__((aligned(16))) __bf16 lds[2 * P::KT + 2 * P::VT];
+  // [K buf0 | K buf1 | V buf0 | V buf1 | P blocks | tile maxima | row sums]
+  __shared__ __attribute__((aligned(16))) char lds[P::LDS_BYTES];
   const int rho = range_of_block(blockIdx.x, a.n_ranges);
   const int64_t S = range_begin(a, rho), E = range_begin(a, rho + 1);
   // Whole items of the aligned rounds, then the pieces of the tail range;

@@ -49,6 +49,15 @@ __device__ inline void dma16(i32x4 rsrc, uint32_t voff, uint32_t lds_addr) {
 #pragma clang diagnostic pop
 }
 
+// As dma16, with a scalar byte offset soff added to the lane's offset.
+__device__ inline void dma16_soff(i32x4 rsrc, uint32_t voff, uint32_t soff, uint32_t lds_addr) {
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+               :: "s"(lds_addr), "v"(voff), "s"(rsrc), "s"(soff) : "memory", "m0");
+#pragma clang diagnostic pop
+}
+
 // s_waitcnt vmcnt(N) alone (gfx9 encoding: expcnt and lgkmcnt at their maxima).
 template <int N>
 __device__ inline void wait_vmcnt() {
