@@ -132,7 +132,7 @@ struct FwdTile {
   // global -> LDS transfers of 1 KB (four rows) per wave instruction.
   static constexpr int KT = BN * 128, VT = BN * 128;  // elements per LDS tile
   static constexpr int NDMA = BN * 256 / 1024 / 4;    // transfers per wave of a group, per tile
-  static constexpr int kLead = 8;                     // operands read ahead of their MFMA
+  static constexpr int kLead = 4;                     // operands read ahead of their MFMA
   static constexpr int LDS_BYTES = 2 * (2 * KT + 2 * VT);
   static_assert(NDMA == 4, "transfer addressing assumes 16 rows per wave");
 };
@@ -601,12 +601,14 @@ void fwd_bf16_kernel(FwdArgs a) {
   }
 }
 
-// Merge the pieces of items split across ranges: block b looks at the
+// Merge the pieces of items split across ranges: block (b, y) looks at the
 // boundary between ranges b and b + 1 and, if it is the first boundary inside
-// an item, combines all of that item's pieces in range order.
+// an item, combines queries [y QS, (y + 1) QS) of all of that item's pieces
+// in range order (the loads of the next piece are issued before the current
+// one is merged).
 template <int D>
-__global__ __launch_bounds__(kFwdThreads) void combine_kernel(FwdArgs a) {
-  constexpr int BM = kFwdBM;
+__global__ __launch_bounds__(kCombineThreads) void combine_kernel(FwdArgs a) {
+  constexpr int BM = kFwdBM, QS = BM / kCombineSplit;
   const int b = blockIdx.x + 1;
   const int64_t Sb = range_begin(a, b);
   if (Sb >= a.total_tiles) return;
@@ -621,45 +623,64 @@ __global__ __launch_bounds__(kFwdThreads) void combine_kernel(FwdArgs a) {
   const int head = L.item / G.n_qtiles;
   const int qtile = L.item - head * G.n_qtiles;
   const int64_t rec_len = partial_record_floats(D);
+  const int q0 = blockIdx.y * QS;
+  // Record of the piece in range j, or null for an empty range.
+  auto piece = [&](int j) -> const float* {
+    const int64_t rj = range_begin(a, j);
+    if (rj == range_begin(a, j + 1)) return nullptr;
+    return a.partial + (T <= rj ? 2 * j : 2 * j + 1) * rec_len;
+  };
   // Each thread owns NE float4 outputs; pieces are merged in range order
   // with a running max, like the online softmax itself.
-  constexpr int NE = BM * D / 4 / kFwdThreads;
-  f32x4 acc[NE];
-  float m[NE], l[NE];
+  constexpr int NE = QS * D / 4 / kCombineThreads;
+  f32x4 acc[NE], ov[NE];
+  float m[NE], l[NE], mv[NE], lv[NE];
+  auto fetch = [&](const float* ro) {
+#pragma unroll
+    for (int it = 0; it < NE; ++it) {
+      const int e = threadIdx.x + it * kCombineThreads;
+      const int ql = q0 + e / (D / 4), d4 = e % (D / 4);
+      ov[it] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(ro + ql * D + 4 * d4));
+      mv[it] = ro[BM * D + ql];
+      lv[it] = ro[BM * D + BM + ql];
+    }
+  };
 #pragma unroll
   for (int it = 0; it < NE; ++it) {
     acc[it] = f32x4{};
     m[it] = -INFINITY;
     l[it] = 0.f;
   }
-  for (int j = b - 1; j <= j_end; ++j) {
-    const int64_t rj = range_begin(a, j);
-    if (rj == range_begin(a, j + 1)) continue;  // empty range: no piece
-    const float* ro = a.partial + (T <= rj ? 2 * j : 2 * j + 1) * rec_len;
-    // issue every load of this piece before using any of them
-    f32x4 ov[NE];
-    float mv[NE], lv[NE];
+  int j = b - 1;  // range b - 1 holds the item's first tile: never empty
+  fetch(piece(j));
+  while (true) {
+    const f32x4* cur_o = ov;
+    f32x4 co[NE];
+    float cm[NE], cl[NE];
 #pragma unroll
     for (int it = 0; it < NE; ++it) {
-      const int e = threadIdx.x + it * kFwdThreads;
-      const int ql = e / (D / 4), d4 = e % (D / 4);
-      ov[it] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(ro + ql * D + 4 * d4));
-      mv[it] = ro[BM * D + ql];
-      lv[it] = ro[BM * D + BM + ql];
+      co[it] = cur_o[it];
+      cm[it] = mv[it];
+      cl[it] = lv[it];
     }
+    const float* rn = nullptr;
+    while (++j <= j_end && !(rn = piece(j))) {
+    }
+    if (rn) fetch(rn);
 #pragma unroll
     for (int it = 0; it < NE; ++it) {
-      const float mn = fmaxf(m[it], mv[it]);
-      const float so = __builtin_amdgcn_exp2f(m[it] - mn), sj = __builtin_amdgcn_exp2f(mv[it] - mn);
-      acc[it] = acc[it] * so + sj * ov[it];
-      l[it] = l[it] * so + sj * lv[it];
+      const float mn = fmaxf(m[it], cm[it]);
+      const float so = __builtin_amdgcn_exp2f(m[it] - mn), sj = __builtin_amdgcn_exp2f(cm[it] - mn);
+      acc[it] = acc[it] * so + sj * co[it];
+      l[it] = l[it] * so + sj * cl[it];
       m[it] = mn;
     }
+    if (!rn) break;
   }
 #pragma unroll
   for (int it = 0; it < NE; ++it) {
-    const int e = threadIdx.x + it * kFwdThreads;
-    const int ql = e / (D / 4), d4 = e % (D / 4);
+    const int e = threadIdx.x + it * kCombineThreads;
+    const int ql = q0 + e / (D / 4), d4 = e % (D / 4);
     const int q_row = G.q_begin + qtile * BM + ql;
     if (q_row >= G.q_end) continue;
     const float inv = 1.0f / l[it];
@@ -730,9 +751,9 @@ hipError_t launch_forward(const FwdArgs& a, int head_dim, bool bf16, hipStream_t
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || a.n_ranges < 2) return e;
     if (head_dim == 128)
-      hipLaunchKernelGGL(combine_kernel<128>, dim3(a.n_ranges - 1), dim3(kFwdThreads), 0, stream, a);
+      hipLaunchKernelGGL(combine_kernel<128>, dim3(a.n_ranges - 1, kCombineSplit), dim3(kCombineThreads), 0, stream, a);
     else
-      hipLaunchKernelGGL(combine_kernel<64>, dim3(a.n_ranges - 1), dim3(kFwdThreads), 0, stream, a);
+      hipLaunchKernelGGL(combine_kernel<64>, dim3(a.n_ranges - 1, kCombineSplit), dim3(kCombineThreads), 0, stream, a);
     return hipGetLastError();
   }
   if (a.n_blocks <= 0) return hipSuccess;

@@ -15,6 +15,9 @@ constexpr int kMaxPoolJobs = 16;   // pool jobs per launch
 constexpr int kFwdBM = 256;
 constexpr int kFwdBN = 64;
 constexpr int kFwdThreads = 512;
+// Merge of split items: blocks per item (each a quarter of its queries) and threads.
+constexpr int kCombineSplit = 4;
+constexpr int kCombineThreads = 256;
 // fp32 attention kernel: one query per lane, one wave per block.
 constexpr int kFwdF32BM = 64;
 
