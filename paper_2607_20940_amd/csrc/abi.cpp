@@ -227,6 +227,7 @@ mssa_status forward_impl(const mssa::Plan& p, const void* q_win, const void* k_s
   a.dp_rounds = p.dp_rounds;
   const char* ws = static_cast<const char*>(workspace);
   a.partial = p.partial_bytes > 0 ? reinterpret_cast<float*>(const_cast<char*>(ws) + p.partial_off) : nullptr;
+  a.range_table = p.partial_bytes > 0 ? reinterpret_cast<int64_t*>(const_cast<char*>(ws) + p.range_table_off) : nullptr;
   int64_t blocks = 0;
   int gi = 0;
   for (int g : p.order) {

@@ -567,6 +567,11 @@ void fwd_bf16_kernel(FwdArgs a) {
   __shared__ __attribute__((aligned(16))) char lds[P::LDS_BYTES];
   const int rho = range_of_block(blockIdx.x, a.n_ranges);
   const int64_t S = range_begin(a, rho), E = range_begin(a, rho + 1);
+  // The merge of split items reads the tail ranges from this table.
+  if (a.range_table && threadIdx.x == 0) {
+    a.range_table[rho] = S;
+    if (rho == a.n_ranges - 1) a.range_table[rho + 1] = E;
+  }
   // Whole items of the aligned rounds, then the pieces of the tail range;
   // one call site keeps a single copy of the attention loop.
   int round = 0;
@@ -601,97 +606,76 @@ void fwd_bf16_kernel(FwdArgs a) {
   }
 }
 
-// Merge the pieces of items split across ranges: block (b, y) looks at the
-// boundary between ranges b and b + 1 and, if it is the first boundary inside
-// an item, combines queries [y QS, (y + 1) QS) of all of that item's pieces
-// in range order (the loads of the next piece are issued before the current
-// one is merged).
+// Merge the pieces of items split across ranges.  Block (j, y) looks at tail
+// range j: if the range ends inside an item whose first tile it holds, it
+// combines queries [y QS, (y + 1) QS) of all of that item's pieces (ranges
+// j .. j1) in range order.  Range bounds come from the table the attention
+// kernel wrote.  Each thread owns one float4 of the output and loads it from
+// up to kMaxMerge pieces at once (an item of the tail may be cut into many
+// short pieces), then merges them in order.
 template <int D>
 __global__ __launch_bounds__(kCombineThreads) void combine_kernel(FwdArgs a) {
-  constexpr int BM = kFwdBM, QS = BM / kCombineSplit;
-  const int b = blockIdx.x + 1;
-  const int64_t Sb = range_begin(a, b);
-  if (Sb >= a.total_tiles) return;
-  const Loc L = locate(a, Sb);
-  if (L.k == 0) return;
+  constexpr int BM = kFwdBM, QS = kCombineThreads * 4 / D, kMaxMerge = 8;
+  const int64_t* tab = a.range_table;
+  const int j = blockIdx.x;
+  const int64_t S = tab[j], E = tab[j + 1];
+  if (S == E || E >= a.total_tiles) return;  // empty range, or nothing after it
+  const Loc L = locate(a, E);
+  if (L.k == 0) return;                      // the range ends at an item boundary
   const int64_t T = L.item_begin;
-  if (range_begin(a, b - 1) > T) return;
+  if (S > T) return;                         // the item's first piece is in an earlier range
   const FwdGroupArgs& G = a.groups[L.g];
   const int64_t Tend = T + G.tiles_per_item;
-  int j_end = b;
-  while (j_end + 1 < a.n_ranges && range_begin(a, j_end + 1) < Tend) ++j_end;
+  // Last range holding a piece of the item: the table is nondecreasing.
+  int j1 = j;
+  for (int w = j + 1; w < a.n_ranges; w += kCombineThreads) {
+    const int jt = w + static_cast<int>(threadIdx.x);
+    const int cnt = __syncthreads_count(jt < a.n_ranges && tab[jt] < Tend);
+    j1 += cnt;
+    if (cnt < kCombineThreads) break;
+  }
   const int head = L.item / G.n_qtiles;
   const int qtile = L.item - head * G.n_qtiles;
   const int64_t rec_len = partial_record_floats(D);
-  const int q0 = blockIdx.y * QS;
-  // Record of the piece in range j, or null for an empty range.
-  auto piece = [&](int j) -> const float* {
-    const int64_t rj = range_begin(a, j);
-    if (rj == range_begin(a, j + 1)) return nullptr;
-    return a.partial + (T <= rj ? 2 * j : 2 * j + 1) * rec_len;
-  };
-  // Each thread owns NE float4 outputs; pieces are merged in range order
-  // with a running max, like the online softmax itself.
-  constexpr int NE = QS * D / 4 / kCombineThreads;
-  f32x4 acc[NE], ov[NE];
-  float m[NE], l[NE], mv[NE], lv[NE];
-  auto fetch = [&](const float* ro) {
+  const int ql = blockIdx.y * QS + static_cast<int>(threadIdx.x) / (D / 4), d4 = threadIdx.x % (D / 4);
+  // Pieces are merged in range order with a running max, like the online
+  // softmax itself.
+  f32x4 acc = f32x4{};
+  float m = -INFINITY, l = 0.f;
+  for (int base = j; base <= j1; base += kMaxMerge) {
+    f32x4 ov[kMaxMerge];
+    float mv[kMaxMerge], lv[kMaxMerge];
+    bool have[kMaxMerge];
 #pragma unroll
-    for (int it = 0; it < NE; ++it) {
-      const int e = threadIdx.x + it * kCombineThreads;
-      const int ql = q0 + e / (D / 4), d4 = e % (D / 4);
-      ov[it] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(ro + ql * D + 4 * d4));
-      mv[it] = ro[BM * D + ql];
-      lv[it] = ro[BM * D + BM + ql];
+    for (int i = 0; i < kMaxMerge; ++i) {
+      const int jj = base + i;
+      have[i] = jj <= j1 && tab[jj] < tab[jj + 1];  // ranges inside the span may be empty
+      if (have[i]) {
+        const float* ro = a.partial + (jj > j || S == T ? 2 * jj : 2 * jj + 1) * rec_len;
+        ov[i] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(ro + ql * D + 4 * d4));
+        mv[i] = ro[BM * D + ql];
+        lv[i] = ro[BM * D + BM + ql];
+      }
     }
-  };
 #pragma unroll
-  for (int it = 0; it < NE; ++it) {
-    acc[it] = f32x4{};
-    m[it] = -INFINITY;
-    l[it] = 0.f;
+    for (int i = 0; i < kMaxMerge; ++i) {
+      if (!have[i]) continue;
+      const float mn = fmaxf(m, mv[i]);
+      const float so = __builtin_amdgcn_exp2f(m - mn), sj = __builtin_amdgcn_exp2f(mv[i] - mn);
+      acc = acc * so + sj * ov[i];
+      l = l * so + sj * lv[i];
+      m = mn;
+    }
   }
-  int j = b - 1;  // range b - 1 holds the item's first tile: never empty
-  fetch(piece(j));
-  while (true) {
-    const f32x4* cur_o = ov;
-    f32x4 co[NE];
-    float cm[NE], cl[NE];
+  const int q_row = G.q_begin + qtile * BM + ql;
+  if (q_row >= G.q_end) return;
+  const float inv = 1.0f / l;
+  if (a.lse && d4 == 0) a.lse[static_cast<int64_t>(head) * a.n_q + q_row] = (m + log2f(l)) * kLn2;
+  bf16x4 v;
 #pragma unroll
-    for (int it = 0; it < NE; ++it) {
-      co[it] = cur_o[it];
-      cm[it] = mv[it];
-      cl[it] = lv[it];
-    }
-    const float* rn = nullptr;
-    while (++j <= j_end && !(rn = piece(j))) {
-    }
-    if (rn) fetch(rn);
-#pragma unroll
-    for (int it = 0; it < NE; ++it) {
-      const float mn = fmaxf(m[it], cm[it]);
-      const float so = __builtin_amdgcn_exp2f(m[it] - mn), sj = __builtin_amdgcn_exp2f(cm[it] - mn);
-      acc[it] = acc[it] * so + sj * co[it];
-      l[it] = l[it] * so + sj * cl[it];
-      m[it] = mn;
-    }
-    if (!rn) break;
-  }
-#pragma unroll
-  for (int it = 0; it < NE; ++it) {
-    const int e = threadIdx.x + it * kCombineThreads;
-    const int ql = q0 + e / (D / 4), d4 = e % (D / 4);
-    const int q_row = G.q_begin + qtile * BM + ql;
-    if (q_row >= G.q_end) continue;
-    const float inv = 1.0f / l[it];
-    if (a.lse && d4 == 0)
-      a.lse[static_cast<int64_t>(head) * a.n_q + q_row] = (m[it] + log2f(l[it])) * kLn2;
-    bf16x4 v;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) v[i] = static_cast<__bf16>(acc[it][i] * inv);
-    *reinterpret_cast<bf16x4*>(static_cast<__bf16*>(a.out) + static_cast<int64_t>(q_row) * a.ld +
-                               static_cast<int64_t>(head) * D + 4 * d4) = v;
-  }
+  for (int i = 0; i < 4; ++i) v[i] = static_cast<__bf16>(acc[i] * inv);
+  *reinterpret_cast<bf16x4*>(static_cast<__bf16*>(a.out) + static_cast<int64_t>(q_row) * a.ld +
+                             static_cast<int64_t>(head) * D + 4 * d4) = v;
 }
 
 template <int D>
@@ -751,9 +735,9 @@ hipError_t launch_forward(const FwdArgs& a, int head_dim, bool bf16, hipStream_t
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || a.n_ranges < 2) return e;
     if (head_dim == 128)
-      hipLaunchKernelGGL(combine_kernel<128>, dim3(a.n_ranges - 1, kCombineSplit), dim3(kCombineThreads), 0, stream, a);
+      hipLaunchKernelGGL(combine_kernel<128>, dim3(a.n_ranges - 1, kFwdBM * 128 / 4 / kCombineThreads), dim3(kCombineThreads), 0, stream, a);
     else
-      hipLaunchKernelGGL(combine_kernel<64>, dim3(a.n_ranges - 1, kCombineSplit), dim3(kCombineThreads), 0, stream, a);
+      hipLaunchKernelGGL(combine_kernel<64>, dim3(a.n_ranges - 1, kFwdBM * 64 / 4 / kCombineThreads), dim3(kCombineThreads), 0, stream, a);
     return hipGetLastError();
   }
   if (a.n_blocks <= 0) return hipSuccess;

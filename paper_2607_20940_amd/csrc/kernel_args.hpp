@@ -15,8 +15,7 @@ constexpr int kMaxPoolJobs = 16;   // pool jobs per launch
 constexpr int kFwdBM = 256;
 constexpr int kFwdBN = 64;
 constexpr int kFwdThreads = 512;
-// Merge of split items: blocks per item (each a quarter of its queries) and threads.
-constexpr int kCombineSplit = 4;
+// Merge of split items: threads per block (one output float4 each).
 constexpr int kCombineThreads = 256;
 // fp32 attention kernel: one query per lane, one wave per block.
 constexpr int kFwdF32BM = 64;
@@ -55,6 +54,7 @@ struct FwdArgs {
   int32_t dp_rounds;        // bf16 kernel: rounds of whole items before the tail ranges
   int32_t pad2;
   float* partial;           // bf16 kernel: 2 * n_ranges partial records
+  int64_t* range_table;     // bf16 kernel: first tile of each tail range (n_ranges + 1), written by the attention kernel
   float* lse;               // optional [heads, n_q]: log of the softmax denominator (natural log)
   int32_t n_q;
   int32_t pad3;

@@ -256,9 +256,12 @@ mssa_status build_plan(const mssa_plan_desc& d, int slots, int ranges_override, 
   }
   p.partial_off = 0;
   p.partial_bytes = 0;
+  p.range_table_off = 0;
   if (d.dtype == MSSA_BF16 && p.n_ranges > 1) {
+    const int64_t rec_bytes = align256(2 * static_cast<int64_t>(p.n_ranges) * partial_record_floats(d.head_dim) * 4);
     p.partial_off = ws;
-    p.partial_bytes = align256(2 * static_cast<int64_t>(p.n_ranges) * partial_record_floats(d.head_dim) * 4);
+    p.range_table_off = ws + rec_bytes;
+    p.partial_bytes = rec_bytes + align256((static_cast<int64_t>(p.n_ranges) + 1) * 8);
     ws += p.partial_bytes;
   }
   p.workspace_bytes = ws;

@@ -97,7 +97,8 @@ struct Plan {
   int32_t n_ranges;
   int32_t dp_rounds;    // rounds of whole items (one per block) before the tail
   int64_t tail_begin;   // first tile of the tail ranges
-  int64_t partial_off, partial_bytes;    // partial records in the workspace
+  int64_t partial_off, partial_bytes;    // partial records and the range table in the workspace
+  int64_t range_table_off;               // n_ranges + 1 int64 first tiles of the tail ranges
   // Backward workspace: the forward's, then rowsum(dO * O) [heads, n_q]
   // fp32, then per group the fp32 context gradients of K and V.
   int64_t bwd_dsum_off;
