@@ -57,6 +57,33 @@ mssa_status check_device(hipError_t e, const char* what) {
 // Launch pool jobs (source and destination pointers filled in), at most
 // kMaxPoolJobs per launch.
 mssa_status launch_pool_jobs(const mssa::Plan& p, std::vector<mssa::PoolJobArgs>& jobs, void* stream) {
+  // Jobs that pool the same source frames by 2 and by 4 (block mean) become
+  // one two-level job, so those frames are read once for both scales.
+  for (mssa::PoolJobArgs& A : jobs) A.levels = 1;
+  if (!p.strided) {
+    std::vector<bool> gone(jobs.size(), false);
+    for (size_t i = 0; i < jobs.size(); ++i) {
+      mssa::PoolJobArgs& A = jobs[i];
+      if (gone[i] || A.factor != 2) continue;
+      for (size_t k = 0; k < jobs.size(); ++k) {
+        const mssa::PoolJobArgs& B = jobs[k];
+        if (k == i || gone[k] || B.factor != 4 || B.src_k != A.src_k || B.src_v != A.src_v ||
+            B.src_gh != A.src_gh || B.src_gw != A.src_gw || B.n_frames != A.n_frames)
+          continue;
+        A.levels = 2;
+        A.dst2_k = B.dst_k;
+        A.dst2_v = B.dst_v;
+        A.dst2_gh = B.dst_gh;
+        A.dst2_gw = B.dst_gw;
+        gone[k] = true;
+        break;
+      }
+    }
+    size_t w = 0;
+    for (size_t i = 0; i < jobs.size(); ++i)
+      if (!gone[i]) jobs[w++] = jobs[i];
+    jobs.resize(w);
+  }
   mssa::PoolArgs a{};
   a.ld = p.ld;
   a.chunks_per_tok = static_cast<int32_t>(p.ld * p.elem_bytes / 16);
@@ -69,7 +96,9 @@ mssa_status launch_pool_jobs(const mssa::Plan& p, std::vector<mssa::PoolJobArgs>
       mssa::PoolJobArgs& A = a.jobs[i];
       A = jobs[j0 + i];
       A.block_begin = static_cast<int32_t>(blocks);
-      const int64_t work = static_cast<int64_t>(A.n_frames) * A.dst_gh * A.dst_gw * a.chunks_per_tok;
+      const int64_t cells = A.levels == 2 ? static_cast<int64_t>(A.dst2_gh) * A.dst2_gw
+                                          : static_cast<int64_t>(A.dst_gh) * A.dst_gw;
+      const int64_t work = static_cast<int64_t>(A.n_frames) * cells * a.chunks_per_tok;
       blocks += (work + mssa::kPoolThreads - 1) / mssa::kPoolThreads;
     }
     if (blocks > 0x7fffffff) return fail(MSSA_ERR_UNSUPPORTED, "pool grid too large");

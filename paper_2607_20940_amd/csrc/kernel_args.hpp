@@ -178,14 +178,17 @@ struct GemmArgs {
 struct PoolJobArgs {
   const void* src_k;        // first source token of the job (head 0, ch 0)
   const void* src_v;
-  void* dst_k;              // first destination token of the job
+  void* dst_k;              // first destination token of the job (pooled by factor)
   void* dst_v;
+  void* dst2_k;             // levels == 2: first destination token pooled by 2 * factor
+  void* dst2_v;
   int32_t src_gh, src_gw;
   int32_t dst_gh, dst_gw;
+  int32_t dst2_gh, dst2_gw;
   int32_t factor;
+  int32_t levels;           // 1, or 2: the same source frames pooled by factor and by 2 * factor
   int32_t n_frames;
   int32_t block_begin;
-  int32_t pad;
 };
 
 struct PoolArgs {
