@@ -162,9 +162,10 @@ __device__ inline float halfwave_sum(float v) { return v + other_half(v); }
 // softmax step on S_{j-1}, and in phase 2j + 1 the roles swap.  Each SIMD
 // thus has one wave issuing MFMAs while the other issues VALU work.
 //
-// Tile traffic is by direct transfers: at the start of phase 2j group 0
-// issues K_{j+1} (waited for at the end of phase 2j + 1) and group 1 issues
-// V_j (waited for at the end of phase 2j, its softmax phase).  The first
+// Tile traffic is by direct transfers, issued by the group in its softmax
+// phase so that the matrix-core phases hold no transfer instructions: at the
+// start of phase 2j group 1 issues V_j and at the start of phase 2j + 1 group
+// 0 issues K_{j+1}, each waited for at the end of the same phase.  The first
 // kLead operands of a matrix-core step (V^T of the previous tile) are read
 // from LDS at the end of the wave's softmax phase, before the barrier, so
 // the step starts with its operands in registers.  K_{j+1} goes to the
@@ -453,21 +454,21 @@ __device__ __forceinline__ void attend_piece(const FwdArgs& a, const FwdGroupArg
   // The tile loops are unrolled by two so that every LDS buffer index is a
   // compile-time constant (par = j & 1) and operand addresses are immediates.
   if (grp == 0) {
-    // phase 2j: K_{j+1} issued, M(j); phase 2j + 1: softmax(j), then the
+    // phase 2j: M(j); phase 2j + 1: K_{j+1} issued, softmax(j), then the
     // first operands of M(j + 1) (V_j, published at the end of phase 2j).
-    transfer(1, 1);
     prefill(F_{}, 0, 0);
     mphase(F_{}, T_{}, 0, 0);
     __syncthreads();
+    transfer(1, 1);
     soft();
     prefill(T_{}, 0, 1);
     wait_vmcnt<0>();
     __syncthreads();
     auto iter = [&](int j, auto par) {
       constexpr int p = decltype(par)::value;
-      transfer(j + 1, p ^ 1);
       mphase(T_{}, T_{}, p ^ 1, p);
       __syncthreads();
+      transfer(j + 1, p ^ 1);
       soft();
       prefill(T_{}, p, p ^ 1);
       wait_vmcnt<0>();
