@@ -338,16 +338,30 @@ __global__ __launch_bounds__(kBwdThreads) void dq_kernel(BwdArgs a) {
 
 // ------------------------------------------------------------------ bf16: dK, dV
 
+// dK/dV: a block owns 128 context keys, four pairs of waves of 32 keys each.
+// In a pair, wave A (waves 0-3) computes S = Q K^T, P = exp2(S c - lse) and
+// dV^T += dO^T P, and hands P (bf16) to its partner through LDS; wave B
+// (waves 4-7, on the same SIMD as its partner) computes dP = dO V^T,
+// dS = P (dP - rowsum) and dK^T += Q^T dS one query stage later.  Each wave
+// keeps one fragment (K or V) and one accumulator (dV or dK), so two waves
+// fit on a SIMD and each has MFMA and VALU work for the hardware to
+// interleave.  Queries stream in 64-query stages (Q, dO and the row
+// statistics) through three LDS buffers: in iteration i the A waves use stage
+// i, the B waves stage i - 1, and the transfers fill stage i + 1; P of stage
+// i goes to exchange buffer i & 1.  One barrier per iteration.
 template <int D>
-__global__ __launch_bounds__(kBwdThreads) void dkdv_kernel(BwdArgs a) {
+__global__ __launch_bounds__(kBwdKVThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void dkdv_kernel(BwdArgs a) {
   using L = Lay<D>;
   constexpr int KS = L::KS, DB = L::DB;
-  constexpr int BQ = kBwdQS, RS = 128;                // queries per stage, LDS row stride (elements)
-  constexpr int QT = BQ * RS * 2;                       // bytes of one swizzled tile
+  constexpr int BQ = kBwdQS, NQB = BQ / 32;             // queries per stage, 32-query blocks
+  constexpr int QT = BQ * 128 * 2;                      // bytes of one swizzled tile (256-byte rows)
   constexpr int STB = 2 * QT + 8 * BQ;                  // Q | dO | lse2 | rowsum (fp32)
-  constexpr int NDMA = QT / 1024 / (kBwdThreads / 64);  // 1 KB transfers per wave, tile and tensor
-  static_assert(NDMA * 1024 * (kBwdThreads / 64) == QT && BQ % 32 == 0 && BQ <= 128, "stage shape");
-  __shared__ __attribute__((aligned(16))) char lds[2 * STB];
+  constexpr int NW = kBwdKVThreads / 64;
+  constexpr int NDMA = 2 * QT / 1024 / NW;              // 1 KB transfers per wave and stage (Q and dO)
+  constexpr int PXB = NQB * 2 * 64 * 16;                // bytes of one pair's P block per stage
+  static_assert(NDMA * 1024 * NW == 2 * QT && BQ % 32 == 0, "stage shape");
+  __shared__ __attribute__((aligned(16))) char lds[3 * STB + 2 * 4 * PXB];
 
   int n_blocks = 0;
   for (int g = 0; g < a.n_groups; ++g) n_blocks += a.groups[g].n_kblocks * a.num_heads;
@@ -360,48 +374,46 @@ __global__ __launch_bounds__(kBwdThreads) void dkdv_kernel(BwdArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int pair = wave & 3, role = wave >> 2;  // role 0: S, P, dV; role 1: dP, dS, dK
   const int n = lane & 31, hh = lane >> 5;
-  const int key = kt * kBwdK + wave * 32 + n;
+  const int key = kt * kBwdK + pair * 32 + n;
   const bool k_ok = key < G.n_kv;
   const int64_t ld = a.ld, hoff = static_cast<int64_t>(head) * D;
   const float c = a.scale_log2e;
 
-  // B operands: this lane's key, 8 channels of its half-wave per k step.
-  bf16x8 kf[KS], vf[KS];
+  // B operand of the wave's first product: this lane's key (K for role 0,
+  // V for role 1), 8 channels of its half-wave per k step.
+  bf16x8 xf[KS];
   {
-    const __bf16* kp = ctx_row<__bf16>(G, key, false, ld);
-    const __bf16* vp = ctx_row<__bf16>(G, key, true, ld);
+    const __bf16* xp = ctx_row<__bf16>(G, key, role != 0, ld);
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      kf[ks] = kp ? *reinterpret_cast<const bf16x8*>(kp + hoff + hh * 8 + ks * 16) : bf16x8{};
-      vf[ks] = vp ? *reinterpret_cast<const bf16x8*>(vp + hoff + hh * 8 + ks * 16) : bf16x8{};
-    }
+    for (int ks = 0; ks < KS; ++ks)
+      xf[ks] = xp ? *reinterpret_cast<const bf16x8*>(xp + hoff + hh * 8 + ks * 16) : bf16x8{};
   }
-  f32x16 dk[DB], dv[DB];
+  f32x16 acc[DB];  // dV^T (role 0) or dK^T (role 1)
 #pragma unroll
-  for (int db = 0; db < DB; ++db) {
-    dk[db] = f32x16{};
-    dv[db] = f32x16{};
-  }
+  for (int db = 0; db < DB; ++db) acc[db] = f32x16{};
 
   // Per-lane global offsets of this wave's transfers (the same every stage):
-  // LDS byte p = tile + 1024 (wave NDMA + i) + 16 lane holds row p / 256,
-  // physical chunk (p / 16) % 16, i.e. logical chunk phys ^ f(row); chunks
-  // past the head's D channels point past the buffer (zero fill).
+  // transfer t = wave NDMA + i covers bytes 1024 (t % (QT / 1024)) of the Q
+  // tile (t < QT / 1024) or of the dO tile; LDS byte p of a tile holds row
+  // p / 256, physical chunk (p / 16) % 16, i.e. logical chunk phys ^ f(row);
+  // chunks past the head's D channels point past the buffer (zero fill).
   const uint32_t row_bytes = static_cast<uint32_t>(ld) * 2;
   uint32_t voff[NDMA];
 #pragma unroll
   for (int i = 0; i < NDMA; ++i) {
-    const int p = (wave * NDMA + i) * 1024 + 16 * lane;
+    const int t = wave * NDMA + i;
+    const int p = (t % (QT / 1024)) * 1024 + 16 * lane;
     const int row = p >> 8, phys = (p >> 4) & 15;
     const int lc = unswz256(row, phys);
     voff[i] = lc < D / 8 ? row * row_bytes + lc * 16 : kPastEnd;
   }
   const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds));
   // Stage queries [q0, q0 + BQ) into LDS buffer buf: Q and dO tiles by
-  // direct transfers (NDMA each per wave); lse (in log2 units, +inf past the
-  // end) and rowsum (0 past the end) through a register of threads 0..2BQ-1,
-  // stored by store_stats once the stage has arrived.
+  // direct transfers; lse (in log2 units, +inf past the end) and rowsum (0
+  // past the end) through a register of threads 0..2BQ-1, stored by
+  // store_stats once the stage has arrived.
   float pstat = 0.f;
   auto issue = [&](int q0, int buf) {
     const int nv = min(BQ, G.q_end - q0);
@@ -412,9 +424,9 @@ __global__ __launch_bounds__(kBwdThreads) void dkdv_kernel(BwdArgs a) {
     const uint32_t base = lds0 + buf * STB;
 #pragma unroll
     for (int i = 0; i < NDMA; ++i) {
-      const uint32_t dst = __builtin_amdgcn_readfirstlane(base + (wave * NDMA + i) * 1024);
-      dma16(rq, voff[i], dst);
-      dma16(rg, voff[i], dst + QT);
+      const int t = wave * NDMA + i;
+      const uint32_t dst = __builtin_amdgcn_readfirstlane(base + t * 1024);
+      dma16(t < QT / 1024 ? rq : rg, voff[i], dst);
     }
     if (tid < 2 * BQ) {
       const int q = q0 + (tid % BQ);
@@ -428,35 +440,55 @@ __global__ __launch_bounds__(kBwdThreads) void dkdv_kernel(BwdArgs a) {
   };
   const int t_lane = 4 * (lane >> 5) + ((lane & 15) >> 2);  // row of this lane's transposing read
   const int t_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  // P exchange block of this pair, buffer pb: [32-query block][16-query half][lane] x 16 bytes
+  auto px = [&](int pbuf) { return reinterpret_cast<bf16x8*>(lds + 3 * STB + (pbuf * 4 + pair) * PXB) + lane; };
 
-  auto compute = [&](int buf) {
+  // One stage of the wave's role on stage buffer buf.  Element e of a 32x32
+  // accumulator in this layout holds query qb*32 + 8(e/4) + 4hh + e%4 of the
+  // lane's key; packed to bf16 in pairs of 8 it is the B operand (16 queries
+  // each) of the accumulating products.
+  auto stage = [&](int buf, int pbuf) {
     const __bf16* Qs = reinterpret_cast<const __bf16*>(lds + buf * STB);
     const __bf16* Gs = reinterpret_cast<const __bf16*>(lds + buf * STB + QT);
     const float* lse_s = reinterpret_cast<const float*>(lds + buf * STB + 2 * QT);
     const float* rsum_s = lse_s + BQ;
+    // role 0 multiplies Q rows with K and dO^T with P; role 1 dO rows with V
+    // and Q^T with dS
+    const __bf16* Xs = role == 0 ? Qs : Gs;
+    const __bf16* Ys = role == 0 ? Gs : Qs;
+    bf16x8* pex = px(pbuf);
 #pragma unroll
-    for (int qb = 0; qb < BQ / 32; ++qb) {
-      f32x16 s, dp;
+    for (int qb = 0; qb < NQB; ++qb) {
+      f32x16 s;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        const int o = swz(qb * 32 + n, hh * 8 + ks * 16);
-        const bf16x8 aq = *reinterpret_cast<const bf16x8*>(Qs + o);
-        const bf16x8 ag = *reinterpret_cast<const bf16x8*>(Gs + o);
-        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(aq, kf[ks], ks == 0 ? f32x16{} : s, 0, 0, 0);
-        dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ag, vf[ks], ks == 0 ? f32x16{} : dp, 0, 0, 0);
+        const bf16x8 ax = *reinterpret_cast<const bf16x8*>(Xs + swz(qb * 32 + n, hh * 8 + ks * 16));
+        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ax, xf[ks], ks == 0 ? f32x16{} : s, 0, 0, 0);
       }
-      // element e holds query qb*32 + 8(e/4) + 4hh + e%4 of this lane's key
-      bf16x8 pb[2], dsb[2];
+      bf16x8 wb[2];  // P (role 0) or dS (role 1)
+      if (role == 0) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const f32x4 l4 = *reinterpret_cast<const f32x4*>(lse_s + qb * 32 + 8 * j + 4 * hh);
-        const f32x4 r4 = *reinterpret_cast<const f32x4*>(rsum_s + qb * 32 + 8 * j + 4 * hh);
+        for (int j = 0; j < 4; ++j) {
+          const f32x4 l4 = *reinterpret_cast<const f32x4*>(lse_s + qb * 32 + 8 * j + 4 * hh);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int e = 4 * j + i;
-          const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e], c, -l4[i]));
-          pb[e >> 3][e & 7] = static_cast<__bf16>(p);
-          dsb[e >> 3][e & 7] = static_cast<__bf16>(p * (dp[e] - r4[i]));
+          for (int i = 0; i < 4; ++i) {
+            const int e = 4 * j + i;
+            wb[e >> 3][e & 7] = static_cast<__bf16>(__builtin_amdgcn_exp2f(__builtin_fmaf(s[e], c, -l4[i])));
+          }
+        }
+        pex[(qb * 2) * 64] = wb[0];
+        pex[(qb * 2 + 1) * 64] = wb[1];
+      } else {
+        const bf16x8 p0 = pex[(qb * 2) * 64], p1 = pex[(qb * 2 + 1) * 64];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const f32x4 r4 = *reinterpret_cast<const f32x4*>(rsum_s + qb * 32 + 8 * j + 4 * hh);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int e = 4 * j + i;
+            const float p = static_cast<float>((e < 8 ? p0 : p1)[e & 7]);
+            wb[e >> 3][e & 7] = static_cast<__bf16>(p * (s[e] - r4[i]));
+          }
         }
       }
 #pragma unroll
@@ -464,14 +496,10 @@ __global__ __launch_bounds__(kBwdThreads) void dkdv_kernel(BwdArgs a) {
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
           const int r0 = qb * 32 + cc * 16 + t_lane, c0 = db * 32 + t_col;
-          const bf16x4 glo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(Gs + swz(r0, c0)));
-          const bf16x4 ghi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(Gs + swz(r0 + 8, c0)));
-          const bf16x4 qlo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(Qs + swz(r0, c0)));
-          const bf16x4 qhi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(Qs + swz(r0 + 8, c0)));
-          dv[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_shufflevector(glo, ghi, 0, 1, 2, 3, 4, 5, 6, 7),
-                                                           pb[cc], dv[db], 0, 0, 0);
-          dk[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_shufflevector(qlo, qhi, 0, 1, 2, 3, 4, 5, 6, 7),
-                                                           dsb[cc], dk[db], 0, 0, 0);
+          const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(Ys + swz(r0, c0)));
+          const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(Ys + swz(r0 + 8, c0)));
+          acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7),
+                                                            wb[cc], acc[db], 0, 0, 0);
         }
     }
   };
@@ -481,28 +509,27 @@ __global__ __launch_bounds__(kBwdThreads) void dkdv_kernel(BwdArgs a) {
   wait_vmcnt<0>();
   store_stats(0);
   __syncthreads();
-  for (int st = 0; st < nst; ++st) {
-    if (st + 1 < nst) issue(G.q_begin + (st + 1) * BQ, (st + 1) & 1);
-    compute(st & 1);
+  for (int it = 0; it <= nst; ++it) {
+    if (it + 1 < nst) issue(G.q_begin + (it + 1) * BQ, (it + 1) % 3);
+    if (role == 0 && it < nst) stage(it % 3, it & 1);
+    if (role != 0 && it >= 1) stage((it - 1) % 3, (it - 1) & 1);
     wait_vmcnt<0>();
-    if (st + 1 < nst) store_stats((st + 1) & 1);
+    if (it + 1 < nst) store_stats((it + 1) % 3);
     __syncthreads();
   }
 
   if (k_ok) {
+    float* dst = role == 0 ? G.dv_ctx : G.dk_ctx;
+    const float sc = role == 0 ? 1.f : a.scale;
     const int64_t off = static_cast<int64_t>(key) * ld + hoff + 4 * hh;
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj) {
-        f32x4 vk, vv;
+        f32x4 v;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          vk[i] = dk[db][4 * jj + i] * a.scale;
-          vv[i] = dv[db][4 * jj + i];
-        }
-        *reinterpret_cast<f32x4*>(G.dk_ctx + off + db * 32 + 8 * jj) = vk;
-        *reinterpret_cast<f32x4*>(G.dv_ctx + off + db * 32 + 8 * jj) = vv;
+        for (int i = 0; i < 4; ++i) v[i] = acc[db][4 * jj + i] * sc;
+        *reinterpret_cast<f32x4*>(dst + off + db * 32 + 8 * jj) = v;
       }
   }
 }
@@ -670,9 +697,9 @@ hipError_t launch_bwd(const BwdArgs& a, int dq_blocks, int kv_blocks, int head_d
   if (kv_blocks > 0) {
     if (bf16) {
       if (head_dim == 128)
-        hipLaunchKernelGGL(dkdv_kernel<128>, dim3(kv_blocks), dim3(kBwdThreads), 0, stream, a);
+        hipLaunchKernelGGL(dkdv_kernel<128>, dim3(kv_blocks), dim3(kBwdKVThreads), 0, stream, a);
       else
-        hipLaunchKernelGGL(dkdv_kernel<64>, dim3(kv_blocks), dim3(kBwdThreads), 0, stream, a);
+        hipLaunchKernelGGL(dkdv_kernel<64>, dim3(kv_blocks), dim3(kBwdKVThreads), 0, stream, a);
     } else {
       if (head_dim == 128)
         hipLaunchKernelGGL(dkdv_f32_kernel<128>, dim3(kv_blocks), dim3(kBwdF32), 0, stream, a);

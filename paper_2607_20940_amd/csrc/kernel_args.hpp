@@ -72,8 +72,9 @@ constexpr int64_t partial_record_floats(int head_dim) { return static_cast<int64
 constexpr int kBwdThreads = 256;
 constexpr int kBwdQ = 128;     // dQ kernel: queries per block
 constexpr int kBwdKS = 128;    // dQ kernel: keys per LDS stage
-constexpr int kBwdK = 128;     // dK/dV kernel: keys per block
-constexpr int kBwdQS = 128;    // dK/dV kernel: queries per LDS stage
+constexpr int kBwdK = 128;     // dK/dV kernel: keys per block (4 wave pairs x 32)
+constexpr int kBwdKVThreads = 512;  // dK/dV kernel: 8 waves, two per SIMD
+constexpr int kBwdQS = 64;     // dK/dV kernel: queries per LDS stage
 constexpr int kBwdF32 = 64;    // fp32 kernels: one query or key per lane
 constexpr int kDotThreads = 256;
 constexpr int kMaxScatterJobs = 10;
