@@ -14,27 +14,28 @@
 // orders and no atomics: the result is the same bits on every run.
 //
 // bf16 path (gfx950 matrix cores, v_mfma_f32_32x32x16_bf16, fp32
-// accumulation), two kernels so that no gradient needs atomics:
-//   dq_kernel    a wave owns 32 queries and walks the context in 128-key
+// accumulation), two kernels so that no gradient needs atomics, each run by
+// pairs of waves that share a SIMD (two waves per SIMD, 8 per block):
+//   dq_kernel    a pair owns 32 queries and walks the context in 64-key
 //                stages through LDS (one swizzled copy each of K and V,
-//                loaded by direct transfers, as below): S^T = K Q^T and
-//                dP^T = V dO^T (A = K, V rows from LDS, B = the wave's Q and
-//                dO fragments in registers), so each lane holds 16 keys of
-//                ONE query and its
-//                lse / rowsum are scalars; dS^T packed to bf16 is already the
-//                B operand of dQ^T += K^T dS^T, with K^T read from LDS by the
-//                transposing read ds_read_b64_tr_b16.
-//   dkdv_kernel  a wave owns 32 context keys (K, V fragments in registers)
-//                and walks the scale's queries in 128-query stages: S = Q K^T,
-//                dP = dO V^T (lane = key), then dV^T += dO^T P and
-//                dK^T += Q^T dS with dO^T, Q^T from transposing reads.  One
-//                XOR-swizzled copy of Q and dO in LDS serves both read
-//                patterns without bank conflicts; it arrives by direct
-//                global -> LDS transfers (no staging registers).
-// The dQ kernel keeps its LDS operand reads several MFMAs ahead and overlaps
-// one key block's softmax with the next block's MFMAs; in the dK/dV kernel
-// (K, V, dK and dV per wave fill the register file) the same scheme measured
-// slower than the plain loop, which is kept.
+//                loaded by direct transfers).  Wave A: S^T = K Q^T (A = K
+//                rows from LDS, B = its Q fragment), so each lane holds 16
+//                keys of ONE query and its lse is a scalar; P = exp2(S c -
+//                lse) to LDS.  Wave B, one stage later: dP^T = V dO^T,
+//                dS^T = P (dP - rowsum), packed to bf16 the B operand of
+//                dQ^T += K^T dS^T, with K^T read by the transposing read
+//                ds_read_b64_tr_b16.
+//   dkdv_kernel  a pair owns 32 context keys and walks the scale's queries in
+//                64-query stages: wave A S = Q K^T, P (lane = key) and
+//                dV^T += dO^T P; wave B, one stage later, dP = dO V^T,
+//                dS = P (dP - rowsum) and dK^T += Q^T dS, with dO^T, Q^T
+//                from transposing reads.
+// Each wave holds one operand fragment and at most one accumulator, which is
+// what lets two waves share a SIMD: one wave's VALU work runs while the
+// other's MFMAs keep the matrix core busy.  One XOR-swizzled copy of each
+// staged tensor serves both read patterns without bank conflicts; stages
+// arrive by direct global -> LDS transfers (no staging registers) into three
+// buffers (the A waves' stage, the B waves' stage, the one arriving).
 // Rows past the end of a context or query range are zero-filled; their
 // probabilities are forced to zero.
 //
@@ -110,37 +111,6 @@ __global__ __launch_bounds__(kDotThreads) void dot_kernel(DotArgs a) {
 
 // ------------------------------------------------------------------ bf16 kernels
 
-// N MFMAs whose A operands come from LDS: operand i is read by rd(i) (NRD LDS
-// instructions) L operands ahead of its MFMA mf(i, a), so LDS latency hides
-// behind L MFMAs.  VALU (TRANS) vector (transcendental) instructions of the
-// same region, e.g. the softmax of the previous 32-row block, are placed
-// after each MFMA so they issue while the matrix core is busy.  Scheduling
-// group barriers fix this interleave (the compiler would otherwise hoist the
-// reads or sink each next to its MFMA).
-template <int N, int L, int NRD, int VALU, int TRANS, typename Rd, typename Mf>
-__device__ __forceinline__ void mfma_pipe(Rd&& rd, Mf&& mf) {
-  bf16x8 ring[L];
-#pragma unroll
-  for (int i = 0; i < L; ++i)
-    if (i < N) ring[i] = rd(i);
-#pragma unroll
-  for (int i = 0; i < N; ++i) {
-    const bf16x8 av = ring[i % L];
-    mf(i, av);
-    if (i + L < N) ring[i % L] = rd(i + L);
-  }
-#pragma unroll
-  for (int i = 0; i < (N < L ? N : L); ++i) __builtin_amdgcn_sched_group_barrier(0x100, NRD, 0);
-#pragma unroll
-  for (int i = 0; i < N; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    if (VALU > 0) __builtin_amdgcn_sched_group_barrier(0x002, VALU, 0);
-    if (TRANS > 0) __builtin_amdgcn_sched_group_barrier(0x400, TRANS, 0);
-    if (i + L < N) __builtin_amdgcn_sched_group_barrier(0x100, NRD, 0);
-  }
-  __builtin_amdgcn_sched_barrier(0);
-}
-
 // Stage rows: one copy per tensor in the 256-byte swizzled layout of
 // lds_stage.hpp (row reads and transposing reads both conflict-free), filled
 // by direct transfers.
@@ -148,16 +118,28 @@ __device__ inline int swz(int row, int col) { return swz256(row, col); }
 
 // ------------------------------------------------------------------ bf16: dQ
 
+// dQ: a block owns 128 queries, four pairs of waves of 32 queries each.  In
+// a pair, wave A (waves 0-3) computes S^T = K Q^T and P = exp2(S c - lse)
+// (keys past a run's end masked to zero) and hands P (bf16) to its partner
+// through LDS; wave B (waves 4-7, on the same SIMD) computes dP^T = V dO^T,
+// dS^T = P (dP - rowsum) and dQ^T += K^T dS^T one key stage later.  The
+// context streams in 64-key stages inside one run at a time (K and V tiles
+// through three LDS buffers: in iteration i the A waves use stage i, the B
+// waves stage i - 1, and the transfers fill stage i + 1; P of stage i goes to
+// exchange buffer i & 1).  One barrier per iteration.
 template <int D>
-__global__ __launch_bounds__(kBwdThreads) void dq_kernel(BwdArgs a) {
+__global__ __launch_bounds__(kBwdQThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void dq_kernel(BwdArgs a) {
   using L = Lay<D>;
   constexpr int KS = L::KS, DB = L::DB;
   constexpr int BN = kBwdKS, NKB = BN / 32;             // keys per stage, 32-key blocks
-  constexpr int KT = BN * 128 * 2;                      // bytes of one swizzled tile
+  constexpr int KT = BN * 128 * 2;                      // bytes of one swizzled tile (256-byte rows)
   constexpr int STB = 2 * KT;                           // K | V
-  constexpr int NDMA = KT / 1024 / (kBwdThreads / 64);  // 1 KB transfers per wave, tile and tensor
-  static_assert(NDMA * 1024 * (kBwdThreads / 64) == KT && BN % 32 == 0 && BN <= 128, "stage shape");
-  __shared__ __attribute__((aligned(16))) char lds[2 * STB];
+  constexpr int NW = kBwdQThreads / 64;
+  constexpr int NDMA = 2 * KT / 1024 / NW;              // 1 KB transfers per wave and stage (K and V)
+  constexpr int PXB = NKB * 2 * 64 * 16;                // bytes of one pair's P block per stage
+  static_assert(NDMA * 1024 * NW == 2 * KT && BN % 32 == 0, "stage shape");
+  __shared__ __attribute__((aligned(16))) char lds[3 * STB + 2 * 4 * PXB];
 
   int n_blocks = 0;
   for (int g = 0; g < a.n_groups; ++g) n_blocks += a.groups[g].n_qblocks * a.num_heads;
@@ -170,29 +152,27 @@ __global__ __launch_bounds__(kBwdThreads) void dq_kernel(BwdArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int pair = wave & 3, role = wave >> 2;  // role 0: S, P; role 1: dP, dS, dQ
   const int n = lane & 31, hh = lane >> 5;
-  const int q_row = G.q_begin + qt * kBwdQ + wave * 32 + n;
+  const int q_row = G.q_begin + qt * kBwdQ + pair * 32 + n;
   const bool q_ok = q_row < G.q_end;
   const int64_t ld = a.ld, hoff = static_cast<int64_t>(head) * D;
   const float c = a.scale_log2e;
 
-  // B operands: this lane's query, 8 channels of its half-wave per k step.
-  bf16x8 qf[KS], gf[KS];
+  // B operand of the wave's first product: this lane's query (Q for role 0,
+  // dO for role 1), 8 channels of its half-wave per k step; and the lane's
+  // row statistic (lse in log2 units, or rowsum(dO * O)).
+  bf16x8 xf[KS];
   {
     const int64_t off = static_cast<int64_t>(q_ok ? q_row : G.q_begin) * ld + hoff + hh * 8;
-    const __bf16* qp = static_cast<const __bf16*>(a.q) + off;
-    const __bf16* gp = static_cast<const __bf16*>(a.d_out) + off;
+    const __bf16* xp = static_cast<const __bf16*>(role == 0 ? a.q : a.d_out) + off;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      qf[ks] = q_ok ? *reinterpret_cast<const bf16x8*>(qp + ks * 16) : bf16x8{};
-      gf[ks] = q_ok ? *reinterpret_cast<const bf16x8*>(gp + ks * 16) : bf16x8{};
-    }
+    for (int ks = 0; ks < KS; ++ks) xf[ks] = q_ok ? *reinterpret_cast<const bf16x8*>(xp + ks * 16) : bf16x8{};
   }
   const int64_t stat = static_cast<int64_t>(head) * a.n_q + (q_ok ? q_row : G.q_begin);
-  const float lse2 = q_ok ? a.lse[stat] * kLog2e : 0.f;
-  const float dsum = q_ok ? a.dsum[stat] : 0.f;
+  const float rstat = !q_ok ? 0.f : role == 0 ? a.lse[stat] * kLog2e : a.dsum[stat];
 
-  f32x16 acc[DB];
+  f32x16 acc[DB];  // dQ^T (role 1)
 #pragma unroll
   for (int db = 0; db < DB; ++db) acc[db] = f32x16{};
 
@@ -224,13 +204,16 @@ __global__ __launch_bounds__(kBwdThreads) void dq_kernel(BwdArgs a) {
     if (s.left <= 0) seek(s, s.r + 1);
   };
 
-  // Per-lane global offsets of this wave's transfers, the same every stage
-  // (see the dK/dV kernel): logical chunk of the fixed LDS slot, zero past D.
+  // Per-lane global offsets of this wave's transfers (the same every stage):
+  // transfer t = wave NDMA + i covers bytes 1024 (t % (KT / 1024)) of the K
+  // tile (t < KT / 1024) or of the V tile; logical chunk of the fixed LDS
+  // slot, zero past D.
   const uint32_t row_bytes = static_cast<uint32_t>(ld) * 2;
   uint32_t voff[NDMA];
 #pragma unroll
   for (int i = 0; i < NDMA; ++i) {
-    const int p = (wave * NDMA + i) * 1024 + 16 * lane;
+    const int t = wave * NDMA + i;
+    const int p = (t % (KT / 1024)) * 1024 + 16 * lane;
     const int row = p >> 8, phys = (p >> 4) & 15;
     const int lc = unswz256(row, phys);
     voff[i] = lc < D / 8 ? row * row_bytes + lc * 16 : kPastEnd;
@@ -242,67 +225,62 @@ __global__ __launch_bounds__(kBwdThreads) void dq_kernel(BwdArgs a) {
     const uint32_t base = lds0 + buf * STB;
 #pragma unroll
     for (int i = 0; i < NDMA; ++i) {
-      const uint32_t dst = __builtin_amdgcn_readfirstlane(base + (wave * NDMA + i) * 1024);
-      dma16(rk, voff[i], dst);
-      dma16(rv, voff[i], dst + KT);
+      const int t = wave * NDMA + i;
+      dma16(t < KT / 1024 ? rk : rv, voff[i], __builtin_amdgcn_readfirstlane(base + t * 1024));
     }
   };
   const int t_lane = 4 * (lane >> 5) + ((lane & 15) >> 2);  // row of this lane's transposing read
   const int t_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  // P exchange block of this pair, buffer pbuf: [32-key block][16-key half][lane] x 16 bytes
+  auto px = [&](int pbuf) { return reinterpret_cast<bf16x8*>(lds + 3 * STB + (pbuf * 4 + pair) * PXB) + lane; };
 
-  // One stage, 32-key blocks kb: S^T, dP^T of block kb with block kb - 1's
-  // softmax interleaved, then dQ^T from block kb - 1.
-  auto compute = [&](int buf, int nvalid) {
+  // One stage of the wave's role on stage buffer buf.  Element e of a 32x32
+  // accumulator in this layout holds key kb*32 + 8(e/4) + 4hh + e%4 of the
+  // lane's query; packed to bf16 in pairs of 8 it is the B operand (16 keys
+  // each) of dQ^T += K^T dS^T.
+  auto stage = [&](int buf, int pbuf, int nvalid) {
     const __bf16* Ks = reinterpret_cast<const __bf16*>(lds + buf * STB);
     const __bf16* Vs = reinterpret_cast<const __bf16*>(lds + buf * STB + KT);
-    f32x16 s[NKB], dp[NKB];
-    bf16x8 dsb[NKB][2];
-    auto rows = [&](int kb) {
-      return [&, kb](int i) {
-        const int o = swz(kb * 32 + n, hh * 8 + (i >> 1) * 16);
-        return *reinterpret_cast<const bf16x8*>(((i & 1) ? Vs : Ks) + o);
-      };
-    };
-    auto sdp = [&](int kb) {
-      return [&, kb](int i, bf16x8 av) {
-        const int ks = i >> 1;
-        if (i & 1)
-          dp[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, gf[ks], ks == 0 ? f32x16{} : dp[kb], 0, 0, 0);
-        else
-          s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qf[ks], ks == 0 ? f32x16{} : s[kb], 0, 0, 0);
-      };
-    };
-    // dS^T = P^T * (dP^T - rowsum); element e of block kb is key kb*32 + 8(e/4) + 4hh + e%4.
-    auto soft = [&](int kb) {
+    const __bf16* Xs = role == 0 ? Ks : Vs;
+    bf16x8* pex = px(pbuf);
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int key = kb * 32 + 8 * (e >> 2) + 4 * hh + (e & 3);
-        const float p = key < nvalid ? __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][e], c, -lse2)) : 0.f;
-        dsb[kb][e >> 3][e & 7] = static_cast<__bf16>(p * (dp[kb][e] - dsum));
+    for (int kb = 0; kb < NKB; ++kb) {
+      f32x16 s;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const bf16x8 ax = *reinterpret_cast<const bf16x8*>(Xs + swz(kb * 32 + n, hh * 8 + ks * 16));
+        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ax, xf[ks], ks == 0 ? f32x16{} : s, 0, 0, 0);
       }
-    };
-    auto trs = [&](int kb) {
-      return [&, kb](int i) {
-        const int r0 = kb * 32 + (i / DB) * 16 + t_lane, c0 = (i % DB) * 32 + t_col;
-        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(Ks + swz(r0, c0)));
-        const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(Ks + swz(r0 + 8, c0)));
-        return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-      };
-    };
-    auto dq = [&](int kb) {
-      return [&, kb](int i, bf16x8 at) {
-        acc[i % DB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(at, dsb[kb][i / DB], acc[i % DB], 0, 0, 0);
-      };
-    };
-    mfma_pipe<2 * KS, 6, 1, 0, 0>(rows(0), sdp(0));
+      if (role == 0) {
+        bf16x8 pb[2];
 #pragma unroll
-    for (int kb = 1; kb < NKB; ++kb) {
-      soft(kb - 1);
-      mfma_pipe<2 * KS, 6, 1, 6, 1>(rows(kb), sdp(kb));
-      mfma_pipe<2 * DB, 4, 2, 0, 0>(trs(kb - 1), dq(kb - 1));
+        for (int e = 0; e < 16; ++e) {
+          const int key = kb * 32 + 8 * (e >> 2) + 4 * hh + (e & 3);
+          const float p = key < nvalid ? __builtin_amdgcn_exp2f(__builtin_fmaf(s[e], c, -rstat)) : 0.f;
+          pb[e >> 3][e & 7] = static_cast<__bf16>(p);
+        }
+        pex[(kb * 2) * 64] = pb[0];
+        pex[(kb * 2 + 1) * 64] = pb[1];
+      } else {
+        const bf16x8 p0 = pex[(kb * 2) * 64], p1 = pex[(kb * 2 + 1) * 64];
+        bf16x8 dsb[2];
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const float p = static_cast<float>((e < 8 ? p0 : p1)[e & 7]);
+          dsb[e >> 3][e & 7] = static_cast<__bf16>(p * (s[e] - rstat));
+        }
+#pragma unroll
+        for (int cc = 0; cc < 2; ++cc)
+#pragma unroll
+          for (int db = 0; db < DB; ++db) {
+            const int r0 = kb * 32 + cc * 16 + t_lane, c0 = db * 32 + t_col;
+            const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(Ks + swz(r0, c0)));
+            const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(Ks + swz(r0 + 8, c0)));
+            acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7),
+                                                              dsb[cc], acc[db], 0, 0, 0);
+          }
+      }
     }
-    soft(NKB - 1);
-    mfma_pipe<2 * DB, 4, 2, 0, 0>(trs(NKB - 1), dq(NKB - 1));
   };
 
   Stream ls, cs;
@@ -311,18 +289,21 @@ __global__ __launch_bounds__(kBwdThreads) void dq_kernel(BwdArgs a) {
   issue(ls, 0);
   wait_vmcnt<0>();
   __syncthreads();
-  for (int st = 0; st < nst; ++st) {
-    if (st + 1 < nst) {
+  for (int it = 0; it <= nst; ++it) {
+    if (it + 1 < nst) {
       step(ls);
-      issue(ls, (st + 1) & 1);
+      issue(ls, (it + 1) % 3);
     }
-    compute(st & 1, min(cs.left, BN));
-    step(cs);
+    if (role == 0 && it < nst) {
+      stage(it % 3, it & 1, min(cs.left, BN));
+      step(cs);
+    }
+    if (role != 0 && it >= 1) stage((it - 1) % 3, (it - 1) & 1, BN);
     wait_vmcnt<0>();
     __syncthreads();
   }
 
-  if (q_ok) {
+  if (role != 0 && q_ok) {
     __bf16* op = static_cast<__bf16*>(a.dq) + static_cast<int64_t>(q_row) * ld + hoff + 4 * hh;
 #pragma unroll
     for (int db = 0; db < DB; ++db)
@@ -682,9 +663,9 @@ hipError_t launch_bwd(const BwdArgs& a, int dq_blocks, int kv_blocks, int head_d
   if (dq_blocks > 0) {
     if (bf16) {
       if (head_dim == 128)
-        hipLaunchKernelGGL(dq_kernel<128>, dim3(dq_blocks), dim3(kBwdThreads), 0, stream, a);
+        hipLaunchKernelGGL(dq_kernel<128>, dim3(dq_blocks), dim3(kBwdQThreads), 0, stream, a);
       else
-        hipLaunchKernelGGL(dq_kernel<64>, dim3(dq_blocks), dim3(kBwdThreads), 0, stream, a);
+        hipLaunchKernelGGL(dq_kernel<64>, dim3(dq_blocks), dim3(kBwdQThreads), 0, stream, a);
     } else {
       if (head_dim == 128)
         hipLaunchKernelGGL(dq_f32_kernel<128>, dim3(dq_blocks), dim3(kBwdF32), 0, stream, a);

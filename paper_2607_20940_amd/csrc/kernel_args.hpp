@@ -70,8 +70,9 @@ constexpr int64_t partial_record_floats(int head_dim) { return static_cast<int64
 // bf16 backward kernels: 4 waves, 32 queries (dQ kernel) or 32 keys (dK/dV
 // kernel) per wave; the other operand streams through LDS in stages.
 constexpr int kBwdThreads = 256;
-constexpr int kBwdQ = 128;     // dQ kernel: queries per block
-constexpr int kBwdKS = 128;    // dQ kernel: keys per LDS stage
+constexpr int kBwdQ = 128;     // dQ kernel: queries per block (4 wave pairs x 32)
+constexpr int kBwdQThreads = 512;   // dQ kernel: 8 waves, two per SIMD
+constexpr int kBwdKS = 64;     // dQ kernel: keys per LDS stage
 constexpr int kBwdK = 128;     // dK/dV kernel: keys per block (4 wave pairs x 32)
 constexpr int kBwdKVThreads = 512;  // dK/dV kernel: 8 waves, two per SIMD
 constexpr int kBwdQS = 64;     // dK/dV kernel: queries per LDS stage
