@@ -229,8 +229,19 @@ void dq_kernel(BwdArgs a) {
       dma16(t < KT / 1024 ? rk : rv, voff[i], __builtin_amdgcn_readfirstlane(base + t * 1024));
     }
   };
-  const int t_lane = 4 * (lane >> 5) + ((lane & 15) >> 2);  // row of this lane's transposing read
+  // Operand offsets in the swizzled tiles (elements).  Row reads: row
+  // 32 kb + n, columns 16 ks + 8 hh at 32 kb * 128 + (r_rd ^ 16 ks).
+  // Transposing reads: rows R + t_lane (+ 8 for the upper half), columns
+  // 32 db + t_col, R a multiple of 16, at R * 128 + t_rd[db][half]: the
+  // swizzle of a row depends only on its index mod 16.
+  const int r_rd = swz(n, hh * 8);
+  const int t_lane = 4 * (lane >> 5) + ((lane & 15) >> 2);
   const int t_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  int t_rd[DB][2];
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int h = 0; h < 2; ++h) t_rd[db][h] = swz(t_lane + 8 * h, db * 32 + t_col);
   // P exchange block of this pair, buffer pbuf: [32-key block][16-key half][lane] x 16 bytes
   auto px = [&](int pbuf) { return reinterpret_cast<bf16x8*>(lds + 3 * STB + (pbuf * 4 + pair) * PXB) + lane; };
 
@@ -248,17 +259,19 @@ void dq_kernel(BwdArgs a) {
       f32x16 s;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        const bf16x8 ax = *reinterpret_cast<const bf16x8*>(Xs + swz(kb * 32 + n, hh * 8 + ks * 16));
+        const bf16x8 ax = *reinterpret_cast<const bf16x8*>(Xs + kb * 32 * 128 + (r_rd ^ (ks * 16)));
         s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ax, xf[ks], ks == 0 ? f32x16{} : s, 0, 0, 0);
       }
       if (role == 0) {
+        if (nvalid < BN) {  // the last stage of a run: keys past its end get P = 0
+#pragma unroll
+          for (int e = 0; e < 16; ++e)
+            if (kb * 32 + 8 * (e >> 2) + 4 * hh + (e & 3) >= nvalid) s[e] = -INFINITY;
+        }
         bf16x8 pb[2];
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int key = kb * 32 + 8 * (e >> 2) + 4 * hh + (e & 3);
-          const float p = key < nvalid ? __builtin_amdgcn_exp2f(__builtin_fmaf(s[e], c, -rstat)) : 0.f;
-          pb[e >> 3][e & 7] = static_cast<__bf16>(p);
-        }
+        for (int e = 0; e < 16; ++e)
+          pb[e >> 3][e & 7] = static_cast<__bf16>(__builtin_amdgcn_exp2f(__builtin_fmaf(s[e], c, -rstat)));
         pex[(kb * 2) * 64] = pb[0];
         pex[(kb * 2 + 1) * 64] = pb[1];
       } else {
@@ -273,9 +286,9 @@ void dq_kernel(BwdArgs a) {
         for (int cc = 0; cc < 2; ++cc)
 #pragma unroll
           for (int db = 0; db < DB; ++db) {
-            const int r0 = kb * 32 + cc * 16 + t_lane, c0 = db * 32 + t_col;
-            const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(Ks + swz(r0, c0)));
-            const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(Ks + swz(r0 + 8, c0)));
+            const __bf16* r0 = Ks + (kb * 32 + cc * 16) * 128;
+            const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(r0 + t_rd[db][0]));
+            const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(r0 + t_rd[db][1]));
             acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7),
                                                               dsb[cc], acc[db], 0, 0, 0);
           }
@@ -419,8 +432,15 @@ void dkdv_kernel(BwdArgs a) {
   auto store_stats = [&](int buf) {
     if (tid < 2 * BQ) reinterpret_cast<float*>(lds + buf * STB + 2 * QT)[tid] = pstat;
   };
-  const int t_lane = 4 * (lane >> 5) + ((lane & 15) >> 2);  // row of this lane's transposing read
+  // Operand offsets in the swizzled tiles (elements), as in the dQ kernel.
+  const int r_rd = swz(n, hh * 8);
+  const int t_lane = 4 * (lane >> 5) + ((lane & 15) >> 2);
   const int t_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  int t_rd[DB][2];
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int h = 0; h < 2; ++h) t_rd[db][h] = swz(t_lane + 8 * h, db * 32 + t_col);
   // P exchange block of this pair, buffer pb: [32-query block][16-query half][lane] x 16 bytes
   auto px = [&](int pbuf) { return reinterpret_cast<bf16x8*>(lds + 3 * STB + (pbuf * 4 + pair) * PXB) + lane; };
 
@@ -443,7 +463,7 @@ void dkdv_kernel(BwdArgs a) {
       f32x16 s;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        const bf16x8 ax = *reinterpret_cast<const bf16x8*>(Xs + swz(qb * 32 + n, hh * 8 + ks * 16));
+        const bf16x8 ax = *reinterpret_cast<const bf16x8*>(Xs + qb * 32 * 128 + (r_rd ^ (ks * 16)));
         s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ax, xf[ks], ks == 0 ? f32x16{} : s, 0, 0, 0);
       }
       bf16x8 wb[2];  // P (role 0) or dS (role 1)
@@ -476,9 +496,9 @@ void dkdv_kernel(BwdArgs a) {
       for (int cc = 0; cc < 2; ++cc)
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
-          const int r0 = qb * 32 + cc * 16 + t_lane, c0 = db * 32 + t_col;
-          const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(Ys + swz(r0, c0)));
-          const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(Ys + swz(r0 + 8, c0)));
+          const __bf16* r0 = Ys + (qb * 32 + cc * 16) * 128;
+          const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(r0 + t_rd[db][0]));
+          const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(r0 + t_rd[db][1]));
           acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7),
                                                             wb[cc], acc[db], 0, 0, 0);
         }
