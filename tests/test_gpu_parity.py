@@ -147,12 +147,25 @@ def _round_bf16(x64):
     return f32_to_bf16_bits(x64.astype(np.float32))
 
 
-@pytest.mark.parametrize("name", ["ragged_3level_d128", "eight_states", "all_coarse_equal"])
+@pytest.mark.parametrize("name", ["ragged_3level_d128", "ragged_3level_d64", "eight_states", "all_coarse_equal"])
 def test_pool_small(name):
+    """Pooled K/V: frames pooled by 2 and by 4 in one pass (the 3-level
+    schedules, at both head dims), factor 2 alone, and factor 8 (generic)."""
     desc, seed = SMALL[name]
     r = GpuRun(desc, "bf16", seed, 1.0)
     r.run()
     _check_pool(r, name)
+
+
+def test_pool_two_levels_sides_3_mod_4():
+    """Both grid sides 3 mod 4: the last 4 x 4 block of every row and column
+    holds a whole 2 x 2 cell and a 1-wide one."""
+    desc = _desc(3, [1, 2, 4], 7, 11, F=2, S=1, Hh=2, nh=2, d=128)
+    r = GpuRun(desc, "bf16", 31, 1.0)
+    r.run()
+    _check_pool(r, "pool_7x11")
+    e = assert_close(r.output(), r.oracle(), "bf16", "pool_7x11_attention")
+    print(f"[parity] pool_7x11 attention ok {e}", flush=True)
 
 
 def test_pool_f32():
