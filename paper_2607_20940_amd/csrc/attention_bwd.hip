@@ -407,8 +407,15 @@ void dkdv_kernel(BwdArgs a) {
   // Stage queries [q0, q0 + BQ) into LDS buffer buf: Q and dO tiles by
   // direct transfers; lse (in log2 units, +inf past the end) and rowsum (0
   // past the end) through a register of threads 0..2BQ-1, stored by
-  // store_stats once the stage has arrived.
+  // store_stats once the stage has arrived.  The statistic is loaded from a
+  // clamped (always valid) index and only converted in store_stats: a
+  // conversion or a per-lane select of the loaded value here would make the
+  // loading waves wait for the load, and with it for the stage transfers
+  // issued just before, at the start of every stage.
+  static_assert(BQ % 64 == 0, "whole waves load the statistics");
+  const bool lse_wave = wave < BQ / 64, stat_wave = wave < 2 * BQ / 64;  // threads [0, BQ), [0, 2 BQ)
   float pstat = 0.f;
+  bool pok = false;
   auto issue = [&](int q0, int buf) {
     const int nv = min(BQ, G.q_end - q0);
     const uint32_t bytes = static_cast<uint32_t>(nv - 1) * row_bytes + D * 2;
@@ -422,15 +429,18 @@ void dkdv_kernel(BwdArgs a) {
       const uint32_t dst = __builtin_amdgcn_readfirstlane(base + t * 1024);
       dma16(t < QT / 1024 ? rq : rg, voff[i], dst);
     }
-    if (tid < 2 * BQ) {
+    if (stat_wave) {
       const int q = q0 + (tid % BQ);
-      const bool ok = q < G.q_end;
-      const int64_t s = static_cast<int64_t>(head) * a.n_q + q;
-      pstat = tid < BQ ? (ok ? a.lse[s] * kLog2e : INFINITY) : (ok ? a.dsum[s] : 0.f);
+      pok = q < G.q_end;
+      const int64_t s = static_cast<int64_t>(head) * a.n_q + min(q, G.q_end - 1);
+      pstat = (lse_wave ? a.lse : a.dsum)[s];
     }
   };
   auto store_stats = [&](int buf) {
-    if (tid < 2 * BQ) reinterpret_cast<float*>(lds + buf * STB + 2 * QT)[tid] = pstat;
+    if (stat_wave) {
+      const float v = lse_wave ? (pok ? pstat * kLog2e : INFINITY) : (pok ? pstat : 0.f);
+      reinterpret_cast<float*>(lds + buf * STB + 2 * QT)[tid] = v;
+    }
   };
   // Operand offsets in the swizzled tiles (elements), as in the dQ kernel.
   const int r_rd = swz(n, hh * 8);
