@@ -332,17 +332,23 @@ void dq_kernel(BwdArgs a) {
 
 // ------------------------------------------------------------------ bf16: dK, dV
 
-// dK/dV: a block owns 128 context keys, four pairs of waves of 32 keys each.
-// In a pair, wave A (waves 0-3) computes S = Q K^T, P = exp2(S c - lse) and
-// dV^T += dO^T P, and hands P (bf16) to its partner through LDS; wave B
-// (waves 4-7, on the same SIMD as its partner) computes dP = dO V^T,
-// dS = P (dP - rowsum) and dK^T += Q^T dS one query stage later.  Each wave
-// keeps one fragment (K or V) and one accumulator (dV or dK), so two waves
-// fit on a SIMD and each has MFMA and VALU work for the hardware to
-// interleave.  Queries stream in 64-query stages (Q, dO and the row
-// statistics) through three LDS buffers: in iteration i the A waves use stage
-// i, the B waves stage i - 1, and the transfers fill stage i + 1; P of stage
-// i goes to exchange buffer i & 1.  One barrier per iteration.
+// dK/dV: a block owns 128 context keys, four pairs of waves of 32 keys each;
+// the waves of a pair share a SIMD.  Wave A (waves 0-3) holds the keys' K
+// fragment and dV accumulator, wave B (waves 4-7) their V fragment and dK
+// accumulator.  Queries stream in 64-query stages t, each taking two phases
+// separated by block barriers, in which one wave of the pair runs MFMAs while
+// the other runs VALU work:
+//   phase 2t:     A  dV^T += dO_{t-1}^T P_{t-1}, then S_t = Q_t K^T
+//                 B  dS_{t-1} = P_{t-1} (dP_{t-1} - rowsum_{t-1})
+//   phase 2t + 1: A  P_t = exp2(S_t c - lse_t), to registers and to LDS for B
+//                 B  dK^T += Q_{t-1}^T dS_{t-1}, then dP_t = dO_t V^T
+// Stage t's Q, dO and row statistics live in LDS buffer t % 3 and are read
+// in phases 2t .. 2t + 3.  B issues stage t + 1 (direct transfers) at the
+// start of phase 2t into buffer (t + 1) % 3, whose stage t - 2 was last read
+// in phase 2t - 1, and waits for it at the end of phase 2t + 1.  P_t is
+// written in phase 2t + 1 and read in 2t + 2; one block per pair suffices.
+// The matrix-core step is one code site for both roles, so that the register
+// allocation holds one set of accumulators, S/dP and P/dS registers.
 template <int D>
 __global__ __launch_bounds__(kBwdKVThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void dkdv_kernel(BwdArgs a) {
@@ -351,11 +357,11 @@ void dkdv_kernel(BwdArgs a) {
   constexpr int BQ = kBwdQS, NQB = BQ / 32;             // queries per stage, 32-query blocks
   constexpr int QT = BQ * 128 * 2;                      // bytes of one swizzled tile (256-byte rows)
   constexpr int STB = 2 * QT + 8 * BQ;                  // Q | dO | lse2 | rowsum (fp32)
-  constexpr int NW = kBwdKVThreads / 64;
-  constexpr int NDMA = 2 * QT / 1024 / NW;              // 1 KB transfers per wave and stage (Q and dO)
-  constexpr int PXB = NQB * 2 * 64 * 16;                // bytes of one pair's P block per stage
-  static_assert(NDMA * 1024 * NW == 2 * QT && BQ % 32 == 0, "stage shape");
-  __shared__ __attribute__((aligned(16))) char lds[3 * STB + 2 * 4 * PXB];
+  constexpr int NDMA = 2 * QT / 1024 / 4;               // 1 KB transfers per B wave and stage (Q and dO)
+  constexpr int PXB = NQB * 2 * 64 * 16;                // bytes of one pair's P block
+  constexpr int kLead = 4;                              // LDS operands read ahead of their MFMA
+  static_assert(NDMA * 1024 * 4 == 2 * QT && BQ % 32 == 0, "stage shape");
+  __shared__ __attribute__((aligned(16))) char lds[3 * STB + 4 * PXB];
 
   int n_blocks = 0;
   for (int g = 0; g < a.n_groups; ++g) n_blocks += a.groups[g].n_kblocks * a.num_heads;
@@ -368,15 +374,15 @@ void dkdv_kernel(BwdArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int pair = wave & 3, role = wave >> 2;  // role 0: S, P, dV; role 1: dP, dS, dK
+  const int pair = wave & 3, role = wave >> 2;  // role 0 (A): S, P, dV; role 1 (B): dP, dS, dK
   const int n = lane & 31, hh = lane >> 5;
   const int key = kt * kBwdK + pair * 32 + n;
   const bool k_ok = key < G.n_kv;
   const int64_t ld = a.ld, hoff = static_cast<int64_t>(head) * D;
   const float c = a.scale_log2e;
 
-  // B operand of the wave's first product: this lane's key (K for role 0,
-  // V for role 1), 8 channels of its half-wave per k step.
+  // B operand of the wave's row product: this lane's key (K for A, V for B),
+  // 8 channels of its half-wave per k step.
   bf16x8 xf[KS];
   {
     const __bf16* xp = ctx_row<__bf16>(G, key, role != 0, ld);
@@ -384,36 +390,40 @@ void dkdv_kernel(BwdArgs a) {
     for (int ks = 0; ks < KS; ++ks)
       xf[ks] = xp ? *reinterpret_cast<const bf16x8*>(xp + hoff + hh * 8 + ks * 16) : bf16x8{};
   }
-  f32x16 acc[DB];  // dV^T (role 0) or dK^T (role 1)
+  f32x16 acc[DB];  // dV^T (A) or dK^T (B)
 #pragma unroll
   for (int db = 0; db < DB; ++db) acc[db] = f32x16{};
+  f32x16 s[NQB];       // S_t (A) or dP_t (B)
+  bf16x8 w[NQB][2];    // P_t (A) or dS_{t-1} (B), packed as the B operand of the accumulating product
+#pragma unroll
+  for (int qb = 0; qb < NQB; ++qb) w[qb][0] = w[qb][1] = bf16x8{};
 
-  // Per-lane global offsets of this wave's transfers (the same every stage):
-  // transfer t = wave NDMA + i covers bytes 1024 (t % (QT / 1024)) of the Q
-  // tile (t < QT / 1024) or of the dO tile; LDS byte p of a tile holds row
-  // p / 256, physical chunk (p / 16) % 16, i.e. logical chunk phys ^ f(row);
-  // chunks past the head's D channels point past the buffer (zero fill).
+  // Per-lane global offsets of the B waves' transfers (the same every
+  // stage): transfer t = (wave - 4) NDMA + i covers bytes 1024 (t % (QT / 1024))
+  // of the Q tile (t < QT / 1024) or of the dO tile; logical chunk of the
+  // fixed LDS slot, zero past D.
   const uint32_t row_bytes = static_cast<uint32_t>(ld) * 2;
   uint32_t voff[NDMA];
 #pragma unroll
   for (int i = 0; i < NDMA; ++i) {
-    const int t = wave * NDMA + i;
+    const int t = (wave & 3) * NDMA + i;
     const int p = (t % (QT / 1024)) * 1024 + 16 * lane;
     const int row = p >> 8, phys = (p >> 4) & 15;
     const int lc = unswz256(row, phys);
     voff[i] = lc < D / 8 ? row * row_bytes + lc * 16 : kPastEnd;
   }
   const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds));
-  // Stage queries [q0, q0 + BQ) into LDS buffer buf: Q and dO tiles by
-  // direct transfers; lse (in log2 units, +inf past the end) and rowsum (0
-  // past the end) through a register of threads 0..2BQ-1, stored by
-  // store_stats once the stage has arrived.  The statistic is loaded from a
-  // clamped (always valid) index and only converted in store_stats: a
-  // conversion or a per-lane select of the loaded value here would make the
-  // loading waves wait for the load, and with it for the stage transfers
-  // issued just before, at the start of every stage.
-  static_assert(BQ % 64 == 0, "whole waves load the statistics");
-  const bool lse_wave = wave < BQ / 64, stat_wave = wave < 2 * BQ / 64;  // threads [0, BQ), [0, 2 BQ)
+  // Stage queries [q0, q0 + BQ) into LDS buffer buf (B waves): Q and dO tiles
+  // by direct transfers; lse (log2 units, +inf past the end) and rowsum (0
+  // past the end) through a register of B's threads 0..2BQ-1, stored by
+  // store_stats once the stage has arrived.
+  // The statistic is loaded from a clamped (always valid) index and only
+  // converted in store_stats: a conversion or a per-lane select of the loaded
+  // value here would make the loading waves wait for the load, and with it
+  // for the stage transfers issued just before.
+  static_assert(BQ == 64, "waves 4 and 5 load the statistics");
+  const int btid = tid - 256;
+  const bool lse_wave = wave == 4, stat_wave = wave == 4 || wave == 5;
   float pstat = 0.f;
   bool pok = false;
   auto issue = [&](int q0, int buf) {
@@ -425,21 +435,20 @@ void dkdv_kernel(BwdArgs a) {
     const uint32_t base = lds0 + buf * STB;
 #pragma unroll
     for (int i = 0; i < NDMA; ++i) {
-      const int t = wave * NDMA + i;
-      const uint32_t dst = __builtin_amdgcn_readfirstlane(base + t * 1024);
-      dma16(t < QT / 1024 ? rq : rg, voff[i], dst);
+      const int t = (wave & 3) * NDMA + i;
+      dma16(t < QT / 1024 ? rq : rg, voff[i], __builtin_amdgcn_readfirstlane(base + t * 1024));
     }
     if (stat_wave) {
-      const int q = q0 + (tid % BQ);
+      const int q = q0 + (btid % BQ);
       pok = q < G.q_end;
-      const int64_t s = static_cast<int64_t>(head) * a.n_q + min(q, G.q_end - 1);
-      pstat = (lse_wave ? a.lse : a.dsum)[s];
+      const int64_t st = static_cast<int64_t>(head) * a.n_q + min(q, G.q_end - 1);
+      pstat = (lse_wave ? a.lse : a.dsum)[st];
     }
   };
   auto store_stats = [&](int buf) {
     if (stat_wave) {
       const float v = lse_wave ? (pok ? pstat * kLog2e : INFINITY) : (pok ? pstat : 0.f);
-      reinterpret_cast<float*>(lds + buf * STB + 2 * QT)[tid] = v;
+      reinterpret_cast<float*>(lds + buf * STB + 2 * QT)[btid] = v;
     }
   };
   // Operand offsets in the swizzled tiles (elements), as in the dQ kernel.
@@ -451,81 +460,141 @@ void dkdv_kernel(BwdArgs a) {
   for (int db = 0; db < DB; ++db)
 #pragma unroll
     for (int h = 0; h < 2; ++h) t_rd[db][h] = swz(t_lane + 8 * h, db * 32 + t_col);
-  // P exchange block of this pair, buffer pb: [32-query block][16-query half][lane] x 16 bytes
-  auto px = [&](int pbuf) { return reinterpret_cast<bf16x8*>(lds + 3 * STB + (pbuf * 4 + pair) * PXB) + lane; };
-
-  // One stage of the wave's role on stage buffer buf.  Element e of a 32x32
-  // accumulator in this layout holds query qb*32 + 8(e/4) + 4hh + e%4 of the
-  // lane's key; packed to bf16 in pairs of 8 it is the B operand (16 queries
-  // each) of the accumulating products.
-  auto stage = [&](int buf, int pbuf) {
-    const __bf16* Qs = reinterpret_cast<const __bf16*>(lds + buf * STB);
-    const __bf16* Gs = reinterpret_cast<const __bf16*>(lds + buf * STB + QT);
-    const float* lse_s = reinterpret_cast<const float*>(lds + buf * STB + 2 * QT);
-    const float* rsum_s = lse_s + BQ;
-    // role 0 multiplies Q rows with K and dO^T with P; role 1 dO rows with V
-    // and Q^T with dS
-    const __bf16* Xs = role == 0 ? Qs : Gs;
-    const __bf16* Ys = role == 0 ? Gs : Qs;
-    bf16x8* pex = px(pbuf);
-#pragma unroll
-    for (int qb = 0; qb < NQB; ++qb) {
-      f32x16 s;
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const bf16x8 ax = *reinterpret_cast<const bf16x8*>(Xs + qb * 32 * 128 + (r_rd ^ (ks * 16)));
-        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ax, xf[ks], ks == 0 ? f32x16{} : s, 0, 0, 0);
-      }
-      bf16x8 wb[2];  // P (role 0) or dS (role 1)
-      if (role == 0) {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const f32x4 l4 = *reinterpret_cast<const f32x4*>(lse_s + qb * 32 + 8 * j + 4 * hh);
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int e = 4 * j + i;
-            wb[e >> 3][e & 7] = static_cast<__bf16>(__builtin_amdgcn_exp2f(__builtin_fmaf(s[e], c, -l4[i])));
-          }
-        }
-        pex[(qb * 2) * 64] = wb[0];
-        pex[(qb * 2 + 1) * 64] = wb[1];
-      } else {
-        const bf16x8 p0 = pex[(qb * 2) * 64], p1 = pex[(qb * 2 + 1) * 64];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const f32x4 r4 = *reinterpret_cast<const f32x4*>(rsum_s + qb * 32 + 8 * j + 4 * hh);
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int e = 4 * j + i;
-            const float p = static_cast<float>((e < 8 ? p0 : p1)[e & 7]);
-            wb[e >> 3][e & 7] = static_cast<__bf16>(p * (s[e] - r4[i]));
-          }
-        }
-      }
-#pragma unroll
-      for (int cc = 0; cc < 2; ++cc)
-#pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          const __bf16* r0 = Ys + (qb * 32 + cc * 16) * 128;
-          const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(r0 + t_rd[db][0]));
-          const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(r0 + t_rd[db][1]));
-          acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7),
-                                                            wb[cc], acc[db], 0, 0, 0);
-        }
-    }
+  bf16x8* const pex = reinterpret_cast<bf16x8*>(lds + 3 * STB + pair * PXB) + lane;
+  auto tile = [&](int buf, int which) {  // 0: Q, 1: dO
+    return reinterpret_cast<const __bf16*>(lds + buf * STB + which * QT);
   };
 
+  // Matrix-core step of a phase: the accumulating product of the previous
+  // stage (if acc_c: A^T rows of Ys, the wave's w as B operand), then the row
+  // product of the current stage (if row_c: rows of Xs times the wave's
+  // fragment), as one stream of MFMAs whose LDS operands run kLead ahead.
+  auto mstep = [&](auto acc_c, auto row_c, const __bf16* Ys, const __bf16* Xs) {
+    constexpr bool kA = decltype(acc_c)::value, kR = decltype(row_c)::value;
+    constexpr int NA = kA ? NQB * 2 * DB : 0;  // (32-row block, 16-row half, column block)
+    constexpr int NR = kR ? NQB * KS : 0;      // (32-row block, k step)
+    constexpr int N = NA + NR;
+    auto operand = [&](int i) -> bf16x8 {
+      if (i < NA) {
+        const int qb = i / (2 * DB), cc = (i / DB) & 1, db = i % DB;
+        const __bf16* r0 = Ys + (qb * 32 + cc * 16) * 128;
+        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(r0 + t_rd[db][0]));
+        const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(r0 + t_rd[db][1]));
+        return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+      }
+      const int j = i - NA, qb = j / KS, ks = j % KS;
+      return *reinterpret_cast<const bf16x8*>(Xs + qb * 32 * 128 + (r_rd ^ (ks * 16)));
+    };
+    bf16x8 ring[kLead];
+#pragma unroll
+    for (int i = 0; i < kLead; ++i)
+      if (i < N) ring[i] = operand(i);
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      const bf16x8 av = ring[i % kLead];
+      if (i < NA) {
+        const int qb = i / (2 * DB), cc = (i / DB) & 1, db = i % DB;
+        acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, w[qb][cc], acc[db], 0, 0, 0);
+      } else {
+        const int j = i - NA, qb = j / KS, ks = j % KS;
+        s[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, xf[ks], ks == 0 ? f32x16{} : s[qb], 0, 0, 0);
+      }
+      if (i + kLead < N) ring[i % kLead] = operand(i + kLead);
+    }
+    auto read_group = [&](int i) {  // an A^T operand is two LDS reads, a row operand one
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      if (i < NA) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    };
+#pragma unroll
+    for (int i = 0; i < (N < kLead ? N : kLead); ++i) read_group(i);
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      if (i + kLead < N) read_group(i + kLead);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  // Element e of a 32x32 accumulator in this layout holds query
+  // qb*32 + 8(e/4) + 4hh + e%4 of the lane's key.
+  // A: P_t = exp2(S_t c - lse_t) into w and into the pair's LDS block.
+  auto softmax_a = [&](int buf) {
+    const float* lse_s = reinterpret_cast<const float*>(lds + buf * STB + 2 * QT);
+#pragma unroll
+    for (int qb = 0; qb < NQB; ++qb) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const f32x4 l4 = *reinterpret_cast<const f32x4*>(lse_s + qb * 32 + 8 * j + 4 * hh);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int e = 4 * j + i;
+          w[qb][e >> 3][e & 7] = static_cast<__bf16>(__builtin_amdgcn_exp2f(__builtin_fmaf(s[qb][e], c, -l4[i])));
+        }
+      }
+      pex[(qb * 2) * 64] = w[qb][0];
+      pex[(qb * 2 + 1) * 64] = w[qb][1];
+    }
+#pragma unroll
+    for (int qb = 0; qb < NQB; ++qb)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) asm volatile("" : "+v"(w[qb][h]));
+  };
+  // B: dS = P (dP - rowsum) of the stage in buffer buf into w.
+  auto softmax_b = [&](int buf) {
+    const float* rsum_s = reinterpret_cast<const float*>(lds + buf * STB + 2 * QT) + BQ;
+#pragma unroll
+    for (int qb = 0; qb < NQB; ++qb) {
+      const bf16x8 p0 = pex[(qb * 2) * 64], p1 = pex[(qb * 2 + 1) * 64];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const f32x4 r4 = *reinterpret_cast<const f32x4*>(rsum_s + qb * 32 + 8 * j + 4 * hh);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int e = 4 * j + i;
+          const float p = static_cast<float>((e < 8 ? p0 : p1)[e & 7]);
+          w[qb][e >> 3][e & 7] = static_cast<__bf16>(p * (s[qb][e] - r4[i]));
+        }
+      }
+    }
+#pragma unroll
+    for (int qb = 0; qb < NQB; ++qb)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) asm volatile("" : "+v"(w[qb][h]));
+  };
+
+  // One matrix-core step for every stage and both roles (one instantiation
+  // keeps the register allocation tight): in the first stage the
+  // accumulating product multiplies the zeroed buffer 2 by w = 0, adding
+  // exact zeros; in the stage after the last, the row product's result is
+  // never used.
+  using T_ = std::true_type;
   const int nst = (G.q_end - G.q_begin + BQ - 1) / BQ;
-  issue(G.q_begin, 0);
+  {
+    bf16x8* z = reinterpret_cast<bf16x8*>(lds + 2 * STB);
+#pragma unroll
+    for (int i = 0; i < 2 * QT / 16 / kBwdKVThreads; ++i) z[tid + i * kBwdKVThreads] = bf16x8{};
+  }
+  if (role != 0) issue(G.q_begin, 0);
   wait_vmcnt<0>();
   store_stats(0);
   __syncthreads();
-  for (int it = 0; it <= nst; ++it) {
-    if (it + 1 < nst) issue(G.q_begin + (it + 1) * BQ, (it + 1) % 3);
-    if (role == 0 && it < nst) stage(it % 3, it & 1);
-    if (role != 0 && it >= 1) stage((it - 1) % 3, (it - 1) & 1);
-    wait_vmcnt<0>();
-    if (it + 1 < nst) store_stats((it + 1) % 3);
+  // Phase ph = 2t + r: role r runs the matrix-core step of stage t, the
+  // other role its VALU work.
+  for (int ph = 0; ph < 2 * nst + 2; ++ph) {
+    const int t = ph >> 1, cur = t % 3, prev = (t + 2) % 3;  // buffers of stages t and t - 1
+    if ((ph & 1) == role) {
+      __builtin_amdgcn_s_setprio(2);
+      mstep(T_{}, T_{}, tile(prev, 1 - role), tile(cur, role));
+      __builtin_amdgcn_s_setprio(0);
+      if (role != 0) {
+        wait_vmcnt<0>();
+        if (t + 1 < nst) store_stats((t + 1) % 3);
+      }
+    } else if (role == 0) {
+      if (t < nst) softmax_a(cur);
+    } else {
+      if (t + 1 < nst) issue(G.q_begin + (t + 1) * BQ, (t + 1) % 3);
+      if (t >= 1) softmax_b(prev);
+    }
     __syncthreads();
   }
 
