@@ -1,6 +1,6 @@
 """Benchmark of the MSSA hot path on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--resample mean|stride]
 
 One step is one rolling pass of one layer: mssa_pool_kv (K/V resampling)
 followed by mssa_forward (multi-scale attention) over inputs already resident
@@ -360,6 +360,9 @@ def main():
                     help="streaming: replay each full pass as one HIP graph (static window buffers)")
     ap.add_argument("--pooled-ring", action="store_true",
                     help="streaming: keep pooled history rings instead of re-pooling history each pass")
+    ap.add_argument("--resample", choices=("mean", "stride"), default="mean",
+                    help="K/V resampling of the layer workloads: block mean (default) or the "
+                         "strided pick of each block's first cell (both timed the same way)")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="only run a plain device copy of this many MiB (5 times), the reference "
                          "for scaling HBM byte counters")
@@ -398,6 +401,8 @@ def main():
     from paper_2607_20940_amd.workloads import WORKLOADS, input_shapes
 
     w = dict(WORKLOADS[args.workload], name=args.workload)
+    if args.resample != "mean":
+        w["desc"] = dict(w["desc"], resample=args.resample)
     desc = w["desc"]
     dtype = w["dtype"]
     plan = mssa.mssa_plan_create(dict(desc, dtype=dtype))
@@ -481,7 +486,7 @@ def main():
             "sink_frames": desc["sink_frames"], "hist_frames": desc["hist_frames"],
             "states": desc["num_states"], "frames_per_state": desc["frames_per_state"],
             "n_q": info["n_q"], "n_kv": info["n_kv"], "flops_alg": flops,
-            "input_sets_rotated": len(sets),
+            "input_sets_rotated": len(sets), "resample": args.resample,
         },
         "pct_of_bf16_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
         "forward_ms": round(float(fwd_ms.mean()), 4),
