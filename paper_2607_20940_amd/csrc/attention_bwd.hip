@@ -29,13 +29,16 @@
 //                64-query stages: wave A S = Q K^T, P (lane = key) and
 //                dV^T += dO^T P; wave B, one stage later, dP = dO V^T,
 //                dS = P (dP - rowsum) and dK^T += Q^T dS, with dO^T, Q^T
-//                from transposing reads.
+//                from transposing reads.  Strict ping-pong: in each of a
+//                stage's two barrier-separated phases one wave of the pair
+//                issues only MFMAs and the other only VALU work.
 // Each wave holds one operand fragment and at most one accumulator, which is
 // what lets two waves share a SIMD: one wave's VALU work runs while the
 // other's MFMAs keep the matrix core busy.  One XOR-swizzled copy of each
 // staged tensor serves both read patterns without bank conflicts; stages
 // arrive by direct global -> LDS transfers (no staging registers) into three
-// buffers (the A waves' stage, the B waves' stage, the one arriving).
+// buffers (the stage the A waves read, the stage the B waves read, the one
+// arriving).
 // Rows past the end of a context or query range are zero-filled; their
 // probabilities are forced to zero.
 //
