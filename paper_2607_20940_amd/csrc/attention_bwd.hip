@@ -429,23 +429,24 @@ void dkdv_kernel(BwdArgs a) {
   const bool lse_wave = wave == 4, stat_wave = wave == 4 || wave == 5;
   float pstat = 0.f;
   bool pok = false;
+  // Loop-invariant values kept in registers (read through G inside the stage
+  // loop, they were reloaded from memory and waited for every stage), and
+  // the one tensor each B wave transfers: Q (waves 4, 5) or dO (waves 6, 7).
+  static_assert(2 * NDMA * 1024 == QT, "two B waves per tile");
+  const int q_begin = G.q_begin, q_end = G.q_end;
+  const __bf16* const x_head = static_cast<const __bf16*>((wave & 3) < 2 ? a.q : a.d_out) + hoff;
+  const float* const s_head = (lse_wave ? a.lse : a.dsum) + static_cast<int64_t>(head) * a.n_q;
   auto issue = [&](int q0, int buf) {
-    const int nv = min(BQ, G.q_end - q0);
+    const int nv = min(BQ, q_end - q0);
     const uint32_t bytes = static_cast<uint32_t>(nv - 1) * row_bytes + D * 2;
-    const int64_t off = static_cast<int64_t>(q0) * ld + hoff;
-    const i32x4 rq = rsrc_of(static_cast<const __bf16*>(a.q) + off, bytes);
-    const i32x4 rg = rsrc_of(static_cast<const __bf16*>(a.d_out) + off, bytes);
-    const uint32_t base = lds0 + buf * STB;
+    const i32x4 rs = rsrc_of(x_head + static_cast<int64_t>(q0) * ld, bytes);
+    const uint32_t base = lds0 + buf * STB + (wave & 3) * NDMA * 1024;
 #pragma unroll
-    for (int i = 0; i < NDMA; ++i) {
-      const int t = (wave & 3) * NDMA + i;
-      dma16(t < QT / 1024 ? rq : rg, voff[i], __builtin_amdgcn_readfirstlane(base + t * 1024));
-    }
+    for (int i = 0; i < NDMA; ++i) dma16(rs, voff[i], __builtin_amdgcn_readfirstlane(base + i * 1024));
     if (stat_wave) {
       const int q = q0 + (btid % BQ);
-      pok = q < G.q_end;
-      const int64_t st = static_cast<int64_t>(head) * a.n_q + min(q, G.q_end - 1);
-      pstat = (lse_wave ? a.lse : a.dsum)[st];
+      pok = q < q_end;
+      pstat = s_head[min(q, q_end - 1)];
     }
   };
   auto store_stats = [&](int buf) {
@@ -570,13 +571,13 @@ void dkdv_kernel(BwdArgs a) {
   // exact zeros; in the stage after the last, the row product's result is
   // never used.
   using T_ = std::true_type;
-  const int nst = (G.q_end - G.q_begin + BQ - 1) / BQ;
+  const int nst = (q_end - q_begin + BQ - 1) / BQ;
   {
     bf16x8* z = reinterpret_cast<bf16x8*>(lds + 2 * STB);
 #pragma unroll
     for (int i = 0; i < 2 * QT / 16 / kBwdKVThreads; ++i) z[tid + i * kBwdKVThreads] = bf16x8{};
   }
-  if (role != 0) issue(G.q_begin, 0);
+  if (role != 0) issue(q_begin, 0);
   wait_vmcnt<0>();
   store_stats(0);
   __syncthreads();
@@ -595,7 +596,7 @@ void dkdv_kernel(BwdArgs a) {
     } else if (role == 0) {
       if (t < nst) softmax_a(cur);
     } else {
-      if (t + 1 < nst) issue(G.q_begin + (t + 1) * BQ, (t + 1) % 3);
+      if (t + 1 < nst) issue(q_begin + (t + 1) * BQ, (t + 1) % 3);
       if (t >= 1) softmax_b(prev);
     }
     __syncthreads();
