@@ -464,11 +464,14 @@ mssa_status mssa_backward(mssa_plan plan, const void* q_win, const void* k_sink,
   auto hs = static_cast<hipStream_t>(stream);
   char* ws = static_cast<char*>(workspace);
   float* dsum = reinterpret_cast<float*>(ws + p.bwd_dsum_off);
+  float* lse2 = reinterpret_cast<float*>(ws + p.bwd_lse2_off);
 
   mssa::DotArgs da{};
   da.out = out;
   da.d_out = d_out;
   da.dsum = dsum;
+  da.lse = bf16 ? lse : nullptr;
+  da.lse2 = lse2;
   da.ld = p.ld;
   da.n_q = static_cast<int32_t>(p.n_q);
   da.num_heads = nh;
@@ -481,6 +484,7 @@ mssa_status mssa_backward(mssa_plan plan, const void* q_win, const void* k_sink,
   a.d_out = d_out;
   a.lse = lse;
   a.dsum = dsum;
+  a.lse2 = lse2;
   a.dq = dq_win;
   a.ld = p.ld;
   a.n_q = static_cast<int32_t>(p.n_q);

@@ -37,8 +37,8 @@
 // other's MFMAs keep the matrix core busy.  One XOR-swizzled copy of each
 // staged tensor serves both read patterns without bank conflicts; stages
 // arrive by direct global -> LDS transfers (no staging registers) into three
-// buffers (the stage the A waves read, the stage the B waves read, the one
-// arriving).
+// buffers in dq_kernel (the stage the A waves read, the stage the B waves
+// read, the one arriving) and four in dkdv_kernel (two arriving).
 // Rows past the end of a context or query range are zero-filled; their
 // probabilities are forced to zero.
 //
@@ -110,6 +110,7 @@ __global__ __launch_bounds__(kDotThreads) void dot_kernel(DotArgs a) {
     for (int e = 0; e < N; ++e) acc = __builtin_fmaf(static_cast<float>(ov[e]), static_cast<float>(gv[e]), acc);
   }
   a.dsum[static_cast<int64_t>(h) * a.n_q + q] = acc;
+  if (a.lse) a.lse2[static_cast<int64_t>(h) * a.n_q + q] = a.lse[static_cast<int64_t>(h) * a.n_q + q] * kLog2e;
 }
 
 // ------------------------------------------------------------------ bf16 kernels
@@ -345,11 +346,12 @@ void dq_kernel(BwdArgs a) {
 //                 B  dS_{t-1} = P_{t-1} (dP_{t-1} - rowsum_{t-1})
 //   phase 2t + 1: A  P_t = exp2(S_t c - lse_t), to registers and to LDS for B
 //                 B  dK^T += Q_{t-1}^T dS_{t-1}, then dP_t = dO_t V^T
-// Stage t's Q, dO and row statistics live in LDS buffer t % 3 and are read
-// in phases 2t .. 2t + 3.  B issues stage t + 1 (direct transfers) at the
-// start of phase 2t into buffer (t + 1) % 3, whose stage t - 2 was last read
-// in phase 2t - 1, and waits for it at the end of phase 2t + 1.  P_t is
-// written in phase 2t + 1 and read in 2t + 2; one block per pair suffices.
+// Stage t's Q, dO and row statistics live in LDS buffer t % 4 and are read
+// in phases 2t .. 2t + 3.  B issues stage t + 2 (direct transfers, the
+// statistics included) at the end of its matrix-core phase 2t + 1 into
+// buffer (t + 2) % 4, whose stage t - 2 was last read in phase 2t - 1, so
+// B's VALU phases hold no transfer work.  P_t is written in phase 2t + 1 and
+// read in 2t + 2; one block per pair suffices.
 // The matrix-core step is one code site for both roles, so that the register
 // allocation holds one set of accumulators, S/dP and P/dS registers.
 template <int D>
@@ -364,7 +366,8 @@ void dkdv_kernel(BwdArgs a) {
   constexpr int PXB = NQB * 2 * 64 * 16;                // bytes of one pair's P block
   constexpr int kLead = 4;                              // LDS operands read ahead of their MFMA
   static_assert(NDMA * 1024 * 4 == 2 * QT && BQ % 32 == 0, "stage shape");
-  __shared__ __attribute__((aligned(16))) char lds[3 * STB + 4 * PXB];
+  constexpr int NBUF = 4;                               // stage buffers
+  __shared__ __attribute__((aligned(16))) char lds[NBUF * STB + 4 * PXB];
 
   int n_blocks = 0;
   for (int g = 0; g < a.n_groups; ++g) n_blocks += a.groups[g].n_kblocks * a.num_heads;
@@ -393,6 +396,10 @@ void dkdv_kernel(BwdArgs a) {
     for (int ks = 0; ks < KS; ++ks)
       xf[ks] = xp ? *reinterpret_cast<const bf16x8*>(xp + hoff + hh * 8 + ks * 16) : bf16x8{};
   }
+  // The fragment loads complete before the first transfer: the compiler does
+  // not count the transfers, so a later partial wait would leave it a full
+  // wait before the first use of the fragment in every stage.
+  wait_vmcnt<0>();
   f32x16 acc[DB];  // dV^T (A) or dK^T (B)
 #pragma unroll
   for (int db = 0; db < DB; ++db) acc[db] = f32x16{};
@@ -416,44 +423,28 @@ void dkdv_kernel(BwdArgs a) {
     voff[i] = lc < D / 8 ? row * row_bytes + lc * 16 : kPastEnd;
   }
   const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds));
-  // Stage queries [q0, q0 + BQ) into LDS buffer buf (B waves): Q and dO tiles
-  // by direct transfers; lse (log2 units, +inf past the end) and rowsum (0
-  // past the end) through a register of B's threads 0..2BQ-1, stored by
-  // store_stats once the stage has arrived.
-  // The statistic is loaded from a clamped (always valid) index and only
-  // converted in store_stats: a conversion or a per-lane select of the loaded
-  // value here would make the loading waves wait for the load, and with it
-  // for the stage transfers issued just before.
-  static_assert(BQ == 64, "waves 4 and 5 load the statistics");
-  const int btid = tid - 256;
-  const bool lse_wave = wave == 4, stat_wave = wave == 4 || wave == 5;
-  float pstat = 0.f;
-  bool pok = false;
-  // Loop-invariant values kept in registers (read through G inside the stage
-  // loop, they were reloaded from memory and waited for every stage), and
-  // the one tensor each B wave transfers: Q (waves 4, 5) or dO (waves 6, 7).
-  static_assert(2 * NDMA * 1024 == QT, "two B waves per tile");
+  // Stage queries [q0, q0 + BQ) into LDS buffer buf (B waves), all by
+  // direct transfers: the Q (waves 4, 5) or dO (waves 6, 7) tile rows, and
+  // the stage's lse in log2 units (wave 4) and rowsum (wave 5), one dword per
+  // lane.  Queries past the end arrive as zero rows with zero statistics:
+  // their P = exp2(0) = 1 meets zero dO rows (no dV contribution) and
+  // dS = 1 (0 - 0) = 0.  Loop-invariant values are kept in registers.
+  static_assert(2 * NDMA * 1024 == QT && BQ == 64, "two B waves per tile, one statistic per lane");
   const int q_begin = G.q_begin, q_end = G.q_end;
   const __bf16* const x_head = static_cast<const __bf16*>((wave & 3) < 2 ? a.q : a.d_out) + hoff;
-  const float* const s_head = (lse_wave ? a.lse : a.dsum) + static_cast<int64_t>(head) * a.n_q;
+  const bool stat_wave = wave == 4 || wave == 5;
+  const float* const s_head = (wave == 4 ? a.lse2 : a.dsum) + static_cast<int64_t>(head) * a.n_q;
   auto issue = [&](int q0, int buf) {
     const int nv = min(BQ, q_end - q0);
     const uint32_t bytes = static_cast<uint32_t>(nv - 1) * row_bytes + D * 2;
     const i32x4 rs = rsrc_of(x_head + static_cast<int64_t>(q0) * ld, bytes);
-    const uint32_t base = lds0 + buf * STB + (wave & 3) * NDMA * 1024;
+    const uint32_t base = lds0 + buf * STB;
 #pragma unroll
-    for (int i = 0; i < NDMA; ++i) dma16(rs, voff[i], __builtin_amdgcn_readfirstlane(base + i * 1024));
-    if (stat_wave) {
-      const int q = q0 + (btid % BQ);
-      pok = q < q_end;
-      pstat = s_head[min(q, q_end - 1)];
-    }
-  };
-  auto store_stats = [&](int buf) {
-    if (stat_wave) {
-      const float v = lse_wave ? (pok ? pstat * kLog2e : INFINITY) : (pok ? pstat : 0.f);
-      reinterpret_cast<float*>(lds + buf * STB + 2 * QT)[btid] = v;
-    }
+    for (int i = 0; i < NDMA; ++i)
+      dma16(rs, voff[i], __builtin_amdgcn_readfirstlane(base + ((wave & 3) * NDMA + i) * 1024));
+    if (stat_wave)
+      dma4(rsrc_of(s_head + q0, static_cast<uint32_t>(nv) * 4), 4 * lane,
+           __builtin_amdgcn_readfirstlane(base + 2 * QT + (wave - 4) * BQ * 4));
   };
   // Operand offsets in the swizzled tiles (elements), as in the dQ kernel.
   const int r_rd = swz(n, hh * 8);
@@ -464,7 +455,7 @@ void dkdv_kernel(BwdArgs a) {
   for (int db = 0; db < DB; ++db)
 #pragma unroll
     for (int h = 0; h < 2; ++h) t_rd[db][h] = swz(t_lane + 8 * h, db * 32 + t_col);
-  bf16x8* const pex = reinterpret_cast<bf16x8*>(lds + 3 * STB + pair * PXB) + lane;
+  bf16x8* const pex = reinterpret_cast<bf16x8*>(lds + NBUF * STB + pair * PXB) + lane;
   auto tile = [&](int buf, int which) {  // 0: Q, 1: dO
     return reinterpret_cast<const __bf16*>(lds + buf * STB + which * QT);
   };
@@ -567,36 +558,54 @@ void dkdv_kernel(BwdArgs a) {
 
   // One matrix-core step for every stage and both roles (one instantiation
   // keeps the register allocation tight): in the first stage the
-  // accumulating product multiplies the zeroed buffer 2 by w = 0, adding
-  // exact zeros; in the stage after the last, the row product's result is
-  // never used.
+  // accumulating product multiplies the zeroed buffer of stage -1 by w = 0,
+  // adding exact zeros; in the stage after the last, the row product's
+  // result is never used.  B issues stage t + 2 at the end of its
+  // matrix-core phase 2t + 1, into the buffer of stage t - 2 (last read in
+  // phase 2t - 1), and ends the phase once stage t + 1 has arrived.
   using T_ = std::true_type;
   const int nst = (q_end - q_begin + BQ - 1) / BQ;
   {
-    bf16x8* z = reinterpret_cast<bf16x8*>(lds + 2 * STB);
+    bf16x8* z = reinterpret_cast<bf16x8*>(lds + (NBUF - 1) * STB);
 #pragma unroll
     for (int i = 0; i < 2 * QT / 16 / kBwdKVThreads; ++i) z[tid + i * kBwdKVThreads] = bf16x8{};
   }
-  if (role != 0) issue(q_begin, 0);
-  wait_vmcnt<0>();
-  store_stats(0);
+  // this wave's transfers of one stage (the stage issued last may stay in flight)
+  auto wait_all_but_last = [&]() {
+    if (stat_wave)
+      wait_vmcnt<NDMA + 1>();
+    else
+      wait_vmcnt<NDMA>();
+  };
+  if (role != 0) {
+    issue(q_begin, 0);
+    if (nst > 1) {
+      issue(q_begin + BQ, 1);
+      wait_all_but_last();
+    } else {
+      wait_vmcnt<0>();
+    }
+  }
   __syncthreads();
   // Phase ph = 2t + r: role r runs the matrix-core step of stage t, the
   // other role its VALU work.
   for (int ph = 0; ph < 2 * nst + 2; ++ph) {
-    const int t = ph >> 1, cur = t % 3, prev = (t + 2) % 3;  // buffers of stages t and t - 1
+    const int t = ph >> 1, cur = t % NBUF, prev = (t + NBUF - 1) % NBUF;  // buffers of stages t, t - 1
     if ((ph & 1) == role) {
       __builtin_amdgcn_s_setprio(2);
       mstep(T_{}, T_{}, tile(prev, 1 - role), tile(cur, role));
       __builtin_amdgcn_s_setprio(0);
       if (role != 0) {
-        wait_vmcnt<0>();
-        if (t + 1 < nst) store_stats((t + 1) % 3);
+        if (t + 2 < nst) {
+          issue(q_begin + (t + 2) * BQ, (t + 2) % NBUF);
+          wait_all_but_last();
+        } else {
+          wait_vmcnt<0>();
+        }
       }
     } else if (role == 0) {
       if (t < nst) softmax_a(cur);
     } else {
-      if (t + 1 < nst) issue(q_begin + (t + 1) * BQ, (t + 1) % 3);
       if (t >= 1) softmax_b(prev);
     }
     __syncthreads();

@@ -98,6 +98,7 @@ struct BwdArgs {
   const void* d_out;
   const float* lse;         // [heads, n_q] from the forward
   const float* dsum;        // [heads, n_q]: rowsum(d_out * out)
+  const float* lse2;        // [heads, n_q]: lse in log2 units (lse * log2 e)
   void* dq;
   int64_t ld;               // elements between tokens: heads * head_dim
   int32_t n_q;
@@ -113,6 +114,8 @@ struct DotArgs {
   const void* out;
   const void* d_out;
   float* dsum;              // [heads, n_q]
+  const float* lse;         // [heads, n_q] natural log (bf16 plans; may be null)
+  float* lse2;              // [heads, n_q] lse * log2 e (written when lse is set)
   int64_t ld;
   int32_t n_q;
   int32_t num_heads;

@@ -49,6 +49,16 @@ __device__ inline void dma16(i32x4 rsrc, uint32_t voff, uint32_t lds_addr) {
 #pragma clang diagnostic pop
 }
 
+// As dma16 for 4 bytes per lane (buffer_load_dword ... lds): lane i's dword
+// at buffer offset voff lands at LDS byte address lds_addr + 4 i.
+__device__ inline void dma4(i32x4 rsrc, uint32_t voff, uint32_t lds_addr) {
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dword %1, %2, 0 offen lds"
+               :: "s"(lds_addr), "v"(voff), "s"(rsrc) : "memory", "m0");
+#pragma clang diagnostic pop
+}
+
 // As dma16, with a scalar byte offset soff added to the lane's offset.
 __device__ inline void dma16_soff(i32x4 rsrc, uint32_t voff, uint32_t soff, uint32_t lds_addr) {
 #pragma clang diagnostic push

@@ -270,6 +270,8 @@ mssa_status build_plan(const mssa_plan_desc& d, int slots, int ranges_override, 
   ws = align256(ws);
   p.bwd_dsum_off = ws;
   ws += align256(static_cast<int64_t>(d.num_heads) * p.n_q * 4);
+  p.bwd_lse2_off = ws;
+  ws += align256(static_cast<int64_t>(d.num_heads) * p.n_q * 4);
   p.bwd_dk_off.assign(G, 0);
   p.bwd_dv_off.assign(G, 0);
   for (int g = 0; g < G; ++g) {

@@ -100,8 +100,9 @@ struct Plan {
   int64_t partial_off, partial_bytes;    // partial records and the range table in the workspace
   int64_t range_table_off;               // n_ranges + 1 int64 first tiles of the tail ranges
   // Backward workspace: the forward's, then rowsum(dO * O) [heads, n_q]
-  // fp32, then per group the fp32 context gradients of K and V.
-  int64_t bwd_dsum_off;
+  // fp32, lse in log2 units [heads, n_q] fp32, then per group the fp32
+  // context gradients of K and V.
+  int64_t bwd_dsum_off, bwd_lse2_off;
   std::vector<int64_t> bwd_dk_off, bwd_dv_off;  // bytes, per group
   int64_t bwd_workspace_bytes;
   std::vector<ScatterJob> scatter_jobs;
