@@ -296,3 +296,21 @@ def test_tier_calls_checked():
     with pytest.raises(mssa.MssaError) as e:
         mssa.mssa_qkv_project(10, 12, fake, fake, fake, fake + 4096, fake + 8192, fake + 12288, stream=0)
     assert e.value.status == mssa.MSSA_ERR_INVALID_ARG
+
+
+def test_backward_workspace_layout():
+    """The backward workspace is the forward's, then rowsum(dO * O) and lse in
+    log2 units ([heads, n_q] fp32 each), then fp32 K and V context gradients
+    per query group, every region 256-byte aligned."""
+    def a256(x):
+        return (x + 255) // 256 * 256
+
+    for d in (128, 64):
+        desc = dict(num_states=4, scales=[1, 1, 2, 4], grid_h=10, grid_w=13, frames_per_state=2,
+                    sink_frames=1, hist_frames=3, num_heads=3, head_dim=d)
+        plan = mssa.mssa_plan_create(dict(desc, dtype="bf16"))
+        info = plan.info()
+        nh, nq = desc["num_heads"], info["n_q"]
+        want = a256(info["workspace_bytes"]) + 2 * a256(nh * nq * 4)
+        want += sum(2 * a256(n_kv * nh * d * 4) for n_kv in info["n_kv"][: info["n_groups"]])
+        assert mssa.mssa_backward_workspace_size(plan) == want
