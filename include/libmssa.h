@@ -123,6 +123,18 @@ typedef struct {
  * release it with mssa_plan_destroy. */
 mssa_status mssa_plan_create(const mssa_plan_desc* desc, mssa_plan* out);
 
+/* mssa_plan_create with the number of persistent attention blocks of the
+ * bf16 forward chosen by the caller.  The forward's work (every query scale,
+ * head and 256-query tile, each a sequence of 64-key tiles) is cut into
+ * attention_blocks equal shares, one per block; a share may end inside an
+ * item, whose pieces are then merged in a fixed order.  attention_blocks ==
+ * 0 takes one block per resident slot of the current device (512 without a
+ * device), as mssa_plan_create does; fewer leaves compute units to other
+ * streams, more runs in several waves.  The plan's workspace size depends on
+ * it.  MSSA_ERR_INVALID_ARG for attention_blocks < 0; otherwise as
+ * mssa_plan_create. */
+mssa_status mssa_plan_create_ex(const mssa_plan_desc* desc, int32_t attention_blocks, mssa_plan* out);
+
 /* Release a plan (NULL is ignored).  The caller must not use it afterwards
  * and must have no work using it still pending on any stream. */
 void mssa_plan_destroy(mssa_plan plan);

@@ -4,8 +4,10 @@
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
+#include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <memory>
 #include <new>
 #include <string>
 #include <vector>
@@ -20,11 +22,31 @@ struct mssa_plan_s {
 
 namespace {
 
-thread_local std::string g_last_error;
+// Message of the last failure on this thread.  A fixed buffer: recording a
+// failure never allocates, so it cannot throw.
+thread_local char g_last_error[512] = "";
 
-mssa_status fail(mssa_status s, const std::string& msg) {
-  g_last_error = msg;
+mssa_status fail(mssa_status s, const char* msg) noexcept {
+  std::snprintf(g_last_error, sizeof g_last_error, "%s", msg);
   return s;
+}
+
+mssa_status fail(mssa_status s, const char* what, const char* detail) noexcept {
+  std::snprintf(g_last_error, sizeof g_last_error, "%s: %s", what, detail);
+  return s;
+}
+
+// Body of an entry point: no C++ exception leaves the library.  A failed
+// host allocation is MSSA_ERR_NO_MEMORY, anything else MSSA_ERR_INVALID_ARG.
+template <class Body>
+mssa_status guarded(const char* where, Body&& body) noexcept {
+  try {
+    return body();
+  } catch (const std::bad_alloc&) {
+    return fail(MSSA_ERR_NO_MEMORY, where, "host allocation failed");
+  } catch (...) {
+    return fail(MSSA_ERR_INVALID_ARG, where, "unexpected internal error");
+  }
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -42,16 +64,9 @@ int resident_attention_blocks(int head_dim) {
   return per_cu > 0 ? cus * per_cu : 0;
 }
 
-// MSSA_FWD_RANGES=<n> forces the number of attention tile ranges (used by the
-// tests to make items split across several ranges).
-int ranges_override() {
-  const char* e = std::getenv("MSSA_FWD_RANGES");
-  return e ? std::atoi(e) : 0;
-}
-
 mssa_status check_device(hipError_t e, const char* what) {
   if (e == hipSuccess) return MSSA_OK;
-  return fail(MSSA_ERR_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
+  return fail(MSSA_ERR_DEVICE, what, hipGetErrorString(e));
 }
 
 // Launch pool jobs (source and destination pointers filled in), at most
@@ -289,140 +304,148 @@ mssa_status forward_impl(const mssa::Plan& p, const void* q_win, const void* k_s
 
 extern "C" {
 
-mssa_status mssa_plan_create(const mssa_plan_desc* desc, mssa_plan* out) {
-  if (!desc || !out) return fail(MSSA_ERR_INVALID_ARG, "desc and out must be non-null");
-  try {
-    auto* h = new mssa_plan_s;
+mssa_status mssa_plan_create_ex(const mssa_plan_desc* desc, int32_t attention_blocks, mssa_plan* out) {
+  return guarded("mssa_plan_create_ex", [&]() -> mssa_status {
+    if (!desc || !out) return fail(MSSA_ERR_INVALID_ARG, "desc and out must be non-null");
+    if (attention_blocks < 0) return fail(MSSA_ERR_INVALID_ARG, "attention_blocks must be >= 0");
+    std::unique_ptr<mssa_plan_s> h(new mssa_plan_s);
     std::string err;
-    const mssa_status s = mssa::build_plan(*desc, resident_attention_blocks(desc->head_dim),
-                                           ranges_override(), h->p, err);
-    if (s != MSSA_OK) {
-      delete h;
-      return fail(s, err);
-    }
-    *out = h;
+    const mssa_status s = mssa::build_plan(*desc, resident_attention_blocks(desc->head_dim), attention_blocks,
+                                           h->p, err);
+    if (s != MSSA_OK) return fail(s, err.c_str());
+    *out = h.release();
     return MSSA_OK;
-  } catch (const std::bad_alloc&) {
-    return fail(MSSA_ERR_NO_MEMORY, "host allocation failed");
-  } catch (...) {
-    return fail(MSSA_ERR_INVALID_ARG, "unexpected error while building the plan");
-  }
+  });
+}
+
+mssa_status mssa_plan_create(const mssa_plan_desc* desc, mssa_plan* out) {
+  return mssa_plan_create_ex(desc, 0, out);
 }
 
 void mssa_plan_destroy(mssa_plan plan) { delete plan; }
 
 mssa_status mssa_plan_query(mssa_plan plan, mssa_plan_info* info) {
-  if (!plan || !info) return fail(MSSA_ERR_INVALID_ARG, "plan and info must be non-null");
-  const mssa::Plan& p = plan->p;
-  std::memset(info, 0, sizeof(*info));
-  info->n_q = p.n_q;
-  info->n_sink_tok = p.n_sink_tok;
-  info->n_hist_tok = p.n_hist_tok;
-  info->workspace_bytes = p.workspace_bytes;
-  info->pairs_per_head = p.pairs_per_head;
-  info->flops_alg = 4 * static_cast<int64_t>(p.desc.head_dim) * p.desc.num_heads * p.pairs_per_head;
-  info->pool_bytes_alg = p.pool_bytes_alg;
-  info->n_groups = static_cast<int32_t>(p.groups.size());
-  for (size_t g = 0; g < p.groups.size(); ++g) {
-    info->group_scale[g] = p.groups[g].scale;
-    info->q_begin[g] = p.groups[g].q_begin;
-    info->q_end[g] = p.groups[g].q_end;
-    info->n_kv[g] = p.groups[g].n_kv;
-    info->pooled_k_offset[g] = p.pooled_k_off[g];
-    info->pooled_v_offset[g] = p.pooled_v_off[g];
-    info->pooled_tokens[g] = p.pooled_tokens[g];
-  }
-  return MSSA_OK;
+  return guarded("mssa_plan_query", [&]() -> mssa_status {
+    if (!plan || !info) return fail(MSSA_ERR_INVALID_ARG, "plan and info must be non-null");
+    const mssa::Plan& p = plan->p;
+    std::memset(info, 0, sizeof(*info));
+    info->n_q = p.n_q;
+    info->n_sink_tok = p.n_sink_tok;
+    info->n_hist_tok = p.n_hist_tok;
+    info->workspace_bytes = p.workspace_bytes;
+    info->pairs_per_head = p.pairs_per_head;
+    info->flops_alg = 4 * static_cast<int64_t>(p.desc.head_dim) * p.desc.num_heads * p.pairs_per_head;
+    info->pool_bytes_alg = p.pool_bytes_alg;
+    info->n_groups = static_cast<int32_t>(p.groups.size());
+    for (size_t g = 0; g < p.groups.size(); ++g) {
+      info->group_scale[g] = p.groups[g].scale;
+      info->q_begin[g] = p.groups[g].q_begin;
+      info->q_end[g] = p.groups[g].q_end;
+      info->n_kv[g] = p.groups[g].n_kv;
+      info->pooled_k_offset[g] = p.pooled_k_off[g];
+      info->pooled_v_offset[g] = p.pooled_v_off[g];
+      info->pooled_tokens[g] = p.pooled_tokens[g];
+    }
+    return MSSA_OK;
+  });
 }
 
 mssa_status mssa_plan_tables(mssa_plan plan, int64_t* dst, int64_t cap, int64_t* needed) {
-  if (!plan || !needed) return fail(MSSA_ERR_INVALID_ARG, "plan and needed must be non-null");
-  try {
+  return guarded("mssa_plan_tables", [&]() -> mssa_status {
+    if (!plan || !needed) return fail(MSSA_ERR_INVALID_ARG, "plan and needed must be non-null");
     const std::vector<int64_t> t = mssa::export_tables(plan->p);
     *needed = static_cast<int64_t>(t.size());
     if (!dst || cap < *needed) return fail(MSSA_ERR_INVALID_ARG, "table buffer too small");
     std::memcpy(dst, t.data(), t.size() * sizeof(int64_t));
     return MSSA_OK;
-  } catch (const std::bad_alloc&) {
-    return fail(MSSA_ERR_NO_MEMORY, "host allocation failed");
-  }
+  });
 }
 
 mssa_status mssa_pool_kv(mssa_plan plan, const void* k_hist, const void* v_hist, const void* k_win,
                          const void* v_win, void* workspace, int64_t workspace_bytes, void* stream) {
-  if (!plan) return fail(MSSA_ERR_INVALID_ARG, "plan must be non-null");
-  const mssa::Plan& p = plan->p;
-  if (p.pool_jobs.empty()) return MSSA_OK;
-  if (!k_win || !v_win) return fail(MSSA_ERR_INVALID_ARG, "k_win and v_win must be non-null");
-  bool reads_hist = false;
-  for (const mssa::PoolJob& J : p.pool_jobs) reads_hist |= J.buffer == mssa::kBufHist;
-  if (reads_hist && (!k_hist || !v_hist))
-    return fail(MSSA_ERR_INVALID_ARG, "k_hist and v_hist must be non-null when history is pooled");
-  if (!workspace || workspace_bytes < p.workspace_bytes)
-    return fail(MSSA_ERR_WORKSPACE, "workspace smaller than mssa_plan_info.workspace_bytes");
-  if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
-    return fail(MSSA_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
-  if (!aligned16(k_win) || !aligned16(v_win) || (k_hist && !aligned16(k_hist)) || (v_hist && !aligned16(v_hist)))
-    return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
+  return guarded("mssa_pool_kv", [&]() -> mssa_status {
+    if (!plan) return fail(MSSA_ERR_INVALID_ARG, "plan must be non-null");
+    const mssa::Plan& p = plan->p;
+    if (p.pool_jobs.empty()) return MSSA_OK;
+    if (!k_win || !v_win) return fail(MSSA_ERR_INVALID_ARG, "k_win and v_win must be non-null");
+    bool reads_hist = false;
+    for (const mssa::PoolJob& J : p.pool_jobs) reads_hist |= J.buffer == mssa::kBufHist;
+    if (reads_hist && (!k_hist || !v_hist))
+      return fail(MSSA_ERR_INVALID_ARG, "k_hist and v_hist must be non-null when history is pooled");
+    if (!workspace || workspace_bytes < p.workspace_bytes)
+      return fail(MSSA_ERR_WORKSPACE, "workspace smaller than mssa_plan_info.workspace_bytes");
+    if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
+      return fail(MSSA_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+    if (!aligned16(k_win) || !aligned16(v_win) || (k_hist && !aligned16(k_hist)) || (v_hist && !aligned16(v_hist)))
+      return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
 
-  const int64_t row_bytes = p.ld * p.elem_bytes;
-  auto* ws = static_cast<char*>(workspace);
-  std::vector<mssa::PoolJobArgs> jobs;
-  for (const mssa::PoolJob& J : p.pool_jobs) {
-    mssa::PoolJobArgs A{};
-    const char* sk = static_cast<const char*>(J.buffer == mssa::kBufHist ? k_hist : k_win);
-    const char* sv = static_cast<const char*>(J.buffer == mssa::kBufHist ? v_hist : v_win);
-    A.src_k = sk + J.src_tok * row_bytes;
-    A.src_v = sv + J.src_tok * row_bytes;
-    A.dst_k = ws + p.pooled_k_off[J.group] + J.dst_tok * row_bytes;
-    A.dst_v = ws + p.pooled_v_off[J.group] + J.dst_tok * row_bytes;
-    A.src_gh = J.src_gh;
-    A.src_gw = J.src_gw;
-    A.dst_gh = J.dst_gh;
-    A.dst_gw = J.dst_gw;
-    A.factor = J.factor;
-    A.n_frames = J.n_frames;
-    jobs.push_back(A);
-  }
-  return launch_pool_jobs(p, jobs, stream);
+    const int64_t row_bytes = p.ld * p.elem_bytes;
+    auto* ws = static_cast<char*>(workspace);
+    std::vector<mssa::PoolJobArgs> jobs;
+    for (const mssa::PoolJob& J : p.pool_jobs) {
+      mssa::PoolJobArgs A{};
+      const char* sk = static_cast<const char*>(J.buffer == mssa::kBufHist ? k_hist : k_win);
+      const char* sv = static_cast<const char*>(J.buffer == mssa::kBufHist ? v_hist : v_win);
+      A.src_k = sk + J.src_tok * row_bytes;
+      A.src_v = sv + J.src_tok * row_bytes;
+      A.dst_k = ws + p.pooled_k_off[J.group] + J.dst_tok * row_bytes;
+      A.dst_v = ws + p.pooled_v_off[J.group] + J.dst_tok * row_bytes;
+      A.src_gh = J.src_gh;
+      A.src_gw = J.src_gw;
+      A.dst_gh = J.dst_gh;
+      A.dst_gw = J.dst_gw;
+      A.factor = J.factor;
+      A.n_frames = J.n_frames;
+      jobs.push_back(A);
+    }
+    return launch_pool_jobs(p, jobs, stream);
+  });
 }
 
 mssa_status mssa_forward(mssa_plan plan, const void* q_win, const void* k_sink, const void* v_sink,
                          const void* k_hist, const void* v_hist, const void* k_win, const void* v_win,
                          const void* workspace, int64_t workspace_bytes, void* out, void* stream) {
-  if (!plan) return fail(MSSA_ERR_INVALID_ARG, "plan must be non-null");
-  if (plan->p.hist_ring)
-    return fail(MSSA_ERR_UNSUPPORTED, "plan has MSSA_PLAN_POOLED_HIST_RING: use mssa_forward_ring");
-  return forward_impl(plan->p, q_win, k_sink, v_sink, k_hist, v_hist, nullptr, nullptr, k_win, v_win, workspace,
-                      workspace_bytes, out, nullptr, stream);
+  return guarded("mssa_forward", [&]() -> mssa_status {
+    if (!plan) return fail(MSSA_ERR_INVALID_ARG, "plan must be non-null");
+    if (plan->p.hist_ring)
+      return fail(MSSA_ERR_UNSUPPORTED, "plan has MSSA_PLAN_POOLED_HIST_RING: use mssa_forward_ring");
+    return forward_impl(plan->p, q_win, k_sink, v_sink, k_hist, v_hist, nullptr, nullptr, k_win, v_win, workspace,
+                        workspace_bytes, out, nullptr, stream);
+  });
 }
 
 mssa_status mssa_forward_ring(mssa_plan plan, const void* q_win, const void* k_sink, const void* v_sink,
                               const void* k_hist, const void* v_hist, const void* const* k_hist_pooled,
                               const void* const* v_hist_pooled, const void* k_win, const void* v_win,
                               const void* workspace, int64_t workspace_bytes, void* out, void* stream) {
-  if (!plan) return fail(MSSA_ERR_INVALID_ARG, "plan must be non-null");
-  if (!plan->p.hist_ring)
-    return fail(MSSA_ERR_UNSUPPORTED, "plan lacks MSSA_PLAN_POOLED_HIST_RING: use mssa_forward");
-  return forward_impl(plan->p, q_win, k_sink, v_sink, k_hist, v_hist, k_hist_pooled, v_hist_pooled, k_win, v_win,
-                      workspace, workspace_bytes, out, nullptr, stream);
+  return guarded("mssa_forward_ring", [&]() -> mssa_status {
+    if (!plan) return fail(MSSA_ERR_INVALID_ARG, "plan must be non-null");
+    if (!plan->p.hist_ring)
+      return fail(MSSA_ERR_UNSUPPORTED, "plan lacks MSSA_PLAN_POOLED_HIST_RING: use mssa_forward");
+    return forward_impl(plan->p, q_win, k_sink, v_sink, k_hist, v_hist, k_hist_pooled, v_hist_pooled, k_win, v_win,
+                        workspace, workspace_bytes, out, nullptr, stream);
+  });
 }
 
 mssa_status mssa_forward_lse(mssa_plan plan, const void* q_win, const void* k_sink, const void* v_sink,
                              const void* k_hist, const void* v_hist, const void* k_win, const void* v_win,
                              const void* workspace, int64_t workspace_bytes, void* out, float* lse, void* stream) {
-  if (!plan) return fail(MSSA_ERR_INVALID_ARG, "plan must be non-null");
-  if (plan->p.hist_ring)
-    return fail(MSSA_ERR_UNSUPPORTED, "mssa_forward_lse takes plans without MSSA_PLAN_POOLED_HIST_RING");
-  if (!lse) return fail(MSSA_ERR_INVALID_ARG, "lse must be non-null");
-  return forward_impl(plan->p, q_win, k_sink, v_sink, k_hist, v_hist, nullptr, nullptr, k_win, v_win, workspace,
-                      workspace_bytes, out, lse, stream);
+  return guarded("mssa_forward_lse", [&]() -> mssa_status {
+    if (!plan) return fail(MSSA_ERR_INVALID_ARG, "plan must be non-null");
+    if (plan->p.hist_ring)
+      return fail(MSSA_ERR_UNSUPPORTED, "mssa_forward_lse takes plans without MSSA_PLAN_POOLED_HIST_RING");
+    if (!lse) return fail(MSSA_ERR_INVALID_ARG, "lse must be non-null");
+    return forward_impl(plan->p, q_win, k_sink, v_sink, k_hist, v_hist, nullptr, nullptr, k_win, v_win, workspace,
+                        workspace_bytes, out, lse, stream);
+  });
 }
 
 mssa_status mssa_backward_workspace_size(mssa_plan plan, int64_t* bytes) {
-  if (!plan || !bytes) return fail(MSSA_ERR_INVALID_ARG, "plan and bytes must be non-null");
-  *bytes = plan->p.bwd_workspace_bytes;
-  return MSSA_OK;
+  return guarded("mssa_backward_workspace_size", [&]() -> mssa_status {
+    if (!plan || !bytes) return fail(MSSA_ERR_INVALID_ARG, "plan and bytes must be non-null");
+    *bytes = plan->p.bwd_workspace_bytes;
+    return MSSA_OK;
+  });
 }
 
 mssa_status mssa_backward(mssa_plan plan, const void* q_win, const void* k_sink, const void* v_sink,
@@ -430,132 +453,134 @@ mssa_status mssa_backward(mssa_plan plan, const void* q_win, const void* k_sink,
                           const void* out, const float* lse, const void* d_out, void* workspace,
                           int64_t workspace_bytes, void* dq_win, void* dk_sink, void* dv_sink, void* dk_hist,
                           void* dv_hist, void* dk_win, void* dv_win, void* stream) {
-  if (!plan) return fail(MSSA_ERR_INVALID_ARG, "plan must be non-null");
-  const mssa::Plan& p = plan->p;
-  if (p.hist_ring)
-    return fail(MSSA_ERR_UNSUPPORTED, "mssa_backward takes plans without MSSA_PLAN_POOLED_HIST_RING");
-  if (!q_win || !k_win || !v_win || !out || !lse || !d_out || !dq_win || !dk_win || !dv_win)
-    return fail(MSSA_ERR_INVALID_ARG, "window tensors, out, lse, d_out and their gradients must be non-null");
-  if (p.n_sink_tok > 0 && (!k_sink || !v_sink || !dk_sink || !dv_sink))
-    return fail(MSSA_ERR_INVALID_ARG, "sink tensors and their gradients must be non-null when sink_frames > 0");
-  if (p.n_hist_tok > 0 && (!k_hist || !v_hist || !dk_hist || !dv_hist))
-    return fail(MSSA_ERR_INVALID_ARG, "history tensors and their gradients must be non-null when hist_frames > 0");
-  if (!workspace || workspace_bytes < p.bwd_workspace_bytes)
-    return fail(MSSA_ERR_WORKSPACE, "workspace smaller than mssa_backward_workspace_size");
-  if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
-    return fail(MSSA_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
-  const void* ins[] = {q_win, k_sink, v_sink, k_hist, v_hist, k_win, v_win, out, lse, d_out};
-  const void* grads[] = {dq_win, dk_sink, dv_sink, dk_hist, dv_hist, dk_win, dv_win};
-  for (const void* t : ins)
-    if (t && !aligned16(t)) return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
-  for (const void* t : grads) {
-    if (!t) continue;
-    if (!aligned16(t)) return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
-    for (const void* u : ins)
-      if (t == u) return fail(MSSA_ERR_INVALID_ARG, "gradients must not alias an input");
-  }
-  const int G = static_cast<int>(p.groups.size());
-  if (G > mssa::kMaxGroups) return fail(MSSA_ERR_UNSUPPORTED, "too many query scales");
-  if (p.scatter_jobs.size() > static_cast<size_t>(mssa::kMaxScatterJobs))
-    return fail(MSSA_ERR_UNSUPPORTED, "too many source frame runs");
-
-  const bool bf16 = p.desc.dtype == MSSA_BF16;
-  const int hd = p.desc.head_dim, nh = p.desc.num_heads;
-  auto hs = static_cast<hipStream_t>(stream);
-  char* ws = static_cast<char*>(workspace);
-  float* dsum = reinterpret_cast<float*>(ws + p.bwd_dsum_off);
-  float* lse2 = reinterpret_cast<float*>(ws + p.bwd_lse2_off);
-
-  mssa::DotArgs da{};
-  da.out = out;
-  da.d_out = d_out;
-  da.dsum = dsum;
-  da.lse = bf16 ? lse : nullptr;
-  da.lse2 = lse2;
-  da.ld = p.ld;
-  da.n_q = static_cast<int32_t>(p.n_q);
-  da.num_heads = nh;
-  da.head_dim = hd;
-  mssa_status s = check_device(mssa::launch_bwd_dot(da, bf16, hs), "backward rowsum launch");
-  if (s != MSSA_OK) return s;
-
-  mssa::BwdArgs a{};
-  a.q = q_win;
-  a.d_out = d_out;
-  a.lse = lse;
-  a.dsum = dsum;
-  a.lse2 = lse2;
-  a.dq = dq_win;
-  a.ld = p.ld;
-  a.n_q = static_cast<int32_t>(p.n_q);
-  a.num_heads = nh;
-  a.n_groups = G;
-  a.scale = p.softmax_scale;
-  a.scale_log2e = p.softmax_scale * 1.4426950408889634f;
-  const int qb = bf16 ? mssa::kBwdQ : mssa::kBwdF32, kb = bf16 ? mssa::kBwdK : mssa::kBwdF32;
-  const KvSources src{k_sink, v_sink, k_hist, v_hist, nullptr, nullptr, k_win, v_win, ws};
-  int64_t dq_blocks = 0, kv_blocks = 0;
-  int gi = 0;
-  for (int g : p.order) {
-    mssa::BwdGroupArgs& A = a.groups[gi++];
-    const mssa::QGroup& Q = p.groups[g];
-    A.q_begin = Q.q_begin;
-    A.q_end = Q.q_end;
-    A.n_kv = static_cast<int32_t>(Q.n_kv);
-    if (p.runs[g].size() > static_cast<size_t>(mssa::kMaxRuns))
-      return fail(MSSA_ERR_UNSUPPORTED, "too many context runs for one query scale");
-    A.n_runs = static_cast<int32_t>(p.runs[g].size());
-    for (size_t r = 0; r < p.runs[g].size(); ++r) {
-      run_pointers(p, g, p.runs[g][r], src, &A.runs[r].k, &A.runs[r].v);
-      A.runs[r].n_tok = static_cast<int32_t>(p.runs[g][r].n_tok);
+  return guarded("mssa_backward", [&]() -> mssa_status {
+    if (!plan) return fail(MSSA_ERR_INVALID_ARG, "plan must be non-null");
+    const mssa::Plan& p = plan->p;
+    if (p.hist_ring)
+      return fail(MSSA_ERR_UNSUPPORTED, "mssa_backward takes plans without MSSA_PLAN_POOLED_HIST_RING");
+    if (!q_win || !k_win || !v_win || !out || !lse || !d_out || !dq_win || !dk_win || !dv_win)
+      return fail(MSSA_ERR_INVALID_ARG, "window tensors, out, lse, d_out and their gradients must be non-null");
+    if (p.n_sink_tok > 0 && (!k_sink || !v_sink || !dk_sink || !dv_sink))
+      return fail(MSSA_ERR_INVALID_ARG, "sink tensors and their gradients must be non-null when sink_frames > 0");
+    if (p.n_hist_tok > 0 && (!k_hist || !v_hist || !dk_hist || !dv_hist))
+      return fail(MSSA_ERR_INVALID_ARG, "history tensors and their gradients must be non-null when hist_frames > 0");
+    if (!workspace || workspace_bytes < p.bwd_workspace_bytes)
+      return fail(MSSA_ERR_WORKSPACE, "workspace smaller than mssa_backward_workspace_size");
+    if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
+      return fail(MSSA_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+    const void* ins[] = {q_win, k_sink, v_sink, k_hist, v_hist, k_win, v_win, out, lse, d_out};
+    const void* grads[] = {dq_win, dk_sink, dv_sink, dk_hist, dv_hist, dk_win, dv_win};
+    for (const void* t : ins)
+      if (t && !aligned16(t)) return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
+    for (const void* t : grads) {
+      if (!t) continue;
+      if (!aligned16(t)) return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
+      for (const void* u : ins)
+        if (t == u) return fail(MSSA_ERR_INVALID_ARG, "gradients must not alias an input");
     }
-    A.dk_ctx = reinterpret_cast<float*>(ws + p.bwd_dk_off[g]);
-    A.dv_ctx = reinterpret_cast<float*>(ws + p.bwd_dv_off[g]);
-    A.n_qblocks = (Q.q_end - Q.q_begin + qb - 1) / qb;
-    A.n_kblocks = static_cast<int32_t>((Q.n_kv + kb - 1) / kb);
-    A.dq_block_begin = static_cast<int32_t>(dq_blocks);
-    A.kv_block_begin = static_cast<int32_t>(kv_blocks);
-    dq_blocks += static_cast<int64_t>(A.n_qblocks) * nh;
-    kv_blocks += static_cast<int64_t>(A.n_kblocks) * nh;
-  }
-  if (dq_blocks > 0x7fffffff || kv_blocks > 0x7fffffff) return fail(MSSA_ERR_UNSUPPORTED, "backward grid too large");
-  s = check_device(mssa::launch_bwd(a, static_cast<int>(dq_blocks), static_cast<int>(kv_blocks), hd, bf16, hs),
-                   "backward attention launch");
-  if (s != MSSA_OK) return s;
+    const int G = static_cast<int>(p.groups.size());
+    if (G > mssa::kMaxGroups) return fail(MSSA_ERR_UNSUPPORTED, "too many query scales");
+    if (p.scatter_jobs.size() > static_cast<size_t>(mssa::kMaxScatterJobs))
+      return fail(MSSA_ERR_UNSUPPORTED, "too many source frame runs");
 
-  mssa::ScatterArgs sa{};
-  for (int g = 0; g < G; ++g) {
-    sa.ctx_k[g] = reinterpret_cast<const float*>(ws + p.bwd_dk_off[g]);
-    sa.ctx_v[g] = reinterpret_cast<const float*>(ws + p.bwd_dv_off[g]);
-  }
-  sa.ld = p.ld;
-  sa.chunks_per_tok = static_cast<int32_t>(p.ld * p.elem_bytes / 16);
-  sa.n_groups = G;
-  sa.pick_first = p.strided ? 1 : 0;
-  const int64_t row_bytes = p.ld * p.elem_bytes;
-  int64_t blocks = 0;
-  int nj = 0;
-  for (const mssa::ScatterJob& J : p.scatter_jobs) {
-    mssa::ScatterJobArgs& A = sa.jobs[nj++];
-    char* dk = static_cast<char*>(J.buffer == mssa::kBufSink ? dk_sink : J.buffer == mssa::kBufHist ? dk_hist : dk_win);
-    char* dv = static_cast<char*>(J.buffer == mssa::kBufSink ? dv_sink : J.buffer == mssa::kBufHist ? dv_hist : dv_win);
-    A.dst_k = dk + J.src_tok * row_bytes;
-    A.dst_v = dv + J.src_tok * row_bytes;
-    A.n_frames = J.n_frames;
-    A.gh = J.gh;
-    A.gw = J.gw;
-    A.block_begin = static_cast<int32_t>(blocks);
+    const bool bf16 = p.desc.dtype == MSSA_BF16;
+    const int hd = p.desc.head_dim, nh = p.desc.num_heads;
+    auto hs = static_cast<hipStream_t>(stream);
+    char* ws = static_cast<char*>(workspace);
+    float* dsum = reinterpret_cast<float*>(ws + p.bwd_dsum_off);
+    float* lse2 = reinterpret_cast<float*>(ws + p.bwd_lse2_off);
+
+    mssa::DotArgs da{};
+    da.out = out;
+    da.d_out = d_out;
+    da.dsum = dsum;
+    da.lse = bf16 ? lse : nullptr;
+    da.lse2 = lse2;
+    da.ld = p.ld;
+    da.n_q = static_cast<int32_t>(p.n_q);
+    da.num_heads = nh;
+    da.head_dim = hd;
+    mssa_status s = check_device(mssa::launch_bwd_dot(da, bf16, hs), "backward rowsum launch");
+    if (s != MSSA_OK) return s;
+
+    mssa::BwdArgs a{};
+    a.q = q_win;
+    a.d_out = d_out;
+    a.lse = lse;
+    a.dsum = dsum;
+    a.lse2 = lse2;
+    a.dq = dq_win;
+    a.ld = p.ld;
+    a.n_q = static_cast<int32_t>(p.n_q);
+    a.num_heads = nh;
+    a.n_groups = G;
+    a.scale = p.softmax_scale;
+    a.scale_log2e = p.softmax_scale * 1.4426950408889634f;
+    const int qb = bf16 ? mssa::kBwdQ : mssa::kBwdF32, kb = bf16 ? mssa::kBwdK : mssa::kBwdF32;
+    const KvSources src{k_sink, v_sink, k_hist, v_hist, nullptr, nullptr, k_win, v_win, ws};
+    int64_t dq_blocks = 0, kv_blocks = 0;
+    int gi = 0;
+    for (int g : p.order) {
+      mssa::BwdGroupArgs& A = a.groups[gi++];
+      const mssa::QGroup& Q = p.groups[g];
+      A.q_begin = Q.q_begin;
+      A.q_end = Q.q_end;
+      A.n_kv = static_cast<int32_t>(Q.n_kv);
+      if (p.runs[g].size() > static_cast<size_t>(mssa::kMaxRuns))
+        return fail(MSSA_ERR_UNSUPPORTED, "too many context runs for one query scale");
+      A.n_runs = static_cast<int32_t>(p.runs[g].size());
+      for (size_t r = 0; r < p.runs[g].size(); ++r) {
+        run_pointers(p, g, p.runs[g][r], src, &A.runs[r].k, &A.runs[r].v);
+        A.runs[r].n_tok = static_cast<int32_t>(p.runs[g][r].n_tok);
+      }
+      A.dk_ctx = reinterpret_cast<float*>(ws + p.bwd_dk_off[g]);
+      A.dv_ctx = reinterpret_cast<float*>(ws + p.bwd_dv_off[g]);
+      A.n_qblocks = (Q.q_end - Q.q_begin + qb - 1) / qb;
+      A.n_kblocks = static_cast<int32_t>((Q.n_kv + kb - 1) / kb);
+      A.dq_block_begin = static_cast<int32_t>(dq_blocks);
+      A.kv_block_begin = static_cast<int32_t>(kv_blocks);
+      dq_blocks += static_cast<int64_t>(A.n_qblocks) * nh;
+      kv_blocks += static_cast<int64_t>(A.n_kblocks) * nh;
+    }
+    if (dq_blocks > 0x7fffffff || kv_blocks > 0x7fffffff) return fail(MSSA_ERR_UNSUPPORTED, "backward grid too large");
+    s = check_device(mssa::launch_bwd(a, static_cast<int>(dq_blocks), static_cast<int>(kv_blocks), hd, bf16, hs),
+                     "backward attention launch");
+    if (s != MSSA_OK) return s;
+
+    mssa::ScatterArgs sa{};
     for (int g = 0; g < G; ++g) {
-      A.g[g].ctx_begin = J.ctx_begin[g];
-      A.g[g].frame_stride = J.frame_stride[g];
-      A.g[g].factor = J.factor[g];
+      sa.ctx_k[g] = reinterpret_cast<const float*>(ws + p.bwd_dk_off[g]);
+      sa.ctx_v[g] = reinterpret_cast<const float*>(ws + p.bwd_dv_off[g]);
     }
-    const int64_t work = static_cast<int64_t>(J.n_frames) * J.gh * J.gw * sa.chunks_per_tok;
-    blocks += (work + mssa::kPoolThreads - 1) / mssa::kPoolThreads;
-  }
-  sa.n_jobs = nj;
-  if (blocks > 0x7fffffff) return fail(MSSA_ERR_UNSUPPORTED, "scatter grid too large");
-  return check_device(mssa::launch_scatter(sa, static_cast<int>(blocks), bf16, hs), "backward scatter launch");
+    sa.ld = p.ld;
+    sa.chunks_per_tok = static_cast<int32_t>(p.ld * p.elem_bytes / 16);
+    sa.n_groups = G;
+    sa.pick_first = p.strided ? 1 : 0;
+    const int64_t row_bytes = p.ld * p.elem_bytes;
+    int64_t blocks = 0;
+    int nj = 0;
+    for (const mssa::ScatterJob& J : p.scatter_jobs) {
+      mssa::ScatterJobArgs& A = sa.jobs[nj++];
+      char* dk = static_cast<char*>(J.buffer == mssa::kBufSink ? dk_sink : J.buffer == mssa::kBufHist ? dk_hist : dk_win);
+      char* dv = static_cast<char*>(J.buffer == mssa::kBufSink ? dv_sink : J.buffer == mssa::kBufHist ? dv_hist : dv_win);
+      A.dst_k = dk + J.src_tok * row_bytes;
+      A.dst_v = dv + J.src_tok * row_bytes;
+      A.n_frames = J.n_frames;
+      A.gh = J.gh;
+      A.gw = J.gw;
+      A.block_begin = static_cast<int32_t>(blocks);
+      for (int g = 0; g < G; ++g) {
+        A.g[g].ctx_begin = J.ctx_begin[g];
+        A.g[g].frame_stride = J.frame_stride[g];
+        A.g[g].factor = J.factor[g];
+      }
+      const int64_t work = static_cast<int64_t>(J.n_frames) * J.gh * J.gw * sa.chunks_per_tok;
+      blocks += (work + mssa::kPoolThreads - 1) / mssa::kPoolThreads;
+    }
+    sa.n_jobs = nj;
+    if (blocks > 0x7fffffff) return fail(MSSA_ERR_UNSUPPORTED, "scatter grid too large");
+    return check_device(mssa::launch_scatter(sa, static_cast<int>(blocks), bf16, hs), "backward scatter launch");
+  });
 }
 
 // ---------------------------------------------------------------- MSP tiers
@@ -599,227 +624,241 @@ mssa_status tier_layout(const mssa::Plan& p, const mssa_tier_desc* t, std::vecto
 }  // namespace
 
 mssa_status mssa_tier_workspace_size(mssa_plan plan, const mssa_tier_desc* tier, int64_t* bytes) {
-  if (!plan || !bytes) return fail(MSSA_ERR_INVALID_ARG, "plan and bytes must be non-null");
-  std::vector<TierGroup> tg;
-  return tier_layout(plan->p, tier, tg, bytes);
+  return guarded("mssa_tier_workspace_size", [&]() -> mssa_status {
+    if (!plan || !bytes) return fail(MSSA_ERR_INVALID_ARG, "plan and bytes must be non-null");
+    std::vector<TierGroup> tg;
+    return tier_layout(plan->p, tier, tg, bytes);
+  });
 }
 
 mssa_status mssa_patch_embed(mssa_plan plan, const mssa_tier_desc* tier, const void* latent,
                              const void* const* w_embed, const void* const* b_embed, void* workspace,
                              int64_t workspace_bytes, void* tokens, void* stream) {
-  if (!plan) return fail(MSSA_ERR_INVALID_ARG, "plan must be non-null");
-  const mssa::Plan& p = plan->p;
-  std::vector<TierGroup> tg;
-  int64_t need = 0;
-  mssa_status s = tier_layout(p, tier, tg, &need);
-  if (s != MSSA_OK) return s;
-  if (!latent || !w_embed || !b_embed || !tokens) return fail(MSSA_ERR_INVALID_ARG, "null argument");
-  if (!workspace || workspace_bytes < need) return fail(MSSA_ERR_WORKSPACE, "workspace smaller than mssa_tier_workspace_size");
-  if (!aligned16(latent) || !aligned16(tokens) || !aligned16(workspace))
-    return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
-  for (size_t g = 0; g < tg.size(); ++g)
-    if (!w_embed[g] || !b_embed[g] || !aligned16(w_embed[g])) return fail(MSSA_ERR_INVALID_ARG, "null or misaligned tier weights");
-  auto hs = static_cast<hipStream_t>(stream);
-  const int32_t H = p.desc.grid_h * tier->patch, W = p.desc.grid_w * tier->patch, hid = tier->hidden;
-  for (size_t g = 0; g < tg.size(); ++g) {
-    const TierGroup& t = tg[g];
-    const mssa::QGroup& Q = p.groups[g];
-    mssa::PatchArgs pa{};
-    pa.latent = const_cast<void*>(latent);
-    pa.rows = static_cast<char*>(workspace) + t.rows_off;
-    pa.frame0 = t.frame0;
-    pa.n_frames = t.n_frames;
-    pa.C = tier->latent_channels;
-    pa.H = H;
-    pa.W = W;
-    pa.P = t.P;
-    pa.gh = (H + t.P - 1) / t.P;
-    pa.gw = (W + t.P - 1) / t.P;
-    s = check_device(mssa::launch_patchify(pa, hs), "patchify launch");
+  return guarded("mssa_patch_embed", [&]() -> mssa_status {
+    if (!plan) return fail(MSSA_ERR_INVALID_ARG, "plan must be non-null");
+    const mssa::Plan& p = plan->p;
+    std::vector<TierGroup> tg;
+    int64_t need = 0;
+    mssa_status s = tier_layout(p, tier, tg, &need);
     if (s != MSSA_OK) return s;
-    mssa::GemmArgs ga{};
-    ga.x = pa.rows;
-    ga.w = w_embed[g];
-    ga.bias = b_embed[g];
-    ga.y[0] = static_cast<char*>(tokens) + static_cast<int64_t>(Q.q_begin) * hid * 2;
-    ga.M = Q.q_end - Q.q_begin;
-    ga.N = hid;
-    ga.K = t.kp;
-    ga.split = hid;
-    ga.ldx = t.kp;
-    ga.ldy = hid;
-    s = check_device(mssa::launch_gemm(ga, hs), "patch embedding GEMM launch");
-    if (s != MSSA_OK) return s;
-  }
-  return MSSA_OK;
+    if (!latent || !w_embed || !b_embed || !tokens) return fail(MSSA_ERR_INVALID_ARG, "null argument");
+    if (!workspace || workspace_bytes < need) return fail(MSSA_ERR_WORKSPACE, "workspace smaller than mssa_tier_workspace_size");
+    if (!aligned16(latent) || !aligned16(tokens) || !aligned16(workspace))
+      return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
+    for (size_t g = 0; g < tg.size(); ++g)
+      if (!w_embed[g] || !b_embed[g] || !aligned16(w_embed[g])) return fail(MSSA_ERR_INVALID_ARG, "null or misaligned tier weights");
+    auto hs = static_cast<hipStream_t>(stream);
+    const int32_t H = p.desc.grid_h * tier->patch, W = p.desc.grid_w * tier->patch, hid = tier->hidden;
+    for (size_t g = 0; g < tg.size(); ++g) {
+      const TierGroup& t = tg[g];
+      const mssa::QGroup& Q = p.groups[g];
+      mssa::PatchArgs pa{};
+      pa.latent = const_cast<void*>(latent);
+      pa.rows = static_cast<char*>(workspace) + t.rows_off;
+      pa.frame0 = t.frame0;
+      pa.n_frames = t.n_frames;
+      pa.C = tier->latent_channels;
+      pa.H = H;
+      pa.W = W;
+      pa.P = t.P;
+      pa.gh = (H + t.P - 1) / t.P;
+      pa.gw = (W + t.P - 1) / t.P;
+      s = check_device(mssa::launch_patchify(pa, hs), "patchify launch");
+      if (s != MSSA_OK) return s;
+      mssa::GemmArgs ga{};
+      ga.x = pa.rows;
+      ga.w = w_embed[g];
+      ga.bias = b_embed[g];
+      ga.y[0] = static_cast<char*>(tokens) + static_cast<int64_t>(Q.q_begin) * hid * 2;
+      ga.M = Q.q_end - Q.q_begin;
+      ga.N = hid;
+      ga.K = t.kp;
+      ga.split = hid;
+      ga.ldx = t.kp;
+      ga.ldy = hid;
+      s = check_device(mssa::launch_gemm(ga, hs), "patch embedding GEMM launch");
+      if (s != MSSA_OK) return s;
+    }
+    return MSSA_OK;
+  });
 }
 
 mssa_status mssa_patch_unembed(mssa_plan plan, const mssa_tier_desc* tier, const void* tokens,
                                const void* const* w_out, const void* const* b_out, void* workspace,
                                int64_t workspace_bytes, void* latent, void* stream) {
-  if (!plan) return fail(MSSA_ERR_INVALID_ARG, "plan must be non-null");
-  const mssa::Plan& p = plan->p;
-  std::vector<TierGroup> tg;
-  int64_t need = 0;
-  mssa_status s = tier_layout(p, tier, tg, &need);
-  if (s != MSSA_OK) return s;
-  if (!latent || !w_out || !b_out || !tokens) return fail(MSSA_ERR_INVALID_ARG, "null argument");
-  if (!workspace || workspace_bytes < need) return fail(MSSA_ERR_WORKSPACE, "workspace smaller than mssa_tier_workspace_size");
-  if (!aligned16(latent) || !aligned16(tokens) || !aligned16(workspace))
-    return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
-  for (size_t g = 0; g < tg.size(); ++g)
-    if (!w_out[g] || !b_out[g] || !aligned16(w_out[g])) return fail(MSSA_ERR_INVALID_ARG, "null or misaligned tier weights");
-  auto hs = static_cast<hipStream_t>(stream);
-  const int32_t H = p.desc.grid_h * tier->patch, W = p.desc.grid_w * tier->patch, hid = tier->hidden;
-  for (size_t g = 0; g < tg.size(); ++g) {
-    const TierGroup& t = tg[g];
-    const mssa::QGroup& Q = p.groups[g];
-    mssa::GemmArgs ga{};
-    ga.x = static_cast<const char*>(tokens) + static_cast<int64_t>(Q.q_begin) * hid * 2;
-    ga.w = w_out[g];
-    ga.bias = b_out[g];
-    ga.y[0] = static_cast<char*>(workspace) + t.rows_off;
-    ga.M = Q.q_end - Q.q_begin;
-    ga.N = t.kp;
-    ga.K = hid;
-    ga.split = t.kp;
-    ga.ldx = hid;
-    ga.ldy = t.kp;
-    s = check_device(mssa::launch_gemm(ga, hs), "patch de-embedding GEMM launch");
+  return guarded("mssa_patch_unembed", [&]() -> mssa_status {
+    if (!plan) return fail(MSSA_ERR_INVALID_ARG, "plan must be non-null");
+    const mssa::Plan& p = plan->p;
+    std::vector<TierGroup> tg;
+    int64_t need = 0;
+    mssa_status s = tier_layout(p, tier, tg, &need);
     if (s != MSSA_OK) return s;
-    mssa::PatchArgs pa{};
-    pa.latent = latent;
-    pa.rows = ga.y[0];
-    pa.frame0 = t.frame0;
-    pa.n_frames = t.n_frames;
-    pa.C = tier->latent_channels;
-    pa.H = H;
-    pa.W = W;
-    pa.P = t.P;
-    pa.gh = (H + t.P - 1) / t.P;
-    pa.gw = (W + t.P - 1) / t.P;
-    s = check_device(mssa::launch_unpatchify(pa, hs), "unpatchify launch");
-    if (s != MSSA_OK) return s;
-  }
-  return MSSA_OK;
+    if (!latent || !w_out || !b_out || !tokens) return fail(MSSA_ERR_INVALID_ARG, "null argument");
+    if (!workspace || workspace_bytes < need) return fail(MSSA_ERR_WORKSPACE, "workspace smaller than mssa_tier_workspace_size");
+    if (!aligned16(latent) || !aligned16(tokens) || !aligned16(workspace))
+      return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
+    for (size_t g = 0; g < tg.size(); ++g)
+      if (!w_out[g] || !b_out[g] || !aligned16(w_out[g])) return fail(MSSA_ERR_INVALID_ARG, "null or misaligned tier weights");
+    auto hs = static_cast<hipStream_t>(stream);
+    const int32_t H = p.desc.grid_h * tier->patch, W = p.desc.grid_w * tier->patch, hid = tier->hidden;
+    for (size_t g = 0; g < tg.size(); ++g) {
+      const TierGroup& t = tg[g];
+      const mssa::QGroup& Q = p.groups[g];
+      mssa::GemmArgs ga{};
+      ga.x = static_cast<const char*>(tokens) + static_cast<int64_t>(Q.q_begin) * hid * 2;
+      ga.w = w_out[g];
+      ga.bias = b_out[g];
+      ga.y[0] = static_cast<char*>(workspace) + t.rows_off;
+      ga.M = Q.q_end - Q.q_begin;
+      ga.N = t.kp;
+      ga.K = hid;
+      ga.split = t.kp;
+      ga.ldx = hid;
+      ga.ldy = t.kp;
+      s = check_device(mssa::launch_gemm(ga, hs), "patch de-embedding GEMM launch");
+      if (s != MSSA_OK) return s;
+      mssa::PatchArgs pa{};
+      pa.latent = latent;
+      pa.rows = ga.y[0];
+      pa.frame0 = t.frame0;
+      pa.n_frames = t.n_frames;
+      pa.C = tier->latent_channels;
+      pa.H = H;
+      pa.W = W;
+      pa.P = t.P;
+      pa.gh = (H + t.P - 1) / t.P;
+      pa.gw = (W + t.P - 1) / t.P;
+      s = check_device(mssa::launch_unpatchify(pa, hs), "unpatchify launch");
+      if (s != MSSA_OK) return s;
+    }
+    return MSSA_OK;
+  });
 }
 
 mssa_status mssa_qkv_project(int64_t n_tokens, int32_t hidden, const void* x, const void* w_qkv, const void* b_qkv,
                              void* q, void* k, void* v, void* stream) {
-  if (n_tokens < 0 || n_tokens > 0x7fffffff || hidden < 8 || hidden % 8 != 0 || hidden > (1 << 20))
-    return fail(MSSA_ERR_INVALID_ARG, "n_tokens must fit int32 and hidden be a positive multiple of 8");
-  if (!x || !w_qkv || !b_qkv || !q || !k || !v) return fail(MSSA_ERR_INVALID_ARG, "null argument");
-  for (const void* t : {x, w_qkv, static_cast<const void*>(q), static_cast<const void*>(k), static_cast<const void*>(v)})
-    if (!aligned16(t)) return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
-  if (q == x || k == x || v == x) return fail(MSSA_ERR_INVALID_ARG, "outputs must not alias x");
-  mssa::GemmArgs ga{};
-  ga.x = x;
-  ga.w = w_qkv;
-  ga.bias = b_qkv;
-  ga.y[0] = q;
-  ga.y[1] = k;
-  ga.y[2] = v;
-  ga.M = static_cast<int32_t>(n_tokens);
-  ga.N = 3 * hidden;
-  ga.K = hidden;
-  ga.split = hidden;
-  ga.ldx = hidden;
-  ga.ldy = hidden;
-  return check_device(mssa::launch_gemm(ga, static_cast<hipStream_t>(stream)), "QKV GEMM launch");
+  return guarded("mssa_qkv_project", [&]() -> mssa_status {
+    if (n_tokens < 0 || n_tokens > 0x7fffffff || hidden < 8 || hidden % 8 != 0 || hidden > (1 << 20))
+      return fail(MSSA_ERR_INVALID_ARG, "n_tokens must fit int32 and hidden be a positive multiple of 8");
+    if (!x || !w_qkv || !b_qkv || !q || !k || !v) return fail(MSSA_ERR_INVALID_ARG, "null argument");
+    for (const void* t : {x, w_qkv, static_cast<const void*>(q), static_cast<const void*>(k), static_cast<const void*>(v)})
+      if (!aligned16(t)) return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
+    if (q == x || k == x || v == x) return fail(MSSA_ERR_INVALID_ARG, "outputs must not alias x");
+    mssa::GemmArgs ga{};
+    ga.x = x;
+    ga.w = w_qkv;
+    ga.bias = b_qkv;
+    ga.y[0] = q;
+    ga.y[1] = k;
+    ga.y[2] = v;
+    ga.M = static_cast<int32_t>(n_tokens);
+    ga.N = 3 * hidden;
+    ga.K = hidden;
+    ga.split = hidden;
+    ga.ldx = hidden;
+    ga.ldy = hidden;
+    return check_device(mssa::launch_gemm(ga, static_cast<hipStream_t>(stream)), "QKV GEMM launch");
+  });
 }
 
 mssa_status mssa_hist_append(mssa_plan plan, const void* k_win, const void* v_win, void* k_ring, void* v_ring,
                              int32_t ring_cap_frames, int32_t* ring_head, int32_t* ring_count, void* stream) {
-  if (!plan) return fail(MSSA_ERR_INVALID_ARG, "null argument");
-  std::vector<int32_t> slots;
-  return append_native(plan->p, k_win, v_win, k_ring, v_ring, ring_cap_frames, ring_head, ring_count, slots,
-                       stream);
+  return guarded("mssa_hist_append", [&]() -> mssa_status {
+    if (!plan) return fail(MSSA_ERR_INVALID_ARG, "null argument");
+    std::vector<int32_t> slots;
+    return append_native(plan->p, k_win, v_win, k_ring, v_ring, ring_cap_frames, ring_head, ring_count, slots,
+                         stream);
+  });
 }
 
 mssa_status mssa_hist_append_ring(mssa_plan plan, const void* k_win, const void* v_win, const void* workspace,
                                   int64_t workspace_bytes, void* k_ring, void* v_ring, void* const* k_ring_pooled,
                                   void* const* v_ring_pooled, int32_t ring_cap_frames, int32_t* ring_head,
                                   int32_t* ring_count, void* stream) {
-  if (!plan) return fail(MSSA_ERR_INVALID_ARG, "null argument");
-  const mssa::Plan& p = plan->p;
-  if (!p.hist_ring)
-    return fail(MSSA_ERR_UNSUPPORTED, "plan lacks MSSA_PLAN_POOLED_HIST_RING: use mssa_hist_append");
-  if (!k_ring_pooled || !v_ring_pooled) return fail(MSSA_ERR_INVALID_ARG, "null pooled ring array");
-  bool coarse = false;
-  for (size_t g = 0; g < p.groups.size(); ++g) {
-    if (p.groups[g].scale == 1) continue;
-    coarse = true;
-    if (!k_ring_pooled[g] || !v_ring_pooled[g])
-      return fail(MSSA_ERR_INVALID_ARG, "null pooled-history ring for a coarse query scale");
-  }
-  if (coarse && (!workspace || workspace_bytes < p.workspace_bytes))
-    return fail(MSSA_ERR_WORKSPACE, "workspace smaller than mssa_plan_info.workspace_bytes");
-  std::vector<int32_t> slots;
-  const mssa_status s0 = append_native(p, k_win, v_win, k_ring, v_ring, ring_cap_frames, ring_head, ring_count,
-                                       slots, stream);
-  if (s0 != MSSA_OK) return s0;
-  // The head state's frames pooled to each coarse scale: window frames
-  // 0 .. F-1 of that group's context, which mssa_pool_kv wrote to the
-  // group's pooled block.
-  const int64_t row_bytes = p.ld * p.elem_bytes;
-  const char* ws = static_cast<const char*>(workspace);
-  const hipStream_t st = static_cast<hipStream_t>(stream);
-  for (size_t g = 0; g < p.groups.size(); ++g) {
-    const int32_t sc = p.groups[g].scale;
-    if (sc == 1) continue;
-    const int64_t tok_s = frame_tokens(p, sc);
-    const size_t fbytes = static_cast<size_t>(tok_s * row_bytes);
-    for (const mssa::SegRow& r : p.segs) {
-      if (r.q_scale != sc || r.kind != mssa::kWin || r.frame >= p.desc.frames_per_state) continue;
-      if (r.buffer != mssa::kBufPooled || r.n_tok != tok_s)
-        return fail(MSSA_ERR_UNSUPPORTED, "head frames are not pooled to a coarse scale in this plan");
-      const size_t slot = static_cast<size_t>(slots[r.frame]);
-      mssa_status s = check_device(
-          hipMemcpyAsync(static_cast<char*>(k_ring_pooled[g]) + slot * fbytes,
-                         ws + p.pooled_k_off[g] + r.tok_offset * row_bytes, fbytes, hipMemcpyDeviceToDevice, st),
-          "pooled history append (K)");
-      if (s != MSSA_OK) return s;
-      s = check_device(
-          hipMemcpyAsync(static_cast<char*>(v_ring_pooled[g]) + slot * fbytes,
-                         ws + p.pooled_v_off[g] + r.tok_offset * row_bytes, fbytes, hipMemcpyDeviceToDevice, st),
-          "pooled history append (V)");
-      if (s != MSSA_OK) return s;
+  return guarded("mssa_hist_append_ring", [&]() -> mssa_status {
+    if (!plan) return fail(MSSA_ERR_INVALID_ARG, "null argument");
+    const mssa::Plan& p = plan->p;
+    if (!p.hist_ring)
+      return fail(MSSA_ERR_UNSUPPORTED, "plan lacks MSSA_PLAN_POOLED_HIST_RING: use mssa_hist_append");
+    if (!k_ring_pooled || !v_ring_pooled) return fail(MSSA_ERR_INVALID_ARG, "null pooled ring array");
+    bool coarse = false;
+    for (size_t g = 0; g < p.groups.size(); ++g) {
+      if (p.groups[g].scale == 1) continue;
+      coarse = true;
+      if (!k_ring_pooled[g] || !v_ring_pooled[g])
+        return fail(MSSA_ERR_INVALID_ARG, "null pooled-history ring for a coarse query scale");
     }
-  }
-  return MSSA_OK;
+    if (coarse && (!workspace || workspace_bytes < p.workspace_bytes))
+      return fail(MSSA_ERR_WORKSPACE, "workspace smaller than mssa_plan_info.workspace_bytes");
+    std::vector<int32_t> slots;
+    const mssa_status s0 = append_native(p, k_win, v_win, k_ring, v_ring, ring_cap_frames, ring_head, ring_count,
+                                         slots, stream);
+    if (s0 != MSSA_OK) return s0;
+    // The head state's frames pooled to each coarse scale: window frames
+    // 0 .. F-1 of that group's context, which mssa_pool_kv wrote to the
+    // group's pooled block.
+    const int64_t row_bytes = p.ld * p.elem_bytes;
+    const char* ws = static_cast<const char*>(workspace);
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    for (size_t g = 0; g < p.groups.size(); ++g) {
+      const int32_t sc = p.groups[g].scale;
+      if (sc == 1) continue;
+      const int64_t tok_s = frame_tokens(p, sc);
+      const size_t fbytes = static_cast<size_t>(tok_s * row_bytes);
+      for (const mssa::SegRow& r : p.segs) {
+        if (r.q_scale != sc || r.kind != mssa::kWin || r.frame >= p.desc.frames_per_state) continue;
+        if (r.buffer != mssa::kBufPooled || r.n_tok != tok_s)
+          return fail(MSSA_ERR_UNSUPPORTED, "head frames are not pooled to a coarse scale in this plan");
+        const size_t slot = static_cast<size_t>(slots[r.frame]);
+        mssa_status s = check_device(
+            hipMemcpyAsync(static_cast<char*>(k_ring_pooled[g]) + slot * fbytes,
+                           ws + p.pooled_k_off[g] + r.tok_offset * row_bytes, fbytes, hipMemcpyDeviceToDevice, st),
+            "pooled history append (K)");
+        if (s != MSSA_OK) return s;
+        s = check_device(
+            hipMemcpyAsync(static_cast<char*>(v_ring_pooled[g]) + slot * fbytes,
+                           ws + p.pooled_v_off[g] + r.tok_offset * row_bytes, fbytes, hipMemcpyDeviceToDevice, st),
+            "pooled history append (V)");
+        if (s != MSSA_OK) return s;
+      }
+    }
+    return MSSA_OK;
+  });
 }
 
 mssa_status mssa_pool_hist_ring(mssa_plan plan, const void* k_ring, const void* v_ring, void* const* k_ring_pooled,
                                 void* const* v_ring_pooled, void* stream) {
-  if (!plan) return fail(MSSA_ERR_INVALID_ARG, "plan must be non-null");
-  const mssa::Plan& p = plan->p;
-  if (!p.hist_ring)
-    return fail(MSSA_ERR_UNSUPPORTED, "plan lacks MSSA_PLAN_POOLED_HIST_RING");
-  if (p.n_hist_tok == 0) return MSSA_OK;
-  if (!k_ring || !v_ring || !k_ring_pooled || !v_ring_pooled) return fail(MSSA_ERR_INVALID_ARG, "null argument");
-  if (!aligned16(k_ring) || !aligned16(v_ring)) return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
-  std::vector<mssa::PoolJobArgs> jobs;
-  for (size_t g = 0; g < p.groups.size(); ++g) {
-    const int32_t sc = p.groups[g].scale;
-    if (sc == 1) continue;
-    if (!k_ring_pooled[g] || !v_ring_pooled[g])
-      return fail(MSSA_ERR_INVALID_ARG, "null pooled-history ring for a coarse query scale");
-    if (!aligned16(k_ring_pooled[g]) || !aligned16(v_ring_pooled[g]))
-      return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
-    mssa::PoolJobArgs A{};
-    A.src_k = k_ring;
-    A.src_v = v_ring;
-    A.dst_k = k_ring_pooled[g];
-    A.dst_v = v_ring_pooled[g];
-    A.src_gh = p.desc.grid_h;
-    A.src_gw = p.desc.grid_w;
-    A.factor = sc;
-    A.dst_gh = (p.desc.grid_h + sc - 1) / sc;
-    A.dst_gw = (p.desc.grid_w + sc - 1) / sc;
-    A.n_frames = p.desc.hist_frames;
-    jobs.push_back(A);
-  }
-  return launch_pool_jobs(p, jobs, stream);
+  return guarded("mssa_pool_hist_ring", [&]() -> mssa_status {
+    if (!plan) return fail(MSSA_ERR_INVALID_ARG, "plan must be non-null");
+    const mssa::Plan& p = plan->p;
+    if (!p.hist_ring)
+      return fail(MSSA_ERR_UNSUPPORTED, "plan lacks MSSA_PLAN_POOLED_HIST_RING");
+    if (p.n_hist_tok == 0) return MSSA_OK;
+    if (!k_ring || !v_ring || !k_ring_pooled || !v_ring_pooled) return fail(MSSA_ERR_INVALID_ARG, "null argument");
+    if (!aligned16(k_ring) || !aligned16(v_ring)) return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
+    std::vector<mssa::PoolJobArgs> jobs;
+    for (size_t g = 0; g < p.groups.size(); ++g) {
+      const int32_t sc = p.groups[g].scale;
+      if (sc == 1) continue;
+      if (!k_ring_pooled[g] || !v_ring_pooled[g])
+        return fail(MSSA_ERR_INVALID_ARG, "null pooled-history ring for a coarse query scale");
+      if (!aligned16(k_ring_pooled[g]) || !aligned16(v_ring_pooled[g]))
+        return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
+      mssa::PoolJobArgs A{};
+      A.src_k = k_ring;
+      A.src_v = v_ring;
+      A.dst_k = k_ring_pooled[g];
+      A.dst_v = v_ring_pooled[g];
+      A.src_gh = p.desc.grid_h;
+      A.src_gw = p.desc.grid_w;
+      A.factor = sc;
+      A.dst_gh = (p.desc.grid_h + sc - 1) / sc;
+      A.dst_gw = (p.desc.grid_w + sc - 1) / sc;
+      A.n_frames = p.desc.hist_frames;
+      jobs.push_back(A);
+    }
+    return launch_pool_jobs(p, jobs, stream);
+  });
 }
 
 const char* mssa_status_string(mssa_status s) {
@@ -834,6 +873,6 @@ const char* mssa_status_string(mssa_status s) {
   return "MSSA_ERR_UNKNOWN";
 }
 
-const char* mssa_last_error(void) { return g_last_error.c_str(); }
+const char* mssa_last_error(void) { return g_last_error; }
 
 }  // extern "C"

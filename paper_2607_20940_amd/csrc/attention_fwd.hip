@@ -68,7 +68,7 @@ constexpr float kRescaleSum = 256.0f;  // 2^kRescaleLog2
 constexpr float kLn2 = 0.6931471805599453f;
 
 // ---------------------------------------------------------------------------
-// Persistent schedule.  An item is one (query scale, head, 128-query tile); its
+// Persistent schedule.  An item is one (query scale, head, 256-query tile); its
 // context is tiles_per_item 64-key tiles.  Items are numbered group by group
 // (longest context first), head-major, and laid out in a linear tile space of
 // total_tiles tiles.  Each of the n_ranges blocks first attends dp_rounds
@@ -279,18 +279,32 @@ __device__ __forceinline__ void attend_piece(const FwdArgs& a, const FwdGroupArg
   };
 
   // Direct transfers of the stream's current tile into K (is_v false) or V
-  // buffer buf; rows past the run's end arrive as zeros through the buffer
-  // range check.  Waited for (vmcnt) before the barrier that publishes it.
+  // buffer buf.  Waited for (vmcnt) before the barrier that publishes it.
+  // Chunks past D (head_dim 64) point past the range and arrive as zeros.
   const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds));
   auto issue = [&](const Stream& st, bool is_v, int buf) {
-    const uint32_t bytes = static_cast<uint32_t>(min(st.left, BN) - 1) * row_bytes + D * 2;
-    const i32x4 rs = rsrc_of(st.p, bytes);
     const uint32_t base = lds0 + (is_v ? 2 * KT * 2 : 0) + buf * KT * 2 + (wave & 3) * NDMA * 1024;
+    if (st.left >= BN) {
+      // A whole tile: every row lies inside the run, so the 4 i rows of
+      // transfer i ride in the scalar offset.
+      const i32x4 rs = rsrc_of(st.p, static_cast<uint32_t>(BN - 1) * row_bytes + D * 2);
 #pragma unroll
-    for (int i = 0; i < NDMA; ++i) {
-      // chunks past D (head_dim 64) read past the range: zeros
-      const uint32_t vo = (D / 8 >= 16 || (t_lc ^ i) < D / 8) ? (t_off ^ (i * 16)) : kPastEnd;
-      dma16_soff(rs, vo, i * 4 * row_bytes, __builtin_amdgcn_readfirstlane(base + i * 1024));
+      for (int i = 0; i < NDMA; ++i) {
+        const uint32_t vo = (D / 8 >= 16 || (t_lc ^ i) < D / 8) ? (t_off ^ (i * 16)) : kPastEnd;
+        dma16_soff(rs, vo, i * 4 * row_bytes, __builtin_amdgcn_readfirstlane(base + i * 1024));
+      }
+    } else {
+      // The run's last, partial tile: the whole row is in the lane's offset,
+      // which the buffer range check covers (the scalar offset is not
+      // checked), so rows past the run's end arrive as zeros and no byte
+      // past the run is read.
+      const i32x4 rs = rsrc_of(st.p, static_cast<uint32_t>(st.left - 1) * row_bytes + D * 2);
+#pragma unroll
+      for (int i = 0; i < NDMA; ++i) {
+        const uint32_t vo = (D / 8 >= 16 || (t_lc ^ i) < D / 8) ? (t_off ^ (i * 16)) + i * 4 * row_bytes
+                                                                : kPastEnd;
+        dma16(rs, vo, __builtin_amdgcn_readfirstlane(base + i * 1024));
+      }
     }
   };
 
@@ -564,7 +578,7 @@ template <int D>
 __global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void fwd_bf16_kernel(FwdArgs a) {
   using P = FwdTile<D>;
-  // [K buf0 | K buf1 | V buf0 | V buf1 | P blocks | tile maxima | row sums]
+  // [K buf0 | K buf1 | V buf0 | V buf1], 64 rows of 256 bytes each
   __shared__ __attribute__((aligned(16))) char lds[P::LDS_BYTES];
   const int rho = range_of_block(blockIdx.x, a.n_ranges);
   const int64_t S = range_begin(a, rho), E = range_begin(a, rho + 1);

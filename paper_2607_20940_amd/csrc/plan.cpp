@@ -23,7 +23,7 @@ int32_t ceil_div(int32_t a, int32_t b) { return (a + b - 1) / b; }
 
 }  // namespace
 
-mssa_status build_plan(const mssa_plan_desc& d, int slots, int ranges_override, Plan& p, std::string& err) {
+mssa_status build_plan(const mssa_plan_desc& d, int slots, int attention_blocks, Plan& p, std::string& err) {
   const int32_t T = d.num_states;
   if (T < 1 || T > MSSA_MAX_STATES) {
     err = "num_states must be in [1, " + std::to_string(MSSA_MAX_STATES) + "]";
@@ -239,7 +239,7 @@ mssa_status build_plan(const mssa_plan_desc& d, int slots, int ranges_override, 
     t_max = std::max(t_max, tiles);
   }
   if (slots <= 0) slots = 512;
-  int64_t ranges = ranges_override > 0 ? ranges_override : std::min<int64_t>(slots, n_items);
+  int64_t ranges = attention_blocks > 0 ? attention_blocks : std::min<int64_t>(slots, n_items);
   ranges = std::max<int64_t>(1, std::min<int64_t>(ranges, p.total_tiles));
   p.n_ranges = static_cast<int32_t>(ranges);
   // Whole-item rounds: as many as fit without any block exceeding its even

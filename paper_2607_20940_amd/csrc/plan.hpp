@@ -110,9 +110,10 @@ struct Plan {
 
 // Validates `d` and fills `p`.  `slots` is the number of attention blocks
 // the device keeps resident at once (<= 0: 512, two per CU of an MI355X);
-// `ranges_override` > 0 forces the number of tile ranges instead.  Returns
-// MSSA_OK or an error status with a message in `err`.
-mssa_status build_plan(const mssa_plan_desc& d, int slots, int ranges_override, Plan& p, std::string& err);
+// `attention_blocks` > 0 sets the number of persistent attention blocks
+// (tile ranges) instead.  Returns MSSA_OK or an error status with a message
+// in `err`.
+mssa_status build_plan(const mssa_plan_desc& d, int slots, int attention_blocks, Plan& p, std::string& err);
 
 // Flat int64 export of GRID / QGRP / SEG / TOTAL (layout in libmssa.h).
 std::vector<int64_t> export_tables(const Plan& p);

@@ -22,7 +22,7 @@ MSSA_PLAN_POOLED_HIST_RING = 1
 MSSA_PLAN_STRIDED_SUBSAMPLE = 2
 
 # Every symbol include/libmssa.h declares.
-EXPORTS = ("mssa_plan_create", "mssa_plan_destroy", "mssa_plan_query", "mssa_plan_tables",
+EXPORTS = ("mssa_plan_create", "mssa_plan_create_ex", "mssa_plan_destroy", "mssa_plan_query", "mssa_plan_tables",
            "mssa_pool_kv", "mssa_forward", "mssa_hist_append", "mssa_pool_hist_ring",
            "mssa_forward_ring", "mssa_hist_append_ring", "mssa_forward_lse", "mssa_backward_workspace_size",
            "mssa_backward", "mssa_tier_workspace_size", "mssa_patch_embed", "mssa_patch_unembed",
@@ -67,6 +67,7 @@ def _load():
     lib = ctypes.CDLL(LIB_PATH)
     P, V, I64 = ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64
     lib.mssa_plan_create.argtypes = [ctypes.POINTER(mssa_plan_desc), ctypes.POINTER(P)]
+    lib.mssa_plan_create_ex.argtypes = [ctypes.POINTER(mssa_plan_desc), ctypes.c_int32, ctypes.POINTER(P)]
     lib.mssa_plan_destroy.argtypes = [P]
     lib.mssa_plan_destroy.restype = None
     lib.mssa_plan_query.argtypes = [P, ctypes.POINTER(mssa_plan_info)]
@@ -92,7 +93,7 @@ def _load():
     lib.mssa_status_string.restype = ctypes.c_char_p
     lib.mssa_last_error.argtypes = []
     lib.mssa_last_error.restype = ctypes.c_char_p
-    for name in ("mssa_plan_create", "mssa_plan_query", "mssa_plan_tables", "mssa_pool_kv",
+    for name in ("mssa_plan_create", "mssa_plan_create_ex", "mssa_plan_query", "mssa_plan_tables", "mssa_pool_kv",
                  "mssa_forward", "mssa_hist_append", "mssa_pool_hist_ring", "mssa_forward_ring",
                  "mssa_hist_append_ring"):
         getattr(lib, name).restype = ctypes.c_int
@@ -204,6 +205,13 @@ def mssa_plan_create(desc):
     h = ctypes.c_void_p()
     d = make_desc(desc)
     _check(lib.mssa_plan_create(ctypes.byref(d), ctypes.byref(h)), "mssa_plan_create")
+    return Plan(h.value, desc)
+
+
+def mssa_plan_create_ex(desc, attention_blocks):
+    h = ctypes.c_void_p()
+    d = make_desc(desc)
+    _check(lib.mssa_plan_create_ex(ctypes.byref(d), int(attention_blocks), ctypes.byref(h)), "mssa_plan_create_ex")
     return Plan(h.value, desc)
 
 

@@ -9,6 +9,7 @@ import pytest
 import torch
 
 import oracle
+from paper_2607_20940_amd.inputs import to_f64
 from paper_2607_20940_amd.streaming import StreamingMSSA, init_inputs, window_inputs
 from paper_2607_20940_amd.workloads import STREAMING
 
@@ -225,3 +226,70 @@ def test_graph_pass_equals_eager(pooled_ring):
                     assert torch.equal(t.view(torch.int16), graph.v_pool[L][g].view(torch.int16)), (p, L, g)
     # 2 + 2 frames per pass: full after pass 1; 3 head positions, each replayed several times
     assert replays == 10 and len(graph._graphs) == 3
+
+
+def test_streaming_full_workload_sampled():
+    """The whole streaming workload: 30 stacked layers of the Wan-1.3B shape
+    over 64 rolling passes with pooled-history rings (history 6 -> 21 frames,
+    then FIFO).  Six (pass, layer) points, including the last layer of the
+    last pass, are compared with the oracle on two heads and every query row.
+    The oracle's history of a tracked layer is rebuilt on the host from that
+    layer's generated inputs (its initial history, then the head-state frames
+    each earlier pass emitted, FIFO-capped)."""
+    w = STREAMING
+    desc = w["layer"]
+    layers, passes, F, cap = w["layers"], w["passes"], desc["frames_per_state"], w["hist_cap_frames"]
+    points = {(0, 0), (4, 29), (5, 14), (20, 7), (47, 21), (63, 29)}
+    tracked = sorted({L for (_, L) in points})
+    heads = [0, 11]
+    st = StreamingMSSA(desc, layers, cap, dtype=w["dtype"], pooled_ring=True)
+    tok1 = st.tok1
+
+    def host(t):  # selected heads, bf16 bits on the host
+        return None if t is None else t[:, heads].contiguous().view(torch.int16).cpu().numpy()
+
+    def f64(a):
+        return None if a is None else to_f64(a.view(np.uint16), "bf16")
+
+    hist = {}
+    init_shapes = st.shapes(w["hist_start_frames"])
+    for L in range(layers):
+        x = init_inputs(w, L, init_shapes)
+        st.init_layer(L, x["k_sink"], x["v_sink"], x["k_hist"], x["v_hist"])
+        if L in tracked:
+            kh, vh = host(x["k_hist"]), host(x["v_hist"])
+            n0 = w["hist_start_frames"]
+            hist[L] = dict(sink=(host(x["k_sink"]), host(x["v_sink"])),
+                           k=[kh[i * tok1:(i + 1) * tok1] for i in range(n0)],
+                           v=[vh[i * tok1:(i + 1) * tok1] for i in range(n0)])
+    win_shapes = st.shapes(0)
+    outs = [torch.empty(win_shapes["q_win"], dtype=torch.bfloat16, device="cuda") for _ in range(layers)]
+    checked = 0
+    for p in range(passes):
+        wins = window_inputs(w, p, layers, win_shapes)
+        for L in range(layers):
+            st.layer_pass(L, wins[L]["q_win"], wins[L]["k_win"], wins[L]["v_win"], outs[L])
+            if L not in tracked:
+                continue
+            h = hist[L]
+            kw, vw = host(wins[L]["k_win"]), host(wins[L]["v_win"])
+            if (p, L) in points:
+                print(f"[stream-full] pass {p} layer {L} history {len(h['k'])} frames", flush=True)
+                d = dict(desc, hist_frames=len(h["k"]), num_heads=len(heads))
+                ref = oracle.mssa_attention(d, f64(host(wins[L]["q_win"])), f64(h["sink"][0]), f64(h["sink"][1]),
+                                            f64(np.concatenate(h["k"])), f64(np.concatenate(h["v"])),
+                                            f64(kw), f64(vw))
+                got = f64(host(outs[L]))
+                e = assert_close(got, ref, w["dtype"], f"pass {p} layer {L}")
+                print(f"[stream-full] ok {e}", flush=True)
+                checked += 1
+            for f in range(F):
+                h["k"].append(kw[f * tok1:(f + 1) * tok1])
+                h["v"].append(vw[f * tok1:(f + 1) * tok1])
+            del h["k"][:-cap]
+            del h["v"][:-cap]
+        if p % 16 == 0:
+            print(f"[stream-full] pass {p} done", flush=True)
+    torch.cuda.synchronize()
+    assert checked == len(points)
+    assert all(r.count == cap for r in st.ring)

@@ -156,6 +156,27 @@ def test_tables_wan13b_context_sizes():
     assert (win[:, 4] == np.maximum(win[:, 0], win[:, 3])).all()
 
 
+def test_tables_wan13b_seg_rows_by_hand():
+    """Every SEG row of the Wan-1.3B-shaped layer written out by hand from
+    Eq. 3 and Eq. 4: 1560 tokens per native frame (30 x 52), 390 per frame at
+    scale 2 (15 x 26); context order sink (3 frames, native), history (6
+    frames, pooled by the query scale), window frames 0..14 (states 1-2 native,
+    states 3-5 at scale 2), kv_begin the running token offset."""
+    t = oracle.tables(WORKLOADS["wan13b_layer"]["desc"])
+    # (q_scale, kind, frame, src_scale, eff_scale, factor, n_tok, kv_begin)
+    s1 = ([(1, 0, f, 1, 1, 1, 1560, 1560 * f) for f in range(3)]
+          + [(1, 1, f, 1, 1, 1, 1560, 4680 + 1560 * f) for f in range(6)]
+          + [(1, 2, w, 1, 1, 1, 1560, 14040 + 1560 * w) for w in range(6)]
+          + [(1, 2, w, 2, 2, 1, 390, 23400 + 390 * (w - 6)) for w in range(6, 15)])
+    s2 = ([(2, 0, f, 1, 1, 1, 1560, 1560 * f) for f in range(3)]
+          + [(2, 1, f, 1, 2, 2, 390, 4680 + 390 * f) for f in range(6)]
+          + [(2, 2, w, 1, 2, 2, 390, 7020 + 390 * w) for w in range(6)]
+          + [(2, 2, w, 2, 2, 1, 390, 9360 + 390 * (w - 6)) for w in range(6, 15)])
+    assert [tuple(r) for r in t["SEG"].tolist()] == s1 + s2
+    # last row ends at n_kv: 23400 + 9 * 390 = 26910 and 9360 + 9 * 390 = 12870
+    assert t["QGRP"][:, 3].tolist() == [23400 + 9 * 390, 9360 + 9 * 390]
+
+
 def test_ragged_grid_uses_ceil():
     desc = WORKLOADS["wan13b_longhist"]["desc"]
     assert oracle.grid(desc, 4) == (8, 13)
