@@ -38,6 +38,76 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+class ClockSampler:
+    """The GPU's current shader clock, sampled from a host thread while named
+    sections of the benchmark run: the starred line of the amdgpu driver's
+    pp_dpm_sclk ("S: <MHz> *" is the measured current clock).  The sustained
+    clock under a long MFMA load is set by power, not by the 2.4 GHz peak the
+    roofline's peak assumes, so the % of peak depends on it."""
+
+    def __init__(self, period_s=0.01):
+        import glob
+        import threading
+
+        paths = sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk"))
+        self.path = paths[0] if paths else None
+        self.period = period_s
+        self.samples = {}
+        self.current = None
+        self._stop = threading.Event()
+        self._thread = threading.Thread(target=self._loop, daemon=True)
+
+    def _read(self):
+        try:
+            with open(self.path) as f:
+                for line in f:
+                    if line.rstrip().endswith("*"):
+                        return float(line.split(":", 1)[1].strip().split("M")[0])
+        except (OSError, ValueError, IndexError):
+            return None
+        return None
+
+    def _loop(self):
+        while not self._stop.is_set():
+            name = self.current
+            if name is not None:
+                mhz = self._read()
+                if mhz is not None:
+                    self.samples.setdefault(name, []).append(mhz)
+            self._stop.wait(self.period)
+
+    def start(self):
+        if self.path:
+            self._thread.start()
+
+    def stop(self):
+        self._stop.set()
+        if self._thread.is_alive():
+            self._thread.join()
+
+    def section(self, name):
+        import contextlib
+
+        @contextlib.contextmanager
+        def cm():
+            self.current = name
+            try:
+                yield
+            finally:
+                self.current = None
+        return cm()
+
+    def summary(self):
+        if not self.path:
+            return {"source": None, "note": "no pp_dpm_sclk readable on this host"}
+        out = {"source": self.path, "period_ms": self.period * 1e3}
+        for name, v in self.samples.items():
+            a = np.array(v)
+            out[name] = {"median": float(np.median(a)), "p10": float(np.percentile(a, 10)),
+                         "p90": float(np.percentile(a, 90)), "samples": int(a.size)}
+        return out
+
+
 def kernel_source_hash():
     with open(FWD_SOURCE, "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()[:16]
@@ -66,7 +136,8 @@ def read_traffic(workload):
 def cpu_baseline(w, x, info, budget_s):
     """Time the fp64 oracle (as it stands) on the host: whole heads of the
     workload (pool + attention for every query), one at a time, until the
-    time budget is used.  Returns the oracle's effective TFLOP/s."""
+    time budget is used.  Returns the oracle's effective TFLOP/s and its
+    outputs {head: [n_q, head_dim] float64}."""
     import oracle
     from paper_2607_20940_amd.inputs import to_f64
 
@@ -79,13 +150,15 @@ def cpu_baseline(w, x, info, budget_s):
     nh = desc["num_heads"]
     flops_per_head = info["flops_alg"] / nh
     done, t_total = 0, 0.0
+    refs = {}
     for h in range(nh):
         xh = {k: (None if v is None else to_f64(v[:, [h]], w["dtype"])) for k, v in x.items()}
         d1 = dict(desc, num_heads=1)
         t0 = time.perf_counter()
-        oracle.mssa_attention(d1, xh["q_win"], xh["k_sink"], xh["v_sink"], xh["k_hist"],
-                              xh["v_hist"], xh["k_win"], xh["v_win"])
+        o = oracle.mssa_attention(d1, xh["q_win"], xh["k_sink"], xh["v_sink"], xh["k_hist"],
+                                  xh["v_hist"], xh["k_win"], xh["v_win"])
         t_total += time.perf_counter() - t0
+        refs[h] = o[:, 0]
         done += 1
         log(f"cpu oracle head {h}: {t_total:.1f} s cumulative")
         if t_total >= budget_s:
@@ -109,13 +182,40 @@ def cpu_baseline(w, x, info, budget_s):
         "sample": f"{done} of {nh} heads of {w['name']} (pool + attention, all {info['n_q']} queries), "
                   f"fp64 numpy, {t_total:.1f} s",
         "ms_per_pass_extrapolated": 1e3 * t_total / done * nh,
-    }
+    }, refs
+
+
+# Parity bounds of the workload (bf16 outputs): absolute max / mean error,
+# plus the relative guard (rms error against the reference rms, max error
+# against the reference's largest magnitude) that rejects near-zero outputs.
+PARITY_TOL = {"max_abs": 2e-2, "mean_abs": 2e-3, "rel_rms": 1e-2, "rel_max": 5e-2}
+
+
+def parity_vs_oracle(out, refs, w):
+    """Every element of the GPU output of the heads the oracle computed
+    against the oracle's float64 output."""
+    import torch
+
+    from paper_2607_20940_amd.inputs import to_f64
+
+    heads = sorted(refs)
+    got = to_f64(out[:, heads].contiguous().view(torch.int16).cpu().numpy().view(np.uint16), "bf16")
+    ref = np.stack([refs[h] for h in heads], axis=1)
+    err = np.abs(got - ref)
+    e = {"max_abs": float(err.max()), "mean_abs": float(err.mean()),
+         "rel_rms": float(np.sqrt((err ** 2).mean()) / np.sqrt((ref ** 2).mean())),
+         "rel_max": float(err.max() / np.abs(ref).max())}
+    return {**{k: float(f"{v:.4g}") for k, v in e.items()},
+            "within_tolerance": bool(np.isfinite(got).all() and all(e[k] <= PARITY_TOL[k] for k in PARITY_TOL)),
+            "tolerance": PARITY_TOL, "heads": f"{len(heads)} of {w['desc']['num_heads']}",
+            "elements": int(got.size), "against": "fp64 oracle, every query row"}
 
 
 def bench_streaming(args):
     """Steady-state streaming: stacked layers over rolling passes (pool +
     forward + history append per layer and pass); window inputs of a pass
-    are generated on the device before that pass is timed."""
+    are generated on the device before that pass is timed.  Returns the
+    result line."""
     import torch
 
     from paper_2607_20940_amd.streaming import StreamingMSSA, init_inputs, window_inputs
@@ -188,7 +288,7 @@ def bench_streaming(args):
         "steady_state_pass_count": len(steady),
         "effective_tflops_steady": round(sum(pass_flops[i] for i in steady) / (st_ms * 1e-3) / 1e12, 2),
     }
-    print(json.dumps(result), flush=True)
+    return result
 
 
 def bench_training(args):
@@ -266,7 +366,7 @@ def bench_training(args):
         "backward_tflops": round(2.5 * F / (bwd_ms.mean() * 1e-3) / 1e12, 2),
         "backward_pct_of_bf16_peak": round(100 * 2.5 * F / (bwd_ms.mean() * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 2),
     }
-    print(json.dumps(result), flush=True)
+    return result
 
 
 def bench_tiers(args):
@@ -348,7 +448,10 @@ def main():
     ap.add_argument("--workload", default="wan13b_layer")
     ap.add_argument("--input-sets", type=int, default=4,
                     help="distinct device copies of the inputs rotated between steps")
-    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time")
+    ap.add_argument("--cpu-budget", type=float, default=30.0,
+                    help="seconds of oracle time (whole heads; the 1.3B-shaped layer needs ~11 s for all)")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="only the named layer workload (skip the other layers, streaming and training)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--layers", type=int, default=0, help="streaming: layers (default 30)")
     ap.add_argument("--passes", type=int, default=0, help="streaming: rolling passes (default 64)")
@@ -375,10 +478,10 @@ def main():
         sys.exit(2)
 
     if args.workload == "streaming":
-        bench_streaming(args)
+        print(json.dumps(bench_streaming(args)), flush=True)
         return
     if args.training:
-        bench_training(args)
+        print(json.dumps(bench_training(args)), flush=True)
         return
     if args.tiers:
         bench_tiers(args)
@@ -394,13 +497,55 @@ def main():
         print(json.dumps({"copy_calibration_bytes": n * 4, "copies": 5}), flush=True)
         return
 
+    clock = ClockSampler()
+    clock.start()
+    result, out0, x, w, info = bench_layer(args, args.workload, host_inputs=True, clock=clock)
+    if not args.no_cpu_baseline:
+        base, ref = cpu_baseline(w, x, info, args.cpu_budget)
+        result["cpu_baseline"] = base
+        result["parity"] = parity_vs_oracle(out0, ref, w)
+        log(f"parity against the oracle: {result['parity']}")
+    if args.workload == "wan13b_layer" and args.resample == "mean" and not args.no_extras:
+        # the other layer workloads, the stacked-layer streaming workload and
+        # the training step, each timed the same way on this GPU
+        result["other_layers"] = {}
+        for name in ("wan13b_longhist", "wan14b_720p"):
+            r, _, _, _, _ = bench_layer(args, name, host_inputs=False, clock=clock)
+            result["other_layers"][name] = {
+                k: r[k] for k in ("ms_per_step", "value", "pct_of_bf16_peak", "forward_ms", "forward_ms_median",
+                                  "forward_ms_p10_p90", "pool_ms")}
+            result["other_layers"][name]["forward_frac_of_bf16_peak"] = r["roofline"]["frac"]
+            result["other_layers"][name]["pool_gbps"] = r["pool"]["achieved"]
+            result["other_layers"][name]["config"] = r["config"]
+        sargs = argparse.Namespace(**vars(args))
+        sargs.pooled_ring, sargs.graph = True, False
+        with clock.section("streaming"):
+            s_res = bench_streaming(sargs)
+        result["streaming"] = {k: s_res[k] for k in ("value", "unit", "all_passes_ms_per_frame", "steady_state_passes",
+                                                     "effective_tflops_steady", "config")}
+        targs = argparse.Namespace(**vars(args))
+        targs.workload = "wan13b_layer"
+        with clock.section("training"):
+            t_res = bench_training(targs)
+        result["training"] = {k: t_res[k] for k in ("ms_per_step", "forward_pool_ms", "backward_ms", "backward_ms_p10_p90",
+                                                    "backward_tflops", "backward_pct_of_bf16_peak", "value", "unit")}
+    clock.stop()
+    result["sclk_mhz"] = clock.summary()
+    print(json.dumps(result), flush=True)
+
+
+def bench_layer(args, workload, host_inputs, clock):
+    """Time K passes (mssa_pool_kv + mssa_forward) of one layer workload.
+    host_inputs: the seeded host inputs the oracle also reads (returned);
+    else device-drawn inputs of the same distribution.  Returns (result
+    line, output of input set 0, host inputs or None, workload, plan info)."""
     import torch
 
     from paper_2607_20940_amd import mssa
-    from paper_2607_20940_amd.inputs import make_inputs
+    from paper_2607_20940_amd.inputs import make_inputs, make_inputs_device
     from paper_2607_20940_amd.workloads import WORKLOADS, input_shapes
 
-    w = dict(WORKLOADS[args.workload], name=args.workload)
+    w = dict(WORKLOADS[workload], name=workload)
     if args.resample != "mean":
         w["desc"] = dict(w["desc"], resample=args.resample)
     desc = w["desc"]
@@ -408,10 +553,8 @@ def main():
     plan = mssa.mssa_plan_create(dict(desc, dtype=dtype))
     info = plan.info()
     shapes = input_shapes(desc, info["n_q"], info["n_sink_tok"], info["n_hist_tok"])
-    log(f"workload {args.workload}: n_q={info['n_q']} n_kv={info['n_kv']} flops={info['flops_alg']:.4e}")
+    log(f"workload {workload}: n_q={info['n_q']} n_kv={info['n_kv']} flops={info['flops_alg']:.4e}")
     t0 = time.perf_counter()
-    x = make_inputs(shapes, w["seed"], w["amplitude"], dtype)
-    log(f"inputs generated in {time.perf_counter() - t0:.1f} s")
 
     def dev(a):
         if a is None:
@@ -420,7 +563,13 @@ def main():
             return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
         return torch.from_numpy(a).cuda()
 
-    base = {k: dev(v) for k, v in x.items()}
+    if host_inputs:
+        x = make_inputs(shapes, w["seed"], w["amplitude"], dtype)
+        base = {k: dev(v) for k, v in x.items()}
+    else:
+        x = None
+        base = make_inputs_device(shapes, w["seed"], w["amplitude"], dtype)
+    log(f"inputs generated in {time.perf_counter() - t0:.1f} s")
     sets = [base] + [{k: (None if v is None else v.clone()) for k, v in base.items()}
                      for _ in range(args.input_sets - 1)]
     ws = [torch.empty(max(256, info["workspace_bytes"]), dtype=torch.uint8, device="cuda")
@@ -448,11 +597,12 @@ def main():
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
-    start.record(stream)
-    for i in range(args.steps):
-        step(i, evs[i])
-    end.record(stream)
-    torch.cuda.synchronize()
+    with clock.section(workload):
+        start.record(stream)
+        for i in range(args.steps):
+            step(i, evs[i])
+        end.record(stream)
+        torch.cuda.synchronize()
     total_ms = start.elapsed_time(end)
     pool_ms = np.array([e[0].elapsed_time(e[1]) for e in evs])
     fwd_ms = np.array([e[1].elapsed_time(e[2]) for e in evs])
@@ -480,13 +630,14 @@ def main():
         "dtype": dtype,
         "data": "synthetic",
         "config": {
-            "workload": args.workload,
+            "workload": workload,
             "heads": desc["num_heads"], "head_dim": desc["head_dim"],
             "grid": f"{desc['grid_h']}x{desc['grid_w']}", "schedule": desc["scales"],
             "sink_frames": desc["sink_frames"], "hist_frames": desc["hist_frames"],
             "states": desc["num_states"], "frames_per_state": desc["frames_per_state"],
             "n_q": info["n_q"], "n_kv": info["n_kv"], "flops_alg": flops,
             "input_sets_rotated": len(sets), "resample": args.resample,
+            "inputs": "seeded host draws" if host_inputs else "device draws",
         },
         "pct_of_bf16_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
         "forward_ms": round(float(fwd_ms.mean()), 4),
@@ -501,11 +652,11 @@ def main():
         "roofline": {"kernel": "mssa_forward (fwd_bf16_kernel + combine_kernel)" if dtype == "bf16" else "mssa_forward (fwd_f32_kernel)",
                      "bound": "mfma", "achieved": round(fwd_tflops, 2), "peak": peak,
                      "unit": "TFLOP/s", "frac": round(fwd_tflops / peak, 4),
-                     "traffic": read_traffic(args.workload)},
+                     "traffic": read_traffic(workload)},
     }
-    if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(w, x, info, args.cpu_budget)
-    print(json.dumps(result), flush=True)
+    out0 = outs[0]
+    del sets, ws
+    return result, out0, x, w, info
 
 
 if __name__ == "__main__":
