@@ -188,6 +188,33 @@ mssa_status mssa_forward(mssa_plan plan, const void* q_win, const void* k_sink,
                          const void* k_win, const void* v_win, const void* workspace,
                          int64_t workspace_bytes, void* out, void* stream);
 
+/* ------------------------------------------------------ no allocation
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): pool +
+ * forward of one pass with the library's own scratch as the workspace.
+ *
+ * mssa_attention_noalloc(plan, ...) enqueues exactly what mssa_pool_kv
+ * followed by mssa_forward enqueue (the same kernels, bitwise the same
+ * output), with the workspace in a device array of
+ * MSSA_NOALLOC_SCRATCH_BYTES that the library holds on every GPU it runs on
+ * until the process ends.  It calls no device allocation routine.  The
+ * scratch of the current device is found on the first call on that device;
+ * `stream` must belong to the current device.  Every call on a GPU shares
+ * that GPU's scratch, which keeps the last call's contents (nothing in it
+ * needs to start at zero): calls that overlap on one GPU (two streams, or
+ * host threads) race and must be ordered by the caller.
+ *   arguments  as for mssa_forward, without the workspace
+ * MSSA_ERR_WORKSPACE if the plan's workspace_bytes exceed
+ * MSSA_NOALLOC_SCRATCH_BYTES (e.g. the 40-head 720p layer);
+ * MSSA_ERR_UNSUPPORTED for plans with MSSA_PLAN_POOLED_HIST_RING; otherwise
+ * the errors of mssa_pool_kv and mssa_forward, all checked before anything
+ * is enqueued. */
+#define MSSA_NOALLOC_SCRATCH_BYTES (256ll << 20)
+
+mssa_status mssa_attention_noalloc(mssa_plan plan, const void* q_win, const void* k_sink, const void* v_sink,
+                                   const void* k_hist, const void* v_hist, const void* k_win, const void* v_win,
+                                   void* out, void* stream);
+
 /* ----------------------------------------------------------------- training
  * The window is trained through its attention (Sec. 3.1; Alg. 1 updates the
  * model by gradient steps on the rolling window), so the backward of Eq. 4:

@@ -14,6 +14,7 @@
 
 #include "../../include/libmssa.h"
 #include "kernels.hpp"
+#include "noalloc.hpp"
 #include "plan.hpp"
 
 struct mssa_plan_s {
@@ -127,6 +128,50 @@ mssa_status launch_pool_jobs(const mssa::Plan& p, std::vector<mssa::PoolJobArgs>
   return MSSA_OK;
 }
 
+// Argument checks of mssa_pool_kv (nothing is enqueued).
+mssa_status pool_check(const mssa::Plan& p, const void* k_hist, const void* v_hist, const void* k_win,
+                       const void* v_win, const void* workspace, int64_t workspace_bytes) {
+  if (p.pool_jobs.empty()) return MSSA_OK;
+  if (!k_win || !v_win) return fail(MSSA_ERR_INVALID_ARG, "k_win and v_win must be non-null");
+  bool reads_hist = false;
+  for (const mssa::PoolJob& J : p.pool_jobs) reads_hist |= J.buffer == mssa::kBufHist;
+  if (reads_hist && (!k_hist || !v_hist))
+    return fail(MSSA_ERR_INVALID_ARG, "k_hist and v_hist must be non-null when history is pooled");
+  if (!workspace || workspace_bytes < p.workspace_bytes)
+    return fail(MSSA_ERR_WORKSPACE, "workspace smaller than mssa_plan_info.workspace_bytes");
+  if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
+    return fail(MSSA_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+  if (!aligned16(k_win) || !aligned16(v_win) || (k_hist && !aligned16(k_hist)) || (v_hist && !aligned16(v_hist)))
+    return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
+  return MSSA_OK;
+}
+
+// The pool jobs of a checked mssa_pool_kv call, enqueued on `stream`.
+mssa_status pool_launch(const mssa::Plan& p, const void* k_hist, const void* v_hist, const void* k_win,
+                        const void* v_win, void* workspace, void* stream) {
+  if (p.pool_jobs.empty()) return MSSA_OK;
+  const int64_t row_bytes = p.ld * p.elem_bytes;
+  auto* ws = static_cast<char*>(workspace);
+  std::vector<mssa::PoolJobArgs> jobs;
+  for (const mssa::PoolJob& J : p.pool_jobs) {
+    mssa::PoolJobArgs A{};
+    const char* sk = static_cast<const char*>(J.buffer == mssa::kBufHist ? k_hist : k_win);
+    const char* sv = static_cast<const char*>(J.buffer == mssa::kBufHist ? v_hist : v_win);
+    A.src_k = sk + J.src_tok * row_bytes;
+    A.src_v = sv + J.src_tok * row_bytes;
+    A.dst_k = ws + p.pooled_k_off[J.group] + J.dst_tok * row_bytes;
+    A.dst_v = ws + p.pooled_v_off[J.group] + J.dst_tok * row_bytes;
+    A.src_gh = J.src_gh;
+    A.src_gw = J.src_gw;
+    A.dst_gh = J.dst_gh;
+    A.dst_gw = J.dst_gw;
+    A.factor = J.factor;
+    A.n_frames = J.n_frames;
+    jobs.push_back(A);
+  }
+  return launch_pool_jobs(p, jobs, stream);
+}
+
 // Ring slots (FIFO once full) that F appended frames take, with the head and
 // count after them; false for an inconsistent head / count.
 bool ring_slots(int32_t cap, int32_t F, int32_t* head, int32_t* count, std::vector<int32_t>& slots) {
@@ -225,10 +270,11 @@ void run_pointers(const mssa::Plan& p, int g, const mssa::Run& R, const KvSource
   *vp = vb + R.tok_offset * row_bytes;
 }
 
-mssa_status forward_impl(const mssa::Plan& p, const void* q_win, const void* k_sink, const void* v_sink,
-                         const void* k_hist, const void* v_hist, const void* const* k_hist_pooled,
-                         const void* const* v_hist_pooled, const void* k_win, const void* v_win,
-                         const void* workspace, int64_t workspace_bytes, void* out, float* lse, void* stream) {
+// Argument checks of forward_impl (nothing is enqueued).
+mssa_status forward_check(const mssa::Plan& p, const void* q_win, const void* k_sink, const void* v_sink,
+                          const void* k_hist, const void* v_hist, const void* const* k_hist_pooled,
+                          const void* const* v_hist_pooled, const void* k_win, const void* v_win,
+                          const void* workspace, int64_t workspace_bytes, const void* out, const float* lse) {
   if (!q_win || !k_win || !v_win || !out)
     return fail(MSSA_ERR_INVALID_ARG, "q_win, k_win, v_win and out must be non-null");
   if (p.n_sink_tok > 0 && (!k_sink || !v_sink))
@@ -237,7 +283,7 @@ mssa_status forward_impl(const mssa::Plan& p, const void* q_win, const void* k_s
     return fail(MSSA_ERR_INVALID_ARG, "k_hist and v_hist must be non-null when hist_frames > 0");
   if (p.workspace_bytes > 0 && (!workspace || workspace_bytes < p.workspace_bytes))
     return fail(MSSA_ERR_WORKSPACE, "workspace smaller than mssa_plan_info.workspace_bytes");
-  for (const void* t : {q_win, k_sink, v_sink, k_hist, v_hist, k_win, v_win, static_cast<const void*>(out)})
+  for (const void* t : {q_win, k_sink, v_sink, k_hist, v_hist, k_win, v_win, out})
     if (t && !aligned16(t)) return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
   if (out == q_win || out == k_win || out == v_win)
     return fail(MSSA_ERR_INVALID_ARG, "out must not alias an input");
@@ -253,7 +299,16 @@ mssa_status forward_impl(const mssa::Plan& p, const void* q_win, const void* k_s
       if (!aligned16(kp) || !aligned16(vp)) return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
     }
   }
+  return MSSA_OK;
+}
 
+mssa_status forward_impl(const mssa::Plan& p, const void* q_win, const void* k_sink, const void* v_sink,
+                         const void* k_hist, const void* v_hist, const void* const* k_hist_pooled,
+                         const void* const* v_hist_pooled, const void* k_win, const void* v_win,
+                         const void* workspace, int64_t workspace_bytes, void* out, float* lse, void* stream) {
+  const mssa_status chk = forward_check(p, q_win, k_sink, v_sink, k_hist, v_hist, k_hist_pooled, v_hist_pooled,
+                                        k_win, v_win, workspace, workspace_bytes, out, lse);
+  if (chk != MSSA_OK) return chk;
   const bool bf16 = p.desc.dtype == MSSA_BF16;
   const int bm = bf16 ? mssa::kFwdBM : mssa::kFwdF32BM;
   mssa::FwdArgs a{};
@@ -365,40 +420,9 @@ mssa_status mssa_pool_kv(mssa_plan plan, const void* k_hist, const void* v_hist,
                          const void* v_win, void* workspace, int64_t workspace_bytes, void* stream) {
   return guarded("mssa_pool_kv", [&]() -> mssa_status {
     if (!plan) return fail(MSSA_ERR_INVALID_ARG, "plan must be non-null");
-    const mssa::Plan& p = plan->p;
-    if (p.pool_jobs.empty()) return MSSA_OK;
-    if (!k_win || !v_win) return fail(MSSA_ERR_INVALID_ARG, "k_win and v_win must be non-null");
-    bool reads_hist = false;
-    for (const mssa::PoolJob& J : p.pool_jobs) reads_hist |= J.buffer == mssa::kBufHist;
-    if (reads_hist && (!k_hist || !v_hist))
-      return fail(MSSA_ERR_INVALID_ARG, "k_hist and v_hist must be non-null when history is pooled");
-    if (!workspace || workspace_bytes < p.workspace_bytes)
-      return fail(MSSA_ERR_WORKSPACE, "workspace smaller than mssa_plan_info.workspace_bytes");
-    if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
-      return fail(MSSA_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
-    if (!aligned16(k_win) || !aligned16(v_win) || (k_hist && !aligned16(k_hist)) || (v_hist && !aligned16(v_hist)))
-      return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
-
-    const int64_t row_bytes = p.ld * p.elem_bytes;
-    auto* ws = static_cast<char*>(workspace);
-    std::vector<mssa::PoolJobArgs> jobs;
-    for (const mssa::PoolJob& J : p.pool_jobs) {
-      mssa::PoolJobArgs A{};
-      const char* sk = static_cast<const char*>(J.buffer == mssa::kBufHist ? k_hist : k_win);
-      const char* sv = static_cast<const char*>(J.buffer == mssa::kBufHist ? v_hist : v_win);
-      A.src_k = sk + J.src_tok * row_bytes;
-      A.src_v = sv + J.src_tok * row_bytes;
-      A.dst_k = ws + p.pooled_k_off[J.group] + J.dst_tok * row_bytes;
-      A.dst_v = ws + p.pooled_v_off[J.group] + J.dst_tok * row_bytes;
-      A.src_gh = J.src_gh;
-      A.src_gw = J.src_gw;
-      A.dst_gh = J.dst_gh;
-      A.dst_gw = J.dst_gw;
-      A.factor = J.factor;
-      A.n_frames = J.n_frames;
-      jobs.push_back(A);
-    }
-    return launch_pool_jobs(p, jobs, stream);
+    const mssa_status s = pool_check(plan->p, k_hist, v_hist, k_win, v_win, workspace, workspace_bytes);
+    if (s != MSSA_OK) return s;
+    return pool_launch(plan->p, k_hist, v_hist, k_win, v_win, workspace, stream);
   });
 }
 
@@ -437,6 +461,32 @@ mssa_status mssa_forward_lse(mssa_plan plan, const void* q_win, const void* k_si
     if (!lse) return fail(MSSA_ERR_INVALID_ARG, "lse must be non-null");
     return forward_impl(plan->p, q_win, k_sink, v_sink, k_hist, v_hist, nullptr, nullptr, k_win, v_win, workspace,
                         workspace_bytes, out, lse, stream);
+  });
+}
+
+mssa_status mssa_attention_noalloc(mssa_plan plan, const void* q_win, const void* k_sink, const void* v_sink,
+                                   const void* k_hist, const void* v_hist, const void* k_win, const void* v_win,
+                                   void* out, void* stream) {
+  return guarded("mssa_attention_noalloc", [&]() -> mssa_status {
+    if (!plan) return fail(MSSA_ERR_INVALID_ARG, "plan must be non-null");
+    const mssa::Plan& p = plan->p;
+    if (p.hist_ring)
+      return fail(MSSA_ERR_UNSUPPORTED, "plan has MSSA_PLAN_POOLED_HIST_RING: use mssa_forward_ring");
+    if (p.workspace_bytes > mssa::kScratchBytes)
+      return fail(MSSA_ERR_WORKSPACE, "the plan's workspace_bytes exceed MSSA_NOALLOC_SCRATCH_BYTES");
+    void* ws = nullptr;
+    mssa_status s = check_device(mssa::scratch_address(&ws), "library scratch lookup");
+    if (s != MSSA_OK) return s;
+    const int64_t wsb = mssa::kScratchBytes;
+    s = pool_check(p, k_hist, v_hist, k_win, v_win, ws, wsb);
+    if (s != MSSA_OK) return s;
+    s = forward_check(p, q_win, k_sink, v_sink, k_hist, v_hist, nullptr, nullptr, k_win, v_win, ws, wsb, out,
+                      nullptr);
+    if (s != MSSA_OK) return s;
+    s = pool_launch(p, k_hist, v_hist, k_win, v_win, ws, stream);
+    if (s != MSSA_OK) return s;
+    return forward_impl(p, q_win, k_sink, v_sink, k_hist, v_hist, nullptr, nullptr, k_win, v_win, ws, wsb, out,
+                        nullptr, stream);
   });
 }
 

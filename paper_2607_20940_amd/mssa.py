@@ -26,7 +26,9 @@ EXPORTS = ("mssa_plan_create", "mssa_plan_create_ex", "mssa_plan_destroy", "mssa
            "mssa_pool_kv", "mssa_forward", "mssa_hist_append", "mssa_pool_hist_ring",
            "mssa_forward_ring", "mssa_hist_append_ring", "mssa_forward_lse", "mssa_backward_workspace_size",
            "mssa_backward", "mssa_tier_workspace_size", "mssa_patch_embed", "mssa_patch_unembed",
-           "mssa_qkv_project", "mssa_status_string", "mssa_last_error")
+           "mssa_qkv_project", "mssa_attention_noalloc", "mssa_status_string", "mssa_last_error")
+
+MSSA_NOALLOC_SCRATCH_BYTES = 256 << 20
 
 
 class mssa_tier_desc(ctypes.Structure):
@@ -82,6 +84,7 @@ def _load():
     lib.mssa_hist_append_ring.argtypes = [P, V, V, V, I64, V, V, PP, PP, ctypes.c_int32,
                                           ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32), V]
     lib.mssa_forward_lse.argtypes = [P, V, V, V, V, V, V, V, V, I64, V, V, V]
+    lib.mssa_attention_noalloc.argtypes = [P, V, V, V, V, V, V, V, V, V]
     lib.mssa_backward_workspace_size.argtypes = [P, ctypes.POINTER(I64)]
     lib.mssa_backward.argtypes = [P, V, V, V, V, V, V, V, V, V, V, V, I64, V, V, V, V, V, V, V, V]
     TD = ctypes.POINTER(mssa_tier_desc)
@@ -267,6 +270,12 @@ def mssa_forward_lse(plan, q_win, k_sink, v_sink, k_hist, v_hist, k_win, v_win, 
     _check(lib.mssa_forward_lse(plan.handle, _ptr(q_win), _ptr(k_sink), _ptr(v_sink), _ptr(k_hist),
                                 _ptr(v_hist), _ptr(k_win), _ptr(v_win), _ptr(workspace), wb,
                                 _ptr(out), _ptr(lse), _stream(stream)), "mssa_forward_lse")
+
+
+def mssa_attention_noalloc(plan, q_win, k_sink, v_sink, k_hist, v_hist, k_win, v_win, out, stream=None):
+    _check(lib.mssa_attention_noalloc(plan.handle, _ptr(q_win), _ptr(k_sink), _ptr(v_sink), _ptr(k_hist),
+                                      _ptr(v_hist), _ptr(k_win), _ptr(v_win), _ptr(out), _stream(stream)),
+           "mssa_attention_noalloc")
 
 
 def mssa_backward_workspace_size(plan):
