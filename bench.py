@@ -218,7 +218,7 @@ def bench_streaming(args):
     result line."""
     import torch
 
-    from paper_2607_20940_amd.streaming import StreamingMSSA, init_inputs, window_inputs
+    from paper_2607_20940_amd.streaming import StreamingMSSA, init_inputs, window_inputs, window_inputs_head_ring
     from paper_2607_20940_amd.workloads import STREAMING
 
     w = STREAMING
@@ -226,7 +226,9 @@ def bench_streaming(args):
     passes = args.passes or w["passes"]
     desc = w["layer"]
     F = desc["frames_per_state"]
-    st = StreamingMSSA(desc, layers, w["hist_cap_frames"], dtype=w["dtype"], pooled_ring=args.pooled_ring)
+    head_in_ring = getattr(args, "head_in_ring", False)
+    st = StreamingMSSA(desc, layers, w["hist_cap_frames"], dtype=w["dtype"], pooled_ring=args.pooled_ring,
+                       head_in_ring=head_in_ring)
     init_shapes = st.shapes(w["hist_start_frames"])
     for L in range(layers):
         x = init_inputs(w, L, init_shapes)
@@ -238,7 +240,9 @@ def bench_streaming(args):
     bufs = st.window_buffers() if args.graph else None
     kinds = []
     for p in range(passes):
-        wins = window_inputs(w, p, layers, win_shapes)
+        # window inputs of the pass (state 1 written into the ring's spare
+        # slots by its producer when the roll moves no data)
+        wins = window_inputs_head_ring(w, p, st) if head_in_ring else window_inputs(w, p, layers, win_shapes)
         flops = sum(st.plan(st.ring[L].count).info()["flops_alg"] for L in range(layers))
         if args.graph:
             for L in range(layers):
@@ -281,7 +285,8 @@ def bench_streaming(args):
         "config": {"workload": "streaming_wan13b", "layers": layers, "passes": passes,
                    "hist_frames": f"{w['hist_start_frames']}->{w['hist_cap_frames']} FIFO",
                    "frames_per_state": F,
-                   "history_pooling": "pooled_ring" if args.pooled_ring else "per_pass",
+                   "history_pooling": "pooled_ring" if st.pooled_ring else "per_pass",
+                   "cache_roll": "in place (head state written into the ring)" if head_in_ring else "device copies",
                    "launch": "hip_graph_per_pass" if args.graph else "eager"},
         "all_passes_ms_per_frame": round(tot_ms / (passes * F), 4),
         "steady_state_passes": [steady[0], steady[-1]],
@@ -463,6 +468,9 @@ def main():
                     help="streaming: replay each full pass as one HIP graph (static window buffers)")
     ap.add_argument("--pooled-ring", action="store_true",
                     help="streaming: keep pooled history rings instead of re-pooling history each pass")
+    ap.add_argument("--head-in-ring", action="store_true",
+                    help="streaming: pooled rings with window state 1 written into the rings' spare slots "
+                         "(the cache roll copies nothing)")
     ap.add_argument("--resample", choices=("mean", "stride"), default="mean",
                     help="K/V resampling of the layer workloads: block mean (default) or the "
                          "strided pick of each block's first cell (both timed the same way)")
@@ -517,12 +525,13 @@ def main():
             result["other_layers"][name]["forward_frac_of_bf16_peak"] = r["roofline"]["frac"]
             result["other_layers"][name]["pool_gbps"] = r["pool"]["achieved"]
             result["other_layers"][name]["config"] = r["config"]
-        sargs = argparse.Namespace(**vars(args))
-        sargs.pooled_ring, sargs.graph = True, False
-        with clock.section("streaming"):
-            s_res = bench_streaming(sargs)
-        result["streaming"] = {k: s_res[k] for k in ("value", "unit", "all_passes_ms_per_frame", "steady_state_passes",
-                                                     "effective_tflops_steady", "config")}
+        for key, head in (("streaming", True), ("streaming_copy_roll", False)):
+            sargs = argparse.Namespace(**vars(args))
+            sargs.pooled_ring, sargs.head_in_ring, sargs.graph = True, head, False
+            with clock.section(key):
+                s_res = bench_streaming(sargs)
+            result[key] = {k: s_res[k] for k in ("value", "unit", "all_passes_ms_per_frame", "steady_state_passes",
+                                                 "effective_tflops_steady", "config")}
         targs = argparse.Namespace(**vars(args))
         targs.workload = "wan13b_layer"
         with clock.section("training"):

@@ -89,6 +89,14 @@ typedef struct {
  * differs.  Combines with MSSA_PLAN_POOLED_HIST_RING. */
 #define MSSA_PLAN_STRIDED_SUBSAMPLE 2
 
+/* Plan flag (with MSSA_PLAN_POOLED_HIST_RING, bf16, scales[0] == 1): the
+ * cache roll moves no data.  Window state 1's K/V are written by their
+ * producer straight into spare slots of the native history ring, and
+ * mssa_pool_kv_head_ring pools them into the same slots of every pooled
+ * ring; the attention reads state 1 from there, and mssa_head_ring_roll only
+ * advances the ring state.  See "Cache roll without copies" below. */
+#define MSSA_PLAN_HEAD_IN_RING 4
+
 /* Sizes derived by the plan.  Group g is the g-th distinct query scale in
  * window token order; its queries are the contiguous range
  * [q_begin[g], q_end[g]) and its context has n_kv[g] tokens per head.
@@ -366,6 +374,57 @@ mssa_status mssa_hist_append_ring(mssa_plan plan, const void* k_win, const void*
                                   int64_t workspace_bytes, void* k_ring, void* v_ring, void* const* k_ring_pooled,
                                   void* const* v_ring_pooled, int32_t ring_cap_frames, int32_t* ring_head,
                                   int32_t* ring_count, void* stream);
+
+/* ------------------------------------------------ cache roll without copies
+ * For plans created with MSSA_PLAN_HEAD_IN_RING (Sec. 3.1, Eq. 2: the head
+ * state emitted by a pass becomes the newest history; Alg. 1's KV-cache
+ * update).  The native ring and every pooled ring (one per query group with
+ * scale s > 1, as for MSSA_PLAN_POOLED_HIST_RING) have ring_frames slots of
+ * one frame each; ring_frames - F is the FIFO cap of the history (F =
+ * frames_per_state), and both ring_frames and the cap are multiples of F.
+ * The ring state is (ring_count, ring_spare):
+ *   - the history is ring_count frames (the plan's hist_frames), oldest
+ *     first, in slots ring_spare - ring_count .. ring_spare - 1 (mod
+ *     ring_frames);
+ *   - slots ring_spare .. ring_spare + F - 1 hold window state 1 of the
+ *     current pass: its producer writes the native K/V there (frame f of the
+ *     state in slot ring_spare + f), in place of the first F frames of the
+ *     window K/V;
+ *   - ring_spare is a multiple of F in [0, ring_frames).
+ * A fresh ring starts with its history in slots [0, count) and ring_spare =
+ * count (mssa_pool_hist_ring fills the pooled rings from it).  A pass is
+ * mssa_pool_kv_head_ring, mssa_forward_head_ring, mssa_head_ring_roll; the
+ * roll copies nothing.
+ *   k_win, v_win   window K/V of states 2..T only: [n_q - F * grid_h *
+ *                  grid_w, H, D] device (the window tokens after state 1)
+ *   k_ring, v_ring the native ring, [ring_frames * grid_h * grid_w, H, D]
+ *   k_ring_pooled, v_ring_pooled  per query group (mssa_plan_info order):
+ *                  [ring_frames * tok_s, H, D] for scale s > 1, else ignored
+ * MSSA_ERR_UNSUPPORTED for a plan without the flag; MSSA_ERR_INVALID_ARG
+ * for a ring state that breaks the rules above or ring_count !=
+ * hist_frames. */
+
+/* Pool window state 1 (read from the native ring's spare slots) into the
+ * spare slots of every pooled ring, and the window frames of states 2..T
+ * that are finer than a query scale into the workspace (Eq. 4). */
+mssa_status mssa_pool_kv_head_ring(mssa_plan plan, const void* k_ring, const void* v_ring, const void* k_win,
+                                   const void* v_win, void* const* k_ring_pooled, void* const* v_ring_pooled,
+                                   void* workspace, int64_t workspace_bytes, int32_t ring_frames,
+                                   int32_t ring_count, int32_t ring_spare, void* stream);
+
+/* Attention of the pass (Eq. 4): as mssa_forward, with the history and
+ * window state 1 read from the rings. */
+mssa_status mssa_forward_head_ring(mssa_plan plan, const void* q_win, const void* k_sink, const void* v_sink,
+                                   const void* k_ring, const void* v_ring, const void* const* k_ring_pooled,
+                                   const void* const* v_ring_pooled, const void* k_win, const void* v_win,
+                                   const void* workspace, int64_t workspace_bytes, void* out, int32_t ring_frames,
+                                   int32_t ring_count, int32_t ring_spare, void* stream);
+
+/* The cache roll after a pass (host only, nothing enqueued): state 1 joins
+ * the history, whose oldest frames leave once it exceeds the cap.
+ * *ring_count becomes min(count + F, ring_frames - F) and *ring_spare
+ * (spare + F) mod ring_frames. */
+mssa_status mssa_head_ring_roll(mssa_plan plan, int32_t ring_frames, int32_t* ring_count, int32_t* ring_spare);
 
 /* Name of a status code (static string). */
 const char* mssa_status_string(mssa_status s);

@@ -302,13 +302,42 @@ mssa_status forward_check(const mssa::Plan& p, const void* q_win, const void* k_
   return MSSA_OK;
 }
 
-mssa_status forward_impl(const mssa::Plan& p, const void* q_win, const void* k_sink, const void* v_sink,
-                         const void* k_hist, const void* v_hist, const void* const* k_hist_pooled,
-                         const void* const* v_hist_pooled, const void* k_win, const void* v_win,
-                         const void* workspace, int64_t workspace_bytes, void* out, float* lse, void* stream) {
-  const mssa_status chk = forward_check(p, q_win, k_sink, v_sink, k_hist, v_hist, k_hist_pooled, v_hist_pooled,
-                                        k_win, v_win, workspace, workspace_bytes, out, lse);
-  if (chk != MSSA_OK) return chk;
+// A context run as device addresses (head 0, channel 0 of its first token).
+struct PtrRun {
+  const void* k;
+  const void* v;
+  int64_t n_tok;
+};
+using GroupRuns = std::vector<std::vector<PtrRun>>;
+
+// Appends a run, merged with the previous one when it continues it in memory.
+void push_run(std::vector<PtrRun>& rs, const void* k, const void* v, int64_t n_tok, int64_t row_bytes) {
+  if (n_tok <= 0) return;
+  if (!rs.empty()) {
+    PtrRun& b = rs.back();
+    if (static_cast<const char*>(b.k) + b.n_tok * row_bytes == k &&
+        static_cast<const char*>(b.v) + b.n_tok * row_bytes == v) {
+      b.n_tok += n_tok;
+      return;
+    }
+  }
+  rs.push_back({k, v, n_tok});
+}
+
+GroupRuns plan_runs(const mssa::Plan& p, const KvSources& src) {
+  GroupRuns out(p.groups.size());
+  for (size_t g = 0; g < p.groups.size(); ++g)
+    for (const mssa::Run& R : p.runs[g]) {
+      PtrRun r{nullptr, nullptr, R.n_tok};
+      run_pointers(p, static_cast<int>(g), R, src, &r.k, &r.v);
+      out[g].push_back(r);
+    }
+  return out;
+}
+
+// Enqueues the attention kernels over the given runs and schedule.
+mssa_status forward_launch(const mssa::Plan& p, const GroupRuns& runs, const mssa::Schedule& sc, const void* q_win,
+                           const void* workspace, void* out, float* lse, void* stream) {
   const bool bf16 = p.desc.dtype == MSSA_BF16;
   const int bm = bf16 ? mssa::kFwdBM : mssa::kFwdF32BM;
   mssa::FwdArgs a{};
@@ -321,9 +350,9 @@ mssa_status forward_impl(const mssa::Plan& p, const void* q_win, const void* k_s
   a.scale = p.softmax_scale;
   a.scale_log2e = p.softmax_scale * 1.4426950408889634f;
   a.n_ranges = p.n_ranges;
-  a.total_tiles = p.total_tiles;
-  a.tail_begin = p.tail_begin;
-  a.dp_rounds = p.dp_rounds;
+  a.total_tiles = sc.total_tiles;
+  a.tail_begin = sc.tail_begin;
+  a.dp_rounds = sc.dp_rounds;
   const char* ws = static_cast<const char*>(workspace);
   a.partial = p.partial_bytes > 0 ? reinterpret_cast<float*>(const_cast<char*>(ws) + p.partial_off) : nullptr;
   a.range_table = p.partial_bytes > 0 ? reinterpret_cast<int64_t*>(const_cast<char*>(ws) + p.range_table_off) : nullptr;
@@ -336,15 +365,15 @@ mssa_status forward_impl(const mssa::Plan& p, const void* q_win, const void* k_s
     A.q_end = Q.q_end;
     A.n_qtiles = (Q.q_end - Q.q_begin + bm - 1) / bm;
     A.block_begin = static_cast<int32_t>(blocks);
-    A.tiles_per_item = p.tiles_per_item[g];
-    A.tile_begin = p.tile_begin[g];
-    if (p.runs[g].size() > static_cast<size_t>(mssa::kMaxRuns))
+    A.tiles_per_item = sc.tiles_per_item[g];
+    A.tile_begin = sc.tile_begin[g];
+    if (runs[g].size() > static_cast<size_t>(mssa::kMaxRuns))
       return fail(MSSA_ERR_UNSUPPORTED, "too many context runs for one query scale");
-    A.n_runs = static_cast<int32_t>(p.runs[g].size());
-    const KvSources src{k_sink, v_sink, k_hist, v_hist, k_hist_pooled, v_hist_pooled, k_win, v_win, ws};
-    for (size_t r = 0; r < p.runs[g].size(); ++r) {
-      run_pointers(p, g, p.runs[g][r], src, &A.runs[r].k, &A.runs[r].v);
-      A.runs[r].n_tok = static_cast<int32_t>(p.runs[g][r].n_tok);
+    A.n_runs = static_cast<int32_t>(runs[g].size());
+    for (size_t r = 0; r < runs[g].size(); ++r) {
+      A.runs[r].k = runs[g][r].k;
+      A.runs[r].v = runs[g][r].v;
+      A.runs[r].n_tok = static_cast<int32_t>(runs[g][r].n_tok);
     }
     blocks += static_cast<int64_t>(A.n_qtiles) * p.desc.num_heads;
   }
@@ -353,6 +382,76 @@ mssa_status forward_impl(const mssa::Plan& p, const void* q_win, const void* k_s
   a.n_blocks = static_cast<int32_t>(blocks);
   return check_device(mssa::launch_forward(a, p.desc.head_dim, bf16, static_cast<hipStream_t>(stream)),
                       "attention kernel launch");
+}
+
+mssa_status forward_impl(const mssa::Plan& p, const void* q_win, const void* k_sink, const void* v_sink,
+                         const void* k_hist, const void* v_hist, const void* const* k_hist_pooled,
+                         const void* const* v_hist_pooled, const void* k_win, const void* v_win,
+                         const void* workspace, int64_t workspace_bytes, void* out, float* lse, void* stream) {
+  const mssa_status chk = forward_check(p, q_win, k_sink, v_sink, k_hist, v_hist, k_hist_pooled, v_hist_pooled,
+                                        k_win, v_win, workspace, workspace_bytes, out, lse);
+  if (chk != MSSA_OK) return chk;
+  const KvSources src{k_sink, v_sink, k_hist, v_hist, k_hist_pooled, v_hist_pooled,
+                      k_win, v_win, static_cast<const char*>(workspace)};
+  return forward_launch(p, plan_runs(p, src), p.sched, q_win, workspace, out, lse, stream);
+}
+
+// ---------------------------------------------------------------- head state in the ring
+
+// Ring state rules of MSSA_PLAN_HEAD_IN_RING plans.
+mssa_status head_ring_check(const mssa::Plan& p, int32_t ring_frames, int32_t count, int32_t spare) {
+  if (!p.head_ring) return fail(MSSA_ERR_UNSUPPORTED, "plan lacks MSSA_PLAN_HEAD_IN_RING");
+  const int32_t F = p.desc.frames_per_state;
+  if (ring_frames < 2 * F || ring_frames % F != 0)
+    return fail(MSSA_ERR_INVALID_ARG, "ring_frames must be a multiple of frames_per_state, at least two of them");
+  if (spare < 0 || spare >= ring_frames || spare % F != 0)
+    return fail(MSSA_ERR_INVALID_ARG, "ring_spare must be a multiple of frames_per_state below ring_frames");
+  if (count != p.desc.hist_frames || count > ring_frames - F)
+    return fail(MSSA_ERR_INVALID_ARG, "ring_count must equal hist_frames and not exceed ring_frames - F");
+  return MSSA_OK;
+}
+
+// Context runs of every group: sink | history and window state 1 in the
+// group's ring, slots spare - count .. spare + F - 1 (mod ring_frames; two
+// runs if they wrap) | the rest of the window as placed by the plan.
+GroupRuns head_ring_runs(const mssa::Plan& p, const void* k_sink, const void* v_sink, const void* k_ring,
+                         const void* v_ring, const void* const* k_pool, const void* const* v_pool, const void* k_win,
+                         const void* v_win, const char* ws, int32_t N, int32_t count, int32_t spare) {
+  const int64_t rb = p.ld * p.elem_bytes;
+  const int32_t F = p.desc.frames_per_state;
+  GroupRuns out(p.groups.size());
+  for (size_t g = 0; g < p.groups.size(); ++g) {
+    const int32_t sc = p.groups[g].scale;
+    std::vector<PtrRun>& rs = out[g];
+    bool ring_done = false;
+    for (const mssa::SegRow& r : p.segs) {
+      if (r.q_scale != sc) continue;
+      if (r.kind == mssa::kSink) {
+        push_run(rs, static_cast<const char*>(k_sink) + r.tok_offset * rb,
+                 static_cast<const char*>(v_sink) + r.tok_offset * rb, r.n_tok, rb);
+      } else if (r.kind == mssa::kHist || r.buffer == mssa::kBufRingHead) {
+        if (ring_done) continue;
+        ring_done = true;
+        const char* kb = static_cast<const char*>(sc == 1 ? k_ring : k_pool[g]);
+        const char* vb = static_cast<const char*>(sc == 1 ? v_ring : v_pool[g]);
+        const int64_t slot_tok = r.n_tok;  // a history frame and a state-1 frame at this scale
+        const int32_t a = ((spare - count) % N + N) % N, b = spare + F;
+        if (a < b) {
+          push_run(rs, kb + a * slot_tok * rb, vb + a * slot_tok * rb, int64_t{b - a} * slot_tok, rb);
+        } else {
+          push_run(rs, kb + a * slot_tok * rb, vb + a * slot_tok * rb, int64_t{N - a} * slot_tok, rb);
+          push_run(rs, kb, vb, int64_t{b} * slot_tok, rb);
+        }
+      } else if (r.buffer == mssa::kBufPooled) {
+        push_run(rs, ws + p.pooled_k_off[g] + r.tok_offset * rb, ws + p.pooled_v_off[g] + r.tok_offset * rb,
+                 r.n_tok, rb);
+      } else {
+        push_run(rs, static_cast<const char*>(k_win) + r.tok_offset * rb,
+                 static_cast<const char*>(v_win) + r.tok_offset * rb, r.n_tok, rb);
+      }
+    }
+  }
+  return out;
 }
 
 }  // namespace
@@ -908,6 +1007,109 @@ mssa_status mssa_pool_hist_ring(mssa_plan plan, const void* k_ring, const void* 
       jobs.push_back(A);
     }
     return launch_pool_jobs(p, jobs, stream);
+  });
+}
+
+mssa_status mssa_pool_kv_head_ring(mssa_plan plan, const void* k_ring, const void* v_ring, const void* k_win,
+                                   const void* v_win, void* const* k_ring_pooled, void* const* v_ring_pooled,
+                                   void* workspace, int64_t workspace_bytes, int32_t ring_frames,
+                                   int32_t ring_count, int32_t ring_spare, void* stream) {
+  return guarded("mssa_pool_kv_head_ring", [&]() -> mssa_status {
+    if (!plan) return fail(MSSA_ERR_INVALID_ARG, "plan must be non-null");
+    const mssa::Plan& p = plan->p;
+    mssa_status s = head_ring_check(p, ring_frames, ring_count, ring_spare);
+    if (s != MSSA_OK) return s;
+    if (!k_ring || !v_ring || !k_ring_pooled || !v_ring_pooled)
+      return fail(MSSA_ERR_INVALID_ARG, "k_ring, v_ring and the pooled ring arrays must be non-null");
+    if (!aligned16(k_ring) || !aligned16(v_ring)) return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
+    for (size_t g = 0; g < p.groups.size(); ++g) {
+      if (p.groups[g].scale == 1) continue;
+      if (!k_ring_pooled[g] || !v_ring_pooled[g] || !aligned16(k_ring_pooled[g]) || !aligned16(v_ring_pooled[g]))
+        return fail(MSSA_ERR_INVALID_ARG, "null or misaligned pooled ring for a coarse query scale");
+    }
+    s = pool_check(p, nullptr, nullptr, k_win, v_win, workspace, workspace_bytes);
+    if (s != MSSA_OK) return s;
+    // the plan's jobs (window states 2..T into the workspace), then state 1
+    // from the native ring's spare slots into every pooled ring's
+    const int64_t rb = p.ld * p.elem_bytes;
+    auto* ws = static_cast<char*>(workspace);
+    std::vector<mssa::PoolJobArgs> jobs;
+    for (const mssa::PoolJob& J : p.pool_jobs) {
+      mssa::PoolJobArgs A{};
+      A.src_k = static_cast<const char*>(k_win) + J.src_tok * rb;
+      A.src_v = static_cast<const char*>(v_win) + J.src_tok * rb;
+      A.dst_k = ws + p.pooled_k_off[J.group] + J.dst_tok * rb;
+      A.dst_v = ws + p.pooled_v_off[J.group] + J.dst_tok * rb;
+      A.src_gh = J.src_gh;
+      A.src_gw = J.src_gw;
+      A.dst_gh = J.dst_gh;
+      A.dst_gw = J.dst_gw;
+      A.factor = J.factor;
+      A.n_frames = J.n_frames;
+      jobs.push_back(A);
+    }
+    for (size_t g = 0; g < p.groups.size(); ++g) {
+      const int32_t sc = p.groups[g].scale;
+      if (sc == 1) continue;
+      mssa::PoolJobArgs A{};
+      const int64_t tok_s = frame_tokens(p, sc);
+      A.src_k = static_cast<const char*>(k_ring) + int64_t{ring_spare} * p.tok1 * rb;
+      A.src_v = static_cast<const char*>(v_ring) + int64_t{ring_spare} * p.tok1 * rb;
+      A.dst_k = static_cast<char*>(k_ring_pooled[g]) + int64_t{ring_spare} * tok_s * rb;
+      A.dst_v = static_cast<char*>(v_ring_pooled[g]) + int64_t{ring_spare} * tok_s * rb;
+      A.src_gh = p.desc.grid_h;
+      A.src_gw = p.desc.grid_w;
+      A.factor = sc;
+      A.dst_gh = (p.desc.grid_h + sc - 1) / sc;
+      A.dst_gw = (p.desc.grid_w + sc - 1) / sc;
+      A.n_frames = p.desc.frames_per_state;
+      jobs.push_back(A);
+    }
+    if (jobs.empty()) return MSSA_OK;
+    return launch_pool_jobs(p, jobs, stream);
+  });
+}
+
+mssa_status mssa_forward_head_ring(mssa_plan plan, const void* q_win, const void* k_sink, const void* v_sink,
+                                   const void* k_ring, const void* v_ring, const void* const* k_ring_pooled,
+                                   const void* const* v_ring_pooled, const void* k_win, const void* v_win,
+                                   const void* workspace, int64_t workspace_bytes, void* out, int32_t ring_frames,
+                                   int32_t ring_count, int32_t ring_spare, void* stream) {
+  return guarded("mssa_forward_head_ring", [&]() -> mssa_status {
+    if (!plan) return fail(MSSA_ERR_INVALID_ARG, "plan must be non-null");
+    const mssa::Plan& p = plan->p;
+    mssa_status s = head_ring_check(p, ring_frames, ring_count, ring_spare);
+    if (s != MSSA_OK) return s;
+    if (!k_ring || !v_ring || !k_ring_pooled || !v_ring_pooled)
+      return fail(MSSA_ERR_INVALID_ARG, "k_ring, v_ring and the pooled ring arrays must be non-null");
+    for (size_t g = 0; g < p.groups.size(); ++g)
+      if (p.groups[g].scale > 1 && (!k_ring_pooled[g] || !v_ring_pooled[g]))
+        return fail(MSSA_ERR_INVALID_ARG, "null pooled ring for a coarse query scale");
+    // state 2 onwards may be empty (a single state): k_win may then be null
+    const bool rest = p.n_q > p.win_shift;
+    s = forward_check(p, q_win, k_sink, v_sink, k_ring, v_ring, k_ring_pooled, v_ring_pooled,
+                      rest ? k_win : k_ring, rest ? v_win : v_ring, workspace, workspace_bytes, out, nullptr);
+    if (s != MSSA_OK) return s;
+    const GroupRuns runs = head_ring_runs(p, k_sink, v_sink, k_ring, v_ring, k_ring_pooled, v_ring_pooled, k_win,
+                                          v_win, static_cast<const char*>(workspace), ring_frames, ring_count,
+                                          ring_spare);
+    std::vector<std::vector<int64_t>> n_tok(runs.size());
+    for (size_t g = 0; g < runs.size(); ++g)
+      for (const PtrRun& r : runs[g]) n_tok[g].push_back(r.n_tok);
+    return forward_launch(p, runs, mssa::make_schedule(p, n_tok), q_win, workspace, out, nullptr, stream);
+  });
+}
+
+mssa_status mssa_head_ring_roll(mssa_plan plan, int32_t ring_frames, int32_t* ring_count, int32_t* ring_spare) {
+  return guarded("mssa_head_ring_roll", [&]() -> mssa_status {
+    if (!plan || !ring_count || !ring_spare) return fail(MSSA_ERR_INVALID_ARG, "null argument");
+    const mssa::Plan& p = plan->p;
+    const mssa_status s = head_ring_check(p, ring_frames, *ring_count, *ring_spare);
+    if (s != MSSA_OK) return s;
+    const int32_t F = p.desc.frames_per_state;
+    *ring_count = std::min(*ring_count + F, ring_frames - F);
+    *ring_spare = (*ring_spare + F) % ring_frames;
+    return MSSA_OK;
   });
 }
 

@@ -7,7 +7,7 @@
 namespace mssa {
 
 constexpr int kMaxGroups = 8;      // distinct query scales (<= num_states)
-constexpr int kMaxRuns = 4;        // contiguous context runs per query scale
+constexpr int kMaxRuns = 6;        // contiguous context runs per query scale
 constexpr int kMaxPoolJobs = 16;   // pool jobs per launch
 
 // Tile shapes of the bf16 attention kernel: 8 waves x 32 queries (two

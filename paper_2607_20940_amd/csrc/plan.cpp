@@ -49,7 +49,7 @@ mssa_status build_plan(const mssa_plan_desc& d, int slots, int attention_blocks,
     err = "softmax_scale must be finite";
     return MSSA_ERR_INVALID_ARG;
   }
-  if ((d.flags & ~(MSSA_PLAN_POOLED_HIST_RING | MSSA_PLAN_STRIDED_SUBSAMPLE)) != 0) {
+  if ((d.flags & ~(MSSA_PLAN_POOLED_HIST_RING | MSSA_PLAN_STRIDED_SUBSAMPLE | MSSA_PLAN_HEAD_IN_RING)) != 0) {
     err = "unknown plan flags";
     return MSSA_ERR_INVALID_ARG;
   }
@@ -67,10 +67,16 @@ mssa_status build_plan(const mssa_plan_desc& d, int slots, int attention_blocks,
     err = "head_dim must be 64 or 128";
     return MSSA_ERR_UNSUPPORTED;
   }
+  if ((d.flags & MSSA_PLAN_HEAD_IN_RING) &&
+      (!(d.flags & MSSA_PLAN_POOLED_HIST_RING) || d.scales[0] != 1 || d.dtype != MSSA_BF16)) {
+    err = "MSSA_PLAN_HEAD_IN_RING needs MSSA_PLAN_POOLED_HIST_RING, a native head state (scales[0] == 1) and bf16";
+    return MSSA_ERR_UNSUPPORTED;
+  }
 
   p = Plan{};
   p.desc = d;
   p.hist_ring = (d.flags & MSSA_PLAN_POOLED_HIST_RING) != 0;
+  p.head_ring = (d.flags & MSSA_PLAN_HEAD_IN_RING) != 0;
   p.strided = (d.flags & MSSA_PLAN_STRIDED_SUBSAMPLE) != 0;
   p.softmax_scale = d.softmax_scale > 0.f ? d.softmax_scale
                                           : 1.0f / std::sqrt(static_cast<float>(d.head_dim));
@@ -83,6 +89,7 @@ mssa_status build_plan(const mssa_plan_desc& d, int slots, int attention_blocks,
   p.elem_bytes = d.dtype == MSSA_BF16 ? 2 : 4;
   p.n_sink_tok = p.tok1 * d.sink_frames;
   p.n_hist_tok = p.tok1 * d.hist_frames;
+  p.win_shift = p.head_ring ? p.tok1 * F : 0;
 
   // GRID: native scale plus every scheduled scale, ascending.
   std::vector<int32_t> sc{1};
@@ -153,8 +160,17 @@ mssa_status build_plan(const mssa_plan_desc& d, int slots, int attention_blocks,
       const WinFrame& w = wf[i];
       const int32_t eff = std::max(s, w.p);
       const int32_t fac = std::max(1, s / w.p);
-      SegRow r{s, kWin, w.w, w.p, eff, fac, static_cast<int32_t>(tok_at(eff)), 0, kBufWin, w.first};
-      if (fac > 1) { r.buffer = kBufPooled; r.tok_offset = pooled; pooled += r.n_tok; win_read[i] = 1; }
+      SegRow r{s, kWin, w.w, w.p, eff, fac, static_cast<int32_t>(tok_at(eff)), 0, kBufWin, w.first - p.win_shift};
+      if (p.head_ring && w.w < F) {
+        // state 1 lives in the spare ring slots, pooled there by pool_kv
+        r.buffer = kBufRingHead;
+        r.tok_offset = w.w * r.n_tok;
+      } else if (fac > 1) {
+        r.buffer = kBufPooled;
+        r.tok_offset = pooled;
+        pooled += r.n_tok;
+        win_read[i] = 1;
+      }
       rows.push_back(r);
     }
     for (SegRow& r : rows) { r.kv_begin = kv; kv += r.n_tok; }
@@ -186,7 +202,7 @@ mssa_status build_plan(const mssa_plan_desc& d, int slots, int attention_blocks,
         src_tok = r.frame * p.tok1;
         src_n = p.tok1;
       } else {
-        src_tok = wf[r.frame].first;
+        src_tok = wf[r.frame].first - p.win_shift;
         src_n = wf[r.frame].n;
       }
       const int32_t sgh = ceil_div(d.grid_h, r.src_scale), sgw = ceil_div(d.grid_w, r.src_scale);
@@ -221,39 +237,19 @@ mssa_status build_plan(const mssa_plan_desc& d, int slots, int attention_blocks,
   for (int g = 0; g < G; ++g) p.order.push_back(g);
   std::stable_sort(p.order.begin(), p.order.end(),
                    [&](int x, int y) { return p.groups[x].n_kv > p.groups[y].n_kv; });
-  p.tiles_per_item.assign(G, 0);
-  p.tile_begin.assign(G, 0);
-  p.total_tiles = 0;
-  int64_t n_items = 0, t_max = 0;
-  std::vector<int64_t> item_first(G, 0);
-  for (int g : p.order) {
-    int64_t tiles = 0;
-    for (const Run& r : p.runs[g]) tiles += (r.n_tok + kFwdBN - 1) / kFwdBN;
-    p.tiles_per_item[g] = static_cast<int32_t>(tiles);
-    p.tile_begin[g] = p.total_tiles;
-    item_first[g] = n_items;
-    const int64_t items =
-        static_cast<int64_t>((p.groups[g].q_end - p.groups[g].q_begin + kFwdBM - 1) / kFwdBM) * d.num_heads;
-    n_items += items;
-    p.total_tiles += items * tiles;
-    t_max = std::max(t_max, tiles);
+  std::vector<std::vector<int64_t>> run_tok(G);
+  int64_t n_items = 0;
+  for (int g = 0; g < G; ++g) {
+    for (const Run& r : p.runs[g]) run_tok[g].push_back(r.n_tok);
+    n_items += static_cast<int64_t>((p.groups[g].q_end - p.groups[g].q_begin + kFwdBM - 1) / kFwdBM) * d.num_heads;
   }
+  p.n_ranges = 1;
+  const int64_t total = make_schedule(p, run_tok).total_tiles;
   if (slots <= 0) slots = 512;
   int64_t ranges = attention_blocks > 0 ? attention_blocks : std::min<int64_t>(slots, n_items);
-  ranges = std::max<int64_t>(1, std::min<int64_t>(ranges, p.total_tiles));
+  ranges = std::max<int64_t>(1, std::min<int64_t>(ranges, total));
   p.n_ranges = static_cast<int32_t>(ranges);
-  // Whole-item rounds: as many as fit without any block exceeding its even
-  // share total_tiles / ranges; the rest is split into per-block tail ranges
-  // sized to make every block's total equal.
-  p.dp_rounds = static_cast<int32_t>(
-      std::min<int64_t>(n_items / ranges, (p.total_tiles / ranges) / std::max<int64_t>(1, t_max)));
-  {
-    const int64_t i = static_cast<int64_t>(p.dp_rounds) * ranges;  // first tail item
-    int gl = p.order.front();
-    for (int g : p.order)
-      if (i >= item_first[g]) gl = g;
-    p.tail_begin = p.tile_begin[gl] + (i - item_first[gl]) * p.tiles_per_item[gl];
-  }
+  p.sched = make_schedule(p, run_tok);
   p.partial_off = 0;
   p.partial_bytes = 0;
   p.range_table_off = 0;
@@ -330,9 +326,53 @@ mssa_status build_plan(const mssa_plan_desc& d, int slots, int attention_blocks,
   int64_t read_tok = hist_read ? p.n_hist_tok : 0;
   for (size_t i = 0; i < wf.size(); ++i)
     if (win_read[i]) read_tok += wf[i].n;
+  if (p.head_ring) {
+    // state 1's frames, read once from the ring and written pooled to every
+    // coarser query scale's ring
+    bool any = false;
+    for (const QGroup& g : p.groups)
+      if (g.scale > 1) {
+        write_tok += F * tok_at(g.scale);
+        any = true;
+      }
+    if (any) read_tok += F * p.tok1;
+  }
   if (p.strided) read_tok = write_tok;
   p.pool_bytes_alg = 2 * (read_tok + write_tok) * p.ld * p.elem_bytes;
   return MSSA_OK;
+}
+
+Schedule make_schedule(const Plan& p, const std::vector<std::vector<int64_t>>& n_tok) {
+  const int G = static_cast<int>(p.groups.size());
+  Schedule sc;
+  sc.tiles_per_item.assign(G, 0);
+  sc.tile_begin.assign(G, 0);
+  int64_t n_items = 0, t_max = 0;
+  std::vector<int64_t> item_first(G, 0);
+  for (int g : p.order) {
+    int64_t tiles = 0;
+    for (int64_t n : n_tok[g]) tiles += (n + kFwdBN - 1) / kFwdBN;
+    sc.tiles_per_item[g] = static_cast<int32_t>(tiles);
+    sc.tile_begin[g] = sc.total_tiles;
+    item_first[g] = n_items;
+    const int64_t items =
+        static_cast<int64_t>((p.groups[g].q_end - p.groups[g].q_begin + kFwdBM - 1) / kFwdBM) * p.desc.num_heads;
+    n_items += items;
+    sc.total_tiles += items * tiles;
+    t_max = std::max(t_max, tiles);
+  }
+  const int64_t ranges = p.n_ranges;
+  // Whole-item rounds: as many as fit without any block exceeding its even
+  // share total_tiles / ranges; the rest is split into per-block tail ranges
+  // sized to make every block's total equal.
+  sc.dp_rounds = static_cast<int32_t>(
+      std::min<int64_t>(n_items / ranges, (sc.total_tiles / ranges) / std::max<int64_t>(1, t_max)));
+  const int64_t i = static_cast<int64_t>(sc.dp_rounds) * ranges;  // first tail item
+  int gl = p.order.front();
+  for (int g : p.order)
+    if (i >= item_first[g]) gl = g;
+  sc.tail_begin = sc.tile_begin[gl] + (i - item_first[gl]) * sc.tiles_per_item[gl];
+  return sc;
 }
 
 std::vector<int64_t> export_tables(const Plan& p) {

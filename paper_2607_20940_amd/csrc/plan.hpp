@@ -16,7 +16,13 @@ enum Kind : int32_t { kSink = 0, kHist = 1, kWin = 2 };
 // Where a run of context tokens lives.
 // kBufHistPooled: the caller's pooled-history ring of the group (plans with
 // MSSA_PLAN_POOLED_HIST_RING), frame f at token f * tok_s.
-enum Buffer : int32_t { kBufSink = 0, kBufHist = 1, kBufWin = 2, kBufPooled = 3, kBufHistPooled = 4 };
+// kBufRingHead: a frame of window state 1 that lives in the ring's spare
+// slots (plans with MSSA_PLAN_HEAD_IN_RING): the native ring for the native
+// query scale, the group's pooled ring for a coarser one; frame f of the
+// state in the f-th spare slot.
+enum Buffer : int32_t {
+  kBufSink = 0, kBufHist = 1, kBufWin = 2, kBufPooled = 3, kBufHistPooled = 4, kBufRingHead = 5
+};
 
 struct GridRow {
   int32_t scale, gh, gw, tok;
@@ -68,9 +74,23 @@ struct ScatterJob {
   std::vector<int32_t> frame_stride, factor;  // per group
 };
 
+// Persistent attention schedule (bf16 forward): groups in launch order
+// (longest context first), 64-key tiles per item of each group, first tile
+// of each group in the linear tile space, whole-item rounds and the first
+// tile of the tail ranges, for a fixed number of tile ranges (blocks).
+struct Schedule {
+  std::vector<int32_t> tiles_per_item;   // per group
+  std::vector<int64_t> tile_begin;       // per group
+  int64_t total_tiles = 0;
+  int32_t dp_rounds = 0;    // rounds of whole items (one per block) before the tail
+  int64_t tail_begin = 0;   // first tile of the tail ranges
+};
+
 struct Plan {
   mssa_plan_desc desc;
   bool hist_ring;  // MSSA_PLAN_POOLED_HIST_RING
+  bool head_ring;  // MSSA_PLAN_HEAD_IN_RING: window state 1 read from the rings' spare slots
+  int64_t win_shift;  // head_ring: window tokens before k_win / v_win (state 1's), else 0
   bool strided;    // MSSA_PLAN_STRIDED_SUBSAMPLE: first cell of each block
   float softmax_scale;
   int64_t tok1;  // native tokens per frame
@@ -87,16 +107,11 @@ struct Plan {
   int64_t workspace_bytes;
   int64_t pairs_per_head;
   int64_t pool_bytes_alg;
-  // Persistent attention schedule (bf16): groups in launch order (longest
-  // context first), 64-key tiles per item, first tile of each group in the
-  // linear tile space, and the number of equal tile ranges (one per block).
+  // Persistent attention schedule over the runs above (bf16): groups in
+  // launch order and n_ranges tile ranges (one per block).
   std::vector<int> order;
-  std::vector<int32_t> tiles_per_item;   // per group
-  std::vector<int64_t> tile_begin;       // per group
-  int64_t total_tiles;
   int32_t n_ranges;
-  int32_t dp_rounds;    // rounds of whole items (one per block) before the tail
-  int64_t tail_begin;   // first tile of the tail ranges
+  Schedule sched;
   int64_t partial_off, partial_bytes;    // partial records and the range table in the workspace
   int64_t range_table_off;               // n_ranges + 1 int64 first tiles of the tail ranges
   // Backward workspace: the forward's, then rowsum(dO * O) [heads, n_q]
@@ -114,6 +129,10 @@ struct Plan {
 // (tile ranges) instead.  Returns MSSA_OK or an error status with a message
 // in `err`.
 mssa_status build_plan(const mssa_plan_desc& d, int slots, int attention_blocks, Plan& p, std::string& err);
+
+// The attention schedule of plan p over per-group runs whose token counts
+// are n_tok[g] (the plan's own runs, or runs placed at call time).
+Schedule make_schedule(const Plan& p, const std::vector<std::vector<int64_t>>& n_tok);
 
 // Flat int64 export of GRID / QGRP / SEG / TOTAL (layout in libmssa.h).
 std::vector<int64_t> export_tables(const Plan& p);

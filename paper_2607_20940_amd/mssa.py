@@ -20,13 +20,15 @@ MSSA_ERR_WORKSPACE, MSSA_ERR_DEVICE, MSSA_ERR_NO_MEMORY = 3, 4, 5
 MSSA_BF16, MSSA_F32 = 0, 1
 MSSA_PLAN_POOLED_HIST_RING = 1
 MSSA_PLAN_STRIDED_SUBSAMPLE = 2
+MSSA_PLAN_HEAD_IN_RING = 4
 
 # Every symbol include/libmssa.h declares.
 EXPORTS = ("mssa_plan_create", "mssa_plan_create_ex", "mssa_plan_destroy", "mssa_plan_query", "mssa_plan_tables",
            "mssa_pool_kv", "mssa_forward", "mssa_hist_append", "mssa_pool_hist_ring",
            "mssa_forward_ring", "mssa_hist_append_ring", "mssa_forward_lse", "mssa_backward_workspace_size",
            "mssa_backward", "mssa_tier_workspace_size", "mssa_patch_embed", "mssa_patch_unembed",
-           "mssa_qkv_project", "mssa_attention_noalloc", "mssa_status_string", "mssa_last_error")
+           "mssa_qkv_project", "mssa_attention_noalloc", "mssa_pool_kv_head_ring", "mssa_forward_head_ring",
+           "mssa_head_ring_roll", "mssa_status_string", "mssa_last_error")
 
 MSSA_NOALLOC_SCRATCH_BYTES = 256 << 20
 
@@ -85,6 +87,10 @@ def _load():
                                           ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32), V]
     lib.mssa_forward_lse.argtypes = [P, V, V, V, V, V, V, V, V, I64, V, V, V]
     lib.mssa_attention_noalloc.argtypes = [P, V, V, V, V, V, V, V, V, V]
+    I32 = ctypes.c_int32
+    lib.mssa_pool_kv_head_ring.argtypes = [P, V, V, V, V, PP, PP, V, I64, I32, I32, I32, V]
+    lib.mssa_forward_head_ring.argtypes = [P, V, V, V, V, V, PP, PP, V, V, V, I64, V, I32, I32, I32, V]
+    lib.mssa_head_ring_roll.argtypes = [P, I32, ctypes.POINTER(I32), ctypes.POINTER(I32)]
     lib.mssa_backward_workspace_size.argtypes = [P, ctypes.POINTER(I64)]
     lib.mssa_backward.argtypes = [P, V, V, V, V, V, V, V, V, V, V, V, I64, V, V, V, V, V, V, V, V]
     TD = ctypes.POINTER(mssa_tier_desc)
@@ -323,6 +329,44 @@ def mssa_patch_unembed(plan, tier, tokens, w_out, b_out, workspace, latent, work
 def mssa_qkv_project(n_tokens, hidden, x, w_qkv, b_qkv, q, k, v, stream=None):
     _check(lib.mssa_qkv_project(int(n_tokens), int(hidden), _ptr(x), _ptr(w_qkv), _ptr(b_qkv), _ptr(q), _ptr(k),
                                 _ptr(v), _stream(stream)), "mssa_qkv_project")
+
+
+class HeadRing:
+    """Host-side state of the rings of a MSSA_PLAN_HEAD_IN_RING plan: slots
+    (ring_frames), history frames (count) and the first spare slot (spare),
+    where window state 1 of the current pass lives."""
+
+    def __init__(self, frames, count=0, spare=None):
+        self.frames = int(frames)
+        self.count = int(count)
+        self.spare = int(count if spare is None else spare)
+
+
+def mssa_pool_kv_head_ring(plan, k_ring, v_ring, k_win, v_win, k_ring_pooled, v_ring_pooled, workspace, ring,
+                           workspace_bytes=None, stream=None):
+    wb = _nbytes(workspace) if workspace_bytes is None else int(workspace_bytes)
+    _check(lib.mssa_pool_kv_head_ring(plan.handle, _ptr(k_ring), _ptr(v_ring), _ptr(k_win), _ptr(v_win),
+                                      _ptr_array(k_ring_pooled), _ptr_array(v_ring_pooled), _ptr(workspace), wb,
+                                      ring.frames, ring.count, ring.spare, _stream(stream)),
+           "mssa_pool_kv_head_ring")
+
+
+def mssa_forward_head_ring(plan, q_win, k_sink, v_sink, k_ring, v_ring, k_ring_pooled, v_ring_pooled, k_win, v_win,
+                           workspace, out, ring, workspace_bytes=None, stream=None):
+    wb = _nbytes(workspace) if workspace_bytes is None else int(workspace_bytes)
+    _check(lib.mssa_forward_head_ring(plan.handle, _ptr(q_win), _ptr(k_sink), _ptr(v_sink), _ptr(k_ring),
+                                      _ptr(v_ring), _ptr_array(k_ring_pooled), _ptr_array(v_ring_pooled),
+                                      _ptr(k_win), _ptr(v_win), _ptr(workspace), wb, _ptr(out), ring.frames,
+                                      ring.count, ring.spare, _stream(stream)),
+           "mssa_forward_head_ring")
+
+
+def mssa_head_ring_roll(plan, ring):
+    count = ctypes.c_int32(ring.count)
+    spare = ctypes.c_int32(ring.spare)
+    _check(lib.mssa_head_ring_roll(plan.handle, ring.frames, ctypes.byref(count), ctypes.byref(spare)),
+           "mssa_head_ring_roll")
+    ring.count, ring.spare = count.value, spare.value
 
 
 class Ring:

@@ -17,6 +17,14 @@ pooled rings hold exactly the bytes re-pooling would give; outputs agree
 with the plain path up to the attention kernel's rounding (key tiles fall
 differently around the separate pooled-history run).
 
+With head_in_ring=True (pooled rings too) the cache roll moves no data: the
+native and pooled rings have cap + F slots, window state 1 of a pass is
+written by its producer straight into the F spare slots of the native ring
+(head_slots()), mssa_pool_kv_head_ring pools it into the same slots of the
+pooled rings, mssa_forward_head_ring reads history and state 1 from the
+rings and the rest of the window from k_win / v_win (states 2..T only), and
+mssa_head_ring_roll advances the ring state on the host.
+
 graph_pass() runs a whole pass (every layer) over static window buffers as
 one HIP graph: once every ring is full the plan no longer changes and the
 ring head cycles through cap / gcd(cap, F) positions, so one graph per head
@@ -33,11 +41,16 @@ from .workloads import input_shapes
 
 
 class StreamingMSSA:
-    def __init__(self, layer_desc, layers, hist_cap_frames, dtype="bf16", device="cuda", pooled_ring=False):
+    def __init__(self, layer_desc, layers, hist_cap_frames, dtype="bf16", device="cuda", pooled_ring=False,
+                 head_in_ring=False):
         import torch
 
-        self.pooled_ring = bool(pooled_ring)
-        self.desc = dict(layer_desc, flags=mssa.MSSA_PLAN_POOLED_HIST_RING if pooled_ring else 0)
+        self.head_in_ring = bool(head_in_ring)
+        self.pooled_ring = bool(pooled_ring) or self.head_in_ring
+        flags = mssa.MSSA_PLAN_POOLED_HIST_RING if self.pooled_ring else 0
+        if self.head_in_ring:
+            flags |= mssa.MSSA_PLAN_HEAD_IN_RING
+        self.desc = dict(layer_desc, flags=flags)
         self.layers = int(layers)
         self.cap = int(hist_cap_frames)
         self.dtype = dtype
@@ -51,13 +64,16 @@ class StreamingMSSA:
         nh, d = int(layer_desc["num_heads"]), int(layer_desc["head_dim"])
         ws = max(self.plan(h).info()["workspace_bytes"] for h in range(self.cap + 1))
         self.workspace = torch.empty(max(256, ws), dtype=torch.uint8, device=device)
-        shape = (self.cap * self.tok1, nh, d)
+        self.F = int(layer_desc["frames_per_state"])
+        # ring slots: the history cap, plus the spare slots of window state 1
+        self.slots = self.cap + (self.F if self.head_in_ring else 0)
+        shape = (self.slots * self.tok1, nh, d)
         self.k_ring = [torch.zeros(shape, dtype=self.tdtype, device=device) for _ in range(self.layers)]
         self.v_ring = [torch.zeros(shape, dtype=self.tdtype, device=device) for _ in range(self.layers)]
-        self.ring = [mssa.Ring(self.cap) for _ in range(self.layers)]
+        self.ring = [mssa.HeadRing(self.slots) if self.head_in_ring else mssa.Ring(self.cap)
+                     for _ in range(self.layers)]
         self.k_sink = [None] * self.layers
         self.v_sink = [None] * self.layers
-        self.F = int(layer_desc["frames_per_state"])
         self._win = None
         self._graphs = {}
         # Pooled-history rings [layer][group] (None for groups at scale 1).
@@ -69,7 +85,7 @@ class StreamingMSSA:
                 if sc == 1:
                     continue
                 tok_s = -(-gh // sc) * -(-gw // sc)
-                pshape = (self.cap * tok_s, nh, d)
+                pshape = (self.slots * tok_s, nh, d)
                 for layer in range(self.layers):
                     self.k_pool[layer][g] = torch.zeros(pshape, dtype=self.tdtype, device=device)
                     self.v_pool[layer][g] = torch.zeros(pshape, dtype=self.tdtype, device=device)
@@ -93,10 +109,17 @@ class StreamingMSSA:
         if n:
             self.k_ring[layer][: n * self.tok1].copy_(k_hist)
             self.v_ring[layer][: n * self.tok1].copy_(v_hist)
-        self.ring[layer] = mssa.Ring(self.cap, count=n, head=0)
+        self.ring[layer] = mssa.HeadRing(self.slots, count=n) if self.head_in_ring else mssa.Ring(self.cap, count=n)
         if self.pooled_ring and n:
             mssa.mssa_pool_hist_ring(self.plan(n), self.k_ring[layer], self.v_ring[layer],
                                      self.k_pool[layer], self.v_pool[layer])
+
+    def head_slots(self, layer):
+        """(k, v) views of the native ring's spare slots, where the producer
+        of window state 1's K/V writes them before the pass (head_in_ring)."""
+        r = self.ring[layer]
+        a, b = r.spare * self.tok1, (r.spare + self.F) * self.tok1
+        return self.k_ring[layer][a:b], self.v_ring[layer][a:b]
 
     def window_buffers(self):
         """Static per-layer window buffers {q_win, k_win, v_win, out} that
@@ -105,7 +128,9 @@ class StreamingMSSA:
 
         if self._win is None:
             sh = self.shapes(0)
-            self._win = [{k: torch.zeros(sh["q_win"], dtype=self.tdtype, device=self.device)
+            rest = (sh["k_win"][0] - (self.F * self.tok1 if self.head_in_ring else 0),) + tuple(sh["k_win"][1:])
+            self._win = [{k: torch.zeros(sh["q_win"] if k in ("q_win", "out") else rest, dtype=self.tdtype,
+                                         device=self.device)
                           for k in ("q_win", "k_win", "v_win", "out")} for _ in range(self.layers)]
         return self._win
 
@@ -122,7 +147,7 @@ class StreamingMSSA:
                 b = bufs[L]
                 self.layer_pass(L, b["q_win"], b["k_win"], b["v_win"], b["out"])
 
-        heads = {r.head for r in self.ring}
+        heads = {r.spare if self.head_in_ring else r.head for r in self.ring}
         if any(r.count != self.cap for r in self.ring) or len(heads) != 1:
             run_all()
             return "eager"
@@ -140,12 +165,25 @@ class StreamingMSSA:
             return "captured"
         g.replay()
         for r in self.ring:  # a full ring overwrites its F oldest slots
-            r.head = (r.head + self.F) % self.cap
+            if self.head_in_ring:
+                r.spare = (r.spare + self.F) % self.slots
+            else:
+                r.head = (r.head + self.F) % self.cap
         return "replayed"
 
     def layer_pass(self, layer, q_win, k_win, v_win, out, stream=None):
+        """One layer's pass.  head_in_ring: k_win / v_win hold window states
+        2..T only (state 1 is already in head_slots(layer))."""
         ring = self.ring[layer]
         plan = self.plan(ring.count)
+        if self.head_in_ring:
+            mssa.mssa_pool_kv_head_ring(plan, self.k_ring[layer], self.v_ring[layer], k_win, v_win, self.k_pool[layer],
+                                        self.v_pool[layer], self.workspace, ring, stream=stream)
+            mssa.mssa_forward_head_ring(plan, q_win, self.k_sink[layer], self.v_sink[layer], self.k_ring[layer],
+                                        self.v_ring[layer], self.k_pool[layer], self.v_pool[layer], k_win, v_win,
+                                        self.workspace, out, ring, stream=stream)
+            mssa.mssa_head_ring_roll(plan, ring)
+            return
         nh = ring.count * self.tok1
         kh = self.k_ring[layer][:nh] if nh else None
         vh = self.v_ring[layer][:nh] if nh else None
@@ -171,6 +209,34 @@ def init_inputs(stream_w, layer, shapes, device="cuda"):
     return make_inputs_device(shapes, stream_w["init_seed_base"] + layer, stream_w["amplitude"],
                               stream_w["dtype"], names=("k_sink", "v_sink", "k_hist", "v_hist"),
                               device=device)
+
+
+def window_inputs_head_ring(stream_w, pass_index, st, device="cuda"):
+    """Window Q/K/V of every layer for one pass of a head_in_ring driver: one
+    generator seeded seed_base + pass_index draws, layer by layer, q, then
+    K of state 1 (written into the layer's spare ring slots, as its producer
+    would), K of states 2..T, V of state 1 (ring) and V of states 2..T.
+    Returns per layer {q_win, k_win, v_win} with k_win / v_win the states
+    2..T only."""
+    import torch
+
+    gen = torch.Generator(device=device)
+    gen.manual_seed(int(stream_w["seed_base"] + pass_index))
+    tdt = torch.bfloat16 if stream_w["dtype"] == "bf16" else torch.float32
+    amp = stream_w["amplitude"]
+    shapes = st.shapes(0)
+    n_head = st.F * st.tok1
+    out = []
+    for layer in range(st.layers):
+        kh, vh = st.head_slots(layer)
+        rest = (shapes["k_win"][0] - n_head,) + tuple(shapes["k_win"][1:])
+        t = {"q_win": (torch.randn(shapes["q_win"], generator=gen, device=device) * amp).to(tdt)}
+        kh.copy_((torch.randn(kh.shape, generator=gen, device=device) * amp).to(tdt))
+        t["k_win"] = (torch.randn(rest, generator=gen, device=device) * amp).to(tdt)
+        vh.copy_((torch.randn(vh.shape, generator=gen, device=device) * amp).to(tdt))
+        t["v_win"] = (torch.randn(rest, generator=gen, device=device) * amp).to(tdt)
+        out.append(t)
+    return out
 
 
 def window_inputs(stream_w, pass_index, layers, shapes, device="cuda"):

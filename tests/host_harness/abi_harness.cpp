@@ -373,6 +373,39 @@ void exercise(const mssa_plan_desc& desc, int32_t attention_blocks) {
       for (int pass = 0; pass < 4; ++pass)
         expect(mssa_hist_append(plan, kw, vw, kr, vr, cap, &head, &count, nullptr), MSSA_OK, "hist_append");
     }
+  } else if (desc.flags & MSSA_PLAN_HEAD_IN_RING) {
+    // rings of N slots (a multiple of F, cap >= history); every spare position
+    const int F = desc.frames_per_state;
+    const int N = (static_cast<int>(ceil_div(desc.hist_frames, F)) + 2) * F;
+    std::vector<void*> kp(MSSA_MAX_STATES, nullptr), vp(MSSA_MAX_STATES, nullptr);
+    for (int g = 0; g < info.n_groups; ++g) {
+      const int s = info.group_scale[g];
+      if (s == 1) continue;
+      const int64_t tok_s = ceil_div(desc.grid_h, s) * ceil_div(desc.grid_w, s);
+      kp[g] = dev_alloc(N * tok_s * rb);
+      vp[g] = dev_alloc(N * tok_s * rb);
+    }
+    void* kr = dev_alloc(int64_t{N} * tok1 * rb);
+    void* vr = dev_alloc(int64_t{N} * tok1 * rb);
+    const int64_t rest = info.n_q - int64_t{F} * tok1;
+    void* kw2 = dev_alloc(rest * rb);
+    void* vw2 = dev_alloc(rest * rb);
+    for (int spare = 0; spare < N; spare += F) {
+      expect(mssa_pool_kv_head_ring(plan, kr, vr, kw2, vw2, kp.data(), vp.data(), ws, wsb, N, desc.hist_frames, spare,
+                                    nullptr),
+             MSSA_OK, "pool_kv_head_ring");
+      expect(mssa_forward_head_ring(plan, q, ks, vs, kr, vr, const_cast<const void* const*>(kp.data()),
+                                    const_cast<const void* const*>(vp.data()), kw2, vw2, ws, wsb, out, N,
+                                    desc.hist_frames, spare, nullptr),
+             MSSA_OK, "forward_head_ring");
+      int32_t c = desc.hist_frames, sp = spare;
+      expect(mssa_head_ring_roll(plan, N, &c, &sp), MSSA_OK, "head_ring_roll");
+      if (sp != (spare + F) % N || c != std::min(desc.hist_frames + F, N - F)) failure("head_ring_roll arithmetic");
+    }
+    expect(mssa_forward_head_ring(plan, q, ks, vs, kr, vr, const_cast<const void* const*>(kp.data()),
+                                  const_cast<const void* const*>(vp.data()), kw2, vw2, ws, wsb, out, N,
+                                  desc.hist_frames, 1, nullptr),
+           F == 1 ? MSSA_OK : MSSA_ERR_INVALID_ARG, "forward_head_ring at a misaligned spare slot");
   } else {
     std::vector<void*> kp(MSSA_MAX_STATES, nullptr), vp(MSSA_MAX_STATES, nullptr);
     const int cap = desc.hist_frames + desc.frames_per_state + 1;
@@ -451,7 +484,8 @@ void invalid_descriptors() {
       {"heads 0", [](mssa_plan_desc& d) { d.num_heads = 0; }, MSSA_ERR_INVALID_ARG},
       {"dtype 7", [](mssa_plan_desc& d) { d.dtype = 7; }, MSSA_ERR_INVALID_ARG},
       {"scale inf", [](mssa_plan_desc& d) { d.softmax_scale = 1.0f / 0.0f; }, MSSA_ERR_INVALID_ARG},
-      {"flags 4", [](mssa_plan_desc& d) { d.flags = 4; }, MSSA_ERR_INVALID_ARG},
+      {"flags 8", [](mssa_plan_desc& d) { d.flags = 8; }, MSSA_ERR_INVALID_ARG},
+      {"head in ring alone", [](mssa_plan_desc& d) { d.flags = MSSA_PLAN_HEAD_IN_RING; }, MSSA_ERR_UNSUPPORTED},
       {"scale 3", [](mssa_plan_desc& d) { d.scales[2] = 3; }, MSSA_ERR_UNSUPPORTED},
       {"scale 128", [](mssa_plan_desc& d) { d.scales[4] = 128; }, MSSA_ERR_UNSUPPORTED},
       {"decreasing", [](mssa_plan_desc& d) { d.scales[4] = 1; }, MSSA_ERR_UNSUPPORTED},
@@ -499,6 +533,10 @@ int main(int argc, char** argv) {
   for (int h = 6; h <= 21; h += 3)
     named.push_back({"streaming history " + std::to_string(h), make_desc(5, s12, 30, 52, 3, 3, h, 12, 128, MSSA_BF16,
                                                                        MSSA_PLAN_POOLED_HIST_RING)});
+  for (int h = 6; h <= 21; h += 3)
+    named.push_back({"streaming head in ring " + std::to_string(h),
+                     make_desc(5, s12, 30, 52, 3, 3, h, 12, 128, MSSA_BF16,
+                               MSSA_PLAN_POOLED_HIST_RING | MSSA_PLAN_HEAD_IN_RING)});
   for (const auto& c : named) {
     g_case = c.first;
     exercise(c.second, 0);
@@ -513,11 +551,13 @@ int main(int argc, char** argv) {
     int T = 1 + static_cast<int>(rnd(8)), sc[8];
     for (int l = 0; l < T; ++l) sc[l] = pick[rnd(5)];
     std::sort(sc, sc + T);
-    const int flags = static_cast<int>(rnd(4));
+    int flags = static_cast<int>(rnd(4));
+    const bool bf = rnd(4) != 0;
+    if ((flags & MSSA_PLAN_POOLED_HIST_RING) && sc[0] == 1 && bf && rnd(2)) flags |= MSSA_PLAN_HEAD_IN_RING;
     const mssa_plan_desc d = make_desc(T, sc, 1 + static_cast<int>(rnd(70)), 1 + static_cast<int>(rnd(90)),
                                        1 + static_cast<int>(rnd(4)), static_cast<int>(rnd(5)),
                                        static_cast<int>(rnd(26)), 1 + static_cast<int>(rnd(48)),
-                                       rnd(2) ? 128 : 64, rnd(4) ? MSSA_BF16 : MSSA_F32, flags);
+                                       rnd(2) ? 128 : 64, bf ? MSSA_BF16 : MSSA_F32, flags);
     g_case = "random descriptor " + std::to_string(i) + " T=" + std::to_string(T) + " sc0=" + std::to_string(sc[0]) +
              " last=" + std::to_string(sc[T - 1]) + " H=" + std::to_string(d.grid_h) + " W=" + std::to_string(d.grid_w) +
              " F=" + std::to_string(d.frames_per_state) + " S=" + std::to_string(d.sink_frames) +

@@ -214,7 +214,7 @@ def test_pooled_hist_ring_calls_checked():
     rejected at plan creation."""
     desc = WORKLOADS["wan13b_layer"]["desc"]
     with pytest.raises(mssa.MssaError) as e:
-        _plan(desc, flags=4)
+        _plan(desc, flags=8)
     assert e.value.status == mssa.MSSA_ERR_INVALID_ARG
     plain, ring = _plan(desc), _plan(desc, flags=RING)
     fake = 1 << 20
@@ -314,3 +314,62 @@ def test_backward_workspace_layout():
         want = a256(info["workspace_bytes"]) + 2 * a256(nh * nq * 4)
         want += sum(2 * a256(n_kv * nh * d * 4) for n_kv in info["n_kv"][: info["n_groups"]])
         assert mssa.mssa_backward_workspace_size(plan) == want
+
+
+HEAD = mssa.MSSA_PLAN_HEAD_IN_RING
+
+
+def test_head_in_ring_plan_rules():
+    """The copy-free cache roll needs pooled rings, a native head state and
+    bf16; its plan keeps the Eq. 4 tables and FLOP, and its pool reads state
+    1 once and writes it pooled to every coarser scale."""
+    desc = STREAMING["layer"]
+    for bad in (dict(flags=HEAD), dict(flags=RING | HEAD, scales=[2, 2, 2, 4, 4]),
+                dict(flags=RING | HEAD, dtype="f32")):
+        with pytest.raises(mssa.MssaError) as e:
+            _plan(dict(desc, hist_frames=6), **bad)
+        assert e.value.status == mssa.MSSA_ERR_UNSUPPORTED
+    ring, head = _plan(dict(desc, hist_frames=21), flags=RING), _plan(dict(desc, hist_frames=21), flags=RING | HEAD)
+    a, b = ring.tables(), head.tables()
+    for key in ("GRID", "QGRP", "SEG", "TOTAL"):
+        assert np.array_equal(a[key], b[key]), key
+    ia, ib = ring.info(), head.info()
+    assert ia["flops_alg"] == ib["flops_alg"]
+    # state 1 (3 native frames) leaves the workspace's pooled block
+    assert ib["pooled_tokens"][1] == ia["pooled_tokens"][1] - 3 * 390
+    # pool traffic: the same, state 1 now pooled into the rings (read 3 x 1560,
+    # write 3 x 390 tokens, K and V)
+    assert ib["pool_bytes_alg"] == ia["pool_bytes_alg"]
+
+
+def test_head_ring_roll_and_state_checks():
+    """The roll is host-only arithmetic on (count, spare); ring states that
+    break the rules are rejected before anything is enqueued."""
+    desc = dict(STREAMING["layer"], dtype="bf16")
+    plans = {h: _plan(dict(desc, hist_frames=h), flags=RING | HEAD) for h in range(0, 22, 3)}
+    r = mssa.HeadRing(24, count=6)
+    seen = []
+    for _ in range(12):
+        mssa.mssa_head_ring_roll(plans[r.count], r)
+        seen.append((r.count, r.spare))
+    assert seen == [(9, 9), (12, 12), (15, 15), (18, 18), (21, 21), (21, 0), (21, 3), (21, 6), (21, 9),
+                    (21, 12), (21, 15), (21, 18)]
+    fake = 1 << 20
+    pools = [None, fake]
+    for frames, count, spare in ((23, 6, 6), (24, 6, 7), (24, 6, 24), (24, 9, 6), (3, 0, 0)):
+        with pytest.raises(mssa.MssaError) as e:
+            mssa.mssa_forward_head_ring(plans[6], fake, fake, fake, fake, fake, pools, pools, fake, fake, fake,
+                                        fake + 4096, mssa.HeadRing(frames, count, spare), workspace_bytes=1 << 30,
+                                        stream=0)
+        assert e.value.status == mssa.MSSA_ERR_INVALID_ARG, (frames, count, spare)
+        with pytest.raises(mssa.MssaError) as e:
+            mssa.mssa_head_ring_roll(plans[6], mssa.HeadRing(frames, count, spare))
+        assert e.value.status == mssa.MSSA_ERR_INVALID_ARG
+    with pytest.raises(mssa.MssaError) as e:
+        mssa.mssa_pool_kv_head_ring(_plan(dict(desc, hist_frames=6), flags=RING), fake, fake, fake, fake, pools,
+                                    pools, fake, mssa.HeadRing(24, 6), workspace_bytes=1 << 30, stream=0)
+    assert e.value.status == mssa.MSSA_ERR_UNSUPPORTED
+    with pytest.raises(mssa.MssaError) as e:
+        mssa.mssa_pool_kv_head_ring(plans[6], fake, fake, fake, fake, [None, None], pools, fake,
+                                    mssa.HeadRing(24, 6), workspace_bytes=1 << 30, stream=0)
+    assert e.value.status == mssa.MSSA_ERR_INVALID_ARG

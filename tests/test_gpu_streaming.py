@@ -10,7 +10,7 @@ import torch
 
 import oracle
 from paper_2607_20940_amd.inputs import to_f64
-from paper_2607_20940_amd.streaming import StreamingMSSA, init_inputs, window_inputs
+from paper_2607_20940_amd.streaming import StreamingMSSA, init_inputs, window_inputs, window_inputs_head_ring
 from paper_2607_20940_amd.workloads import STREAMING
 
 from gpu_common import assert_close
@@ -22,11 +22,28 @@ def _f64(t):
     return None if t is None else t.float().cpu().numpy().astype(np.float64)
 
 
-def _run(stream_w, layers, passes, check, pooled_ring=False):
+def _window(stream_w, p, st, win_shapes):
+    """This pass's window inputs of every layer: (what layer_pass takes,
+    the full window {q_win, k_win, v_win} the oracle reads).  With the head
+    state in the ring, its K/V are read back from the spare slots its
+    producer wrote."""
+    if not st.head_in_ring:
+        wins = window_inputs(stream_w, p, st.layers, win_shapes)
+        return wins, wins
+    wins = window_inputs_head_ring(stream_w, p, st)
+    full = []
+    for L in range(st.layers):
+        kh, vh = st.head_slots(L)
+        full.append({"q_win": wins[L]["q_win"], "k_win": torch.cat([kh, wins[L]["k_win"]]),
+                     "v_win": torch.cat([vh, wins[L]["v_win"]])})
+    return wins, full
+
+
+def _run(stream_w, layers, passes, check, pooled_ring=False, head_in_ring=False):
     desc = stream_w["layer"]
     F = desc["frames_per_state"]
     st = StreamingMSSA(desc, layers, stream_w["hist_cap_frames"], dtype=stream_w["dtype"],
-                       pooled_ring=pooled_ring)
+                       pooled_ring=pooled_ring, head_in_ring=head_in_ring)
     tok1 = st.tok1
     hist = {}
     init_shapes = st.shapes(stream_w["hist_start_frames"])
@@ -41,11 +58,11 @@ def _run(stream_w, layers, passes, check, pooled_ring=False):
     win_shapes = st.shapes(0)
     checked = 0
     for p in range(passes):
-        wins = window_inputs(stream_w, p, layers, win_shapes)
+        args, wins = _window(stream_w, p, st, win_shapes)
         for L in range(layers):
             w = wins[L]
             out = torch.empty_like(w["q_win"])
-            st.layer_pass(L, w["q_win"], w["k_win"], w["v_win"], out)
+            st.layer_pass(L, args[L]["q_win"], args[L]["k_win"], args[L]["v_win"], out)
             h = hist[L]
             if check(p, L):
                 torch.cuda.synchronize()
@@ -128,6 +145,67 @@ def test_streaming_pooled_ring_stride_every_output():
     w = dict(SMALL, layer=dict(SMALL["layer"], resample="stride"))
     st, n = _run(w, layers=2, passes=7, check=lambda p, L: (None, None), pooled_ring=True)
     assert n == 14
+
+
+@pytest.mark.parametrize("layer", [
+    SMALL["layer"],
+    # two coarse query scales, ragged at scale 4; strided subsampling
+    dict(num_states=4, scales=[1, 2, 4, 4], grid_h=6, grid_w=10, frames_per_state=1, sink_frames=1,
+         hist_frames=0, num_heads=2, head_dim=64, resample="stride"),
+])
+def test_streaming_head_in_ring_every_output(layer):
+    """The cache roll without copies: window state 1 written by its producer
+    into the rings' spare slots, history and state 1 read from the rings
+    through several wrap-arounds (cap + F slots), every output of two layers
+    against the oracle."""
+    w = dict(SMALL, layer=layer)
+    st, n = _run(w, layers=2, passes=9, check=lambda p, L: (None, None), head_in_ring=True)
+    assert n == 18
+    F = layer["frames_per_state"]
+    assert [r.count for r in st.ring] == [w["hist_cap_frames"]] * 2
+    # 9 passes, each advancing the spare slots by F, modulo cap + F slots
+    assert [r.spare for r in st.ring] == [(w["hist_start_frames"] + 9 * F) % (w["hist_cap_frames"] + F)] * 2
+
+
+def test_graph_pass_equals_eager_head_in_ring():
+    """Whole passes of the copy-free cache roll replayed as HIP graphs (one
+    per spare-slot position) equal the eager passes bit for bit: outputs and
+    every ring, over several cycles of positions."""
+    w = dict(SMALL, hist_cap_frames=6)
+    layers = 2
+    eager = StreamingMSSA(w["layer"], layers, w["hist_cap_frames"], dtype="bf16", head_in_ring=True)
+    graph = StreamingMSSA(w["layer"], layers, w["hist_cap_frames"], dtype="bf16", head_in_ring=True)
+    shapes = eager.shapes(w["hist_start_frames"])
+    for L in range(layers):
+        x = init_inputs(w, L, shapes)
+        eager.init_layer(L, x["k_sink"], x["v_sink"], x["k_hist"], x["v_hist"])
+        graph.init_layer(L, x["k_sink"], x["v_sink"], x["k_hist"], x["v_hist"])
+    bufs = graph.window_buffers()
+    replays = 0
+    for p in range(14):
+        wins = window_inputs_head_ring(w, p, eager)
+        outs = []
+        for L in range(layers):
+            for dst, src in zip(graph.head_slots(L), eager.head_slots(L)):
+                dst.copy_(src)
+            for k in ("q_win", "k_win", "v_win"):
+                bufs[L][k].copy_(wins[L][k])
+            o = torch.empty_like(wins[L]["q_win"])
+            eager.layer_pass(L, wins[L]["q_win"], wins[L]["k_win"], wins[L]["v_win"], o)
+            outs.append(o)
+        replays += graph.graph_pass() != "eager"
+        torch.cuda.synchronize()
+        print(f"[graph-head] pass {p} graph={replays} spare={graph.ring[0].spare} count={graph.ring[0].count}",
+              flush=True)
+        for L in range(layers):
+            assert torch.equal(outs[L].view(torch.int16), bufs[L]["out"].view(torch.int16)), (p, L)
+            assert (eager.ring[L].spare, eager.ring[L].count) == (graph.ring[L].spare, graph.ring[L].count)
+            assert torch.equal(eager.k_ring[L].view(torch.int16), graph.k_ring[L].view(torch.int16)), (p, L)
+            for g, t in enumerate(eager.v_pool[L]):
+                if t is not None:
+                    assert torch.equal(t.view(torch.int16), graph.v_pool[L][g].view(torch.int16)), (p, L, g)
+    # 2 + 2 frames per pass: full after pass 1; 8 slots = 4 spare positions
+    assert replays == 12 and len(graph._graphs) == 4
 
 
 @pytest.mark.parametrize("layer", [
@@ -228,7 +306,8 @@ def test_graph_pass_equals_eager(pooled_ring):
     assert replays == 10 and len(graph._graphs) == 3
 
 
-def test_streaming_full_workload_sampled():
+@pytest.mark.parametrize("head_in_ring", [False, True])
+def test_streaming_full_workload_sampled(head_in_ring):
     """The whole streaming workload: 30 stacked layers of the Wan-1.3B shape
     over 64 rolling passes with pooled-history rings (history 6 -> 21 frames,
     then FIFO).  Six (pass, layer) points, including the last layer of the
@@ -242,7 +321,7 @@ def test_streaming_full_workload_sampled():
     points = {(0, 0), (4, 29), (5, 14), (20, 7), (47, 21), (63, 29)}
     tracked = sorted({L for (_, L) in points})
     heads = [0, 11]
-    st = StreamingMSSA(desc, layers, cap, dtype=w["dtype"], pooled_ring=True)
+    st = StreamingMSSA(desc, layers, cap, dtype=w["dtype"], pooled_ring=True, head_in_ring=head_in_ring)
     tok1 = st.tok1
 
     def host(t):  # selected heads, bf16 bits on the host
@@ -266,9 +345,9 @@ def test_streaming_full_workload_sampled():
     outs = [torch.empty(win_shapes["q_win"], dtype=torch.bfloat16, device="cuda") for _ in range(layers)]
     checked = 0
     for p in range(passes):
-        wins = window_inputs(w, p, layers, win_shapes)
+        args, wins = _window(w, p, st, win_shapes)
         for L in range(layers):
-            st.layer_pass(L, wins[L]["q_win"], wins[L]["k_win"], wins[L]["v_win"], outs[L])
+            st.layer_pass(L, args[L]["q_win"], args[L]["k_win"], args[L]["v_win"], outs[L])
             if L not in tracked:
                 continue
             h = hist[L]
