@@ -16,7 +16,9 @@
 //                      output columns may be split over up to three tensors
 //                      (q | k | v); gemm_dma_kernel is the same product for
 //                      K a multiple of 64 with 64-deep stages filled by
-//                      direct global -> LDS transfers;
+//                      direct global -> LDS transfers; gemm256_kernel the
+//                      same in 256 x 256 tiles (K a multiple of 64, at least
+//                      256 rows and features);
 //   unpatchify_kernel  patch rows [tokens, C*P*P] -> latent pixels.
 #include <hip/hip_runtime.h>
 
@@ -267,6 +269,132 @@ __global__ __launch_bounds__(kTierThreads, 2) void gemm_dma_kernel(GemmArgs a) {
   }
 }
 
+// The same product for K a multiple of 64 and at least 256 rows and output
+// features, in 256 x 256 output tiles: the operand bytes each tile streams
+// from L2 per multiply-add are half those of a 128 x 128 tile.  A block of 8
+// waves (two per SIMD) owns the tile; wave w owns rows 128 (w & 1) .. +127
+// and features 64 (w >> 1) .. +63 as 4 x 2 matrix-core tiles (A = W rows,
+// B = X rows).  K streams in 64-deep stages of 128-byte rows (whole cache
+// lines; the swizzle of lds_stage.hpp's 128-byte rows) through two LDS
+// buffers, each stage filled by direct global -> LDS transfers issued while
+// the previous one is multiplied; one barrier per stage.  Tiles are taken in
+// panels of four feature tiles, each XCD a contiguous run of them, so that
+// the blocks of an XCD share operand rows in its L2.
+constexpr int kBM = 256, kBN = 256, kBK = 64, kBStages = 2, kBThreads = 512, kBPanel = 4;
+constexpr int kBTile = kBM * kBK * 2;  // bytes of one operand tile of a stage
+
+__global__ __launch_bounds__(kBThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void gemm256_kernel(GemmArgs a) {
+  __shared__ __attribute__((aligned(16))) char lds[kBStages][2][kBTile];  // [stage][X | W]
+  const int tiles_m = (a.M + kBM - 1) / kBM, tiles_n = (a.N + kBN - 1) / kBN, T = tiles_m * tiles_n;
+  // blockIdx -> tile: blocks are dispatched round-robin over the 8 XCDs
+  const int b = blockIdx.x, q8 = T / 8, r8 = T % 8, x8 = b % 8, j8 = b / 8;
+  const int t = (x8 < r8 ? x8 * (q8 + 1) : r8 * (q8 + 1) + (x8 - r8) * q8) + j8;
+  const int panel = t / (tiles_m * kBPanel), pw = min(kBPanel, tiles_n - panel * kBPanel);
+  const int ip = t - panel * tiles_m * kBPanel;
+  const int tm = ip / pw, tn = panel * kBPanel + ip % pw;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave & 1, wn = wave >> 1;
+  const int n32 = lane & 31, hh = lane >> 5;
+
+  // This wave's transfers of a stage: 1 KB (8 rows of 128 bytes) each, rows
+  // 8 (4 wave + i) + lane / 8, physical chunk lane % 8 holding logical chunk
+  // unswz128(row, lane % 8).  Rows past the matrix edge fall past the range:
+  // zeros.
+  const uint32_t xrb = static_cast<uint32_t>(a.ldx) * 2, wrb = static_cast<uint32_t>(a.K) * 2;
+  uint32_t xo[4], wo[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = (wave * 4 + i) * 8 + (lane >> 3), lc = unswz128(row, lane & 7);
+    xo[i] = row * xrb + lc * 16;
+    wo[i] = row * wrb + lc * 16;
+  }
+  const int mrows = min(kBM, a.M - tm * kBM), nrows = min(kBN, a.N - tn * kBN);
+  const __bf16* X = static_cast<const __bf16*>(a.x) + static_cast<int64_t>(tm) * kBM * a.ldx;
+  const __bf16* W = static_cast<const __bf16*>(a.w) + static_cast<int64_t>(tn) * kBN * a.K;
+  const uint32_t xbytes = static_cast<uint32_t>(mrows - 1) * xrb + kBK * 2;
+  const uint32_t wbytes = static_cast<uint32_t>(nrows - 1) * wrb + kBK * 2;
+  const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(&lds[0][0][0]));
+  auto issue = [&](int st) {
+    const i32x4 rx = rsrc_of(X + st * kBK, xbytes), rw = rsrc_of(W + st * kBK, wbytes);
+    const uint32_t base = lds0 + (st % kBStages) * 2 * kBTile + wave * 4096;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      dma16(rx, xo[i], __builtin_amdgcn_readfirstlane(base + i * 1024));
+      dma16(rw, wo[i], __builtin_amdgcn_readfirstlane(base + kBTile + i * 1024));
+    }
+  };
+
+  f32x16 acc[4][2];
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) acc[mb][nb] = f32x16{};
+
+  // The bias of this lane's 32 output features, loaded before the loop.
+  bf16x4 bias[2][4];
+#pragma unroll
+  for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+      const int col = tn * kBN + wn * 64 + nb * 32 + 8 * jj + 4 * hh;
+      bias[nb][jj] = col < a.N ? *reinterpret_cast<const bf16x4*>(static_cast<const __bf16*>(a.bias) + col) : bf16x4{};
+    }
+
+  // Operand reads: row (block base + n32), columns 16 ks + 8 hh; the swizzle
+  // of a row depends only on n32 (block bases are multiples of 32).
+  int rd[4];
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) rd[ks] = (swz128(n32, ks * 16 + hh * 8)) * 2;
+
+  const int nst = a.K / kBK;
+  issue(0);
+  for (int st = 0; st < nst; ++st) {
+    wait_vmcnt<0>();
+    __syncthreads();
+    if (st + 1 < nst) issue(st + 1);
+    const char* Xs = lds[st % kBStages][0];
+    const char* Ws = lds[st % kBStages][1];
+#pragma unroll
+    for (int ks = 0; ks < kBK / 16; ++ks) {
+      bf16x8 wa[2], xb[4];
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+        wa[nb] = *reinterpret_cast<const bf16x8*>(Ws + (wn * 64 + nb * 32) * 128 + rd[ks]);
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb)
+        xb[mb] = *reinterpret_cast<const bf16x8*>(Xs + (wm * 128 + mb * 32) * 128 + rd[ks]);
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb)
+          acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wa[nb], xb[mb], acc[mb][nb], 0, 0, 0);
+    }
+  }
+
+  // acc[mb][nb] element e: row (wm*128 + mb*32 + n32), feature
+  // (wn*64 + nb*32 + 8(e/4) + 4hh + e%4) of the tile.
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb) {
+    const int64_t row = static_cast<int64_t>(tm) * kBM + wm * 128 + mb * 32 + n32;
+    if (row >= a.M) continue;
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        const int col = tn * kBN + wn * 64 + nb * 32 + 8 * jj + 4 * hh;
+        if (col >= a.N) continue;
+        const int part = col / a.split, pc = col % a.split;  // 4 features never straddle a split (split % 4 == 0)
+        bf16x4 v;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] = static_cast<__bf16>(acc[mb][nb][4 * jj + i] + static_cast<float>(bias[nb][jj][i]));
+        *reinterpret_cast<bf16x4*>(static_cast<__bf16*>(a.y[part]) + row * a.ldy + pc) = v;
+      }
+  }
+}
+
 }  // namespace
 
 hipError_t launch_patchify(const PatchArgs& a, hipStream_t stream) {
@@ -287,6 +415,12 @@ hipError_t launch_unpatchify(const PatchArgs& a, hipStream_t stream) {
 
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t stream) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
+  const int64_t tiles = static_cast<int64_t>((a.M + kBM - 1) / kBM) * ((a.N + kBN - 1) / kBN);
+  // enough tiles to fill the CUs; the bias read in 8-byte pieces
+  if (a.K % kBK == 0 && a.N >= kBN && a.M >= kBM && tiles >= 256 && (reinterpret_cast<uintptr_t>(a.bias) & 7) == 0) {
+    hipLaunchKernelGGL(gemm256_kernel, dim3(static_cast<uint32_t>(tiles)), dim3(kBThreads), 0, stream, a);
+    return hipGetLastError();
+  }
   const int64_t blocks = static_cast<int64_t>((a.M + kGM - 1) / kGM) * ((a.N + kGN - 1) / kGN);
   if (a.K % kG2K == 0)
     hipLaunchKernelGGL(gemm_dma_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kTierThreads), 0, stream, a);

@@ -153,6 +153,22 @@ def test_tiers_wan13b_layer_shapes():
     torch.cuda.synchronize()
     _close(_f64(tok), oracle.patch_embed(desc, patch, lat64, wd, bd), "wan13b embed")
     _close(_f64(out), oracle.patch_unembed(desc, patch, C, x64, wod, bod), "wan13b unembed")
-    rows = np.unique(np.concatenate([[0, 1, 127, 128, 9359, 9360, nq - 1], rng.integers(0, nq, 40)]))
-    for got, ref, nm in zip((q, k, v), oracle.qkv_project(x64[rows], wq64, bq64, 12), "qkv"):
-        _close(_f64(got)[rows], ref, f"wan13b {nm}")
+    for got, ref, nm in zip((q, k, v), oracle.qkv_project(x64, wq64, bq64, 12), "qkv"):
+        _close(_f64(got), ref, f"wan13b {nm}")
+
+
+def test_qkv_projection_large_ragged():
+    """The 256 x 256-tile product with both edges ragged: 4452 tokens (17
+    full row tiles and 100 rows) and 3 x 1344 = 4032 features (15 full
+    feature tiles and 192 features), every output against the oracle."""
+    n, heads, d = 4452, 21, 64
+    rng = np.random.default_rng(41)
+    hidden = heads * d
+    x, x64 = _bf16(rng, (n, hidden))
+    w, w64 = _bf16(rng, (3 * hidden, hidden), 1.0 / np.sqrt(hidden))
+    b, b64 = _bf16(rng, (3 * hidden,), 0.1)
+    q, k, v = (torch.empty((n, heads, d), dtype=torch.bfloat16, device="cuda") for _ in range(3))
+    mssa.mssa_qkv_project(n, hidden, x, w, b, q, k, v)
+    torch.cuda.synchronize()
+    for got, ref, nm in zip((q, k, v), oracle.qkv_project(x64, w64, b64, heads), "qkv"):
+        _close(_f64(got), ref, f"qkv ragged {nm}")
