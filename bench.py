@@ -442,6 +442,27 @@ def bench_tiers(args):
         "qkv_pct_of_bf16_peak": round(100 * qkv_flops / (t[1] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 2),
         "embed_unembed_tflops": round(2 * emb_flops / ((t[0] + t[2]) * 1e-3) / 1e12, 2),
     }
+    # The same projection at the Wan-14B-shaped 720p window (width 40 x 128):
+    # enough output tiles that the last round of blocks is a small share.
+    d14 = WORKLOADS["wan14b_720p"]["desc"]
+    n14 = mssa.mssa_plan_create(dict(d14, dtype="bf16")).info()["n_q"]
+    h14 = d14["num_heads"] * d14["head_dim"]
+    x14, w14, b14 = rnd(n14, h14), rnd(3 * h14, h14), rnd(3 * h14)
+    o14 = [torch.empty((n14, h14), dtype=torch.bfloat16, device="cuda") for _ in range(3)]
+    for _ in range(max(args.warmup, 2)):
+        mssa.mssa_qkv_project(n14, h14, x14, w14, b14, *o14)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = max(args.steps // 4, 3)
+    e0.record(stream)
+    for _ in range(reps):
+        mssa.mssa_qkv_project(n14, h14, x14, w14, b14, *o14)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms14 = e0.elapsed_time(e1) / reps
+    f14 = 2.0 * n14 * h14 * 3 * h14
+    result["qkv_wan14b_720p"] = {"m_n_k": [n14, 3 * h14, h14], "ms": round(ms14, 4),
+                                 "tflops": round(f14 / (ms14 * 1e-3) / 1e12, 2),
+                                 "pct_of_bf16_peak": round(100 * f14 / (ms14 * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 2)}
     print(json.dumps(result), flush=True)
 
 
