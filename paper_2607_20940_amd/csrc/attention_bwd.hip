@@ -249,43 +249,53 @@ void dq_kernel(BwdArgs a) {
   // P exchange block of this pair, buffer pbuf: [32-key block][16-key half][lane] x 16 bytes
   auto px = [&](int pbuf) { return reinterpret_cast<bf16x8*>(lds + 3 * STB + (pbuf * 4 + pair) * PXB) + lane; };
 
-  // One stage of the wave's role on stage buffer buf.  Element e of a 32x32
-  // accumulator in this layout holds key kb*32 + 8(e/4) + 4hh + e%4 of the
-  // lane's query; packed to bf16 in pairs of 8 it is the B operand (16 keys
-  // each) of dQ^T += K^T dS^T.
+  // One stage of the wave's role on stage buffer buf: the row products of
+  // both 32-key blocks first, then the VALU work on both, then (B) the dQ
+  // products, so that one block's VALU work can run under the other's MFMAs.
+  // Element e of a 32x32 accumulator in this layout holds key
+  // kb*32 + 8(e/4) + 4hh + e%4 of the lane's query; packed to bf16 in pairs
+  // of 8 it is the B operand (16 keys each) of dQ^T += K^T dS^T.
   auto stage = [&](int buf, int pbuf, int nvalid) {
     const __bf16* Ks = reinterpret_cast<const __bf16*>(lds + buf * STB);
     const __bf16* Vs = reinterpret_cast<const __bf16*>(lds + buf * STB + KT);
     const __bf16* Xs = role == 0 ? Ks : Vs;
     bf16x8* pex = px(pbuf);
+    f32x16 s[NKB];
 #pragma unroll
-    for (int kb = 0; kb < NKB; ++kb) {
-      f32x16 s;
+    for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
         const bf16x8 ax = *reinterpret_cast<const bf16x8*>(Xs + kb * 32 * 128 + (r_rd ^ (ks * 16)));
-        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ax, xf[ks], ks == 0 ? f32x16{} : s, 0, 0, 0);
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ax, xf[ks], ks == 0 ? f32x16{} : s[kb], 0, 0, 0);
       }
-      if (role == 0) {
+    if (role == 0) {
+#pragma unroll
+      for (int kb = 0; kb < NKB; ++kb) {
         if (nvalid < BN) {  // the last stage of a run: keys past its end get P = 0
 #pragma unroll
           for (int e = 0; e < 16; ++e)
-            if (kb * 32 + 8 * (e >> 2) + 4 * hh + (e & 3) >= nvalid) s[e] = -INFINITY;
+            if (kb * 32 + 8 * (e >> 2) + 4 * hh + (e & 3) >= nvalid) s[kb][e] = -INFINITY;
         }
         bf16x8 pb[2];
 #pragma unroll
         for (int e = 0; e < 16; ++e)
-          pb[e >> 3][e & 7] = static_cast<__bf16>(__builtin_amdgcn_exp2f(__builtin_fmaf(s[e], c, -rstat)));
+          pb[e >> 3][e & 7] = static_cast<__bf16>(__builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][e], c, -rstat)));
         pex[(kb * 2) * 64] = pb[0];
         pex[(kb * 2 + 1) * 64] = pb[1];
-      } else {
+      }
+    } else {
+      bf16x8 dsb[NKB][2];
+#pragma unroll
+      for (int kb = 0; kb < NKB; ++kb) {
         const bf16x8 p0 = pex[(kb * 2) * 64], p1 = pex[(kb * 2 + 1) * 64];
-        bf16x8 dsb[2];
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const float p = static_cast<float>((e < 8 ? p0 : p1)[e & 7]);
-          dsb[e >> 3][e & 7] = static_cast<__bf16>(p * (s[e] - rstat));
+          dsb[kb][e >> 3][e & 7] = static_cast<__bf16>(p * (s[kb][e] - rstat));
         }
+      }
+#pragma unroll
+      for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
         for (int cc = 0; cc < 2; ++cc)
 #pragma unroll
@@ -294,9 +304,8 @@ void dq_kernel(BwdArgs a) {
             const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(r0 + t_rd[db][0]));
             const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(r0 + t_rd[db][1]));
             acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7),
-                                                              dsb[cc], acc[db], 0, 0, 0);
+                                                              dsb[kb][cc], acc[db], 0, 0, 0);
           }
-      }
     }
   };
 
@@ -315,7 +324,13 @@ void dq_kernel(BwdArgs a) {
       stage(it % 3, it & 1, min(cs.left, BN));
       step(cs);
     }
-    if (role != 0 && it >= 1) stage((it - 1) % 3, (it - 1) & 1, BN);
+    if (role != 0 && it >= 1) {
+      // B carries two thirds of the MFMAs and the dependent chain
+      // dP -> dS -> dQ: its instructions go first when both waves are ready.
+      __builtin_amdgcn_s_setprio(2);
+      stage((it - 1) % 3, (it - 1) & 1, BN);
+      __builtin_amdgcn_s_setprio(0);
+    }
     wait_vmcnt<0>();
     __syncthreads();
   }
