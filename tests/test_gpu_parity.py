@@ -107,6 +107,19 @@ def test_deterministic():
     assert torch.equal(a.view(torch.int16), b.view(torch.int16))
 
 
+def test_deterministic_full_size():
+    """Bitwise-equal outputs over three passes of the 21-frame-history layer
+    in the benchmark's launch configuration (persistent schedule, split
+    items merged in range order)."""
+    w = WORKLOADS["wan13b_longhist"]
+    print("[parity] full-size determinism", flush=True)
+    r = GpuRun(w["desc"], w["dtype"], w["seed"], w["amplitude"])
+    a = r.run().clone()
+    for _ in range(2):
+        b = r.run(torch.empty_like(a))
+        assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
 # ------------------------------------------------------------------ pooling
 
 
