@@ -32,6 +32,7 @@ PEAK_HBM_GBPS = 8000.0
 METRIC = "MSSA effective TFLOP/s + ms per rolling pass; % of bf16 MFMA peak (1 GPU)"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "mssa_fwd_traffic_{workload}.txt")
 FWD_SOURCE = os.path.join(ROOT, "paper_2607_20940_amd", "csrc", "attention_fwd.hip")
+POOL_SOURCE = os.path.join(ROOT, "paper_2607_20940_amd", "csrc", "pool_kv.hip")
 
 
 def log(msg):
@@ -39,18 +40,20 @@ def log(msg):
 
 
 class ClockSampler:
-    """The GPU's current shader clock, sampled from a host thread while named
-    sections of the benchmark run: the starred line of the amdgpu driver's
-    pp_dpm_sclk ("S: <MHz> *" is the measured current clock).  The sustained
-    clock under a long MFMA load is set by power, not by the 2.4 GHz peak the
-    roofline's peak assumes, so the % of peak depends on it."""
+    """The GPU's current shader and memory clocks, sampled from a host thread
+    while named sections of the benchmark run: the starred lines of the amdgpu
+    driver's pp_dpm_sclk and pp_dpm_mclk ("S: <MHz> *" is the current level).
+    The sustained shader clock under a long MFMA load is set by power, not by
+    the 2.4 GHz peak the roofline's peak assumes, so the % of peak depends on
+    it."""
 
-    def __init__(self, period_s=0.01):
+    def __init__(self, period_s=0.01, kind="sclk"):
         import glob
         import threading
 
-        paths = sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk"))
+        paths = sorted(glob.glob(f"/sys/class/drm/card*/device/pp_dpm_{kind}"))
         self.path = paths[0] if paths else None
+        self.kind = kind
         self.period = period_s
         self.samples = {}
         self.current = None
@@ -99,7 +102,7 @@ class ClockSampler:
 
     def summary(self):
         if not self.path:
-            return {"source": None, "note": "no pp_dpm_sclk readable on this host"}
+            return {"source": None, "note": f"no pp_dpm_{self.kind} readable on this host"}
         out = {"source": self.path, "period_ms": self.period * 1e3}
         for name, v in self.samples.items():
             a = np.array(v)
@@ -108,14 +111,41 @@ class ClockSampler:
         return out
 
 
-def kernel_source_hash():
-    with open(FWD_SOURCE, "rb") as f:
+class Clocks:
+    """Shader and memory clocks sampled together (see ClockSampler)."""
+
+    def __init__(self):
+        self.samplers = [ClockSampler(kind="sclk"), ClockSampler(kind="mclk")]
+
+    def start(self):
+        for c in self.samplers:
+            c.start()
+
+    def stop(self):
+        for c in self.samplers:
+            c.stop()
+
+    def section(self, name):
+        import contextlib
+
+        stack = contextlib.ExitStack()
+        for c in self.samplers:
+            stack.enter_context(c.section(name))
+        return stack
+
+    def summary(self):
+        return {f"{c.kind}_mhz": c.summary() for c in self.samplers}
+
+
+def kernel_source_hash(path=None):
+    with open(path or FWD_SOURCE, "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def read_traffic(workload):
-    """HBM bytes per forward launch from the committed counter summary, if it
-    was taken on the current attention kernel source (else None)."""
+def read_traffic(workload, kernel="forward"):
+    """HBM bytes per launch of the attention call (kernel="forward") or of
+    mssa_pool_kv (kernel="pool") from the committed counter summary, if it
+    was taken on the current source of that kernel (else None)."""
     path = TRAFFIC_FILE.format(workload=workload)
     if not os.path.exists(path):
         return None
@@ -125,10 +155,14 @@ def read_traffic(workload):
             if ":" in line and not line.startswith("#"):
                 k, v = line.split(":", 1)
                 vals[k.strip()] = v.strip()
-    if vals.get("kernel_source_sha256_16") != kernel_source_hash():
+    if kernel == "pool":
+        key_hash, key_bytes, src = "pool_source_sha256_16", "pool_hbm_bytes_per_launch", POOL_SOURCE
+    else:
+        key_hash, key_bytes, src = "kernel_source_sha256_16", "hbm_bytes_per_launch", FWD_SOURCE
+    if vals.get(key_hash) != kernel_source_hash(src):
         return None
     try:
-        return float(vals["hbm_bytes_per_launch"])
+        return float(vals[key_bytes])
     except (KeyError, ValueError):
         return None
 
@@ -526,7 +560,7 @@ def main():
         print(json.dumps({"copy_calibration_bytes": n * 4, "copies": 5}), flush=True)
         return
 
-    clock = ClockSampler()
+    clock = Clocks()
     clock.start()
     result, out0, x, w, info = bench_layer(args, args.workload, host_inputs=True, clock=clock)
     if not args.no_cpu_baseline:
@@ -560,7 +594,7 @@ def main():
         result["training"] = {k: t_res[k] for k in ("ms_per_step", "forward_pool_ms", "backward_ms", "backward_ms_p10_p90",
                                                     "backward_tflops", "backward_pct_of_bf16_peak", "value", "unit")}
     clock.stop()
-    result["sclk_mhz"] = clock.summary()
+    result.update(clock.summary())
     print(json.dumps(result), flush=True)
 
 
@@ -678,7 +712,7 @@ def bench_layer(args, workload, host_inputs, clock):
         "pool": {"bound": "hbm", "achieved": None if pool_gbps is None else round(pool_gbps, 1),
                  "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                  "frac": None if pool_gbps is None else round(pool_gbps / PEAK_HBM_GBPS, 4),
-                 "bytes_alg": info["pool_bytes_alg"]},
+                 "bytes_alg": info["pool_bytes_alg"], "traffic": read_traffic(workload, "pool")},
         "roofline": {"kernel": "mssa_forward (fwd_bf16_kernel + combine_kernel)" if dtype == "bf16" else "mssa_forward (fwd_f32_kernel)",
                      "bound": "mfma", "achieved": round(fwd_tflops, 2), "peak": peak,
                      "unit": "TFLOP/s", "frac": round(fwd_tflops / peak, 4),
