@@ -742,6 +742,7 @@ struct TierGroup {
   int64_t frame0, n_frames;
   int32_t P, kp;
   int64_t rows_off;
+  int64_t partial_off;  // fp32 partial tiles of a GEMM split over K (shared by the groups, used in turn)
 };
 
 mssa_status tier_layout(const mssa::Plan& p, const mssa_tier_desc* t, std::vector<TierGroup>& out, int64_t* bytes) {
@@ -766,7 +767,16 @@ mssa_status tier_layout(const mssa::Plan& p, const mssa_tier_desc* t, std::vecto
     off += (static_cast<int64_t>(g.q_end - g.q_begin) * kp * 2 + 255) / 256 * 256;
     out.push_back(tg);
   }
-  *bytes = off;
+  // the embedding (K = C (p s)^2) and de-embedding (N = C (p s)^2) GEMMs of
+  // every group may split over K into this region
+  int64_t partial = 0;
+  for (size_t i = 0; i < out.size(); ++i) {
+    const int32_t m = p.groups[i].q_end - p.groups[i].q_begin;
+    partial = std::max({partial, mssa::gemm_split_bytes(m, t->hidden, out[i].kp),
+                        mssa::gemm_split_bytes(m, out[i].kp, t->hidden)});
+  }
+  for (TierGroup& tg : out) tg.partial_off = off;
+  *bytes = off + (partial + 255) / 256 * 256;
   return MSSA_OK;
 }
 
@@ -825,7 +835,8 @@ mssa_status mssa_patch_embed(mssa_plan plan, const mssa_tier_desc* tier, const v
       ga.split = hid;
       ga.ldx = t.kp;
       ga.ldy = hid;
-      s = check_device(mssa::launch_gemm(ga, hs), "patch embedding GEMM launch");
+      s = check_device(mssa::launch_gemm_split(ga, reinterpret_cast<float*>(static_cast<char*>(workspace) + t.partial_off), hs),
+                       "patch embedding GEMM launch");
       if (s != MSSA_OK) return s;
     }
     return MSSA_OK;
@@ -864,7 +875,8 @@ mssa_status mssa_patch_unembed(mssa_plan plan, const mssa_tier_desc* tier, const
       ga.split = t.kp;
       ga.ldx = hid;
       ga.ldy = t.kp;
-      s = check_device(mssa::launch_gemm(ga, hs), "patch de-embedding GEMM launch");
+      s = check_device(mssa::launch_gemm_split(ga, reinterpret_cast<float*>(static_cast<char*>(workspace) + t.partial_off), hs),
+                       "patch de-embedding GEMM launch");
       if (s != MSSA_OK) return s;
       mssa::PatchArgs pa{};
       pa.latent = latent;

@@ -156,6 +156,8 @@ struct ScatterArgs {
 // ---------------------------------------------------------------- MSP tiers
 
 constexpr int kTierThreads = 256;
+// Output tile (rows x features) and K stage of the 4-wave GEMM kernels.
+constexpr int kGemmTile = 128, kGemmStage = 64;
 
 // Patch rows of consecutive latent frames of one tier: frame frame0 + f of
 // `latent` [frames, C, H, W] <-> rows [(f * gh + Y) * gw + X][C * P * P].
@@ -178,6 +180,9 @@ struct GemmArgs {
   int32_t M, N, K;
   int32_t split;
   int64_t ldx, ldy;
+  float* partial;     // k_splits > 1: fp32 partial tiles of every K slice (launch_gemm_split)
+  int32_t k_splits;   // 0 or 1: the whole K in one block
+  int32_t pad;
 };
 
 struct PoolJobArgs {

@@ -31,6 +31,17 @@ hipError_t launch_patchify(const PatchArgs& a, hipStream_t stream);
 hipError_t launch_unpatchify(const PatchArgs& a, hipStream_t stream);
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t stream);
 
+// The same product with K split over several blocks per output tile when the
+// output alone has too few tiles to fill the GPU (narrow outputs with a long
+// K, such as the patch de-embedding): fp32 partial tiles into `partial`
+// (gemm_split_bytes bytes, 256-byte aligned), then their sum in a fixed order
+// plus the bias.  With gemm_split_bytes == 0 this is launch_gemm and partial
+// may be null.
+// (Host code in plan.cpp: the rule is part of the static launch plan.)
+int gemm_k_splits(int32_t M, int32_t N, int32_t K);
+int64_t gemm_split_bytes(int32_t M, int32_t N, int32_t K);
+hipError_t launch_gemm_split(const GemmArgs& a, float* partial, hipStream_t stream);
+
 // Resident blocks per CU of the bf16 attention kernel (0 if unknown).
 int forward_blocks_per_cu(int head_dim);
 

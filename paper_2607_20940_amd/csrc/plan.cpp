@@ -389,4 +389,26 @@ std::vector<int64_t> export_tables(const Plan& p) {
   return t;
 }
 
+
+// K slices of a narrow GEMM (launch_gemm_split): enough blocks for two per
+// CU at most, each slice at least three stages; 1 when the output tiles alone
+// fill 256 CUs or K does not split into such slices.
+int gemm_k_splits(int32_t M, int32_t N, int32_t K) {
+  if (M <= 0 || N <= 0 || K % kGemmStage != 0) return 1;
+  const int64_t tiles = static_cast<int64_t>((M + kGemmTile - 1) / kGemmTile) * ((N + kGemmTile - 1) / kGemmTile);
+  if (tiles >= 256) return 1;
+  const int stages = K / kGemmStage;
+  int best = 1;
+  for (int s = 2; s <= stages; ++s)
+    if (stages % s == 0 && stages / s >= 3 && tiles * s <= 512) best = s;
+  return best;
+}
+
+int64_t gemm_split_bytes(int32_t M, int32_t N, int32_t K) {
+  const int s = gemm_k_splits(M, N, K);
+  if (s <= 1) return 0;
+  const int64_t tiles = static_cast<int64_t>((M + kGemmTile - 1) / kGemmTile) * ((N + kGemmTile - 1) / kGemmTile);
+  return s * tiles * kGemmTile * kGemmTile * 4;
+}
+
 }  // namespace mssa

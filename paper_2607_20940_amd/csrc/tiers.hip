@@ -30,6 +30,7 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 // One thread per 8-feature chunk of one patch row: feature k = (c, dy, dx) of
@@ -82,7 +83,7 @@ __global__ __launch_bounds__(kTierThreads) void unpatchify_kernel(PatchArgs a) {
 // stores).  K advances in 32-deep stages; the next stage's global loads are
 // in flight during the current stage's MFMAs.  Rows and features past the
 // matrix edges load as zeros and are not stored.
-constexpr int kGM = 128, kGN = 128, kGK = 32, kGStr = kGK + 8;  // LDS row stride: conflict-free 16-byte reads
+constexpr int kGM = kGemmTile, kGN = kGemmTile, kGK = 32, kGStr = kGK + 8;  // LDS row stride: conflict-free 16-byte reads
 
 __global__ __launch_bounds__(kTierThreads) void gemm_kernel(GemmArgs a) {
   __shared__ __attribute__((aligned(16))) __bf16 lds[2][2][kGM * kGStr];  // [stage][X | W]
@@ -175,14 +176,18 @@ __global__ __launch_bounds__(kTierThreads) void gemm_kernel(GemmArgs a) {
 // the swizzled layout of lds_stage.hpp, filled by direct global -> LDS
 // transfers (no staging registers), 64 KB of LDS so that two blocks share a
 // CU (two waves per SIMD); 16 MFMAs per wave between barriers.
-constexpr int kG2K = 64, kG2Tile = kGM * kG2K * 2;  // bytes of one 128 x 64 operand tile
+constexpr int kG2K = kGemmStage, kG2Tile = kGM * kG2K * 2;  // bytes of one 128 x 64 operand tile
 
 __global__ __launch_bounds__(kTierThreads, 2) void gemm_dma_kernel(GemmArgs a) {
   constexpr int NDMA = kG2Tile / 1024 / (kTierThreads / 64);
   static_assert(NDMA * 1024 * (kTierThreads / 64) == kG2Tile, "tile must split into 1 KB transfers per wave");
   __shared__ __attribute__((aligned(16))) char lds[2][2][kG2Tile];  // [stage][X | W]
-  const int tiles_m = (a.M + kGM - 1) / kGM;
-  const int tm = blockIdx.x % tiles_m, tn = blockIdx.x / tiles_m;
+  const int tiles_m = (a.M + kGM - 1) / kGM, tiles = tiles_m * ((a.N + kGN - 1) / kGN);
+  // k_splits > 1: block b takes K slice b / tiles of output tile b % tiles
+  const int ks_n = a.k_splits > 1 ? a.k_splits : 1;
+  const int tile = blockIdx.x % tiles, slice = blockIdx.x / tiles;
+  const int tm = tile % tiles_m, tn = tile / tiles_m;
+  const int k_len = a.K / ks_n, k_begin = slice * k_len;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave & 1, wn = wave >> 1;
@@ -201,8 +206,8 @@ __global__ __launch_bounds__(kTierThreads, 2) void gemm_dma_kernel(GemmArgs a) {
     wo[i] = row * wrb + lc * 16;
   }
   const int mrows = min(kGM, a.M - tm * kGM), nrows = min(kGN, a.N - tn * kGN);
-  const __bf16* X = static_cast<const __bf16*>(a.x) + static_cast<int64_t>(tm) * kGM * a.ldx;
-  const __bf16* W = static_cast<const __bf16*>(a.w) + static_cast<int64_t>(tn) * kGN * a.K;
+  const __bf16* X = static_cast<const __bf16*>(a.x) + static_cast<int64_t>(tm) * kGM * a.ldx + k_begin;
+  const __bf16* W = static_cast<const __bf16*>(a.w) + static_cast<int64_t>(tn) * kGN * a.K + k_begin;
   const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(&lds[0][0][0]));
   auto issue = [&](int k0, int s) {
     // rows past the matrix edge fall past the range: zeros
@@ -223,7 +228,7 @@ __global__ __launch_bounds__(kTierThreads, 2) void gemm_dma_kernel(GemmArgs a) {
 #pragma unroll
     for (int cb = 0; cb < 2; ++cb) acc[rb][cb] = f32x16{};
 
-  const int nst = a.K / kG2K;
+  const int nst = k_len / kG2K;
   issue(0, 0);
   wait_vmcnt<0>();
   __syncthreads();
@@ -249,24 +254,86 @@ __global__ __launch_bounds__(kTierThreads, 2) void gemm_dma_kernel(GemmArgs a) {
     __syncthreads();
   }
 
+  if (ks_n > 1) {
+    // A K slice's fp32 partial tile, in the lanes' own order: each store of a
+    // wave is 1 KB contiguous.  gemm_reduce_kernel sums the slices.
+    f32x4* P = reinterpret_cast<f32x4*>(a.partial) + ((static_cast<int64_t>(slice) * tiles + tile) * 4 + wave) * 1024 + lane;
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+      for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          f32x4 v;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) v[i] = acc[rb][cb][4 * jj + i];
+          P[((rb * 2 + cb) * 4 + jj) * 64] = v;
+        }
+    return;
+  }
+  // Epilogue through LDS (the stage buffers are free after the last barrier):
+  // each wave writes its outputs plus bias, rounded to bf16, into a
+  // row-major 128 x 128 tile (rows padded to 272 bytes: the 8-byte writes of
+  // 16 consecutive rows hit distinct banks), then every thread stores 16-byte
+  // pieces of whole rows, 16 threads per 256-byte row, coalesced.
+  constexpr int kEStr = kGN + 8;
+  static_assert(kGM * kEStr * 2 <= 2 * 2 * kG2Tile, "epilogue tile fits the stage buffers");
+  __bf16* E = reinterpret_cast<__bf16*>(&lds[0][0][0]);
   const __bf16* B = static_cast<const __bf16*>(a.bias);
 #pragma unroll
-  for (int rb = 0; rb < 2; ++rb) {
-    const int64_t row = static_cast<int64_t>(tm) * kGM + wm * 64 + rb * 32 + n32;
-    if (row >= a.M) continue;
+  for (int cb = 0; cb < 2; ++cb)
 #pragma unroll
-    for (int cb = 0; cb < 2; ++cb)
+    for (int jj = 0; jj < 4; ++jj) {
+      const int ct = wn * 64 + cb * 32 + 8 * jj + 4 * hh;
+      const int col = tn * kGN + ct;
+      const bf16x4 bv = col < a.N ? *reinterpret_cast<const bf16x4*>(B + col) : bf16x4{};
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj) {
-        const int col = tn * kGN + wn * 64 + cb * 32 + 8 * jj + 4 * hh;
-        if (col >= a.N) continue;
-        const int part = col / a.split, pc = col % a.split;
+      for (int rb = 0; rb < 2; ++rb) {
         bf16x4 v;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) v[i] = static_cast<__bf16>(acc[rb][cb][4 * jj + i] + static_cast<float>(B[col + i]));
-        *reinterpret_cast<bf16x4*>(static_cast<__bf16*>(a.y[part]) + row * a.ldy + pc) = v;
+        for (int i = 0; i < 4; ++i) v[i] = static_cast<__bf16>(acc[rb][cb][4 * jj + i] + static_cast<float>(bv[i]));
+        *reinterpret_cast<bf16x4*>(E + (wm * 64 + rb * 32 + n32) * kEStr + ct) = v;
       }
+    }
+  __syncthreads();
+#pragma unroll
+  for (int p = 0; p < kGM * kGN / 8 / kTierThreads; ++p) {
+    const int c = p * kTierThreads + tid, rt = c / (kGN / 8), ch = c % (kGN / 8);
+    const int64_t row = static_cast<int64_t>(tm) * kGM + rt;
+    const int col = tn * kGN + ch * 8;
+    if (row < a.M && col < a.N) {
+      const int part = col / a.split, pc = col % a.split;  // 8 features never straddle a split (split % 8 == 0)
+      *reinterpret_cast<bf16x8*>(static_cast<__bf16*>(a.y[part]) + row * a.ldy + pc) =
+          *reinterpret_cast<const bf16x8*>(E + rt * kEStr + ch * 8);
+    }
   }
+}
+
+// Sum of the K slices' partial tiles of gemm_dma_kernel, slice 0 first, plus
+// the bias, rounded to bf16: one thread per 4 output features of one row,
+// reading the partials in the order they were written (coalesced).
+__global__ __launch_bounds__(kTierThreads) void gemm_reduce_kernel(GemmArgs a) {
+  const int tiles_m = (a.M + kGM - 1) / kGM, tiles = tiles_m * ((a.N + kGN - 1) / kGN);
+  const int64_t u = static_cast<int64_t>(blockIdx.x) * kTierThreads + threadIdx.x;
+  const int64_t per_slice = static_cast<int64_t>(tiles) * 4 * 1024;
+  if (u >= per_slice) return;
+  const int lane = static_cast<int>(u % 64), jj = static_cast<int>((u / 64) % 4), cb = static_cast<int>((u / 256) % 2);
+  const int rb = static_cast<int>((u / 512) % 2), wave = static_cast<int>((u / 1024) % 4);
+  const int tile = static_cast<int>(u / 4096);
+  const int tm = tile % tiles_m, tn = tile / tiles_m;
+  const int wm = wave & 1, wn = wave >> 1, n32 = lane & 31, hh = lane >> 5;
+  const int64_t row = static_cast<int64_t>(tm) * kGM + wm * 64 + rb * 32 + n32;
+  const int col = tn * kGN + wn * 64 + cb * 32 + 8 * jj + 4 * hh;
+  if (row >= a.M || col >= a.N) return;
+  const f32x4* P = reinterpret_cast<const f32x4*>(a.partial) + u;
+  f32x4 s = P[0];
+  for (int k = 1; k < a.k_splits; ++k) s += P[k * per_slice];
+  const __bf16* B = static_cast<const __bf16*>(a.bias) + col;
+  bf16x4 v;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) v[i] = static_cast<__bf16>(s[i] + static_cast<float>(B[i]));
+  const int part = col / a.split, pc = col % a.split;
+  *reinterpret_cast<bf16x4*>(static_cast<__bf16*>(a.y[part]) + row * a.ldy + pc) = v;
 }
 
 // The same product for K a multiple of 64 and at least 256 rows and output
@@ -413,6 +480,19 @@ hipError_t launch_unpatchify(const PatchArgs& a, hipStream_t stream) {
   return hipGetLastError();
 }
 
+namespace {
+
+// gemm_dma_kernel stores 16-byte pieces of output rows and reads the bias in
+// 8-byte pieces.
+bool dma_epilogue_ok(const GemmArgs& a) {
+  bool ok = a.K % kG2K == 0 && a.N % 8 == 0 && a.split % 8 == 0 && a.ldy % 8 == 0 &&
+            (reinterpret_cast<uintptr_t>(a.bias) & 7) == 0;
+  for (int i = 0; i < 3; ++i) ok = ok && (reinterpret_cast<uintptr_t>(a.y[i]) & 15) == 0;
+  return ok;
+}
+
+}  // namespace
+
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t stream) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
   const int64_t tiles = static_cast<int64_t>((a.M + kBM - 1) / kBM) * ((a.N + kBN - 1) / kBN);
@@ -422,10 +502,29 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t stream) {
     return hipGetLastError();
   }
   const int64_t blocks = static_cast<int64_t>((a.M + kGM - 1) / kGM) * ((a.N + kGN - 1) / kGN);
-  if (a.K % kG2K == 0)
-    hipLaunchKernelGGL(gemm_dma_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kTierThreads), 0, stream, a);
-  else
+  if (dma_epilogue_ok(a)) {
+    GemmArgs b = a;
+    b.k_splits = 1;
+    hipLaunchKernelGGL(gemm_dma_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kTierThreads), 0, stream, b);
+  } else {
     hipLaunchKernelGGL(gemm_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kTierThreads), 0, stream, a);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_split(const GemmArgs& a, float* partial, hipStream_t stream) {
+  const int s = gemm_k_splits(a.M, a.N, a.K);
+  if (s <= 1 || !partial || !dma_epilogue_ok(a)) return launch_gemm(a, stream);
+  GemmArgs b = a;
+  b.partial = partial;
+  b.k_splits = s;
+  const int64_t tiles = static_cast<int64_t>((a.M + kGM - 1) / kGM) * ((a.N + kGN - 1) / kGN);
+  hipLaunchKernelGGL(gemm_dma_kernel, dim3(static_cast<uint32_t>(tiles * s)), dim3(kTierThreads), 0, stream, b);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int64_t units = tiles * 4 * 1024;
+  hipLaunchKernelGGL(gemm_reduce_kernel, dim3(static_cast<uint32_t>((units + kTierThreads - 1) / kTierThreads)),
+                     dim3(kTierThreads), 0, stream, b);
   return hipGetLastError();
 }
 

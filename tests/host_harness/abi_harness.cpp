@@ -261,6 +261,12 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t) {
   return hipSuccess;
 }
 
+hipError_t launch_gemm_split(const GemmArgs& a, float* partial, hipStream_t s) {
+  const int64_t bytes = gemm_split_bytes(a.M, a.N, a.K);
+  if (bytes > 0 && partial) check_range(partial, bytes, "gemm partial tiles");
+  return launch_gemm(a, s);
+}
+
 }  // namespace mssa
 
 // ------------------------------------------------------------ driving the entry points
