@@ -346,7 +346,8 @@ __global__ __launch_bounds__(kTierThreads) void gemm_reduce_kernel(GemmArgs a) {
 // buffers, each stage filled by direct global -> LDS transfers issued while
 // the previous one is multiplied; one barrier per stage.  Tiles are taken in
 // panels of four feature tiles, each XCD a contiguous run of them, so that
-// the blocks of an XCD share operand rows in its L2.
+// the blocks of an XCD share operand rows in its L2.  The outputs leave
+// through LDS as whole-row 16-byte stores, as in gemm_dma_kernel.
 constexpr int kBM = 256, kBN = 256, kBK = 64, kBStages = 2, kBThreads = 512, kBPanel = 4;
 constexpr int kBTile = kBM * kBK * 2;  // bytes of one operand tile of a stage
 
@@ -441,24 +442,42 @@ void gemm256_kernel(GemmArgs a) {
     }
   }
 
-  // acc[mb][nb] element e: row (wm*128 + mb*32 + n32), feature
-  // (wn*64 + nb*32 + 8(e/4) + 4hh + e%4) of the tile.
+  // Epilogue through LDS in two halves of 128 rows (a padded 128 x 256 bf16
+  // half tile is 67.6 KB of the 128 KB of stage buffers): the waves owning
+  // the half write their outputs plus bias, then all threads store whole-row
+  // 16-byte pieces, 32 threads per 512-byte row.
+  constexpr int kEStr = kBN + 8;
+  static_assert(128 * kEStr * 2 <= static_cast<int>(sizeof(lds)), "half tile fits the stage buffers");
+  __bf16* E = reinterpret_cast<__bf16*>(&lds[0][0][0]);
 #pragma unroll
-  for (int mb = 0; mb < 4; ++mb) {
-    const int64_t row = static_cast<int64_t>(tm) * kBM + wm * 128 + mb * 32 + n32;
-    if (row >= a.M) continue;
+  for (int half = 0; half < 2; ++half) {
+    __syncthreads();  // the stage buffers (half 0) or the previous half are free
+    if (wm == half) {
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb)
+      for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj) {
-        const int col = tn * kBN + wn * 64 + nb * 32 + 8 * jj + 4 * hh;
-        if (col >= a.N) continue;
-        const int part = col / a.split, pc = col % a.split;  // 4 features never straddle a split (split % 4 == 0)
-        bf16x4 v;
+        for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) v[i] = static_cast<__bf16>(acc[mb][nb][4 * jj + i] + static_cast<float>(bias[nb][jj][i]));
-        *reinterpret_cast<bf16x4*>(static_cast<__bf16*>(a.y[part]) + row * a.ldy + pc) = v;
+          for (int jj = 0; jj < 4; ++jj) {
+            bf16x4 v;
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              v[i] = static_cast<__bf16>(acc[mb][nb][4 * jj + i] + static_cast<float>(bias[nb][jj][i]));
+            *reinterpret_cast<bf16x4*>(E + (mb * 32 + n32) * kEStr + wn * 64 + nb * 32 + 8 * jj + 4 * hh) = v;
+          }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int p = 0; p < 128 * kBN / 8 / kBThreads; ++p) {
+      const int c = p * kBThreads + tid, rt = c / (kBN / 8), ch = c % (kBN / 8);
+      const int64_t row = static_cast<int64_t>(tm) * kBM + half * 128 + rt;
+      const int col = tn * kBN + ch * 8;
+      if (row < a.M && col < a.N) {
+        const int part = col / a.split, pc = col % a.split;  // 8 features never straddle a split (split % 8 == 0)
+        *reinterpret_cast<bf16x8*>(static_cast<__bf16*>(a.y[part]) + row * a.ldy + pc) =
+            *reinterpret_cast<const bf16x8*>(E + rt * kEStr + ch * 8);
       }
+    }
   }
 }
 
@@ -497,7 +516,7 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t stream) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
   const int64_t tiles = static_cast<int64_t>((a.M + kBM - 1) / kBM) * ((a.N + kBN - 1) / kBN);
   // enough tiles to fill the CUs; the bias read in 8-byte pieces
-  if (a.K % kBK == 0 && a.N >= kBN && a.M >= kBM && tiles >= 256 && (reinterpret_cast<uintptr_t>(a.bias) & 7) == 0) {
+  if (a.K % kBK == 0 && a.N >= kBN && a.M >= kBM && tiles >= 256 && dma_epilogue_ok(a)) {
     hipLaunchKernelGGL(gemm256_kernel, dim3(static_cast<uint32_t>(tiles)), dim3(kBThreads), 0, stream, a);
     return hipGetLastError();
   }
