@@ -29,6 +29,22 @@ sys.path.insert(0, ROOT)
 PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 MFMA: 256 CU x 4096 flop/clk x 2.4 GHz
 PEAK_F32_TFLOPS = 157.3
 PEAK_HBM_GBPS = 8000.0
+LOG2E = 1.4426950408889634
+
+
+def q_factor(desc, args):
+    """Factor on the query draws: softmax_scale * log2(e) for the pre-scaled
+    query layout (MSSA_PLAN_Q_PRESCALED: the producer folds the score scale
+    into its epilogue, and the values are drawn at that amplitude and rounded
+    once), 1 for the plain layout."""
+    if getattr(args, "q_layout", "plain") != "prescaled":
+        return 1.0
+    s = float(desc.get("softmax_scale", 0.0) or 0.0)
+    return (s if s > 0.0 else 1.0 / np.sqrt(float(desc["head_dim"]))) * LOG2E
+
+
+Q_LAYOUT_NOTE = {"prescaled": "queries pre-scaled by softmax_scale*log2(e) (MSSA_PLAN_Q_PRESCALED)",
+                 "plain": "plain queries (the kernel applies softmax_scale)"}
 METRIC = "MSSA effective TFLOP/s + ms per rolling pass; % of bf16 MFMA peak (1 GPU)"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "mssa_fwd_traffic_{workload}.txt")
 FWD_SOURCE = os.path.join(ROOT, "paper_2607_20940_amd", "csrc", "attention_fwd.hip")
@@ -167,7 +183,7 @@ def read_traffic(workload, kernel="forward"):
         return None
 
 
-def cpu_baseline(w, x, info, budget_s):
+def cpu_baseline(w, x, info, budget_s, qf=1.0):
     """Time the fp64 oracle (as it stands) on the host: whole heads of the
     workload (pool + attention for every query), one at a time, until the
     time budget is used.  Returns the oracle's effective TFLOP/s and its
@@ -187,6 +203,7 @@ def cpu_baseline(w, x, info, budget_s):
     refs = {}
     for h in range(nh):
         xh = {k: (None if v is None else to_f64(v[:, [h]], w["dtype"])) for k, v in x.items()}
+        xh["q_win"] = xh["q_win"] / qf  # the oracle takes the unscaled queries
         d1 = dict(desc, num_heads=1)
         t0 = time.perf_counter()
         o = oracle.mssa_attention(d1, xh["q_win"], xh["k_sink"], xh["v_sink"], xh["k_hist"],
@@ -261,8 +278,9 @@ def bench_streaming(args):
     desc = w["layer"]
     F = desc["frames_per_state"]
     head_in_ring = getattr(args, "head_in_ring", False)
+    qf = q_factor(desc, args)
     st = StreamingMSSA(desc, layers, w["hist_cap_frames"], dtype=w["dtype"], pooled_ring=args.pooled_ring,
-                       head_in_ring=head_in_ring)
+                       head_in_ring=head_in_ring, q_prescaled=qf != 1.0)
     init_shapes = st.shapes(w["hist_start_frames"])
     for L in range(layers):
         x = init_inputs(w, L, init_shapes)
@@ -276,7 +294,8 @@ def bench_streaming(args):
     for p in range(passes):
         # window inputs of the pass (state 1 written into the ring's spare
         # slots by its producer when the roll moves no data)
-        wins = window_inputs_head_ring(w, p, st) if head_in_ring else window_inputs(w, p, layers, win_shapes)
+        wins = (window_inputs_head_ring(w, p, st, q_scale=qf) if head_in_ring
+                else window_inputs(w, p, layers, win_shapes, q_scale=qf))
         flops = sum(st.plan(st.ring[L].count).info()["flops_alg"] for L in range(layers))
         if args.graph:
             for L in range(layers):
@@ -321,7 +340,8 @@ def bench_streaming(args):
                    "frames_per_state": F,
                    "history_pooling": "pooled_ring" if st.pooled_ring else "per_pass",
                    "cache_roll": "in place (head state written into the ring)" if head_in_ring else "device copies",
-                   "launch": "hip_graph_per_pass" if args.graph else "eager"},
+                   "launch": "hip_graph_per_pass" if args.graph else "eager",
+                   "q_layout": Q_LAYOUT_NOTE[getattr(args, "q_layout", "plain")]},
         "all_passes_ms_per_frame": round(tot_ms / (passes * F), 4),
         "steady_state_passes": [steady[0], steady[-1]],
         "steady_state_pass_count": len(steady),
@@ -344,10 +364,12 @@ def bench_training(args):
 
     w = dict(WORKLOADS[args.workload], name=args.workload)
     desc, dtype = w["desc"], w["dtype"]
-    plan = mssa.mssa_plan_create(dict(desc, dtype=dtype))
+    qf = q_factor(desc, args)
+    plan = mssa.mssa_plan_create(dict(desc, dtype=dtype, q_prescaled=qf != 1.0))
     info = plan.info()
     shapes = input_shapes(desc, info["n_q"], info["n_sink_tok"], info["n_hist_tok"])
-    x = make_inputs(shapes, w["seed"], w["amplitude"], dtype)
+    x = make_inputs(shapes, w["seed"], w["amplitude"], dtype,
+                    q_amplitude=w["amplitude"] * qf if qf != 1.0 else None)
     go = make_grad_output(shapes["q_win"], w["seed"] + 7919, 1.0, dtype)
 
     def dev(a):
@@ -397,7 +419,8 @@ def bench_training(args):
         "ms_per_step": round(float(step_ms.mean()), 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": dtype, "data": "synthetic",
-        "config": {"workload": args.workload, "flops_alg_forward": F, "flops_alg_backward": 2.5 * F},
+        "config": {"workload": args.workload, "flops_alg_forward": F, "flops_alg_backward": 2.5 * F,
+                   "q_layout": Q_LAYOUT_NOTE[getattr(args, "q_layout", "plain")]},
         "forward_pool_ms": round(float(fwd_ms.mean()), 4),
         "backward_ms": round(float(bwd_ms.mean()), 4),
         "backward_ms_p10_p90": [round(float(np.percentile(bwd_ms, 10)), 4),
@@ -529,6 +552,9 @@ def main():
     ap.add_argument("--resample", choices=("mean", "stride"), default="mean",
                     help="K/V resampling of the layer workloads: block mean (default) or the "
                          "strided pick of each block's first cell (both timed the same way)")
+    ap.add_argument("--q-layout", choices=("prescaled", "plain"), default="prescaled",
+                    help="queries handed over pre-scaled by softmax_scale*log2(e) (the producer folds the "
+                         "score scale into its epilogue; MSSA_PLAN_Q_PRESCALED, default) or plain")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="only run a plain device copy of this many MiB (5 times), the reference "
                          "for scaling HBM byte counters")
@@ -564,13 +590,23 @@ def main():
     clock.start()
     result, out0, x, w, info = bench_layer(args, args.workload, host_inputs=True, clock=clock)
     if not args.no_cpu_baseline:
-        base, ref = cpu_baseline(w, x, info, args.cpu_budget)
+        base, ref = cpu_baseline(w, x, info, args.cpu_budget, qf=q_factor(w["desc"], args))
         result["cpu_baseline"] = base
         result["parity"] = parity_vs_oracle(out0, ref, w)
         log(f"parity against the oracle: {result['parity']}")
     if args.workload == "wan13b_layer" and args.resample == "mean" and not args.no_extras:
-        # the other layer workloads, the stacked-layer streaming workload and
-        # the training step, each timed the same way on this GPU
+        # the same layer with the other query layout, the other layer
+        # workloads, the stacked-layer streaming workload and the training
+        # step, each timed the same way on this GPU
+        oargs = argparse.Namespace(**vars(args))
+        oargs.q_layout = "plain" if args.q_layout == "prescaled" else "prescaled"
+        r, _, _, _, _ = bench_layer(oargs, args.workload, host_inputs=False, clock=clock,
+                                    section=args.workload + "_" + oargs.q_layout)
+        result[oargs.q_layout + "_q"] = {
+            "q_layout": Q_LAYOUT_NOTE[oargs.q_layout],
+            **{k: r[k] for k in ("ms_per_step", "value", "pct_of_bf16_peak", "forward_ms", "forward_ms_median",
+                                 "forward_ms_p10_p90")},
+            "forward_frac_of_bf16_peak": r["roofline"]["frac"]}
         result["other_layers"] = {}
         for name in ("wan13b_longhist", "wan14b_720p"):
             r, _, _, _, _ = bench_layer(args, name, host_inputs=False, clock=clock)
@@ -598,7 +634,7 @@ def main():
     print(json.dumps(result), flush=True)
 
 
-def bench_layer(args, workload, host_inputs, clock):
+def bench_layer(args, workload, host_inputs, clock, section=None):
     """Time K passes (mssa_pool_kv + mssa_forward) of one layer workload.
     host_inputs: the seeded host inputs the oracle also reads (returned);
     else device-drawn inputs of the same distribution.  Returns (result
@@ -614,7 +650,9 @@ def bench_layer(args, workload, host_inputs, clock):
         w["desc"] = dict(w["desc"], resample=args.resample)
     desc = w["desc"]
     dtype = w["dtype"]
-    plan = mssa.mssa_plan_create(dict(desc, dtype=dtype))
+    qf = q_factor(desc, args)
+    qa = w["amplitude"] * qf if qf != 1.0 else None
+    plan = mssa.mssa_plan_create(dict(desc, dtype=dtype, q_prescaled=qf != 1.0))
     info = plan.info()
     shapes = input_shapes(desc, info["n_q"], info["n_sink_tok"], info["n_hist_tok"])
     log(f"workload {workload}: n_q={info['n_q']} n_kv={info['n_kv']} flops={info['flops_alg']:.4e}")
@@ -628,11 +666,11 @@ def bench_layer(args, workload, host_inputs, clock):
         return torch.from_numpy(a).cuda()
 
     if host_inputs:
-        x = make_inputs(shapes, w["seed"], w["amplitude"], dtype)
+        x = make_inputs(shapes, w["seed"], w["amplitude"], dtype, q_amplitude=qa)
         base = {k: dev(v) for k, v in x.items()}
     else:
         x = None
-        base = make_inputs_device(shapes, w["seed"], w["amplitude"], dtype)
+        base = make_inputs_device(shapes, w["seed"], w["amplitude"], dtype, q_amplitude=qa)
     log(f"inputs generated in {time.perf_counter() - t0:.1f} s")
     sets = [base] + [{k: (None if v is None else v.clone()) for k, v in base.items()}
                      for _ in range(args.input_sets - 1)]
@@ -661,7 +699,7 @@ def bench_layer(args, workload, host_inputs, clock):
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
-    with clock.section(workload):
+    with clock.section(section or workload):
         start.record(stream)
         for i in range(args.steps):
             step(i, evs[i])
@@ -702,6 +740,7 @@ def bench_layer(args, workload, host_inputs, clock):
             "n_q": info["n_q"], "n_kv": info["n_kv"], "flops_alg": flops,
             "input_sets_rotated": len(sets), "resample": args.resample,
             "inputs": "seeded host draws" if host_inputs else "device draws",
+            "q_layout": Q_LAYOUT_NOTE[getattr(args, "q_layout", "plain")],
         },
         "pct_of_bf16_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
         "forward_ms": round(float(fwd_ms.mean()), 4),

@@ -97,6 +97,18 @@ typedef struct {
  * advances the ring state.  See "Cache roll without copies" below. */
 #define MSSA_PLAN_HEAD_IN_RING 4
 
+/* Plan flag: every q_win passed with this plan holds the queries already
+ * multiplied by softmax_scale * log2(e), i.e. Eq. 4's scaled scores
+ * scale q k^T taken into the base-2 exponent domain, so that
+ * softmax(scale q k^T) = 2^(q' k^T) / sum 2^(q' k^T) for q' = scale log2(e) q.
+ * A producer can fold the factor into its own epilogue before its single
+ * rounding to the plan dtype (the query projection's weights, or the query
+ * norm's gain), and the bf16 attention then spends no instruction per score
+ * on the scale.  Outputs and lse are those of the unscaled queries q; the
+ * backward's dq_win is the gradient with respect to q' (dL/dq' = dL/dq /
+ * (softmax_scale log2(e))).  softmax_scale still names the factor. */
+#define MSSA_PLAN_Q_PRESCALED 8
+
 /* Sizes derived by the plan.  Group g is the g-th distinct query scale in
  * window token order; its queries are the contiguous range
  * [q_begin[g], q_end[g]) and its context has n_kv[g] tokens per head.

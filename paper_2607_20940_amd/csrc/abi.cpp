@@ -335,6 +335,21 @@ GroupRuns plan_runs(const mssa::Plan& p, const KvSources& src) {
   return out;
 }
 
+// The kernels' two score factors: `scale` turns q k^T into natural-log
+// logits (the fp32 paths and the gradients), `scale_log2e` into base-2 ones
+// (the bf16 softmax).  For queries supplied pre-scaled by
+// softmax_scale * log2(e), q' k^T already is the base-2 logit: the factors
+// become ln 2 and 1.
+void set_score_scales(const mssa::Plan& p, float& scale, float& scale_log2e) {
+  if (p.q_prescaled) {
+    scale = 0.69314718055994531f;
+    scale_log2e = 1.0f;
+  } else {
+    scale = p.softmax_scale;
+    scale_log2e = p.softmax_scale * 1.4426950408889634f;
+  }
+}
+
 // Enqueues the attention kernels over the given runs and schedule.
 mssa_status forward_launch(const mssa::Plan& p, const GroupRuns& runs, const mssa::Schedule& sc, const void* q_win,
                            const void* workspace, void* out, float* lse, void* stream) {
@@ -347,8 +362,8 @@ mssa_status forward_launch(const mssa::Plan& p, const GroupRuns& runs, const mss
   a.n_q = static_cast<int32_t>(p.n_q);
   a.ld = p.ld;
   a.num_heads = p.desc.num_heads;
-  a.scale = p.softmax_scale;
-  a.scale_log2e = p.softmax_scale * 1.4426950408889634f;
+  set_score_scales(p, a.scale, a.scale_log2e);
+  a.q_prescaled = p.q_prescaled ? 1 : 0;
   a.n_ranges = p.n_ranges;
   a.total_tiles = sc.total_tiles;
   a.tail_begin = sc.tail_begin;
@@ -663,8 +678,7 @@ mssa_status mssa_backward(mssa_plan plan, const void* q_win, const void* k_sink,
     a.n_q = static_cast<int32_t>(p.n_q);
     a.num_heads = nh;
     a.n_groups = G;
-    a.scale = p.softmax_scale;
-    a.scale_log2e = p.softmax_scale * 1.4426950408889634f;
+    set_score_scales(p, a.scale, a.scale_log2e);
     const int qb = bf16 ? mssa::kBwdQ : mssa::kBwdF32, kb = bf16 ? mssa::kBwdK : mssa::kBwdF32;
     const KvSources src{k_sink, v_sink, k_hist, v_hist, nullptr, nullptr, k_win, v_win, ws};
     int64_t dq_blocks = 0, kv_blocks = 0;

@@ -12,7 +12,10 @@
 //                 holds 16 keys of ONE query: the softmax row reductions are
 //                 in-lane plus one exchange between the two half-waves;
 //   online softmax in fp32 in the exp2 domain (scale * log2 e folded into
-//                 one FMA per score);
+//                 one FMA per score; for queries supplied pre-scaled by
+//                 scale * log2 e the running max enters the MFMA as its
+//                 accumulator input instead, and a score needs nothing but
+//                 its exponential);
 //   O^T += V^T P^T with the same MFMA: the exponentiated scores are already
 //                 laid out as the B operand (their key order defines the
 //                 contraction order), and V^T comes from row-major V in LDS
@@ -171,7 +174,9 @@ __device__ inline float halfwave_sum(float v) { return v + other_half(v); }
 // the step starts with its operands in registers.  K_{j+1} goes to the
 // buffer of K_{j-1} (last read in phase 2j - 1), V_j to that of V_{j-2}
 // (last read in phase 2j - 1, prefetched in phase 2j - 2 at the latest).
-template <int D>
+//
+// kQS: the queries arrive multiplied by scale * log2 e (MSSA_PLAN_Q_PRESCALED).
+template <int D, bool kQS>
 __device__ __forceinline__ void attend_piece(const FwdArgs& a, const FwdGroupArgs& G, int item, int k,
                                              int nt, bool whole, int rec, char* lds) {
   using P = FwdTile<D>;
@@ -213,6 +218,13 @@ __device__ __forceinline__ void attend_piece(const FwdArgs& a, const FwdGroupArg
   for (int db = 0; db < DB; ++db) o[db] = f32x16{};
   float m_run = -INFINITY;  // running max in the exp2 domain (shared by both half-waves)
   float l_part = 0.f;       // this lane's share of the row sum
+  // kQS only.  Accumulator input of the first MFMA of every S chain: -m_c in
+  // all 16 elements (a lane's 16 elements all belong to its query), with
+  // m_c = m_run once the first tile has set it and 0 before, so S arrives as
+  // S - m_c.  The first tile's row sum is seeded with +inf (lbias), which
+  // sends that tile through the max path whatever the size of its scores.
+  f32x16 cneg = f32x16{};
+  float lbias = INFINITY;
   f32x16 s[BN / 32];
   bf16x8 pb[BN / 32][2];
   bf16x8 ring[kLead];       // LDS operands of the matrix-core step, kLead ahead
@@ -353,7 +365,8 @@ __device__ __forceinline__ void attend_piece(const FwdArgs& a, const FwdGroupArg
         o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[kb][cc], o[db], 0, 0, 0);
       } else {
         const int j = i - NPV, ks = j / (BN / 32), kb = j % (BN / 32);
-        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qf[ks], ks == 0 ? f32x16{} : s[kb], 0, 0, 0);
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qf[ks], ks == 0 ? (kQS ? cneg : f32x16{}) : s[kb],
+                                                         0, 0, 0);
       }
       if (i + kLead < N) ring[i % kLead] = operand(pv_c, i + kLead, vb, kb_);
     }
@@ -371,13 +384,15 @@ __device__ __forceinline__ void attend_piece(const FwdArgs& a, const FwdGroupArg
   };
 
   // Softmax step on S (keys >= nvalid of this tile masked): P = exp2(S c - m)
-  // packed to bf16 as the B operand of the next P V, with m the running max.
-  // Lazy rescaling without a per-tile max: P is first computed against the
-  // current m; if every lane's sum over its 32 keys stays <= 2^kRescaleLog2,
-  // so does every P and nothing else is needed.  Otherwise (the first tile,
-  // where m is -inf, or scores well above m) the tile max is taken, m is
-  // raised if the max exceeds it by more than kRescaleLog2 (O and l scaled
-  // down), and P is recomputed.  Either way P <= 2^kRescaleLog2.
+  // (kQS: exp2(S), m already subtracted by the MFMA) packed to bf16 as the B
+  // operand of the next P V, with m the running max.  Lazy rescaling without
+  // a per-tile max: P is first computed against the current m; if every
+  // lane's sum over its 32 keys stays <= 2^kRescaleLog2, so does every P and
+  // nothing else is needed.  Otherwise (the first tile, where m is -inf, or
+  // scores well above m) the tile max is taken, m is raised if the max
+  // exceeds it by more than kRescaleLog2 (O and l scaled down), and P is
+  // recomputed (kQS: the new -m also goes into the accumulator input of the
+  // next S).  Either way P <= 2^kRescaleLog2.
   auto sstep = [&](int nvalid) {
     if (nvalid < BN) {
 #pragma unroll
@@ -391,22 +406,25 @@ __device__ __forceinline__ void attend_piece(const FwdArgs& a, const FwdGroupArg
     // Row sum in fp32 VALU adds (four independent partial sums): the bf16 dot
     // instruction would wait on the matrix core that the other wave of this
     // SIMD keeps busy.
-    auto exps = [&]() {
-      const float mneg = -m_run;
-      float ls[4] = {0.f, 0.f, 0.f, 0.f};
+    // Exponent of a score: S c + off (plain), S (kQS, first pass) or S + off
+    // (kQS, after the max path moved m); bias seeds the row sum.
+    auto exps = [&](auto shift_c, float off, float bias) {
+      constexpr bool kShift = decltype(shift_c)::value;
+      auto arg = [&](float x) { return kQS ? (kShift ? x + off : x) : __builtin_fmaf(x, c, off); };
+      float ls[4] = {bias, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kb = 0; kb < BN / 32; ++kb)
 #pragma unroll
         for (int e = 0; e < 16; e += 2) {
-          const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][e], c, mneg));
-          const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][e + 1], c, mneg));
+          const float p0 = __builtin_amdgcn_exp2f(arg(s[kb][e]));
+          const float p1 = __builtin_amdgcn_exp2f(arg(s[kb][e + 1]));
           ls[(e >> 1) & 3] += p0 + p1;
           pb[kb][e >> 3][e & 7] = static_cast<__bf16>(p0);
           pb[kb][e >> 3][(e & 7) + 1] = static_cast<__bf16>(p1);
         }
       return (ls[0] + ls[1]) + (ls[2] + ls[3]);
     };
-    float lt = exps();
+    float lt = kQS ? exps(std::false_type{}, 0.f, lbias) : exps(std::false_type{}, -m_run, 0.f);
     if (__any(!(lt <= kRescaleSum))) {  // also true for inf / NaN sums
       float mx = fmaxf(s[0][0], s[0][1]);
 #pragma unroll
@@ -415,7 +433,8 @@ __device__ __forceinline__ void attend_piece(const FwdArgs& a, const FwdGroupArg
       for (int kb = 1; kb < BN / 32; ++kb)
 #pragma unroll
         for (int e = 0; e < 16; e += 2) mx = fmaxf(fmaxf(mx, s[kb][e]), s[kb][e + 1]);
-      const float mt = halfwave_max(mx) * c;
+      const float m_c = kQS ? -cneg[0] : 0.f;  // kQS: what the MFMA subtracted
+      const float mt = kQS ? halfwave_max(mx) + m_c : halfwave_max(mx) * c;
       if (__any(mt > m_run + kRescaleLog2)) {
         const float m_new = fmaxf(m_run, mt);
         const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
@@ -424,7 +443,14 @@ __device__ __forceinline__ void attend_piece(const FwdArgs& a, const FwdGroupArg
 #pragma unroll
         for (int db = 0; db < DB; ++db) o[db] *= alpha;
       }
-      lt = exps();
+      if constexpr (kQS) {
+        lt = exps(std::true_type{}, m_c - m_run, 0.f);
+#pragma unroll
+        for (int e = 0; e < 16; ++e) cneg[e] = -m_run;
+        lbias = 0.f;
+      } else {
+        lt = exps(std::false_type{}, -m_run, 0.f);
+      }
     }
     l_part += lt;
     // P and the row sum are pure register values, so the compiler is free to
@@ -574,7 +600,7 @@ __device__ __forceinline__ void attend_piece(const FwdArgs& a, const FwdGroupArg
   }
 }
 
-template <int D>
+template <int D, bool kQS>
 __global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void fwd_bf16_kernel(FwdArgs a) {
   using P = FwdTile<D>;
@@ -617,7 +643,7 @@ void fwd_bf16_kernel(FwdArgs a) {
     } else {
       break;
     }
-    attend_piece<D>(a, a.groups[g], item, k, nt, whole, rec, lds);
+    attend_piece<D, kQS>(a, a.groups[g], item, k, nt, whole, rec, lds);
   }
 }
 
@@ -743,10 +769,14 @@ __global__ __launch_bounds__(kFwdF32BM) void fwd_f32_kernel(FwdArgs a) {
 hipError_t launch_forward(const FwdArgs& a, int head_dim, bool bf16, hipStream_t stream) {
   if (bf16) {
     if (a.n_ranges <= 0) return hipSuccess;
-    if (head_dim == 128)
-      hipLaunchKernelGGL(fwd_bf16_kernel<128>, dim3(a.n_ranges), dim3(kFwdThreads), 0, stream, a);
+    if (head_dim == 128 && a.q_prescaled)
+      hipLaunchKernelGGL((fwd_bf16_kernel<128, true>), dim3(a.n_ranges), dim3(kFwdThreads), 0, stream, a);
+    else if (head_dim == 128)
+      hipLaunchKernelGGL((fwd_bf16_kernel<128, false>), dim3(a.n_ranges), dim3(kFwdThreads), 0, stream, a);
+    else if (a.q_prescaled)
+      hipLaunchKernelGGL((fwd_bf16_kernel<64, true>), dim3(a.n_ranges), dim3(kFwdThreads), 0, stream, a);
     else
-      hipLaunchKernelGGL(fwd_bf16_kernel<64>, dim3(a.n_ranges), dim3(kFwdThreads), 0, stream, a);
+      hipLaunchKernelGGL((fwd_bf16_kernel<64, false>), dim3(a.n_ranges), dim3(kFwdThreads), 0, stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || a.n_ranges < 2) return e;
     if (head_dim == 128)
@@ -766,8 +796,8 @@ hipError_t launch_forward(const FwdArgs& a, int head_dim, bool bf16, hipStream_t
 int forward_blocks_per_cu(int head_dim) {
   int n = 0;
   const hipError_t e = head_dim == 128
-      ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fwd_bf16_kernel<128>, kFwdThreads, 0)
-      : hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fwd_bf16_kernel<64>, kFwdThreads, 0);
+      ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fwd_bf16_kernel<128, false>, kFwdThreads, 0)
+      : hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fwd_bf16_kernel<64, false>, kFwdThreads, 0);
   if (e != hipSuccess) {
     (void)hipGetLastError();
     return 0;

@@ -57,7 +57,7 @@ struct FwdArgs {
   int64_t* range_table;     // bf16 kernel: first tile of each tail range (n_ranges + 1), written by the attention kernel
   float* lse;               // optional [heads, n_q]: log of the softmax denominator (natural log)
   int32_t n_q;
-  int32_t pad3;
+  int32_t q_prescaled;      // bf16 kernel: queries arrive multiplied by scale * log2(e)
   FwdGroupArgs groups[kMaxGroups];  // in launch order (longest context first)
 };
 

@@ -49,7 +49,8 @@ mssa_status build_plan(const mssa_plan_desc& d, int slots, int attention_blocks,
     err = "softmax_scale must be finite";
     return MSSA_ERR_INVALID_ARG;
   }
-  if ((d.flags & ~(MSSA_PLAN_POOLED_HIST_RING | MSSA_PLAN_STRIDED_SUBSAMPLE | MSSA_PLAN_HEAD_IN_RING)) != 0) {
+  if ((d.flags & ~(MSSA_PLAN_POOLED_HIST_RING | MSSA_PLAN_STRIDED_SUBSAMPLE | MSSA_PLAN_HEAD_IN_RING |
+                   MSSA_PLAN_Q_PRESCALED)) != 0) {
     err = "unknown plan flags";
     return MSSA_ERR_INVALID_ARG;
   }
@@ -78,6 +79,7 @@ mssa_status build_plan(const mssa_plan_desc& d, int slots, int attention_blocks,
   p.hist_ring = (d.flags & MSSA_PLAN_POOLED_HIST_RING) != 0;
   p.head_ring = (d.flags & MSSA_PLAN_HEAD_IN_RING) != 0;
   p.strided = (d.flags & MSSA_PLAN_STRIDED_SUBSAMPLE) != 0;
+  p.q_prescaled = (d.flags & MSSA_PLAN_Q_PRESCALED) != 0;
   p.softmax_scale = d.softmax_scale > 0.f ? d.softmax_scale
                                           : 1.0f / std::sqrt(static_cast<float>(d.head_dim));
   const int32_t F = d.frames_per_state;

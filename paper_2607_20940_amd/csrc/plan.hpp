@@ -92,6 +92,7 @@ struct Plan {
   bool head_ring;  // MSSA_PLAN_HEAD_IN_RING: window state 1 read from the rings' spare slots
   int64_t win_shift;  // head_ring: window tokens before k_win / v_win (state 1's), else 0
   bool strided;    // MSSA_PLAN_STRIDED_SUBSAMPLE: first cell of each block
+  bool q_prescaled;  // MSSA_PLAN_Q_PRESCALED: queries arrive multiplied by softmax_scale * log2(e)
   float softmax_scale;
   int64_t tok1;  // native tokens per frame
   int64_t n_q, n_sink_tok, n_hist_tok;

@@ -40,10 +40,11 @@ def to_f64(x, dtype):
     return np.asarray(x, dtype=np.float32).astype(np.float64)
 
 
-def make_inputs(shapes, seed, amplitude=1.0, dtype="bf16"):
+def make_inputs(shapes, seed, amplitude=1.0, dtype="bf16", q_amplitude=None):
     """shapes: mapping name -> shape tuple for the names in DRAW_ORDER (a
     missing or zero-sized entry is empty).  Returns name -> stored array
-    (uint16 bf16 bits, or float32), None for empty tensors."""
+    (uint16 bf16 bits, or float32), None for empty tensors.  q_amplitude, if
+    given, replaces the amplitude of q_win (the draws are the same)."""
     rng = np.random.default_rng(seed)
     out = {}
     for name in DRAW_ORDER:
@@ -51,7 +52,8 @@ def make_inputs(shapes, seed, amplitude=1.0, dtype="bf16"):
         if int(np.prod(shape)) == 0:
             out[name] = None
             continue
-        x = (rng.standard_normal(shape) * amplitude).astype(np.float32)
+        amp = q_amplitude if (name == "q_win" and q_amplitude is not None) else amplitude
+        x = (rng.standard_normal(shape) * amp).astype(np.float32)
         out[name] = f32_to_bf16_bits(x) if dtype == "bf16" else x
     return out
 
@@ -63,12 +65,14 @@ def make_grad_output(shape, seed, amplitude=1.0, dtype="bf16"):
     return f32_to_bf16_bits(x) if dtype == "bf16" else x
 
 
-def make_inputs_device(shapes, seed, amplitude=1.0, dtype="bf16", names=DRAW_ORDER, device="cuda"):
+def make_inputs_device(shapes, seed, amplitude=1.0, dtype="bf16", names=DRAW_ORDER, device="cuda",
+                       q_amplitude=None):
     """Device-side variant for workloads too large to draw on the host:
     torch's generator on `device` seeded with `seed` draws N(0,1) float32
-    tensors in the order of `names`, scaled by the amplitude and rounded to
-    bf16 (round-to-nearest-even) or kept float32.  The values are defined by
-    this function (the oracle reads them back from the device)."""
+    tensors in the order of `names`, scaled by the amplitude (q_amplitude
+    for q_win if given) and rounded to bf16 (round-to-nearest-even) or kept
+    float32.  The values are defined by this function (the oracle reads them
+    back from the device)."""
     import torch
 
     gen = torch.Generator(device=device)
@@ -79,6 +83,7 @@ def make_inputs_device(shapes, seed, amplitude=1.0, dtype="bf16", names=DRAW_ORD
         if int(np.prod(shape)) == 0:
             out[name] = None
             continue
-        x = torch.randn(shape, generator=gen, device=device, dtype=torch.float32) * amplitude
+        amp = q_amplitude if (name == "q_win" and q_amplitude is not None) else amplitude
+        x = torch.randn(shape, generator=gen, device=device, dtype=torch.float32) * amp
         out[name] = x.to(torch.bfloat16) if dtype == "bf16" else x
     return out

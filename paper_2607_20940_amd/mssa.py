@@ -21,6 +21,7 @@ MSSA_BF16, MSSA_F32 = 0, 1
 MSSA_PLAN_POOLED_HIST_RING = 1
 MSSA_PLAN_STRIDED_SUBSAMPLE = 2
 MSSA_PLAN_HEAD_IN_RING = 4
+MSSA_PLAN_Q_PRESCALED = 8
 
 # Every symbol include/libmssa.h declares.
 EXPORTS = ("mssa_plan_create", "mssa_plan_create_ex", "mssa_plan_destroy", "mssa_plan_query", "mssa_plan_tables",
@@ -207,6 +208,8 @@ def make_desc(desc):
         raise ValueError("resample must be 'mean' or 'stride'")
     if resample == "stride":
         d.flags |= MSSA_PLAN_STRIDED_SUBSAMPLE
+    if desc.get("q_prescaled"):
+        d.flags |= MSSA_PLAN_Q_PRESCALED
     return d
 
 

@@ -42,7 +42,7 @@ from .workloads import input_shapes
 
 class StreamingMSSA:
     def __init__(self, layer_desc, layers, hist_cap_frames, dtype="bf16", device="cuda", pooled_ring=False,
-                 head_in_ring=False):
+                 head_in_ring=False, q_prescaled=False):
         import torch
 
         self.head_in_ring = bool(head_in_ring)
@@ -50,7 +50,7 @@ class StreamingMSSA:
         flags = mssa.MSSA_PLAN_POOLED_HIST_RING if self.pooled_ring else 0
         if self.head_in_ring:
             flags |= mssa.MSSA_PLAN_HEAD_IN_RING
-        self.desc = dict(layer_desc, flags=flags)
+        self.desc = dict(layer_desc, flags=flags, q_prescaled=bool(q_prescaled))
         self.layers = int(layers)
         self.cap = int(hist_cap_frames)
         self.dtype = dtype
@@ -211,11 +211,12 @@ def init_inputs(stream_w, layer, shapes, device="cuda"):
                               device=device)
 
 
-def window_inputs_head_ring(stream_w, pass_index, st, device="cuda"):
+def window_inputs_head_ring(stream_w, pass_index, st, device="cuda", q_scale=1.0):
     """Window Q/K/V of every layer for one pass of a head_in_ring driver: one
     generator seeded seed_base + pass_index draws, layer by layer, q, then
     K of state 1 (written into the layer's spare ring slots, as its producer
     would), K of states 2..T, V of state 1 (ring) and V of states 2..T.
+    q_scale multiplies the query draws before rounding (pre-scaled queries).
     Returns per layer {q_win, k_win, v_win} with k_win / v_win the states
     2..T only."""
     import torch
@@ -230,7 +231,7 @@ def window_inputs_head_ring(stream_w, pass_index, st, device="cuda"):
     for layer in range(st.layers):
         kh, vh = st.head_slots(layer)
         rest = (shapes["k_win"][0] - n_head,) + tuple(shapes["k_win"][1:])
-        t = {"q_win": (torch.randn(shapes["q_win"], generator=gen, device=device) * amp).to(tdt)}
+        t = {"q_win": (torch.randn(shapes["q_win"], generator=gen, device=device) * (amp * q_scale)).to(tdt)}
         kh.copy_((torch.randn(kh.shape, generator=gen, device=device) * amp).to(tdt))
         t["k_win"] = (torch.randn(rest, generator=gen, device=device) * amp).to(tdt)
         vh.copy_((torch.randn(vh.shape, generator=gen, device=device) * amp).to(tdt))
@@ -239,9 +240,10 @@ def window_inputs_head_ring(stream_w, pass_index, st, device="cuda"):
     return out
 
 
-def window_inputs(stream_w, pass_index, layers, shapes, device="cuda"):
+def window_inputs(stream_w, pass_index, layers, shapes, device="cuda", q_scale=1.0):
     """Window Q/K/V of every layer for one pass: one generator seeded
-    seed_base + pass_index draws q, k, v of layer 0, then layer 1, ..."""
+    seed_base + pass_index draws q, k, v of layer 0, then layer 1, ...
+    (q_scale multiplies the query draws before rounding)."""
     import torch
 
     gen = torch.Generator(device=device)
@@ -252,6 +254,6 @@ def window_inputs(stream_w, pass_index, layers, shapes, device="cuda"):
         t = {}
         for name in ("q_win", "k_win", "v_win"):
             x = torch.randn(shapes[name], generator=gen, device=device, dtype=torch.float32)
-            t[name] = (x * stream_w["amplitude"]).to(tdt)
+            t[name] = (x * (stream_w["amplitude"] * (q_scale if name == "q_win" else 1.0))).to(tdt)
         out.append(t)
     return out

@@ -26,8 +26,19 @@ def from_device(t, dtype):
     return t.cpu().numpy().astype(np.float64)
 
 
+LOG2E = 1.4426950408889634
+
+
+def q_prescale(desc):
+    """The factor softmax_scale * log2(e) that a MSSA_PLAN_Q_PRESCALED plan
+    expects on the queries (float64)."""
+    return oracle.softmax_scale(desc) * LOG2E
+
+
 class GpuRun:
-    """Plan + seeded inputs + one pool_kv/forward pass on cuda:0."""
+    """Plan + seeded inputs + one pool_kv/forward pass on cuda:0.  With
+    desc["q_prescaled"] the queries are drawn at amplitude * softmax_scale *
+    log2(e) (rounded once) and the oracle gets them divided by that factor."""
 
     def __init__(self, desc, dtype, seed, amplitude, inputs=None, attention_blocks=0):
         self.desc = dict(desc)
@@ -38,7 +49,8 @@ class GpuRun:
             self.plan = mssa.mssa_plan_create(dict(desc, dtype=dtype))
         self.info = self.plan.info()
         shapes = input_shapes(desc, self.info["n_q"], self.info["n_sink_tok"], self.info["n_hist_tok"])
-        self.x = inputs if inputs is not None else make_inputs(shapes, seed, amplitude, dtype)
+        qa = amplitude * q_prescale(desc) if desc.get("q_prescaled") else None
+        self.x = inputs if inputs is not None else make_inputs(shapes, seed, amplitude, dtype, q_amplitude=qa)
         self.d = {k: to_device(v, dtype) for k, v in self.x.items()}
         self.ws = torch.empty(max(256, self.info["workspace_bytes"]), dtype=torch.uint8, device="cuda")
         self.out = torch.empty_like(self.d["q_win"])
@@ -77,6 +89,8 @@ class GpuRun:
                 continue
             v = v if heads is None else v[:, heads]
             out[k] = to_f64(v, self.dtype)
+        if self.desc.get("q_prescaled"):
+            out["q_win"] = out["q_win"] / q_prescale(self.desc)
         return out
 
     def oracle(self, heads=None, q_index=None):

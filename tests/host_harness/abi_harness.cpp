@@ -490,7 +490,7 @@ void invalid_descriptors() {
       {"heads 0", [](mssa_plan_desc& d) { d.num_heads = 0; }, MSSA_ERR_INVALID_ARG},
       {"dtype 7", [](mssa_plan_desc& d) { d.dtype = 7; }, MSSA_ERR_INVALID_ARG},
       {"scale inf", [](mssa_plan_desc& d) { d.softmax_scale = 1.0f / 0.0f; }, MSSA_ERR_INVALID_ARG},
-      {"flags 8", [](mssa_plan_desc& d) { d.flags = 8; }, MSSA_ERR_INVALID_ARG},
+      {"flags 16", [](mssa_plan_desc& d) { d.flags = 16; }, MSSA_ERR_INVALID_ARG},
       {"head in ring alone", [](mssa_plan_desc& d) { d.flags = MSSA_PLAN_HEAD_IN_RING; }, MSSA_ERR_UNSUPPORTED},
       {"scale 3", [](mssa_plan_desc& d) { d.scales[2] = 3; }, MSSA_ERR_UNSUPPORTED},
       {"scale 128", [](mssa_plan_desc& d) { d.scales[4] = 128; }, MSSA_ERR_UNSUPPORTED},
@@ -560,6 +560,7 @@ int main(int argc, char** argv) {
     int flags = static_cast<int>(rnd(4));
     const bool bf = rnd(4) != 0;
     if ((flags & MSSA_PLAN_POOLED_HIST_RING) && sc[0] == 1 && bf && rnd(2)) flags |= MSSA_PLAN_HEAD_IN_RING;
+    if (rnd(2)) flags |= MSSA_PLAN_Q_PRESCALED;
     const mssa_plan_desc d = make_desc(T, sc, 1 + static_cast<int>(rnd(70)), 1 + static_cast<int>(rnd(90)),
                                        1 + static_cast<int>(rnd(4)), static_cast<int>(rnd(5)),
                                        static_cast<int>(rnd(26)), 1 + static_cast<int>(rnd(48)),

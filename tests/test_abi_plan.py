@@ -214,7 +214,7 @@ def test_pooled_hist_ring_calls_checked():
     rejected at plan creation."""
     desc = WORKLOADS["wan13b_layer"]["desc"]
     with pytest.raises(mssa.MssaError) as e:
-        _plan(desc, flags=8)
+        _plan(desc, flags=16)
     assert e.value.status == mssa.MSSA_ERR_INVALID_ARG
     plain, ring = _plan(desc), _plan(desc, flags=RING)
     fake = 1 << 20

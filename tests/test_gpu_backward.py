@@ -18,7 +18,7 @@ from paper_2607_20940_amd import mssa
 from paper_2607_20940_amd.inputs import make_grad_output, make_inputs, to_f64
 from paper_2607_20940_amd.workloads import WORKLOADS, input_shapes
 
-from gpu_common import errors, from_device, to_device
+from gpu_common import errors, from_device, q_prescale, to_device
 
 pytestmark = pytest.mark.gpu
 
@@ -40,7 +40,12 @@ class BwdRun:
         self.plan = mssa.mssa_plan_create(dict(desc, dtype=dtype))
         self.info = self.plan.info()
         shapes = input_shapes(desc, self.info["n_q"], self.info["n_sink_tok"], self.info["n_hist_tok"])
-        self.x = make_inputs(shapes, seed, amp, dtype)
+        # desc["q_prescaled"]: queries drawn at amp * softmax_scale * log2(e);
+        # the oracle sees them divided by that factor, and dq_win is the
+        # gradient with respect to the scaled queries.
+        self.qf = q_prescale(desc) if desc.get("q_prescaled") else 1.0
+        self.x = make_inputs(shapes, seed, amp, dtype,
+                             q_amplitude=amp * self.qf if desc.get("q_prescaled") else None)
         self.go = make_grad_output(shapes["q_win"], seed + 7919, gamp, dtype)
         self.d = {k: to_device(v, dtype) for k, v in self.x.items()}
         self.d_out = to_device(self.go, dtype)
@@ -68,12 +73,16 @@ class BwdRun:
         return {k: (None if t is None else from_device(t, self.dtype)) for k, t in self.g.items()}
 
     def x64(self):
-        return {k: (None if v is None else to_f64(v, self.dtype)) for k, v in self.x.items()}
+        x = {k: (None if v is None else to_f64(v, self.dtype)) for k, v in self.x.items()}
+        x["q_win"] = x["q_win"] / self.qf
+        return x
 
     def oracle(self, heads=None):
         x = self.x64()
-        return oracle.mssa_backward(self.desc, *(x[k] for k in NAMES), to_f64(self.go, self.dtype),
-                                    heads=heads)
+        ref = oracle.mssa_backward(self.desc, *(x[k] for k in NAMES), to_f64(self.go, self.dtype),
+                                   heads=heads)
+        ref["dq_win"] = ref["dq_win"] / self.qf
+        return ref
 
     def oracle_lse(self):
         """log sum exp of the scaled scores over each query's context (from
@@ -143,6 +152,22 @@ SMALL = {
 def test_backward_bf16_small(name):
     desc, seed = SMALL[name]
     _check(desc, "bf16", seed, AMP, name)
+
+
+@pytest.mark.parametrize("name", ["ragged_3level_d128", "ragged_3level_d64", "paper_schedule_small"])
+@pytest.mark.parametrize("unit", [False, True])
+def test_backward_q_prescaled(name, unit):
+    """MSSA_PLAN_Q_PRESCALED: forward with lse and backward on queries scaled
+    by softmax_scale * log2(e); dq_win is the gradient with respect to them
+    (the oracle's dq divided by the factor), the other gradients unchanged."""
+    desc, seed = SMALL[name]
+    _check(dict(desc, q_prescaled=True), "bf16", seed + 400, 1.0 if unit else AMP,
+           name + ("_unit" if unit else "") + "_prescaled")
+
+
+def test_backward_q_prescaled_f32():
+    _check(_desc(3, [1, 2, 4], 7, 11, F=2, S=1, Hh=2, nh=2, q_prescaled=True), "f32", 23, 1.0,
+           "f32_prescaled")
 
 
 @pytest.mark.parametrize("name", ["ragged_3level_d128", "paper_schedule_small", "stride_ragged"])

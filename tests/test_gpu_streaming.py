@@ -13,7 +13,7 @@ from paper_2607_20940_amd.inputs import to_f64
 from paper_2607_20940_amd.streaming import StreamingMSSA, init_inputs, window_inputs, window_inputs_head_ring
 from paper_2607_20940_amd.workloads import STREAMING
 
-from gpu_common import assert_close
+from gpu_common import assert_close, q_prescale
 
 pytestmark = pytest.mark.gpu
 
@@ -22,15 +22,15 @@ def _f64(t):
     return None if t is None else t.float().cpu().numpy().astype(np.float64)
 
 
-def _window(stream_w, p, st, win_shapes):
+def _window(stream_w, p, st, win_shapes, q_scale=1.0):
     """This pass's window inputs of every layer: (what layer_pass takes,
     the full window {q_win, k_win, v_win} the oracle reads).  With the head
     state in the ring, its K/V are read back from the spare slots its
     producer wrote."""
     if not st.head_in_ring:
-        wins = window_inputs(stream_w, p, st.layers, win_shapes)
+        wins = window_inputs(stream_w, p, st.layers, win_shapes, q_scale=q_scale)
         return wins, wins
-    wins = window_inputs_head_ring(stream_w, p, st)
+    wins = window_inputs_head_ring(stream_w, p, st, q_scale=q_scale)
     full = []
     for L in range(st.layers):
         kh, vh = st.head_slots(L)
@@ -39,11 +39,14 @@ def _window(stream_w, p, st, win_shapes):
     return wins, full
 
 
-def _run(stream_w, layers, passes, check, pooled_ring=False, head_in_ring=False):
+def _run(stream_w, layers, passes, check, pooled_ring=False, head_in_ring=False, q_prescaled=False):
+    """q_prescaled: queries drawn pre-scaled by softmax_scale * log2(e)
+    (MSSA_PLAN_Q_PRESCALED); the oracle gets them divided by that factor."""
     desc = stream_w["layer"]
     F = desc["frames_per_state"]
+    qf = q_prescale(desc) if q_prescaled else 1.0
     st = StreamingMSSA(desc, layers, stream_w["hist_cap_frames"], dtype=stream_w["dtype"],
-                       pooled_ring=pooled_ring, head_in_ring=head_in_ring)
+                       pooled_ring=pooled_ring, head_in_ring=head_in_ring, q_prescaled=q_prescaled)
     tok1 = st.tok1
     hist = {}
     init_shapes = st.shapes(stream_w["hist_start_frames"])
@@ -58,7 +61,7 @@ def _run(stream_w, layers, passes, check, pooled_ring=False, head_in_ring=False)
     win_shapes = st.shapes(0)
     checked = 0
     for p in range(passes):
-        args, wins = _window(stream_w, p, st, win_shapes)
+        args, wins = _window(stream_w, p, st, win_shapes, q_scale=qf)
         for L in range(layers):
             w = wins[L]
             out = torch.empty_like(w["q_win"])
@@ -71,7 +74,7 @@ def _run(stream_w, layers, passes, check, pooled_ring=False, head_in_ring=False)
                 got = out.float().cpu().numpy().astype(np.float64)
                 ks = np.concatenate(h["k"]) if h["k"] else None
                 vs = np.concatenate(h["v"]) if h["v"] else None
-                kw, vw, qw = _f64(w["k_win"]), _f64(w["v_win"]), _f64(w["q_win"])
+                kw, vw, qw = _f64(w["k_win"]), _f64(w["v_win"]), _f64(w["q_win"]) / qf
                 rows, heads = check(p, L)
                 if heads is not None:
                     d["num_heads"] = len(heads)
@@ -165,6 +168,15 @@ def test_streaming_head_in_ring_every_output(layer):
     assert [r.count for r in st.ring] == [w["hist_cap_frames"]] * 2
     # 9 passes, each advancing the spare slots by F, modulo cap + F slots
     assert [r.spare for r in st.ring] == [(w["hist_start_frames"] + 9 * F) % (w["hist_cap_frames"] + F)] * 2
+
+
+def test_streaming_head_in_ring_q_prescaled_every_output():
+    """The copy-free streaming path with queries handed over pre-scaled by
+    softmax_scale * log2(e): every output of two layers over ring
+    wrap-arounds against the oracle on the unscaled queries."""
+    w = dict(SMALL)
+    st, n = _run(w, layers=2, passes=9, check=lambda p, L: (None, None), head_in_ring=True, q_prescaled=True)
+    assert n == 18
 
 
 def test_graph_pass_equals_eager_head_in_ring():
