@@ -679,6 +679,7 @@ mssa_status mssa_backward(mssa_plan plan, const void* q_win, const void* k_sink,
     a.num_heads = nh;
     a.n_groups = G;
     set_score_scales(p, a.scale, a.scale_log2e);
+    a.q_prescaled = p.q_prescaled ? 1 : 0;
     const int qb = bf16 ? mssa::kBwdQ : mssa::kBwdF32, kb = bf16 ? mssa::kBwdK : mssa::kBwdF32;
     const KvSources src{k_sink, v_sink, k_hist, v_hist, nullptr, nullptr, k_win, v_win, ws};
     int64_t dq_blocks = 0, kv_blocks = 0;

@@ -130,8 +130,12 @@ __device__ inline int swz(int row, int col) { return swz256(row, col); }
 // context streams in 64-key stages inside one run at a time (K and V tiles
 // through three LDS buffers: in iteration i the A waves use stage i, the B
 // waves stage i - 1, and the transfers fill stage i + 1; P of stage i goes to
-// exchange buffer i & 1).  One barrier per iteration.
-template <int D>
+// exchange buffer i & 1).  One barrier per iteration.  Both waves start their
+// first product from an accumulator holding the lane's row statistic
+// negated, so B's dP arrives as dP - rowsum and (kQS: queries pre-scaled by
+// scale * log2 e, c = 1) A's S as S - lse, leaving one VALU instruction less
+// per score.
+template <int D, bool kQS>
 __global__ __launch_bounds__(kBwdQThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void dq_kernel(BwdArgs a) {
   using L = Lay<D>;
@@ -175,6 +179,11 @@ void dq_kernel(BwdArgs a) {
   }
   const int64_t stat = static_cast<int64_t>(head) * a.n_q + (q_ok ? q_row : G.q_begin);
   const float rstat = !q_ok ? 0.f : role == 0 ? a.lse[stat] * kLog2e : a.dsum[stat];
+  // Accumulator input of the first product: -rowsum for B (dP arrives as
+  // dP - rowsum), -lse for A with pre-scaled queries (S arrives as S - lse).
+  f32x16 cinit;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) cinit[e] = (role != 0 || kQS) ? -rstat : 0.f;
 
   f32x16 acc[DB];  // dQ^T (role 1)
 #pragma unroll
@@ -266,7 +275,7 @@ void dq_kernel(BwdArgs a) {
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
         const bf16x8 ax = *reinterpret_cast<const bf16x8*>(Xs + kb * 32 * 128 + (r_rd ^ (ks * 16)));
-        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ax, xf[ks], ks == 0 ? f32x16{} : s[kb], 0, 0, 0);
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ax, xf[ks], ks == 0 ? cinit : s[kb], 0, 0, 0);
       }
     if (role == 0) {
 #pragma unroll
@@ -279,7 +288,8 @@ void dq_kernel(BwdArgs a) {
         bf16x8 pb[2];
 #pragma unroll
         for (int e = 0; e < 16; ++e)
-          pb[e >> 3][e & 7] = static_cast<__bf16>(__builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][e], c, -rstat)));
+          pb[e >> 3][e & 7] =
+              static_cast<__bf16>(__builtin_amdgcn_exp2f(kQS ? s[kb][e] : __builtin_fmaf(s[kb][e], c, -rstat)));
         pex[(kb * 2) * 64] = pb[0];
         pex[(kb * 2 + 1) * 64] = pb[1];
       }
@@ -291,7 +301,7 @@ void dq_kernel(BwdArgs a) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const float p = static_cast<float>((e < 8 ? p0 : p1)[e & 7]);
-          dsb[kb][e >> 3][e & 7] = static_cast<__bf16>(p * (s[kb][e] - rstat));
+          dsb[kb][e >> 3][e & 7] = static_cast<__bf16>(p * s[kb][e]);
         }
       }
 #pragma unroll
@@ -789,10 +799,14 @@ hipError_t launch_bwd(const BwdArgs& a, int dq_blocks, int kv_blocks, int head_d
                       hipStream_t stream) {
   if (dq_blocks > 0) {
     if (bf16) {
-      if (head_dim == 128)
-        hipLaunchKernelGGL(dq_kernel<128>, dim3(dq_blocks), dim3(kBwdQThreads), 0, stream, a);
+      if (head_dim == 128 && a.q_prescaled)
+        hipLaunchKernelGGL((dq_kernel<128, true>), dim3(dq_blocks), dim3(kBwdQThreads), 0, stream, a);
+      else if (head_dim == 128)
+        hipLaunchKernelGGL((dq_kernel<128, false>), dim3(dq_blocks), dim3(kBwdQThreads), 0, stream, a);
+      else if (a.q_prescaled)
+        hipLaunchKernelGGL((dq_kernel<64, true>), dim3(dq_blocks), dim3(kBwdQThreads), 0, stream, a);
       else
-        hipLaunchKernelGGL(dq_kernel<64>, dim3(dq_blocks), dim3(kBwdQThreads), 0, stream, a);
+        hipLaunchKernelGGL((dq_kernel<64, false>), dim3(dq_blocks), dim3(kBwdQThreads), 0, stream, a);
     } else {
       if (head_dim == 128)
         hipLaunchKernelGGL(dq_f32_kernel<128>, dim3(dq_blocks), dim3(kBwdF32), 0, stream, a);

@@ -106,7 +106,7 @@ struct BwdArgs {
   int32_t n_groups;
   float scale;              // softmax scale
   float scale_log2e;
-  int32_t pad;
+  int32_t q_prescaled;      // queries arrive multiplied by scale * log2(e)
   BwdGroupArgs groups[kMaxGroups];  // longest query range first
 };
 
