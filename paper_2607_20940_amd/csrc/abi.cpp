@@ -664,6 +664,11 @@ mssa_status mssa_backward(mssa_plan plan, const void* q_win, const void* k_sink,
     da.n_q = static_cast<int32_t>(p.n_q);
     da.num_heads = nh;
     da.head_dim = hd;
+    {
+      float sc = 0.f, sc2 = 0.f;
+      set_score_scales(p, sc, sc2);
+      da.inv_scale = 1.0f / sc;
+    }
     mssa_status s = check_device(mssa::launch_bwd_dot(da, bf16, hs), "backward rowsum launch");
     if (s != MSSA_OK) return s;
 

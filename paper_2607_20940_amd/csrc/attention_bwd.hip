@@ -109,8 +109,11 @@ __global__ __launch_bounds__(kDotThreads) void dot_kernel(DotArgs a) {
 #pragma unroll
     for (int e = 0; e < N; ++e) acc = __builtin_fmaf(static_cast<float>(ov[e]), static_cast<float>(gv[e]), acc);
   }
-  a.dsum[static_cast<int64_t>(h) * a.n_q + q] = acc;
-  if (a.lse) a.lse2[static_cast<int64_t>(h) * a.n_q + q] = a.lse[static_cast<int64_t>(h) * a.n_q + q] * kLog2e;
+  // Both statistics are stored negated, as the dK/dV kernel's accumulator
+  // inputs: -rowsum, and -lse / scale (the row's log-sum-exp in units of the
+  // unscaled scores q k^T).
+  a.dsum[static_cast<int64_t>(h) * a.n_q + q] = -acc;
+  if (a.lse) a.lse2[static_cast<int64_t>(h) * a.n_q + q] = -a.lse[static_cast<int64_t>(h) * a.n_q + q] * a.inv_scale;
 }
 
 // ------------------------------------------------------------------ bf16 kernels
@@ -178,7 +181,7 @@ void dq_kernel(BwdArgs a) {
     for (int ks = 0; ks < KS; ++ks) xf[ks] = q_ok ? *reinterpret_cast<const bf16x8*>(xp + ks * 16) : bf16x8{};
   }
   const int64_t stat = static_cast<int64_t>(head) * a.n_q + (q_ok ? q_row : G.q_begin);
-  const float rstat = !q_ok ? 0.f : role == 0 ? a.lse[stat] * kLog2e : a.dsum[stat];
+  const float rstat = !q_ok ? 0.f : role == 0 ? a.lse[stat] * kLog2e : -a.dsum[stat];
   // Accumulator input of the first product: -rowsum for B (dP arrives as
   // dP - rowsum), -lse for A with pre-scaled queries (S arrives as S - lse).
   f32x16 cinit;
@@ -378,15 +381,19 @@ void dq_kernel(BwdArgs a) {
 // B's VALU phases hold no transfer work.  P_t is written in phase 2t + 1 and
 // read in 2t + 2; one block per pair suffices.
 // The matrix-core step is one code site for both roles, so that the register
-// allocation holds one set of accumulators, S/dP and P/dS registers.
-template <int D>
+// allocation holds one set of accumulators, S/dP and P/dS registers.  Its row
+// product starts from an accumulator loaded with the stage's negated row
+// statistics (-lse / scale for A, -rowsum for B), so that S arrives as
+// S - lse / scale (P = exp2(c S'); kQS, queries pre-scaled: c = 1 and
+// P = exp2(S')) and dP as dP - rowsum (dS = P dP').
+template <int D, bool kQS>
 __global__ __launch_bounds__(kBwdKVThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void dkdv_kernel(BwdArgs a) {
   using L = Lay<D>;
   constexpr int KS = L::KS, DB = L::DB;
   constexpr int BQ = kBwdQS, NQB = BQ / 32;             // queries per stage, 32-query blocks
   constexpr int QT = BQ * 128 * 2;                      // bytes of one swizzled tile (256-byte rows)
-  constexpr int STB = 2 * QT + 8 * BQ;                  // Q | dO | lse2 | rowsum (fp32)
+  constexpr int STB = 2 * QT + 8 * BQ;                  // Q | dO | -lse / scale | -rowsum (fp32)
   constexpr int NDMA = 2 * QT / 1024 / 4;               // 1 KB transfers per B wave and stage (Q and dO)
   constexpr int PXB = NQB * 2 * 64 * 16;                // bytes of one pair's P block
   constexpr int kLead = 4;                              // LDS operands read ahead of their MFMA
@@ -450,10 +457,10 @@ void dkdv_kernel(BwdArgs a) {
   const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds));
   // Stage queries [q0, q0 + BQ) into LDS buffer buf (B waves), all by
   // direct transfers: the Q (waves 4, 5) or dO (waves 6, 7) tile rows, and
-  // the stage's lse in log2 units (wave 4) and rowsum (wave 5), one dword per
-  // lane.  Queries past the end arrive as zero rows with zero statistics:
-  // their P = exp2(0) = 1 meets zero dO rows (no dV contribution) and
-  // dS = 1 (0 - 0) = 0.  Loop-invariant values are kept in registers.
+  // the stage's negated statistics -lse / scale (wave 4) and -rowsum (wave
+  // 5), one dword per lane.  Queries past the end arrive as zero rows with
+  // zero statistics: their P = exp2(0) = 1 meets zero dO rows (no dV
+  // contribution) and dS = 1 (0 - 0) = 0.  Loop-invariant values are kept in registers.
   static_assert(2 * NDMA * 1024 == QT && BQ == 64, "two B waves per tile, one statistic per lane");
   const int q_begin = G.q_begin, q_end = G.q_end;
   const __bf16* const x_head = static_cast<const __bf16*>((wave & 3) < 2 ? a.q : a.d_out) + hoff;
@@ -488,12 +495,23 @@ void dkdv_kernel(BwdArgs a) {
   // Matrix-core step of a phase: the accumulating product of the previous
   // stage (if acc_c: A^T rows of Ys, the wave's w as B operand), then the row
   // product of the current stage (if row_c: rows of Xs times the wave's
-  // fragment), as one stream of MFMAs whose LDS operands run kLead ahead.
-  auto mstep = [&](auto acc_c, auto row_c, const __bf16* Ys, const __bf16* Xs) {
+  // fragment, starting from the statistics at Cs), as one stream of MFMAs
+  // whose LDS operands run kLead ahead.
+  auto mstep = [&](auto acc_c, auto row_c, const __bf16* Ys, const __bf16* Xs, const float* Cs) {
     constexpr bool kA = decltype(acc_c)::value, kR = decltype(row_c)::value;
     constexpr int NA = kA ? NQB * 2 * DB : 0;  // (32-row block, 16-row half, column block)
     constexpr int NR = kR ? NQB * KS : 0;      // (32-row block, k step)
     constexpr int N = NA + NR;
+    if constexpr (kR) {
+#pragma unroll
+      for (int qb = 0; qb < NQB; ++qb)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const f32x4 c4 = *reinterpret_cast<const f32x4*>(Cs + qb * 32 + 8 * j + 4 * hh);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) s[qb][4 * j + i] = c4[i];
+        }
+    }
     auto operand = [&](int i) -> bf16x8 {
       if (i < NA) {
         const int qb = i / (2 * DB), cc = (i / DB) & 1, db = i % DB;
@@ -517,7 +535,7 @@ void dkdv_kernel(BwdArgs a) {
         acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, w[qb][cc], acc[db], 0, 0, 0);
       } else {
         const int j = i - NA, qb = j / KS, ks = j % KS;
-        s[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, xf[ks], ks == 0 ? f32x16{} : s[qb], 0, 0, 0);
+        s[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, xf[ks], s[qb], 0, 0, 0);
       }
       if (i + kLead < N) ring[i % kLead] = operand(i + kLead);
     }
@@ -525,6 +543,7 @@ void dkdv_kernel(BwdArgs a) {
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       if (i < NA) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     };
+    if (kR) __builtin_amdgcn_sched_group_barrier(0x100, 4 * NQB, 0);  // the statistics
 #pragma unroll
     for (int i = 0; i < (N < kLead ? N : kLead); ++i) read_group(i);
 #pragma unroll
@@ -536,20 +555,14 @@ void dkdv_kernel(BwdArgs a) {
   };
   // Element e of a 32x32 accumulator in this layout holds query
   // qb*32 + 8(e/4) + 4hh + e%4 of the lane's key.
-  // A: P_t = exp2(S_t c - lse_t) into w and into the pair's LDS block.
-  auto softmax_a = [&](int buf) {
-    const float* lse_s = reinterpret_cast<const float*>(lds + buf * STB + 2 * QT);
+  // A: P_t = exp2(S'_t c) (S' = S - lse / scale) into w and into the pair's
+  // LDS block.
+  auto softmax_a = [&]() {
 #pragma unroll
     for (int qb = 0; qb < NQB; ++qb) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const f32x4 l4 = *reinterpret_cast<const f32x4*>(lse_s + qb * 32 + 8 * j + 4 * hh);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int e = 4 * j + i;
-          w[qb][e >> 3][e & 7] = static_cast<__bf16>(__builtin_amdgcn_exp2f(__builtin_fmaf(s[qb][e], c, -l4[i])));
-        }
-      }
+      for (int e = 0; e < 16; ++e)
+        w[qb][e >> 3][e & 7] = static_cast<__bf16>(__builtin_amdgcn_exp2f(kQS ? s[qb][e] : s[qb][e] * c));
       pex[(qb * 2) * 64] = w[qb][0];
       pex[(qb * 2 + 1) * 64] = w[qb][1];
     }
@@ -558,21 +571,15 @@ void dkdv_kernel(BwdArgs a) {
 #pragma unroll
       for (int h = 0; h < 2; ++h) asm volatile("" : "+v"(w[qb][h]));
   };
-  // B: dS = P (dP - rowsum) of the stage in buffer buf into w.
-  auto softmax_b = [&](int buf) {
-    const float* rsum_s = reinterpret_cast<const float*>(lds + buf * STB + 2 * QT) + BQ;
+  // B: dS = P dP' (dP' = dP - rowsum) into w.
+  auto softmax_b = [&]() {
 #pragma unroll
     for (int qb = 0; qb < NQB; ++qb) {
       const bf16x8 p0 = pex[(qb * 2) * 64], p1 = pex[(qb * 2 + 1) * 64];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const f32x4 r4 = *reinterpret_cast<const f32x4*>(rsum_s + qb * 32 + 8 * j + 4 * hh);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int e = 4 * j + i;
-          const float p = static_cast<float>((e < 8 ? p0 : p1)[e & 7]);
-          w[qb][e >> 3][e & 7] = static_cast<__bf16>(p * (s[qb][e] - r4[i]));
-        }
+      for (int e = 0; e < 16; ++e) {
+        const float p = static_cast<float>((e < 8 ? p0 : p1)[e & 7]);
+        w[qb][e >> 3][e & 7] = static_cast<__bf16>(p * s[qb][e]);
       }
     }
 #pragma unroll
@@ -618,7 +625,8 @@ void dkdv_kernel(BwdArgs a) {
     const int t = ph >> 1, cur = t % NBUF, prev = (t + NBUF - 1) % NBUF;  // buffers of stages t, t - 1
     if ((ph & 1) == role) {
       __builtin_amdgcn_s_setprio(2);
-      mstep(T_{}, T_{}, tile(prev, 1 - role), tile(cur, role));
+      mstep(T_{}, T_{}, tile(prev, 1 - role), tile(cur, role),
+            reinterpret_cast<const float*>(lds + cur * STB + 2 * QT) + role * BQ);
       __builtin_amdgcn_s_setprio(0);
       if (role != 0) {
         if (t + 2 < nst) {
@@ -629,9 +637,9 @@ void dkdv_kernel(BwdArgs a) {
         }
       }
     } else if (role == 0) {
-      if (t < nst) softmax_a(cur);
+      if (t < nst) softmax_a();
     } else {
-      if (t >= 1) softmax_b(prev);
+      if (t >= 1) softmax_b();
     }
     __syncthreads();
   }
@@ -667,7 +675,7 @@ __global__ __launch_bounds__(kBwdF32) void dq_f32_kernel(BwdArgs a) {
   const float* qp = static_cast<const float*>(a.q) + static_cast<int64_t>(q_row) * ld + hoff;
   const float* gp = static_cast<const float*>(a.d_out) + static_cast<int64_t>(q_row) * ld + hoff;
   const int64_t stat = static_cast<int64_t>(head) * a.n_q + q_row;
-  const float lse = a.lse[stat], dsum = a.dsum[stat];
+  const float lse = a.lse[stat], dsum = -a.dsum[stat];
   float acc[D];
 #pragma unroll
   for (int d = 0; d < D; ++d) acc[d] = 0.f;
@@ -718,7 +726,7 @@ __global__ __launch_bounds__(kBwdF32) void dkdv_f32_kernel(BwdArgs a) {
       dp = __builtin_fmaf(gp[d], vp[d], dp);
     }
     const float p = expf(s * a.scale - a.lse[stat]);
-    const float ds = p * (dp - a.dsum[stat]);
+    const float ds = p * (dp + a.dsum[stat]);
 #pragma unroll
     for (int d = 0; d < D; ++d) {
       dv[d] = __builtin_fmaf(p, gp[d], dv[d]);
@@ -818,10 +826,14 @@ hipError_t launch_bwd(const BwdArgs& a, int dq_blocks, int kv_blocks, int head_d
   }
   if (kv_blocks > 0) {
     if (bf16) {
-      if (head_dim == 128)
-        hipLaunchKernelGGL(dkdv_kernel<128>, dim3(kv_blocks), dim3(kBwdKVThreads), 0, stream, a);
+      if (head_dim == 128 && a.q_prescaled)
+        hipLaunchKernelGGL((dkdv_kernel<128, true>), dim3(kv_blocks), dim3(kBwdKVThreads), 0, stream, a);
+      else if (head_dim == 128)
+        hipLaunchKernelGGL((dkdv_kernel<128, false>), dim3(kv_blocks), dim3(kBwdKVThreads), 0, stream, a);
+      else if (a.q_prescaled)
+        hipLaunchKernelGGL((dkdv_kernel<64, true>), dim3(kv_blocks), dim3(kBwdKVThreads), 0, stream, a);
       else
-        hipLaunchKernelGGL(dkdv_kernel<64>, dim3(kv_blocks), dim3(kBwdKVThreads), 0, stream, a);
+        hipLaunchKernelGGL((dkdv_kernel<64, false>), dim3(kv_blocks), dim3(kBwdKVThreads), 0, stream, a);
     } else {
       if (head_dim == 128)
         hipLaunchKernelGGL(dkdv_f32_kernel<128>, dim3(kv_blocks), dim3(kBwdF32), 0, stream, a);

@@ -97,8 +97,8 @@ struct BwdArgs {
   const void* q;
   const void* d_out;
   const float* lse;         // [heads, n_q] from the forward
-  const float* dsum;        // [heads, n_q]: rowsum(d_out * out)
-  const float* lse2;        // [heads, n_q]: lse in log2 units (lse * log2 e)
+  const float* dsum;        // [heads, n_q]: -rowsum(d_out * out)
+  const float* lse2;        // [heads, n_q]: -lse / scale, the statistic in units of q k^T
   void* dq;
   int64_t ld;               // elements between tokens: heads * head_dim
   int32_t n_q;
@@ -113,14 +113,14 @@ struct BwdArgs {
 struct DotArgs {
   const void* out;
   const void* d_out;
-  float* dsum;              // [heads, n_q]
+  float* dsum;              // [heads, n_q]: -rowsum(d_out * out)
   const float* lse;         // [heads, n_q] natural log (bf16 plans; may be null)
-  float* lse2;              // [heads, n_q] lse * log2 e (written when lse is set)
+  float* lse2;              // [heads, n_q] -lse / scale: minus the row max of q k^T (written when lse is set)
   int64_t ld;
   int32_t n_q;
   int32_t num_heads;
   int32_t head_dim;
-  int32_t pad;
+  float inv_scale;          // 1 / the natural-log score factor
 };
 
 // One run of source frames (sink, history, or window frames of one scale)
