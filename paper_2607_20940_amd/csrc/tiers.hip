@@ -425,21 +425,35 @@ void gemm256_kernel(GemmArgs a) {
     if (st + 1 < nst) issue(st + 1);
     const char* Xs = lds[st % kBStages][0];
     const char* Ws = lds[st % kBStages][1];
+    // Operands of k step ks in register set ks & 1: the reads of step ks + 1
+    // run between the MFMAs of step ks.
+    bf16x8 op[2][6];  // [set][W nb 0..1, X mb 0..3]
+    auto rd_op = [&](int ks, int j) -> bf16x8 {
+      return j < 2 ? *reinterpret_cast<const bf16x8*>(Ws + (wn * 64 + j * 32) * 128 + rd[ks])
+                   : *reinterpret_cast<const bf16x8*>(Xs + (wm * 128 + (j - 2) * 32) * 128 + rd[ks]);
+    };
+#pragma unroll
+    for (int j = 0; j < 6; ++j) op[0][j] = rd_op(0, j);
 #pragma unroll
     for (int ks = 0; ks < kBK / 16; ++ks) {
-      bf16x8 wa[2], xb[4];
+      const int c = ks & 1;
 #pragma unroll
-      for (int nb = 0; nb < 2; ++nb)
-        wa[nb] = *reinterpret_cast<const bf16x8*>(Ws + (wn * 64 + nb * 32) * 128 + rd[ks]);
-#pragma unroll
-      for (int mb = 0; mb < 4; ++mb)
-        xb[mb] = *reinterpret_cast<const bf16x8*>(Xs + (wm * 128 + mb * 32) * 128 + rd[ks]);
-#pragma unroll
-      for (int mb = 0; mb < 4; ++mb)
-#pragma unroll
-        for (int nb = 0; nb < 2; ++nb)
-          acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wa[nb], xb[mb], acc[mb][nb], 0, 0, 0);
+      for (int i = 0; i < 8; ++i) {
+        const int mb = i >> 1, nb = i & 1;
+        acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(op[c][nb], op[c][2 + mb], acc[mb][nb], 0, 0, 0);
+        if (ks + 1 < kBK / 16 && i < 6) op[c ^ 1][i] = rd_op(ks + 1, i);
+      }
     }
+#pragma unroll
+    for (int j = 0; j < 6; ++j) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+#pragma unroll
+    for (int ks = 0; ks < kBK / 16; ++ks)
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        if (ks + 1 < kBK / 16 && i < 6) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+    __builtin_amdgcn_sched_barrier(0);
   }
 
   // Epilogue through LDS in two halves of 128 rows (a padded 128 x 256 bf16
