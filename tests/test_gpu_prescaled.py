@@ -78,11 +78,13 @@ def test_prescaled_f32():
     _check(desc, "f32", seed + 900, 1.0, "f32")
 
 
-def test_prescaled_full_size_sampled():
-    """wan13b_layer at full size with pre-scaled queries: sampled rows of three
-    heads against the oracle, in the launch configuration bench.py times."""
-    w = WORKLOADS["wan13b_layer"]
+@pytest.mark.parametrize("name", ["wan13b_layer", "wan13b_longhist", "wan14b_720p"])
+def test_prescaled_full_size_sampled(name):
+    """The layer workloads at full size with pre-scaled queries (the layout
+    bench.py times): sampled rows of three heads against the oracle."""
+    w = WORKLOADS[name]
     desc = dict(w["desc"], q_prescaled=True)
+    print(f"[prescaled] full-size {name}", flush=True)
     r = GpuRun(desc, w["dtype"], w["seed"] + 1000, w["amplitude"])
     r.run()
     rng = np.random.default_rng(321)
@@ -91,8 +93,8 @@ def test_prescaled_full_size_sampled():
     heads = sorted({0, nh - 1, int(rng.integers(0, nh))})
     ref = r.oracle(heads=heads, q_index=rows)[rows]
     got = r.output()[rows][:, heads]
-    e = assert_close_by_group(got, ref, rows, _groups(r.info), w["dtype"], "wan13b_layer_prescaled")
-    print(f"[prescaled] full-size rows={len(rows)} heads={heads} {e}", flush=True)
+    e = assert_close_by_group(got, ref, rows, _groups(r.info), w["dtype"], name + "_prescaled")
+    print(f"[prescaled] full-size {name} rows={len(rows)} heads={heads} {e}", flush=True)
 
 
 def test_prescaled_matches_plain_within_rounding():

@@ -318,8 +318,8 @@ def test_graph_pass_equals_eager(pooled_ring):
     assert replays == 10 and len(graph._graphs) == 3
 
 
-@pytest.mark.parametrize("head_in_ring", [False, True])
-def test_streaming_full_workload_sampled(head_in_ring):
+@pytest.mark.parametrize("head_in_ring, q_prescaled", [(False, False), (True, False), (True, True)])
+def test_streaming_full_workload_sampled(head_in_ring, q_prescaled):
     """The whole streaming workload: 30 stacked layers of the Wan-1.3B shape
     over 64 rolling passes with pooled-history rings (history 6 -> 21 frames,
     then FIFO).  Six (pass, layer) points, including the last layer of the
@@ -333,7 +333,11 @@ def test_streaming_full_workload_sampled(head_in_ring):
     points = {(0, 0), (4, 29), (5, 14), (20, 7), (47, 21), (63, 29)}
     tracked = sorted({L for (_, L) in points})
     heads = [0, 11]
-    st = StreamingMSSA(desc, layers, cap, dtype=w["dtype"], pooled_ring=True, head_in_ring=head_in_ring)
+    # q_prescaled: queries pre-scaled by softmax_scale * log2(e), the layout
+    # bench.py times; the oracle reads them divided by the factor
+    qf = q_prescale(desc) if q_prescaled else 1.0
+    st = StreamingMSSA(desc, layers, cap, dtype=w["dtype"], pooled_ring=True, head_in_ring=head_in_ring,
+                       q_prescaled=q_prescaled)
     tok1 = st.tok1
 
     def host(t):  # selected heads, bf16 bits on the host
@@ -357,7 +361,7 @@ def test_streaming_full_workload_sampled(head_in_ring):
     outs = [torch.empty(win_shapes["q_win"], dtype=torch.bfloat16, device="cuda") for _ in range(layers)]
     checked = 0
     for p in range(passes):
-        args, wins = _window(w, p, st, win_shapes)
+        args, wins = _window(w, p, st, win_shapes, q_scale=qf)
         for L in range(layers):
             st.layer_pass(L, args[L]["q_win"], args[L]["k_win"], args[L]["v_win"], outs[L])
             if L not in tracked:
@@ -367,7 +371,7 @@ def test_streaming_full_workload_sampled(head_in_ring):
             if (p, L) in points:
                 print(f"[stream-full] pass {p} layer {L} history {len(h['k'])} frames", flush=True)
                 d = dict(desc, hist_frames=len(h["k"]), num_heads=len(heads))
-                ref = oracle.mssa_attention(d, f64(host(wins[L]["q_win"])), f64(h["sink"][0]), f64(h["sink"][1]),
+                ref = oracle.mssa_attention(d, f64(host(wins[L]["q_win"])) / qf, f64(h["sink"][0]), f64(h["sink"][1]),
                                             f64(np.concatenate(h["k"])), f64(np.concatenate(h["v"])),
                                             f64(kw), f64(vw))
                 got = f64(host(outs[L]))
