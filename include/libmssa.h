@@ -250,7 +250,8 @@ mssa_status mssa_attention_noalloc(mssa_plan plan, const void* q_win, const void
 
 /* mssa_forward that also writes lse [H, n_q] (fp32, device, head-major):
  * lse[h * n_q + i] = log sum_j exp(softmax_scale q_i . k_j) over query i's
- * context, natural log.  Same arguments and errors as mssa_forward; lse must
+ * context, natural log (q the unscaled queries also for
+ * MSSA_PLAN_Q_PRESCALED plans).  Same arguments and errors as mssa_forward; lse must
  * be non-null and 16-byte aligned. */
 mssa_status mssa_forward_lse(mssa_plan plan, const void* q_win, const void* k_sink,
                              const void* v_sink, const void* k_hist, const void* v_hist,
@@ -271,7 +272,9 @@ mssa_status mssa_backward_workspace_size(mssa_plan plan, int64_t* bytes);
  *                    mssa_pool_kv wrote for these inputs (the forward's
  *                    workspace can be reused as is)
  *   dq_win .. dv_win device outputs shaped like the inputs, plan dtype,
- *                    written (not accumulated); dk_sink / dv_sink may be
+ *                    written (not accumulated; dq_win is the gradient with
+ *                    respect to q_win as passed, i.e. the scaled queries of
+ *                    a MSSA_PLAN_Q_PRESCALED plan); dk_sink / dv_sink may be
  *                    NULL iff sink_frames == 0, dk_hist / dv_hist iff
  *                    hist_frames == 0; no gradient may alias an input.
  * bf16 plans use bf16 matrix cores with fp32 accumulation (probabilities
