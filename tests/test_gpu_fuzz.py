@@ -63,3 +63,28 @@ def test_backward_random_descriptor(case):
     i, desc, dtype, seed = case
     amp = 1.0 if dtype == "f32" else 1.0 / np.sqrt(128.0)
     bwd_check(desc, dtype, seed, amp, f"fuzz {_id(case)}")
+
+
+QPRE_FWD_CASES = _cases(7777, 24)
+QPRE_BWD_CASES = _cases(8888, 8)
+
+
+@pytest.mark.parametrize("case", QPRE_FWD_CASES, ids=_id)
+def test_forward_random_descriptor_q_prescaled(case):
+    """The same generator with queries pre-scaled by softmax_scale * log2(e)
+    (MSSA_PLAN_Q_PRESCALED) at unit amplitude, so that the first-tile max
+    path and the lazy rescale run often; the oracle reads the unscaled
+    queries."""
+    i, desc, dtype, seed = case
+    desc = dict(desc, q_prescaled=True)
+    print(f"[fuzz] forward pre-scaled {_id(case)} desc={desc} seed={seed}", flush=True)
+    r = GpuRun(desc, dtype, seed, 1.0)
+    r.run()
+    e = assert_close(r.output(), r.oracle(), dtype, _id(case))
+    print(f"[fuzz] ok {e}", flush=True)
+
+
+@pytest.mark.parametrize("case", QPRE_BWD_CASES, ids=_id)
+def test_backward_random_descriptor_q_prescaled(case):
+    i, desc, dtype, seed = case
+    bwd_check(dict(desc, q_prescaled=True), dtype, seed, 1.0, f"fuzz pre-scaled {_id(case)}")
