@@ -328,6 +328,15 @@ mssa_status mssa_patch_unembed(mssa_plan plan, const mssa_tier_desc* tier, const
 mssa_status mssa_qkv_project(int64_t n_tokens, int32_t hidden, const void* x, const void* w_qkv,
                              const void* b_qkv, void* q, void* k, void* v, void* stream);
 
+/* mssa_qkv_project with the queries multiplied by q_scale: q = (x W_q^T +
+ * b_q) * q_scale, taken on the fp32 sum and rounded to bf16 once; k and v
+ * as mssa_qkv_project writes them.  With q_scale = softmax_scale * log2(e)
+ * it hands over the queries of a MSSA_PLAN_Q_PRESCALED plan (Eq. 4's score
+ * scale folded into the query projection's epilogue) with no second
+ * rounding.  MSSA_ERR_INVALID_ARG also for a non-finite q_scale. */
+mssa_status mssa_qkv_project_scaled(int64_t n_tokens, int32_t hidden, const void* x, const void* w_qkv,
+                                    const void* b_qkv, float q_scale, void* q, void* k, void* v, void* stream);
+
 /* Streaming cache roll (Sec. 3.1, Eq. 2; Alg. 1 KV-cache update): after a
  * rolling pass the head state (window state 1, which must be at native
  * scale: scales[0] == 1) is emitted, and its F native frames of K and V

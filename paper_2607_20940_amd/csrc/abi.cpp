@@ -4,6 +4,7 @@
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
@@ -845,6 +846,7 @@ mssa_status mssa_patch_embed(mssa_plan plan, const mssa_tier_desc* tier, const v
       s = check_device(mssa::launch_patchify(pa, hs), "patchify launch");
       if (s != MSSA_OK) return s;
       mssa::GemmArgs ga{};
+      ga.y0_scale = 1.f;
       ga.x = pa.rows;
       ga.w = w_embed[g];
       ga.bias = b_embed[g];
@@ -885,6 +887,7 @@ mssa_status mssa_patch_unembed(mssa_plan plan, const mssa_tier_desc* tier, const
       const TierGroup& t = tg[g];
       const mssa::QGroup& Q = p.groups[g];
       mssa::GemmArgs ga{};
+      ga.y0_scale = 1.f;
       ga.x = static_cast<const char*>(tokens) + static_cast<int64_t>(Q.q_begin) * hid * 2;
       ga.w = w_out[g];
       ga.bias = b_out[g];
@@ -916,12 +919,15 @@ mssa_status mssa_patch_unembed(mssa_plan plan, const mssa_tier_desc* tier, const
   });
 }
 
-mssa_status mssa_qkv_project(int64_t n_tokens, int32_t hidden, const void* x, const void* w_qkv, const void* b_qkv,
-                             void* q, void* k, void* v, void* stream) {
-  return guarded("mssa_qkv_project", [&]() -> mssa_status {
+namespace {
+
+mssa_status qkv_project(const char* who, int64_t n_tokens, int32_t hidden, const void* x, const void* w_qkv,
+                        const void* b_qkv, float q_scale, void* q, void* k, void* v, void* stream) {
+  return guarded(who, [&]() -> mssa_status {
     if (n_tokens < 0 || n_tokens > 0x7fffffff || hidden < 8 || hidden % 8 != 0 || hidden > (1 << 20))
       return fail(MSSA_ERR_INVALID_ARG, "n_tokens must fit int32 and hidden be a positive multiple of 8");
     if (!x || !w_qkv || !b_qkv || !q || !k || !v) return fail(MSSA_ERR_INVALID_ARG, "null argument");
+    if (!std::isfinite(q_scale)) return fail(MSSA_ERR_INVALID_ARG, "q_scale must be finite");
     for (const void* t : {x, w_qkv, static_cast<const void*>(q), static_cast<const void*>(k), static_cast<const void*>(v)})
       if (!aligned16(t)) return fail(MSSA_ERR_INVALID_ARG, "tensors must be 16-byte aligned");
     if (q == x || k == x || v == x) return fail(MSSA_ERR_INVALID_ARG, "outputs must not alias x");
@@ -938,8 +944,21 @@ mssa_status mssa_qkv_project(int64_t n_tokens, int32_t hidden, const void* x, co
     ga.split = hidden;
     ga.ldx = hidden;
     ga.ldy = hidden;
+    ga.y0_scale = q_scale;
     return check_device(mssa::launch_gemm(ga, static_cast<hipStream_t>(stream)), "QKV GEMM launch");
   });
+}
+
+}  // namespace
+
+mssa_status mssa_qkv_project(int64_t n_tokens, int32_t hidden, const void* x, const void* w_qkv, const void* b_qkv,
+                             void* q, void* k, void* v, void* stream) {
+  return qkv_project("mssa_qkv_project", n_tokens, hidden, x, w_qkv, b_qkv, 1.f, q, k, v, stream);
+}
+
+mssa_status mssa_qkv_project_scaled(int64_t n_tokens, int32_t hidden, const void* x, const void* w_qkv,
+                                    const void* b_qkv, float q_scale, void* q, void* k, void* v, void* stream) {
+  return qkv_project("mssa_qkv_project_scaled", n_tokens, hidden, x, w_qkv, b_qkv, q_scale, q, k, v, stream);
 }
 
 mssa_status mssa_hist_append(mssa_plan plan, const void* k_win, const void* v_win, void* k_ring, void* v_ring,

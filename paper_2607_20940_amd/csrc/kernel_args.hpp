@@ -182,7 +182,7 @@ struct GemmArgs {
   int64_t ldx, ldy;
   float* partial;     // k_splits > 1: fp32 partial tiles of every K slice (launch_gemm_split)
   int32_t k_splits;   // 0 or 1: the whole K in one block
-  int32_t pad;
+  float y0_scale;     // factor on the outputs of y[0] (columns < split), applied to the fp32 sum before rounding
 };
 
 struct PoolJobArgs {

@@ -164,9 +164,11 @@ __global__ __launch_bounds__(kTierThreads) void gemm_kernel(GemmArgs a) {
         const int col = tn * kGN + wn * 64 + cb * 32 + 8 * jj + 4 * hh;
         if (col >= a.N) continue;
         const int part = col / a.split, pc = col % a.split;  // 4 features never straddle a split (split % 4 == 0)
+        const float sc = part == 0 ? a.y0_scale : 1.f;
         bf16x4 v;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) v[i] = static_cast<__bf16>(acc[rb][cb][4 * jj + i] + static_cast<float>(B[col + i]));
+        for (int i = 0; i < 4; ++i)
+          v[i] = static_cast<__bf16>((acc[rb][cb][4 * jj + i] + static_cast<float>(B[col + i])) * sc);
         *reinterpret_cast<bf16x4*>(static_cast<__bf16*>(a.y[part]) + row * a.ldy + pc) = v;
       }
   }
@@ -287,11 +289,13 @@ __global__ __launch_bounds__(kTierThreads, 2) void gemm_dma_kernel(GemmArgs a) {
       const int ct = wn * 64 + cb * 32 + 8 * jj + 4 * hh;
       const int col = tn * kGN + ct;
       const bf16x4 bv = col < a.N ? *reinterpret_cast<const bf16x4*>(B + col) : bf16x4{};
+      const float sc = col < a.split ? a.y0_scale : 1.f;
 #pragma unroll
       for (int rb = 0; rb < 2; ++rb) {
         bf16x4 v;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) v[i] = static_cast<__bf16>(acc[rb][cb][4 * jj + i] + static_cast<float>(bv[i]));
+        for (int i = 0; i < 4; ++i)
+          v[i] = static_cast<__bf16>((acc[rb][cb][4 * jj + i] + static_cast<float>(bv[i])) * sc);
         *reinterpret_cast<bf16x4*>(E + (wm * 64 + rb * 32 + n32) * kEStr + ct) = v;
       }
     }
@@ -329,10 +333,11 @@ __global__ __launch_bounds__(kTierThreads) void gemm_reduce_kernel(GemmArgs a) {
   f32x4 s = P[0];
   for (int k = 1; k < a.k_splits; ++k) s += P[k * per_slice];
   const __bf16* B = static_cast<const __bf16*>(a.bias) + col;
+  const int part = col / a.split, pc = col % a.split;
+  const float sc = part == 0 ? a.y0_scale : 1.f;
   bf16x4 v;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) v[i] = static_cast<__bf16>(s[i] + static_cast<float>(B[i]));
-  const int part = col / a.split, pc = col % a.split;
+  for (int i = 0; i < 4; ++i) v[i] = static_cast<__bf16>((s[i] + static_cast<float>(B[i])) * sc);
   *reinterpret_cast<bf16x4*>(static_cast<__bf16*>(a.y[part]) + row * a.ldy + pc) = v;
 }
 
@@ -403,12 +408,14 @@ void gemm256_kernel(GemmArgs a) {
 
   // The bias of this lane's 32 output features, loaded before the loop.
   bf16x4 bias[2][4];
+  float osc[2][4];  // y0_scale for the features of y[0], else 1
 #pragma unroll
   for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
     for (int jj = 0; jj < 4; ++jj) {
       const int col = tn * kBN + wn * 64 + nb * 32 + 8 * jj + 4 * hh;
       bias[nb][jj] = col < a.N ? *reinterpret_cast<const bf16x4*>(static_cast<const __bf16*>(a.bias) + col) : bf16x4{};
+      osc[nb][jj] = col < a.split ? a.y0_scale : 1.f;
     }
 
   // Operand reads: row (block base + n32), columns 16 ks + 8 hh; the swizzle
@@ -476,7 +483,7 @@ void gemm256_kernel(GemmArgs a) {
             bf16x4 v;
 #pragma unroll
             for (int i = 0; i < 4; ++i)
-              v[i] = static_cast<__bf16>(acc[mb][nb][4 * jj + i] + static_cast<float>(bias[nb][jj][i]));
+              v[i] = static_cast<__bf16>((acc[mb][nb][4 * jj + i] + static_cast<float>(bias[nb][jj][i])) * osc[nb][jj]);
             *reinterpret_cast<bf16x4*>(E + (mb * 32 + n32) * kEStr + wn * 64 + nb * 32 + 8 * jj + 4 * hh) = v;
           }
     }

@@ -28,7 +28,7 @@ EXPORTS = ("mssa_plan_create", "mssa_plan_create_ex", "mssa_plan_destroy", "mssa
            "mssa_pool_kv", "mssa_forward", "mssa_hist_append", "mssa_pool_hist_ring",
            "mssa_forward_ring", "mssa_hist_append_ring", "mssa_forward_lse", "mssa_backward_workspace_size",
            "mssa_backward", "mssa_tier_workspace_size", "mssa_patch_embed", "mssa_patch_unembed",
-           "mssa_qkv_project", "mssa_attention_noalloc", "mssa_pool_kv_head_ring", "mssa_forward_head_ring",
+           "mssa_qkv_project", "mssa_qkv_project_scaled", "mssa_attention_noalloc", "mssa_pool_kv_head_ring", "mssa_forward_head_ring",
            "mssa_head_ring_roll", "mssa_status_string", "mssa_last_error")
 
 MSSA_NOALLOC_SCRATCH_BYTES = 256 << 20
@@ -99,6 +99,7 @@ def _load():
     lib.mssa_patch_embed.argtypes = [P, TD, V, PP, PP, V, I64, V, V]
     lib.mssa_patch_unembed.argtypes = [P, TD, V, PP, PP, V, I64, V, V]
     lib.mssa_qkv_project.argtypes = [I64, ctypes.c_int32, V, V, V, V, V, V, V]
+    lib.mssa_qkv_project_scaled.argtypes = [I64, ctypes.c_int32, V, V, V, ctypes.c_float, V, V, V, V]
     lib.mssa_status_string.argtypes = [ctypes.c_int]
     lib.mssa_status_string.restype = ctypes.c_char_p
     lib.mssa_last_error.argtypes = []
@@ -332,6 +333,12 @@ def mssa_patch_unembed(plan, tier, tokens, w_out, b_out, workspace, latent, work
 def mssa_qkv_project(n_tokens, hidden, x, w_qkv, b_qkv, q, k, v, stream=None):
     _check(lib.mssa_qkv_project(int(n_tokens), int(hidden), _ptr(x), _ptr(w_qkv), _ptr(b_qkv), _ptr(q), _ptr(k),
                                 _ptr(v), _stream(stream)), "mssa_qkv_project")
+
+
+def mssa_qkv_project_scaled(n_tokens, hidden, x, w_qkv, b_qkv, q_scale, q, k, v, stream=None):
+    _check(lib.mssa_qkv_project_scaled(int(n_tokens), int(hidden), _ptr(x), _ptr(w_qkv), _ptr(b_qkv),
+                                       float(q_scale), _ptr(q), _ptr(k), _ptr(v), _stream(stream)),
+           "mssa_qkv_project_scaled")
 
 
 class HeadRing:

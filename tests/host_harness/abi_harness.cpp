@@ -18,6 +18,7 @@
 #include <hip/hip_runtime_api.h>
 
 #include <cinttypes>
+#include <cmath>
 #include <cstdio>
 #include <cstring>
 #include <string>
@@ -258,6 +259,8 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t) {
   check_range(a.bias, int64_t{a.N} * 2, "gemm bias");
   for (int j = 0; j * a.split < a.N; ++j)
     check_range(a.y[j], (int64_t{a.M} - 1) * a.ldy * 2 + int64_t{a.split} * 2, "gemm y");
+  // only the QKV projection (three outputs) may scale its first output
+  if (!std::isfinite(a.y0_scale) || (a.split == a.N && a.y0_scale != 1.f)) failure("gemm y0_scale");
   return hipSuccess;
 }
 
@@ -457,6 +460,8 @@ void exercise(const mssa_plan_desc& desc, int32_t attention_blocks) {
     void* o3[3] = {dev_alloc(info.n_q * tier.hidden * 2), dev_alloc(info.n_q * tier.hidden * 2),
                    dev_alloc(info.n_q * tier.hidden * 2)};
     expect(mssa_qkv_project(info.n_q, tier.hidden, tok, wq, bq, o3[0], o3[1], o3[2], nullptr), MSSA_OK, "qkv");
+    expect(mssa_qkv_project_scaled(info.n_q, tier.hidden, tok, wq, bq, 0.1275f, o3[0], o3[1], o3[2], nullptr), MSSA_OK,
+           "qkv scaled");
   }
   // rejected calls: nothing enqueued, the documented status
   expect(mssa_forward(plan, nullptr, ks, vs, kh, vh, kw, vw, ws, wsb, out, nullptr),

@@ -296,6 +296,10 @@ def test_tier_calls_checked():
     with pytest.raises(mssa.MssaError) as e:
         mssa.mssa_qkv_project(10, 12, fake, fake, fake, fake + 4096, fake + 8192, fake + 12288, stream=0)
     assert e.value.status == mssa.MSSA_ERR_INVALID_ARG
+    with pytest.raises(mssa.MssaError) as e:
+        mssa.mssa_qkv_project_scaled(10, 128, fake, fake, fake, float("nan"), fake + 4096, fake + 8192,
+                                     fake + 12288, stream=0)
+    assert e.value.status == mssa.MSSA_ERR_INVALID_ARG
 
 
 def test_backward_workspace_layout():

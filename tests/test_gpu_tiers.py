@@ -127,6 +127,74 @@ def test_qkv_projection_small(n, heads, d):
         _close(_f64(got), ref, f"qkv n={n} {nm}")
 
 
+LOG2E = 1.4426950408889634
+
+
+# (n, heads, d): the register-staged GEMM (K = 72, not a multiple of 64), the
+# 128 x 128 direct-transfer GEMM, and the 256 x 256 GEMM (1.3B window width)
+@pytest.mark.parametrize("n,heads,d", [(50, 1, 72), (300, 3, 128), (12870, 12, 128)])
+def test_qkv_projection_scaled(n, heads, d):
+    """mssa_qkv_project_scaled with q_scale = softmax_scale log2(e): q is the
+    oracle's projection times the factor (taken on the fp32 sum, rounded
+    once), k and v are bit for bit those of mssa_qkv_project."""
+    rng = np.random.default_rng(n + 1)
+    hidden = heads * d
+    c = LOG2E / np.sqrt(d)
+    x, x64 = _bf16(rng, (n, hidden))
+    w, w64 = _bf16(rng, (3 * hidden, hidden), 1.0 / np.sqrt(hidden))
+    b, b64 = _bf16(rng, (3 * hidden,), 0.1)
+    out = [torch.empty((n, heads, d), dtype=torch.bfloat16, device="cuda") for _ in range(6)]
+    mssa.mssa_qkv_project(n, hidden, x, w, b, *out[:3])
+    mssa.mssa_qkv_project_scaled(n, hidden, x, w, b, c, *out[3:])
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([np.arange(min(n, 64)), rng.integers(0, n, 64), [n - 1]]))
+    ref = oracle.qkv_project(x64[rows], w64, b64, heads)
+    _close(_f64(out[3])[rows], ref[0] * np.float32(c), f"scaled q n={n}")
+    for i in (1, 2):
+        assert torch.equal(out[3 + i].view(torch.int16), out[i].view(torch.int16)), "k / v changed"
+
+
+def test_qkv_scaled_feeds_prescaled_attention():
+    """The library's own pipeline for MSSA_PLAN_Q_PRESCALED: tokens -> scaled
+    QKV projection -> pool + attention with pre-scaled queries, against the
+    oracle on the projected (unscaled) queries and the same K / V, and close
+    to the plain pipeline's output."""
+    desc = dict(_desc([1, 1, 2, 2, 2], 10, 13, F=2, nh=2, d=128), sink_frames=1, hist_frames=2)
+    plain = mssa.mssa_plan_create(dict(desc, dtype="bf16"))
+    pre = mssa.mssa_plan_create(dict(desc, dtype="bf16", q_prescaled=True))
+    info = plain.info()
+    nq, hidden, d = info["n_q"], 256, 128
+    c = LOG2E / np.sqrt(d)
+    rng = np.random.default_rng(17)
+    x, _ = _bf16(rng, (nq, hidden))
+    w, _ = _bf16(rng, (3 * hidden, hidden), 1.0 / np.sqrt(hidden))
+    b, _ = _bf16(rng, (3 * hidden,), 0.1)
+    shapes = {k: (n, 2, d) for k, n in (("k_sink", info["n_sink_tok"]), ("v_sink", info["n_sink_tok"]),
+                                          ("k_hist", info["n_hist_tok"]), ("v_hist", info["n_hist_tok"]))}
+    ctx = {k: _bf16(rng, s)[0] if s[0] else None for k, s in shapes.items()}
+    outs = {}
+    for name, plan, scaled in (("plain", plain, False), ("pre", pre, True)):
+        q, k, v = (torch.empty((nq, 2, d), dtype=torch.bfloat16, device="cuda") for _ in range(3))
+        if scaled:
+            mssa.mssa_qkv_project_scaled(nq, hidden, x, w, b, c, q, k, v)
+        else:
+            mssa.mssa_qkv_project(nq, hidden, x, w, b, q, k, v)
+        ws = torch.empty(max(256, plan.info()["workspace_bytes"]), dtype=torch.uint8, device="cuda")
+        o = torch.empty_like(q)
+        mssa.mssa_pool_kv(plan, ctx["k_hist"], ctx["v_hist"], k, v, ws)
+        mssa.mssa_forward(plan, q, ctx["k_sink"], ctx["v_sink"], ctx["k_hist"], ctx["v_hist"], k, v, ws, o)
+        torch.cuda.synchronize()
+        f = {kk: (None if t is None else _f64(t)) for kk, t in ctx.items()}
+        qf = _f64(q) / (c if scaled else 1.0)
+        ref = oracle.mssa_attention(desc, qf, f["k_sink"], f["v_sink"], f["k_hist"], f["v_hist"], _f64(k), _f64(v))
+        got = _f64(o)
+        e = errors(got, ref)
+        assert np.isfinite(got).all() and e["max_abs"] <= 2e-2 and e["mean_abs"] <= 2e-3 and e["rel_rms"] <= 1e-2, (name, e)
+        print(f"[tiers] pipeline {name} {e}", flush=True)
+        outs[name] = got
+    assert np.abs(outs["pre"] - outs["plain"]).max() <= 2e-2
+
+
 def test_tiers_wan13b_layer_shapes():
     """The 1.3B-shaped window (30 x 52 tokens of 2 x 2 patches over 16 latent
     channels, schedule (p, p, 2p, 2p, 2p), width 1536 = 12 x 128): every
