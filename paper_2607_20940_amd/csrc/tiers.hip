@@ -356,6 +356,9 @@ __global__ __launch_bounds__(kTierThreads) void gemm_reduce_kernel(GemmArgs a) {
 constexpr int kBM = 256, kBN = 256, kBK = 64, kBStages = 2, kBThreads = 512, kBPanel = 4;
 constexpr int kBTile = kBM * kBK * 2;  // bytes of one operand tile of a stage
 
+// kScale: y[0]'s outputs multiplied by y0_scale (an instance of its own, so
+// that the unscaled product keeps its register allocation).
+template <bool kScale>
 __global__ __launch_bounds__(kBThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void gemm256_kernel(GemmArgs a) {
   __shared__ __attribute__((aligned(16))) char lds[kBStages][2][kBTile];  // [stage][X | W]
@@ -408,14 +411,12 @@ void gemm256_kernel(GemmArgs a) {
 
   // The bias of this lane's 32 output features, loaded before the loop.
   bf16x4 bias[2][4];
-  float osc[2][4];  // y0_scale for the features of y[0], else 1
 #pragma unroll
   for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
     for (int jj = 0; jj < 4; ++jj) {
       const int col = tn * kBN + wn * 64 + nb * 32 + 8 * jj + 4 * hh;
       bias[nb][jj] = col < a.N ? *reinterpret_cast<const bf16x4*>(static_cast<const __bf16*>(a.bias) + col) : bf16x4{};
-      osc[nb][jj] = col < a.split ? a.y0_scale : 1.f;
     }
 
   // Operand reads: row (block base + n32), columns 16 ks + 8 hh; the swizzle
@@ -481,9 +482,17 @@ void gemm256_kernel(GemmArgs a) {
 #pragma unroll
           for (int jj = 0; jj < 4; ++jj) {
             bf16x4 v;
+            if constexpr (kScale) {
+              // y0_scale for the features of y[0], else 1
+              const float sc = tn * kBN + wn * 64 + nb * 32 + 8 * jj + 4 * hh < a.split ? a.y0_scale : 1.f;
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-              v[i] = static_cast<__bf16>((acc[mb][nb][4 * jj + i] + static_cast<float>(bias[nb][jj][i])) * osc[nb][jj]);
+              for (int i = 0; i < 4; ++i)
+                v[i] = static_cast<__bf16>((acc[mb][nb][4 * jj + i] + static_cast<float>(bias[nb][jj][i])) * sc);
+            } else {
+#pragma unroll
+              for (int i = 0; i < 4; ++i)
+                v[i] = static_cast<__bf16>(acc[mb][nb][4 * jj + i] + static_cast<float>(bias[nb][jj][i]));
+            }
             *reinterpret_cast<bf16x4*>(E + (mb * 32 + n32) * kEStr + wn * 64 + nb * 32 + 8 * jj + 4 * hh) = v;
           }
     }
@@ -538,7 +547,10 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t stream) {
   const int64_t tiles = static_cast<int64_t>((a.M + kBM - 1) / kBM) * ((a.N + kBN - 1) / kBN);
   // enough tiles to fill the CUs; the bias read in 8-byte pieces
   if (a.K % kBK == 0 && a.N >= kBN && a.M >= kBM && tiles >= 256 && dma_epilogue_ok(a)) {
-    hipLaunchKernelGGL(gemm256_kernel, dim3(static_cast<uint32_t>(tiles)), dim3(kBThreads), 0, stream, a);
+    if (a.y0_scale != 1.f)
+      hipLaunchKernelGGL(gemm256_kernel<true>, dim3(static_cast<uint32_t>(tiles)), dim3(kBThreads), 0, stream, a);
+    else
+      hipLaunchKernelGGL(gemm256_kernel<false>, dim3(static_cast<uint32_t>(tiles)), dim3(kBThreads), 0, stream, a);
     return hipGetLastError();
   }
   const int64_t blocks = static_cast<int64_t>((a.M + kGM - 1) / kGM) * ((a.N + kGN - 1) / kGN);
