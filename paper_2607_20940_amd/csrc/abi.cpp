@@ -670,8 +670,13 @@ mssa_status mssa_backward(mssa_plan plan, const void* q_win, const void* k_sink,
       set_score_scales(p, sc, sc2);
       da.inv_scale = 1.0f / sc;
     }
-    mssa_status s = check_device(mssa::launch_bwd_dot(da, bf16, hs), "backward rowsum launch");
-    if (s != MSSA_OK) return s;
+    // bf16: the dQ kernel computes both row statistics itself (its B waves
+    // hold dO already); fp32 plans use the rowsum kernel.
+    mssa_status s = MSSA_OK;
+    if (!bf16) {
+      s = check_device(mssa::launch_bwd_dot(da, bf16, hs), "backward rowsum launch");
+      if (s != MSSA_OK) return s;
+    }
 
     mssa::BwdArgs a{};
     a.q = q_win;
@@ -686,6 +691,8 @@ mssa_status mssa_backward(mssa_plan plan, const void* q_win, const void* k_sink,
     a.n_groups = G;
     set_score_scales(p, a.scale, a.scale_log2e);
     a.q_prescaled = p.q_prescaled ? 1 : 0;
+    a.out = out;
+    a.inv_scale = da.inv_scale;
     const int qb = bf16 ? mssa::kBwdQ : mssa::kBwdF32, kb = bf16 ? mssa::kBwdK : mssa::kBwdF32;
     const KvSources src{k_sink, v_sink, k_hist, v_hist, nullptr, nullptr, k_win, v_win, ws};
     int64_t dq_blocks = 0, kv_blocks = 0;

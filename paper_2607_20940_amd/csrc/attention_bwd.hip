@@ -181,7 +181,33 @@ void dq_kernel(BwdArgs a) {
     for (int ks = 0; ks < KS; ++ks) xf[ks] = q_ok ? *reinterpret_cast<const bf16x8*>(xp + ks * 16) : bf16x8{};
   }
   const int64_t stat = static_cast<int64_t>(head) * a.n_q + (q_ok ? q_row : G.q_begin);
-  const float rstat = !q_ok ? 0.f : role == 0 ? a.lse[stat] * kLog2e : -a.dsum[stat];
+  // The row statistics, which the dK/dV kernel then reads (negated) from
+  // the workspace: A takes lse (log2 units here; -lse / scale stored), B
+  // rowsum(dO * O) over its lane's 64 channels of dO (already in xf) and
+  // the same channels of O, summed over the half-waves (-rowsum stored).
+  float rstat = 0.f;
+  if (role == 0) {
+    if (q_ok) {
+      const float lse = a.lse[stat];
+      rstat = lse * kLog2e;
+      if (hh == 0) a.lse2[stat] = -lse * a.inv_scale;
+    }
+  } else {
+    const int64_t off = static_cast<int64_t>(q_ok ? q_row : G.q_begin) * ld + hoff + hh * 8;
+    const __bf16* op = static_cast<const __bf16*>(a.out) + off;
+    float part = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const bf16x8 ov = *reinterpret_cast<const bf16x8*>(op + ks * 16);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) part = __builtin_fmaf(static_cast<float>(xf[ks][e]), static_cast<float>(ov[e]), part);
+    }
+    const float rs = part + other_half(part);
+    if (q_ok) {
+      rstat = rs;
+      if (hh == 0) a.dsum[stat] = -rs;
+    }
+  }
   // Accumulator input of the first product: -rowsum for B (dP arrives as
   // dP - rowsum), -lse for A with pre-scaled queries (S arrives as S - lse).
   f32x16 cinit;

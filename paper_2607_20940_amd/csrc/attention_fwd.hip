@@ -140,16 +140,6 @@ struct FwdTile {
   static_assert(NDMA == 4, "transfer addressing assumes 16 rows per wave");
 };
 
-// Value of lane l ^ 32.  v_permlane32_swap exchanges the upper half of its
-// first operand with the lower half of its second; whether the compiler gives
-// the two operands one register or two, lane l < 32 finds lane l + 32 in the
-// second result and lane l >= 32 finds lane l - 32 in the first.
-__device__ inline float other_half(float v) {
-  const int b = __builtin_bit_cast(int, v);
-  const auto sw = __builtin_amdgcn_permlane32_swap(b, b, false, false);
-  return __builtin_bit_cast(float, (threadIdx.x & 32) ? sw[0] : sw[1]);
-}
-
 __device__ inline float halfwave_max(float v) { return fmaxf(v, other_half(v)); }
 
 __device__ inline float halfwave_sum(float v) { return v + other_half(v); }

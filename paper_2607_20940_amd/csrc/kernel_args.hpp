@@ -97,8 +97,8 @@ struct BwdArgs {
   const void* q;
   const void* d_out;
   const float* lse;         // [heads, n_q] from the forward
-  const float* dsum;        // [heads, n_q]: -rowsum(d_out * out)
-  const float* lse2;        // [heads, n_q]: -lse / scale, the statistic in units of q k^T
+  float* dsum;              // [heads, n_q]: -rowsum(d_out * out) (bf16: written by the dQ kernel)
+  float* lse2;              // [heads, n_q]: -lse / scale, in units of q k^T (bf16: written by the dQ kernel)
   void* dq;
   int64_t ld;               // elements between tokens: heads * head_dim
   int32_t n_q;
@@ -107,6 +107,9 @@ struct BwdArgs {
   float scale;              // softmax scale
   float scale_log2e;
   int32_t q_prescaled;      // queries arrive multiplied by scale * log2(e)
+  const void* out;          // bf16: the forward's output, for rowsum(d_out * out) in the dQ kernel
+  float inv_scale;          // bf16: 1 / scale, for -lse / scale
+  int32_t pad;
   BwdGroupArgs groups[kMaxGroups];  // longest query range first
 };
 

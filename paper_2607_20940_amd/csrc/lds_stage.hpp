@@ -1,5 +1,6 @@
 // Device helpers for LDS stages filled by direct global -> LDS transfers and
-// read through XOR-swizzled rows (gfx950).  Included by the HIP kernels only.
+// read through XOR-swizzled rows (gfx950), and the half-wave exchange of the
+// attention kernels.  Included by the HIP kernels only.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -89,5 +90,15 @@ __device__ inline i32x4 rsrc_of(const void* base, uint32_t bytes) {
 // Byte offset past any buffer this library builds: a transfer lane pointed
 // here writes zeros (no 32-bit wrap of offset + 16).
 constexpr uint32_t kPastEnd = 0x7ffffff0u;
+
+// Value of lane l ^ 32.  v_permlane32_swap exchanges the upper half of its
+// first operand with the lower half of its second; whether the compiler gives
+// the two operands one register or two, lane l < 32 finds lane l + 32 in the
+// second result and lane l >= 32 finds lane l - 32 in the first.
+__device__ inline float other_half(float v) {
+  const int b = __builtin_bit_cast(int, v);
+  const auto sw = __builtin_amdgcn_permlane32_swap(b, b, false, false);
+  return __builtin_bit_cast(float, (threadIdx.x & 32) ? sw[0] : sw[1]);
+}
 
 }  // namespace mssa
