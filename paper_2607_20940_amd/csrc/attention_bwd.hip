@@ -6,7 +6,8 @@
 //   dV_s = P^T dO,  dS = P * (dO V_s^T - rowsum(dO * O)),
 //   dQ = scale dS K_s,  dK_s = scale dS^T Q.
 // The statistics come from the forward: the log of each row's softmax
-// denominator (lse) and rowsum(dO * O) (dot_kernel).  Context gradients are
+// denominator (lse) and rowsum(dO * O) (computed by the bf16 dQ kernel for
+// the rows it owns, by dot_kernel for fp32 plans).  Context gradients are
 // kept per query scale in fp32; scatter_kernel then sums, for every sink,
 // history and window token, the gradients of the context rows made from it
 // (the adjoint of the resampling: the block mean hands g / c to each of its c
