@@ -46,6 +46,21 @@ def test_noalloc_equals_workspace_path_twice():
     assert torch.equal(got.view(torch.int16), big.run().view(torch.int16))
 
 
+def test_noalloc_q_prescaled():
+    """A plan with pre-scaled queries (the layout bench.py times) through the
+    no-alloc entry point: bitwise the workspace path's output, which meets
+    the oracle on the unscaled queries."""
+    w = WORKLOADS["wan13b_layer"]
+    r = GpuRun(dict(w["desc"], q_prescaled=True), w["dtype"], w["seed"], w["amplitude"])
+    small = GpuRun(dict(SMALL, q_prescaled=True), "bf16", 8, 1.0)
+    for label, run in (("wan13b_layer", r), ("small", small)):
+        print(f"[noalloc] pre-scaled {label}", flush=True)
+        want = run.run().clone()
+        got = _noalloc(run)
+        assert torch.equal(got.view(torch.int16), want.view(torch.int16)), label
+    assert_close(small.output(), small.oracle(), "bf16", "small pre-scaled")
+
+
 def test_noalloc_rejects_plans_beyond_the_scratch():
     w = WORKLOADS["wan14b_720p"]
     plan = mssa.mssa_plan_create(dict(w["desc"], dtype=w["dtype"]))
