@@ -179,14 +179,19 @@ def test_streaming_head_in_ring_q_prescaled_every_output():
     assert n == 18
 
 
-def test_graph_pass_equals_eager_head_in_ring():
+@pytest.mark.parametrize("q_prescaled", [False, True])
+def test_graph_pass_equals_eager_head_in_ring(q_prescaled):
     """Whole passes of the copy-free cache roll replayed as HIP graphs (one
     per spare-slot position) equal the eager passes bit for bit: outputs and
-    every ring, over several cycles of positions."""
+    every ring, over several cycles of positions; with plain and with
+    pre-scaled queries (the streaming layout bench.py times)."""
     w = dict(SMALL, hist_cap_frames=6)
     layers = 2
-    eager = StreamingMSSA(w["layer"], layers, w["hist_cap_frames"], dtype="bf16", head_in_ring=True)
-    graph = StreamingMSSA(w["layer"], layers, w["hist_cap_frames"], dtype="bf16", head_in_ring=True)
+    qf = q_prescale(w["layer"]) if q_prescaled else 1.0
+    eager = StreamingMSSA(w["layer"], layers, w["hist_cap_frames"], dtype="bf16", head_in_ring=True,
+                          q_prescaled=q_prescaled)
+    graph = StreamingMSSA(w["layer"], layers, w["hist_cap_frames"], dtype="bf16", head_in_ring=True,
+                          q_prescaled=q_prescaled)
     shapes = eager.shapes(w["hist_start_frames"])
     for L in range(layers):
         x = init_inputs(w, L, shapes)
@@ -195,7 +200,7 @@ def test_graph_pass_equals_eager_head_in_ring():
     bufs = graph.window_buffers()
     replays = 0
     for p in range(14):
-        wins = window_inputs_head_ring(w, p, eager)
+        wins = window_inputs_head_ring(w, p, eager, q_scale=qf)
         outs = []
         for L in range(layers):
             for dst, src in zip(graph.head_slots(L), eager.head_slots(L)):
