@@ -260,7 +260,10 @@ mssa_status mssa_forward_lse(mssa_plan plan, const void* q_win, const void* k_si
 
 /* Bytes of device workspace mssa_backward needs (>= workspace_bytes: the
  * pooled K/V sit at the same offsets as for mssa_forward, followed by the
- * backward's own fp32 buffers). */
+ * backward's own buffers: fp32 row statistics and context gradients, and for
+ * bf16 plans the bf16 dS = P * (dP - rowsum) of as many whole heads as fit
+ * in 8 GiB (at least one; the backward runs the heads in such chunks), i.e.
+ * about 2 bytes per (query, context token) pair of each head of a chunk). */
 mssa_status mssa_backward_workspace_size(mssa_plan plan, int64_t* bytes);
 
 /* Gradients of MSSA with respect to all seven inputs.

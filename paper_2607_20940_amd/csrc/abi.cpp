@@ -670,13 +670,8 @@ mssa_status mssa_backward(mssa_plan plan, const void* q_win, const void* k_sink,
       set_score_scales(p, sc, sc2);
       da.inv_scale = 1.0f / sc;
     }
-    // bf16: the dQ kernel computes both row statistics itself (its B waves
-    // hold dO already); fp32 plans use the rowsum kernel.
-    mssa_status s = MSSA_OK;
-    if (!bf16) {
-      s = check_device(mssa::launch_bwd_dot(da, bf16, hs), "backward rowsum launch");
-      if (s != MSSA_OK) return s;
-    }
+    mssa_status s = check_device(mssa::launch_bwd_dot(da, bf16, hs), "backward rowsum launch");
+    if (s != MSSA_OK) return s;
 
     mssa::BwdArgs a{};
     a.q = q_win;
@@ -691,11 +686,8 @@ mssa_status mssa_backward(mssa_plan plan, const void* q_win, const void* k_sink,
     a.n_groups = G;
     set_score_scales(p, a.scale, a.scale_log2e);
     a.q_prescaled = p.q_prescaled ? 1 : 0;
-    a.out = out;
-    a.inv_scale = da.inv_scale;
     const int qb = bf16 ? mssa::kBwdQ : mssa::kBwdF32, kb = bf16 ? mssa::kBwdK : mssa::kBwdF32;
     const KvSources src{k_sink, v_sink, k_hist, v_hist, nullptr, nullptr, k_win, v_win, ws};
-    int64_t dq_blocks = 0, kv_blocks = 0;
     int gi = 0;
     for (int g : p.order) {
       mssa::BwdGroupArgs& A = a.groups[gi++];
@@ -712,17 +704,32 @@ mssa_status mssa_backward(mssa_plan plan, const void* q_win, const void* k_sink,
       }
       A.dk_ctx = reinterpret_cast<float*>(ws + p.bwd_dk_off[g]);
       A.dv_ctx = reinterpret_cast<float*>(ws + p.bwd_dv_off[g]);
+      A.ds = bf16 ? ws + p.bwd_ds_off[g] : nullptr;
+      A.ds_stages = p.bwd_ds_stages[g];
+      A.ds_qblocks = p.bwd_ds_qblocks[g];
       A.n_qblocks = (Q.q_end - Q.q_begin + qb - 1) / qb;
       A.n_kblocks = static_cast<int32_t>((Q.n_kv + kb - 1) / kb);
-      A.dq_block_begin = static_cast<int32_t>(dq_blocks);
-      A.kv_block_begin = static_cast<int32_t>(kv_blocks);
-      dq_blocks += static_cast<int64_t>(A.n_qblocks) * nh;
-      kv_blocks += static_cast<int64_t>(A.n_kblocks) * nh;
     }
-    if (dq_blocks > 0x7fffffff || kv_blocks > 0x7fffffff) return fail(MSSA_ERR_UNSUPPORTED, "backward grid too large");
-    s = check_device(mssa::launch_bwd(a, static_cast<int>(dq_blocks), static_cast<int>(kv_blocks), hd, bf16, hs),
-                     "backward attention launch");
-    if (s != MSSA_OK) return s;
+    // bf16: heads in chunks of bwd_ds_heads, each chunk's dK/dV kernel
+    // writing the dS tiles its dQ kernel reads; fp32: one launch of each.
+    const int chunk = bf16 ? p.bwd_ds_heads : nh;
+    for (int h0 = 0; h0 < nh; h0 += chunk) {
+      a.head0 = h0;
+      a.num_heads = std::min(chunk, nh - h0);
+      int64_t dq_blocks = 0, kv_blocks = 0;
+      for (int g = 0; g < G; ++g) {
+        mssa::BwdGroupArgs& A = a.groups[g];
+        A.dq_block_begin = static_cast<int32_t>(dq_blocks);
+        A.kv_block_begin = static_cast<int32_t>(kv_blocks);
+        dq_blocks += static_cast<int64_t>(A.n_qblocks) * a.num_heads;
+        kv_blocks += static_cast<int64_t>(A.n_kblocks) * a.num_heads;
+      }
+      if (dq_blocks > 0x7fffffff || kv_blocks > 0x7fffffff)
+        return fail(MSSA_ERR_UNSUPPORTED, "backward grid too large");
+      s = check_device(mssa::launch_bwd(a, static_cast<int>(dq_blocks), static_cast<int>(kv_blocks), hd, bf16, hs),
+                       "backward attention launch");
+      if (s != MSSA_OK) return s;
+    }
 
     mssa::ScatterArgs sa{};
     for (int g = 0; g < G; ++g) {

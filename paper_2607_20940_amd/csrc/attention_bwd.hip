@@ -6,42 +6,36 @@
 //   dV_s = P^T dO,  dS = P * (dO V_s^T - rowsum(dO * O)),
 //   dQ = scale dS K_s,  dK_s = scale dS^T Q.
 // The statistics come from the forward: the log of each row's softmax
-// denominator (lse) and rowsum(dO * O) (computed by the bf16 dQ kernel for
-// the rows it owns, by dot_kernel for fp32 plans).  Context gradients are
-// kept per query scale in fp32; scatter_kernel then sums, for every sink,
-// history and window token, the gradients of the context rows made from it
-// (the adjoint of the resampling: the block mean hands g / c to each of its c
-// cells, the strided pick g to the block's first cell).  Fixed summation
-// orders and no atomics: the result is the same bits on every run.
+// denominator (lse), and rowsum(dO * O) (dot_kernel, which stores both
+// negated in the units the kernels use).  Context gradients are kept per
+// query scale in fp32; scatter_kernel then sums, for every sink, history and
+// window token, the gradients of the context rows made from it (the adjoint
+// of the resampling: the block mean hands g / c to each of its c cells, the
+// strided pick g to the block's first cell).  Fixed summation orders and no
+// atomics: the result is the same bits on every run.
 //
 // bf16 path (gfx950 matrix cores, v_mfma_f32_32x32x16_bf16, fp32
-// accumulation), two kernels so that no gradient needs atomics, each run by
-// pairs of waves that share a SIMD (two waves per SIMD, 8 per block):
-//   dq_kernel    a pair owns 32 queries and walks the context in 64-key
-//                stages through LDS (one swizzled copy each of K and V,
-//                loaded by direct transfers).  Wave A: S^T = K Q^T (A = K
-//                rows from LDS, B = its Q fragment), so each lane holds 16
-//                keys of ONE query and its lse is a scalar; P = exp2(S c -
-//                lse) to LDS.  Wave B, one stage later: dP^T = V dO^T,
-//                dS^T = P (dP - rowsum), packed to bf16 the B operand of
-//                dQ^T += K^T dS^T, with K^T read by the transposing read
-//                ds_read_b64_tr_b16.
-//   dkdv_kernel  a pair owns 32 context keys and walks the scale's queries in
-//                64-query stages: wave A S = Q K^T, P (lane = key) and
-//                dV^T += dO^T P; wave B, one stage later, dP = dO V^T,
-//                dS = P (dP - rowsum) and dK^T += Q^T dS, with dO^T, Q^T
-//                from transposing reads.  Strict ping-pong: in each of a
-//                stage's two barrier-separated phases one wave of the pair
-//                issues only MFMAs and the other only VALU work.
-// Each wave holds one operand fragment and at most one accumulator, which is
-// what lets two waves share a SIMD: one wave's VALU work runs while the
-// other's MFMAs keep the matrix core busy.  One XOR-swizzled copy of each
-// staged tensor serves both read patterns without bank conflicts; stages
-// arrive by direct global -> LDS transfers (no staging registers) into three
-// buffers in dq_kernel (the stage the A waves read, the stage the B waves
-// read, the one arriving) and four in dkdv_kernel (two arriving).
-// Rows past the end of a context or query range are zero-filled; their
-// probabilities are forced to zero.
+// accumulation), five products in two kernels so that no gradient needs
+// atomics:
+//   dkdv_kernel  pairs of waves sharing a SIMD (two waves per SIMD, 8 per
+//                block); a pair owns 32 context keys and walks the scale's
+//                queries in 64-query stages: wave A S = Q K^T, P (lane =
+//                key) and dV^T += dO^T P; wave B, one stage later, dP = dO
+//                V^T, dS = P (dP - rowsum), dK^T += Q^T dS, with dO^T, Q^T
+//                from transposing reads, and dS (bf16, the value its own
+//                product uses) to a tile in HBM.  Strict ping-pong: in each
+//                of a stage's two barrier-separated phases one wave of the
+//                pair issues only MFMAs and the other only VALU work.  Each
+//                wave holds one operand fragment and one accumulator, which
+//                is what lets two waves share a SIMD.
+//   dq_kernel    dQ^T += K^T dS^T over the context, 32 queries per wave, K
+//                rows and the wave's dS tiles streamed through LDS and read
+//                transposed; it reads each dS element once from HBM instead
+//                of recomputing S and dP.
+// One XOR-swizzled copy of each staged K / Q / dO tile serves both read
+// patterns without bank conflicts; stages arrive by direct global -> LDS
+// transfers (no staging registers).  Rows past the end of a context or query
+// range are zero-filled and add nothing to any gradient.
 //
 // fp32 path (correctness path for fp32 plans): one lane per query (dQ) or
 // per context key (dK, dV), plain fp32 arithmetic with expf.
@@ -58,8 +52,6 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
-
-constexpr float kLog2e = 1.4426950408889634f;
 
 // Blocks are dispatched round-robin over the 8 XCDs; give each XCD a
 // contiguous eighth of the logical blocks so that its L2 serves few heads.
@@ -126,32 +118,32 @@ __device__ inline int swz(int row, int col) { return swz256(row, col); }
 
 // ------------------------------------------------------------------ bf16: dQ
 
-// dQ: a block owns 128 queries, four pairs of waves of 32 queries each.  In
-// a pair, wave A (waves 0-3) computes S^T = K Q^T and P = exp2(S c - lse)
-// (keys past a run's end masked to zero) and hands P (bf16) to its partner
-// through LDS; wave B (waves 4-7, on the same SIMD) computes dP^T = V dO^T,
-// dS^T = P (dP - rowsum) and dQ^T += K^T dS^T one key stage later.  The
-// context streams in 64-key stages inside one run at a time (K and V tiles
-// through three LDS buffers: in iteration i the A waves use stage i, the B
-// waves stage i - 1, and the transfers fill stage i + 1; P of stage i goes to
-// exchange buffer i & 1).  One barrier per iteration.  Both waves start their
-// first product from an accumulator holding the lane's row statistic
-// negated, so B's dP arrives as dP - rowsum and (kQS: queries pre-scaled by
-// scale * log2 e, c = 1) A's S as S - lse, leaving one VALU instruction less
-// per score.
-template <int D, bool kQS>
+// dQ = scale dS K, from the dS tiles the dK/dV kernel wrote.  A block owns
+// 256 queries, eight waves of 32 (two per SIMD).  The context streams through
+// LDS in 64-key stages inside one run at a time, cut as the tiles were: the
+// stage's K rows (one swizzled copy for the block) and each wave's own 4 KB
+// dS tile arrive by direct transfers into three stage buffers (the one read
+// and two in flight: the tiles come from HBM once, and HBM latency needs that
+// depth).  Rows past a run's end arrive as zeros in both, so they add
+// nothing.  Each wave accumulates dQ^T += K^T dS^T with both operands from
+// transposing reads: K^T from the K rows, dS^T from the tile's 64-byte rows
+// (keys) of 32 query positions, which become the accumulator's columns.
+// Position p of a tile row holds query 8 ((p % 16) / 4) + 4 (p / 16) + p % 4
+// of the 32-query block: the order in which the dK/dV kernel's lanes hold
+// them.
+template <int D>
 __global__ __launch_bounds__(kBwdQThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void dq_kernel(BwdArgs a) {
-  using L = Lay<D>;
-  constexpr int KS = L::KS, DB = L::DB;
-  constexpr int BN = kBwdKS, NKB = BN / 32;             // keys per stage, 32-key blocks
-  constexpr int KT = BN * 128 * 2;                      // bytes of one swizzled tile (256-byte rows)
-  constexpr int STB = 2 * KT;                           // K | V
-  constexpr int NW = kBwdQThreads / 64;
-  constexpr int NDMA = 2 * KT / 1024 / NW;              // 1 KB transfers per wave and stage (K and V)
-  constexpr int PXB = NKB * 2 * 64 * 16;                // bytes of one pair's P block per stage
-  static_assert(NDMA * 1024 * NW == 2 * KT && BN % 32 == 0, "stage shape");
-  __shared__ __attribute__((aligned(16))) char lds[3 * STB + 2 * 4 * PXB];
+  constexpr int DB = Lay<D>::DB;
+  constexpr int BN = kBwdKS;                       // keys per stage
+  constexpr int NW = kBwdQThreads / 64;            // waves of 32 queries
+  constexpr int KT = BN * 256;                     // bytes of the stage's K rows (256-byte swizzled rows)
+  constexpr int DT = BN * 64;                      // bytes of one wave's dS tile (64-byte rows)
+  constexpr int STB = KT + NW * DT;
+  constexpr int NK = KT / 1024 / NW;               // 1 KB K transfers per wave and stage
+  constexpr int NDS = DT / 1024;                   // 1 KB dS transfers per wave and stage
+  static_assert(NK * 1024 * NW == KT && NW * 32 == kBwdQ && BN % 32 == 0 && NDS % 2 == 0, "stage shape");
+  __shared__ __attribute__((aligned(16))) char lds[3 * STB];
 
   int n_blocks = 0;
   for (int g = 0; g < a.n_groups; ++g) n_blocks += a.groups[g].n_qblocks * a.num_heads;
@@ -160,73 +152,26 @@ void dq_kernel(BwdArgs a) {
   while (g + 1 < a.n_groups && b >= a.groups[g + 1].dq_block_begin) ++g;
   const BwdGroupArgs& G = a.groups[g];
   const int idx = b - G.dq_block_begin;
-  const int head = idx / G.n_qblocks, qt = idx % G.n_qblocks;
+  const int hl = idx / G.n_qblocks, qt = idx % G.n_qblocks;  // head of the launch
+  const int head = a.head0 + hl;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int pair = wave & 3, role = wave >> 2;  // role 0: S, P; role 1: dP, dS, dQ
   const int n = lane & 31, hh = lane >> 5;
-  const int q_row = G.q_begin + qt * kBwdQ + pair * 32 + n;
-  const bool q_ok = q_row < G.q_end;
+  const int qb = qt * NW + wave;                   // the wave's 32-query block of the group
+  const bool wave_ok = G.q_begin + qb * 32 < G.q_end;
+  const int q_row = G.q_begin + qb * 32 + 8 * ((n & 15) >> 2) + 4 * (n >> 4) + (n & 3);
   const int64_t ld = a.ld, hoff = static_cast<int64_t>(head) * D;
-  const float c = a.scale_log2e;
 
-  // B operand of the wave's first product: this lane's query (Q for role 0,
-  // dO for role 1), 8 channels of its half-wave per k step; and the lane's
-  // row statistic (lse in log2 units, or rowsum(dO * O)).
-  bf16x8 xf[KS];
-  {
-    const int64_t off = static_cast<int64_t>(q_ok ? q_row : G.q_begin) * ld + hoff + hh * 8;
-    const __bf16* xp = static_cast<const __bf16*>(role == 0 ? a.q : a.d_out) + off;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) xf[ks] = q_ok ? *reinterpret_cast<const bf16x8*>(xp + ks * 16) : bf16x8{};
-  }
-  const int64_t stat = static_cast<int64_t>(head) * a.n_q + (q_ok ? q_row : G.q_begin);
-  // The row statistics, which the dK/dV kernel then reads (negated) from
-  // the workspace: A takes lse (log2 units here; -lse / scale stored), B
-  // rowsum(dO * O) over its lane's 64 channels of dO (already in xf) and
-  // the same channels of O, summed over the half-waves (-rowsum stored).
-  float rstat = 0.f;
-  if (role == 0) {
-    if (q_ok) {
-      const float lse = a.lse[stat];
-      rstat = lse * kLog2e;
-      if (hh == 0) a.lse2[stat] = -lse * a.inv_scale;
-    }
-  } else {
-    const int64_t off = static_cast<int64_t>(q_ok ? q_row : G.q_begin) * ld + hoff + hh * 8;
-    const __bf16* op = static_cast<const __bf16*>(a.out) + off;
-    float part = 0.f;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      const bf16x8 ov = *reinterpret_cast<const bf16x8*>(op + ks * 16);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) part = __builtin_fmaf(static_cast<float>(xf[ks][e]), static_cast<float>(ov[e]), part);
-    }
-    const float rs = part + other_half(part);
-    if (q_ok) {
-      rstat = rs;
-      if (hh == 0) a.dsum[stat] = -rs;
-    }
-  }
-  // Accumulator input of the first product: -rowsum for B (dP arrives as
-  // dP - rowsum), -lse for A with pre-scaled queries (S arrives as S - lse).
-  f32x16 cinit;
-#pragma unroll
-  for (int e = 0; e < 16; ++e) cinit[e] = (role != 0 || kQS) ? -rstat : 0.f;
-
-  f32x16 acc[DB];  // dQ^T (role 1)
+  f32x16 acc[DB];  // dQ^T: lane n holds tile position n's query
 #pragma unroll
   for (int db = 0; db < DB; ++db) acc[db] = f32x16{};
 
-  // Stage tiles of BN keys inside one run at a time; rows past the run's end
-  // arrive as zeros and are masked.
   const int nr = G.n_runs;
   int nst = 0;
   for (int r = 0; r < nr; ++r) nst += (G.runs[r].n_tok + BN - 1) / BN;
   struct Stream {
     const __bf16* k;
-    const __bf16* v;
     int left;  // tokens of the current run from k on
     int r;
   };
@@ -236,146 +181,112 @@ void dq_kernel(BwdArgs a) {
     s.r = r;
     if (r < nr) {
       s.k = static_cast<const __bf16*>(G.runs[r].k) + hoff;
-      s.v = static_cast<const __bf16*>(G.runs[r].v) + hoff;
       s.left = G.runs[r].n_tok;
     }
   };
   auto step = [&](Stream& s) {
     s.left -= BN;
     s.k += tile_step;
-    s.v += tile_step;
     if (s.left <= 0) seek(s, s.r + 1);
   };
 
-  // Per-lane global offsets of this wave's transfers (the same every stage):
-  // transfer t = wave NDMA + i covers bytes 1024 (t % (KT / 1024)) of the K
-  // tile (t < KT / 1024) or of the V tile; logical chunk of the fixed LDS
-  // slot, zero past D.
+  // Per-lane global offsets of this wave's K transfers (the same every
+  // stage): transfer t = wave NK + i covers bytes 1024 t of the K rows,
+  // logical chunk of the fixed LDS slot, zero past D.  The dS tile is copied
+  // as it lies, 1 KB per transfer.
   const uint32_t row_bytes = static_cast<uint32_t>(ld) * 2;
-  uint32_t voff[NDMA];
+  uint32_t voff[NK];
 #pragma unroll
-  for (int i = 0; i < NDMA; ++i) {
-    const int t = wave * NDMA + i;
-    const int p = (t % (KT / 1024)) * 1024 + 16 * lane;
+  for (int i = 0; i < NK; ++i) {
+    const int p = (wave * NK + i) * 1024 + 16 * lane;
     const int row = p >> 8, phys = (p >> 4) & 15;
     const int lc = unswz256(row, phys);
     voff[i] = lc < D / 8 ? row * row_bytes + lc * 16 : kPastEnd;
   }
+  const __bf16* const ds_wave = static_cast<const __bf16*>(G.ds) +
+      (static_cast<int64_t>(hl) * G.ds_qblocks + (wave_ok ? qb : 0)) * G.ds_stages * (BN * 32);
   const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds));
-  auto issue = [&](const Stream& s, int buf) {
-    const uint32_t bytes = static_cast<uint32_t>(min(s.left, BN) - 1) * row_bytes + D * 2;
-    const i32x4 rk = rsrc_of(s.k, bytes), rv = rsrc_of(s.v, bytes);
+  auto issue = [&](const Stream& s, int st, int buf) {
+    const int nv = min(s.left, BN);
+    const i32x4 rk = rsrc_of(s.k, static_cast<uint32_t>(nv - 1) * row_bytes + D * 2);
     const uint32_t base = lds0 + buf * STB;
 #pragma unroll
-    for (int i = 0; i < NDMA; ++i) {
-      const int t = wave * NDMA + i;
-      dma16(t < KT / 1024 ? rk : rv, voff[i], __builtin_amdgcn_readfirstlane(base + t * 1024));
+    for (int i = 0; i < NK; ++i) dma16(rk, voff[i], __builtin_amdgcn_readfirstlane(base + (wave * NK + i) * 1024));
+    if (wave_ok) {
+      // the tile's two halves (positions 16 hh + 8 j + e of every slot, j = 0, 1)
+      // each hold 32 bytes per slot; slots past the run's end read as zeros
+      const __bf16* tile = ds_wave + static_cast<int64_t>(st) * (BN * 32);
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const i32x4 rd = rsrc_of(tile + j * (BN * 16), static_cast<uint32_t>(nv) * 32);
+#pragma unroll
+        for (int i = 0; i < NDS / 2; ++i)
+          dma16(rd, i * 1024 + 16 * lane,
+                __builtin_amdgcn_readfirstlane(base + KT + wave * DT + j * (DT / 2) + i * 1024));
+      }
     }
   };
-  // Operand offsets in the swizzled tiles (elements).  Row reads: row
-  // 32 kb + n, columns 16 ks + 8 hh at 32 kb * 128 + (r_rd ^ 16 ks).
-  // Transposing reads: rows R + t_lane (+ 8 for the upper half), columns
-  // 32 db + t_col, R a multiple of 16, at R * 128 + t_rd[db][half]: the
-  // swizzle of a row depends only on its index mod 16.
-  const int r_rd = swz(n, hh * 8);
+  // all of this wave's transfers but the last stage's
+  auto wait_but_one = [&]() {
+    if (wave_ok)
+      wait_vmcnt<NK + NDS>();
+    else
+      wait_vmcnt<NK>();
+  };
+  // Transposing reads: rows R + t_lane (+ 8 for the upper half), R a
+  // multiple of 16; K at columns 32 db + t_col (swizzled rows), dS at t_col.
   const int t_lane = 4 * (lane >> 5) + ((lane & 15) >> 2);
   const int t_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-  int t_rd[DB][2];
+  int k_rd[DB][2], d_rd[2];
 #pragma unroll
-  for (int db = 0; db < DB; ++db)
+  for (int h = 0; h < 2; ++h) {
+    d_rd[h] = ((t_col >> 3) & 1) * (BN * 16) + (t_lane + 8 * h) * 16 + (t_col >> 4) * 8 + (t_col & 7);
 #pragma unroll
-    for (int h = 0; h < 2; ++h) t_rd[db][h] = swz(t_lane + 8 * h, db * 32 + t_col);
-  // P exchange block of this pair, buffer pbuf: [32-key block][16-key half][lane] x 16 bytes
-  auto px = [&](int pbuf) { return reinterpret_cast<bf16x8*>(lds + 3 * STB + (pbuf * 4 + pair) * PXB) + lane; };
-
-  // One stage of the wave's role on stage buffer buf: the row products of
-  // both 32-key blocks first, then the VALU work on both, then (B) the dQ
-  // products, so that one block's VALU work can run under the other's MFMAs.
-  // Element e of a 32x32 accumulator in this layout holds key
-  // kb*32 + 8(e/4) + 4hh + e%4 of the lane's query; packed to bf16 in pairs
-  // of 8 it is the B operand (16 keys each) of dQ^T += K^T dS^T.
-  auto stage = [&](int buf, int pbuf, int nvalid) {
+    for (int db = 0; db < DB; ++db) k_rd[db][h] = swz(t_lane + 8 * h, db * 32 + t_col);
+  }
+  auto tr = [](const __bf16* p0, int o0, int o1) {
+    const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p0 + o0));
+    const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p0 + o1));
+    return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  };
+  auto stage = [&](int buf) {
     const __bf16* Ks = reinterpret_cast<const __bf16*>(lds + buf * STB);
-    const __bf16* Vs = reinterpret_cast<const __bf16*>(lds + buf * STB + KT);
-    const __bf16* Xs = role == 0 ? Ks : Vs;
-    bf16x8* pex = px(pbuf);
-    f32x16 s[NKB];
+    const __bf16* Ds = reinterpret_cast<const __bf16*>(lds + buf * STB + KT + wave * DT);
 #pragma unroll
-    for (int kb = 0; kb < NKB; ++kb)
+    for (int rb = 0; rb < BN / 16; ++rb) {
+      const bf16x8 dst = tr(Ds + rb * 16 * 16, d_rd[0], d_rd[1]);
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const bf16x8 ax = *reinterpret_cast<const bf16x8*>(Xs + kb * 32 * 128 + (r_rd ^ (ks * 16)));
-        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ax, xf[ks], ks == 0 ? cinit : s[kb], 0, 0, 0);
-      }
-    if (role == 0) {
-#pragma unroll
-      for (int kb = 0; kb < NKB; ++kb) {
-        if (nvalid < BN) {  // the last stage of a run: keys past its end get P = 0
-#pragma unroll
-          for (int e = 0; e < 16; ++e)
-            if (kb * 32 + 8 * (e >> 2) + 4 * hh + (e & 3) >= nvalid) s[kb][e] = -INFINITY;
-        }
-        bf16x8 pb[2];
-#pragma unroll
-        for (int e = 0; e < 16; ++e)
-          pb[e >> 3][e & 7] =
-              static_cast<__bf16>(__builtin_amdgcn_exp2f(kQS ? s[kb][e] : __builtin_fmaf(s[kb][e], c, -rstat)));
-        pex[(kb * 2) * 64] = pb[0];
-        pex[(kb * 2 + 1) * 64] = pb[1];
-      }
-    } else {
-      bf16x8 dsb[NKB][2];
-#pragma unroll
-      for (int kb = 0; kb < NKB; ++kb) {
-        const bf16x8 p0 = pex[(kb * 2) * 64], p1 = pex[(kb * 2 + 1) * 64];
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const float p = static_cast<float>((e < 8 ? p0 : p1)[e & 7]);
-          dsb[kb][e >> 3][e & 7] = static_cast<__bf16>(p * s[kb][e]);
-        }
-      }
-#pragma unroll
-      for (int kb = 0; kb < NKB; ++kb)
-#pragma unroll
-        for (int cc = 0; cc < 2; ++cc)
-#pragma unroll
-          for (int db = 0; db < DB; ++db) {
-            const __bf16* r0 = Ks + (kb * 32 + cc * 16) * 128;
-            const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(r0 + t_rd[db][0]));
-            const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(r0 + t_rd[db][1]));
-            acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7),
-                                                              dsb[kb][cc], acc[db], 0, 0, 0);
-          }
+      for (int db = 0; db < DB; ++db)
+        acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr(Ks + rb * 16 * 128, k_rd[db][0], k_rd[db][1]), dst,
+                                                          acc[db], 0, 0, 0);
     }
   };
 
-  Stream ls, cs;
+  Stream ls;
   seek(ls, 0);
-  cs = ls;
-  issue(ls, 0);
-  wait_vmcnt<0>();
-  __syncthreads();
-  for (int it = 0; it <= nst; ++it) {
-    if (it + 1 < nst) {
-      step(ls);
-      issue(ls, (it + 1) % 3);
-    }
-    if (role == 0 && it < nst) {
-      stage(it % 3, it & 1, min(cs.left, BN));
-      step(cs);
-    }
-    if (role != 0 && it >= 1) {
-      // B carries two thirds of the MFMAs and the dependent chain
-      // dP -> dS -> dQ: its instructions go first when both waves are ready.
-      __builtin_amdgcn_s_setprio(2);
-      stage((it - 1) % 3, (it - 1) & 1, BN);
-      __builtin_amdgcn_s_setprio(0);
-    }
+  if (nst > 0) issue(ls, 0, 0);
+  if (nst > 1) {
+    step(ls);
+    issue(ls, 1, 1);
+    wait_but_one();
+  } else {
     wait_vmcnt<0>();
+  }
+  __syncthreads();
+  for (int it = 0; it < nst; ++it) {
+    if (it + 2 < nst) {
+      step(ls);
+      issue(ls, it + 2, (it + 2) % 3);
+    }
+    if (wave_ok) stage(it % 3);
+    if (it + 2 < nst)
+      wait_but_one();
+    else
+      wait_vmcnt<0>();
     __syncthreads();
   }
 
-  if (role != 0 && q_ok) {
+  if (wave_ok && q_row < G.q_end) {
     __bf16* op = static_cast<__bf16*>(a.dq) + static_cast<int64_t>(q_row) * ld + hoff + 4 * hh;
 #pragma unroll
     for (int db = 0; db < DB; ++db)
@@ -402,11 +313,13 @@ void dq_kernel(BwdArgs a) {
 //   phase 2t + 1: A  P_t = exp2(S_t c - lse_t), to registers and to LDS for B
 //                 B  dK^T += Q_{t-1}^T dS_{t-1}, then dP_t = dO_t V^T
 // Stage t's Q, dO and row statistics live in LDS buffer t % 4 and are read
-// in phases 2t .. 2t + 3.  B issues stage t + 2 (direct transfers, the
-// statistics included) at the end of its matrix-core phase 2t + 1 into
-// buffer (t + 2) % 4, whose stage t - 2 was last read in phase 2t - 1, so
-// B's VALU phases hold no transfer work.  P_t is written in phase 2t + 1 and
-// read in 2t + 2; one block per pair suffices.
+// in phases 2t .. 2t + 3.  A issues stage t + 2 (direct transfers, the
+// statistics included) at the end of its matrix-core phase 2t into buffer
+// (t + 2) % 4, whose stage t - 2 was last read in phase 2t - 1, and waits
+// for stage t + 1 at the end of its VALU phase 2t + 1.  B also stores dS_{t-1}
+// to HBM in phase 2t and never waits for memory: a wave's wait for its
+// transfers would also wait for its earlier stores to complete.  P_t is
+// written in phase 2t + 1 and read in 2t + 2; one block per pair suffices.
 // The matrix-core step is one code site for both roles, so that the register
 // allocation holds one set of accumulators, S/dP and P/dS registers.  Its row
 // product starts from an accumulator loaded with the stage's negated row
@@ -435,7 +348,8 @@ void dkdv_kernel(BwdArgs a) {
   while (g + 1 < a.n_groups && b >= a.groups[g + 1].kv_block_begin) ++g;
   const BwdGroupArgs& G = a.groups[g];
   const int idx = b - G.kv_block_begin;
-  const int head = idx / G.n_kblocks, kt = idx % G.n_kblocks;
+  const int hl = idx / G.n_kblocks, kt = idx % G.n_kblocks;  // head of the launch
+  const int head = a.head0 + hl;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -445,6 +359,23 @@ void dkdv_kernel(BwdArgs a) {
   const bool k_ok = key < G.n_kv;
   const int64_t ld = a.ld, hoff = static_cast<int64_t>(head) * D;
   const float c = a.scale_log2e;
+
+  // Where B stores its key's dS: the key's run, 64-key stage of the run
+  // (the stages the dQ kernel walks) and slot in the stage; the lane's 16
+  // queries of a 32-query block at positions 16 hh .. 16 hh + 15 of the row.
+  __bf16* ds_lane = nullptr;
+  if (role != 0 && k_ok) {
+    int j = key, st = 0, r = 0;
+    while (r + 1 < G.n_runs && j >= G.runs[r].n_tok) {
+      st += (G.runs[r].n_tok + kBwdKS - 1) / kBwdKS;
+      j -= G.runs[r].n_tok;
+      ++r;
+    }
+    ds_lane = static_cast<__bf16*>(G.ds) +
+              (static_cast<int64_t>(hl) * G.ds_qblocks * G.ds_stages + st + j / kBwdKS) * (kBwdKS * 32) +
+              (j % kBwdKS) * 16 + 8 * hh;
+  }
+  const int64_t ds_qstride = static_cast<int64_t>(G.ds_stages) * (kBwdKS * 32);
 
   // B operand of the wave's row product: this lane's key (K for A, V for B),
   // 8 channels of its half-wave per k step.
@@ -467,8 +398,8 @@ void dkdv_kernel(BwdArgs a) {
 #pragma unroll
   for (int qb = 0; qb < NQB; ++qb) w[qb][0] = w[qb][1] = bf16x8{};
 
-  // Per-lane global offsets of the B waves' transfers (the same every
-  // stage): transfer t = (wave - 4) NDMA + i covers bytes 1024 (t % (QT / 1024))
+  // Per-lane global offsets of the A waves' transfers (the same every
+  // stage): transfer t = wave NDMA + i covers bytes 1024 (t % (QT / 1024))
   // of the Q tile (t < QT / 1024) or of the dO tile; logical chunk of the
   // fixed LDS slot, zero past D.
   const uint32_t row_bytes = static_cast<uint32_t>(ld) * 2;
@@ -482,17 +413,17 @@ void dkdv_kernel(BwdArgs a) {
     voff[i] = lc < D / 8 ? row * row_bytes + lc * 16 : kPastEnd;
   }
   const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds));
-  // Stage queries [q0, q0 + BQ) into LDS buffer buf (B waves), all by
-  // direct transfers: the Q (waves 4, 5) or dO (waves 6, 7) tile rows, and
-  // the stage's negated statistics -lse / scale (wave 4) and -rowsum (wave
-  // 5), one dword per lane.  Queries past the end arrive as zero rows with
+  // Stage queries [q0, q0 + BQ) into LDS buffer buf (A waves), all by
+  // direct transfers: the Q (waves 0, 1) or dO (waves 2, 3) tile rows, and
+  // the stage's negated statistics -lse / scale (wave 0) and -rowsum (wave
+  // 1), one dword per lane.  Queries past the end arrive as zero rows with
   // zero statistics: their P = exp2(0) = 1 meets zero dO rows (no dV
   // contribution) and dS = 1 (0 - 0) = 0.  Loop-invariant values are kept in registers.
-  static_assert(2 * NDMA * 1024 == QT && BQ == 64, "two B waves per tile, one statistic per lane");
+  static_assert(2 * NDMA * 1024 == QT && BQ == 64, "two A waves per tile, one statistic per lane");
   const int q_begin = G.q_begin, q_end = G.q_end;
   const __bf16* const x_head = static_cast<const __bf16*>((wave & 3) < 2 ? a.q : a.d_out) + hoff;
-  const bool stat_wave = wave == 4 || wave == 5;
-  const float* const s_head = (wave == 4 ? a.lse2 : a.dsum) + static_cast<int64_t>(head) * a.n_q;
+  const bool stat_wave = wave == 0 || wave == 1;
+  const float* const s_head = (wave == 0 ? a.lse2 : a.dsum) + static_cast<int64_t>(head) * a.n_q;
   auto issue = [&](int q0, int buf) {
     const int nv = min(BQ, q_end - q0);
     const uint32_t bytes = static_cast<uint32_t>(nv - 1) * row_bytes + D * 2;
@@ -503,7 +434,7 @@ void dkdv_kernel(BwdArgs a) {
       dma16(rs, voff[i], __builtin_amdgcn_readfirstlane(base + ((wave & 3) * NDMA + i) * 1024));
     if (stat_wave)
       dma4(rsrc_of(s_head + q0, static_cast<uint32_t>(nv) * 4), 4 * lane,
-           __builtin_amdgcn_readfirstlane(base + 2 * QT + (wave - 4) * BQ * 4));
+           __builtin_amdgcn_readfirstlane(base + 2 * QT + wave * BQ * 4));
   };
   // Operand offsets in the swizzled tiles (elements), as in the dQ kernel.
   const int r_rd = swz(n, hh * 8);
@@ -598,8 +529,9 @@ void dkdv_kernel(BwdArgs a) {
 #pragma unroll
       for (int h = 0; h < 2; ++h) asm volatile("" : "+v"(w[qb][h]));
   };
-  // B: dS = P dP' (dP' = dP - rowsum) into w.
-  auto softmax_b = [&]() {
+  // B: dS = P dP' (dP' = dP - rowsum) of stage ts into w, and to the dS
+  // tiles of the stage's 32-query blocks 2 ts + qb for the dQ kernel.
+  auto softmax_b = [&](int ts) {
 #pragma unroll
     for (int qb = 0; qb < NQB; ++qb) {
       const bf16x8 p0 = pex[(qb * 2) * 64], p1 = pex[(qb * 2 + 1) * 64];
@@ -607,6 +539,11 @@ void dkdv_kernel(BwdArgs a) {
       for (int e = 0; e < 16; ++e) {
         const float p = static_cast<float>((e < 8 ? p0 : p1)[e & 7]);
         w[qb][e >> 3][e & 7] = static_cast<__bf16>(p * s[qb][e]);
+      }
+      if (ds_lane) {
+        __bf16* dp = ds_lane + (NQB * ts + qb) * ds_qstride;
+        __builtin_nontemporal_store(w[qb][0], reinterpret_cast<bf16x8*>(dp));
+        __builtin_nontemporal_store(w[qb][1], reinterpret_cast<bf16x8*>(dp + kBwdKS * 16));
       }
     }
 #pragma unroll
@@ -619,9 +556,9 @@ void dkdv_kernel(BwdArgs a) {
   // keeps the register allocation tight): in the first stage the
   // accumulating product multiplies the zeroed buffer of stage -1 by w = 0,
   // adding exact zeros; in the stage after the last, the row product's
-  // result is never used.  B issues stage t + 2 at the end of its
-  // matrix-core phase 2t + 1, into the buffer of stage t - 2 (last read in
-  // phase 2t - 1), and ends the phase once stage t + 1 has arrived.
+  // result is never used.  A issues stage t + 2 at the end of its
+  // matrix-core phase 2t, into the buffer of stage t - 2 (last read in phase
+  // 2t - 1), and ends its VALU phase 2t + 1 once stage t + 1 has arrived.
   using T_ = std::true_type;
   const int nst = (q_end - q_begin + BQ - 1) / BQ;
   {
@@ -636,7 +573,7 @@ void dkdv_kernel(BwdArgs a) {
     else
       wait_vmcnt<NDMA>();
   };
-  if (role != 0) {
+  if (role == 0) {
     issue(q_begin, 0);
     if (nst > 1) {
       issue(q_begin + BQ, 1);
@@ -655,18 +592,15 @@ void dkdv_kernel(BwdArgs a) {
       mstep(T_{}, T_{}, tile(prev, 1 - role), tile(cur, role),
             reinterpret_cast<const float*>(lds + cur * STB + 2 * QT) + role * BQ);
       __builtin_amdgcn_s_setprio(0);
-      if (role != 0) {
-        if (t + 2 < nst) {
-          issue(q_begin + (t + 2) * BQ, (t + 2) % NBUF);
-          wait_all_but_last();
-        } else {
-          wait_vmcnt<0>();
-        }
-      }
+      if (role == 0 && t + 2 < nst) issue(q_begin + (t + 2) * BQ, (t + 2) % NBUF);
     } else if (role == 0) {
       if (t < nst) softmax_a();
+      if (t + 2 < nst)
+        wait_all_but_last();
+      else
+        wait_vmcnt<0>();
     } else {
-      if (t >= 1) softmax_b();
+      if (t >= 1) softmax_b(t - 1);
     }
     __syncthreads();
   }
@@ -832,25 +766,7 @@ hipError_t launch_bwd_dot(const DotArgs& a, bool bf16, hipStream_t stream) {
 
 hipError_t launch_bwd(const BwdArgs& a, int dq_blocks, int kv_blocks, int head_dim, bool bf16,
                       hipStream_t stream) {
-  if (dq_blocks > 0) {
-    if (bf16) {
-      if (head_dim == 128 && a.q_prescaled)
-        hipLaunchKernelGGL((dq_kernel<128, true>), dim3(dq_blocks), dim3(kBwdQThreads), 0, stream, a);
-      else if (head_dim == 128)
-        hipLaunchKernelGGL((dq_kernel<128, false>), dim3(dq_blocks), dim3(kBwdQThreads), 0, stream, a);
-      else if (a.q_prescaled)
-        hipLaunchKernelGGL((dq_kernel<64, true>), dim3(dq_blocks), dim3(kBwdQThreads), 0, stream, a);
-      else
-        hipLaunchKernelGGL((dq_kernel<64, false>), dim3(dq_blocks), dim3(kBwdQThreads), 0, stream, a);
-    } else {
-      if (head_dim == 128)
-        hipLaunchKernelGGL(dq_f32_kernel<128>, dim3(dq_blocks), dim3(kBwdF32), 0, stream, a);
-      else
-        hipLaunchKernelGGL(dq_f32_kernel<64>, dim3(dq_blocks), dim3(kBwdF32), 0, stream, a);
-    }
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
+  // dK/dV first: for bf16 plans it writes the dS tiles the dQ kernel reads.
   if (kv_blocks > 0) {
     if (bf16) {
       if (head_dim == 128 && a.q_prescaled)
@@ -866,6 +782,21 @@ hipError_t launch_bwd(const BwdArgs& a, int dq_blocks, int kv_blocks, int head_d
         hipLaunchKernelGGL(dkdv_f32_kernel<128>, dim3(kv_blocks), dim3(kBwdF32), 0, stream, a);
       else
         hipLaunchKernelGGL(dkdv_f32_kernel<64>, dim3(kv_blocks), dim3(kBwdF32), 0, stream, a);
+    }
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (dq_blocks > 0) {
+    if (bf16) {
+      if (head_dim == 128)
+        hipLaunchKernelGGL(dq_kernel<128>, dim3(dq_blocks), dim3(kBwdQThreads), 0, stream, a);
+      else
+        hipLaunchKernelGGL(dq_kernel<64>, dim3(dq_blocks), dim3(kBwdQThreads), 0, stream, a);
+    } else {
+      if (head_dim == 128)
+        hipLaunchKernelGGL(dq_f32_kernel<128>, dim3(dq_blocks), dim3(kBwdF32), 0, stream, a);
+      else
+        hipLaunchKernelGGL(dq_f32_kernel<64>, dim3(dq_blocks), dim3(kBwdF32), 0, stream, a);
     }
     return hipGetLastError();
   }

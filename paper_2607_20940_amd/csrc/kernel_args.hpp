@@ -67,15 +67,16 @@ constexpr int64_t partial_record_floats(int head_dim) { return static_cast<int64
 
 // ---------------------------------------------------------------- backward
 
-// bf16 backward kernels: 4 waves, 32 queries (dQ kernel) or 32 keys (dK/dV
-// kernel) per wave; the other operand streams through LDS in stages.
-constexpr int kBwdThreads = 256;
-constexpr int kBwdQ = 128;     // dQ kernel: queries per block (4 wave pairs x 32)
+// bf16 backward kernels: 8 waves, 32 queries (dQ kernel) or 32 keys (dK/dV
+// kernel) per wave or wave pair; the other operands stream through LDS in
+// stages.
+constexpr int kBwdQ = 256;     // dQ kernel: queries per block (8 waves x 32)
 constexpr int kBwdQThreads = 512;   // dQ kernel: 8 waves, two per SIMD
-constexpr int kBwdKS = 64;     // dQ kernel: keys per LDS stage
+constexpr int kBwdKS = 64;     // dQ kernel: keys per LDS stage (and per dS tile)
 constexpr int kBwdK = 128;     // dK/dV kernel: keys per block (4 wave pairs x 32)
 constexpr int kBwdKVThreads = 512;  // dK/dV kernel: 8 waves, two per SIMD
 constexpr int kBwdQS = 64;     // dK/dV kernel: queries per LDS stage
+constexpr int64_t kBwdDsBudget = int64_t(8) << 30;  // bytes of dS tiles held at once (whole heads, at least one)
 constexpr int kBwdF32 = 64;    // fp32 kernels: one query or key per lane
 constexpr int kDotThreads = 256;
 constexpr int kMaxScatterJobs = 10;
@@ -91,27 +92,29 @@ struct BwdGroupArgs {
   FwdRunArgs runs[kMaxRuns];  // context runs (K, V source tokens), context order
   float* dk_ctx;              // [n_kv, heads * head_dim] fp32 context gradients
   float* dv_ctx;
+  void* ds;                   // bf16: dS tiles [launch heads][ds_qblocks][ds_stages][64 keys][32 queries]
+  int32_t ds_stages;          // 64-key stages of the runs (each run starts a stage)
+  int32_t ds_qblocks;         // 32-query blocks (even)
 };
 
 struct BwdArgs {
   const void* q;
   const void* d_out;
   const float* lse;         // [heads, n_q] from the forward
-  float* dsum;              // [heads, n_q]: -rowsum(d_out * out) (bf16: written by the dQ kernel)
-  float* lse2;              // [heads, n_q]: -lse / scale, in units of q k^T (bf16: written by the dQ kernel)
+  float* dsum;              // [heads, n_q]: -rowsum(d_out * out), written by dot_kernel
+  float* lse2;              // [heads, n_q]: -lse / scale, in units of q k^T (bf16), written by dot_kernel
   void* dq;
   int64_t ld;               // elements between tokens: heads * head_dim
   int32_t n_q;
-  int32_t num_heads;
+  int32_t num_heads;        // heads of this launch: head0 .. head0 + num_heads - 1
+  int32_t head0;            // first head of this launch (the dS tiles hold these heads)
   int32_t n_groups;
   float scale;              // softmax scale
   float scale_log2e;
   int32_t q_prescaled;      // queries arrive multiplied by scale * log2(e)
-  const void* out;          // bf16: the forward's output, for rowsum(d_out * out) in the dQ kernel
-  float inv_scale;          // bf16: 1 / scale, for -lse / scale
-  int32_t pad;
   BwdGroupArgs groups[kMaxGroups];  // longest query range first
 };
+static_assert(sizeof(BwdArgs) <= 4096, "kernel argument block");
 
 struct DotArgs {
   const void* out;

@@ -279,6 +279,33 @@ mssa_status build_plan(const mssa_plan_desc& d, int slots, int attention_blocks,
     p.bwd_dv_off[g] = ws;
     ws += bytes;
   }
+  p.bwd_ds_off.assign(G, 0);
+  p.bwd_ds_stages.assign(G, 0);
+  p.bwd_ds_qblocks.assign(G, 0);
+  p.bwd_ds_heads = d.num_heads;
+  if (d.dtype == MSSA_BF16) {
+    int64_t per_head = 0;
+    for (int g = 0; g < G; ++g) {
+      int64_t stages = 0;
+      for (const Run& r : p.runs[g]) stages += (r.n_tok + kBwdKS - 1) / kBwdKS;
+      const int64_t nq = p.groups[g].q_end - p.groups[g].q_begin;
+      const int64_t qblocks = 2 * ((nq + kBwdQS - 1) / kBwdQS);
+      if (stages > 0x7fffffff || qblocks > 0x7fffffff) {
+        err = "backward dS buffer too large";
+        return MSSA_ERR_UNSUPPORTED;
+      }
+      p.bwd_ds_stages[g] = static_cast<int32_t>(stages);
+      p.bwd_ds_qblocks[g] = static_cast<int32_t>(qblocks);
+      per_head += qblocks * stages * kBwdKS * 32 * 2;
+    }
+    // whole heads per chunk within the budget, at least one
+    p.bwd_ds_heads = static_cast<int32_t>(
+        std::max<int64_t>(1, std::min<int64_t>(d.num_heads, kBwdDsBudget / std::max<int64_t>(1, per_head))));
+    for (int g = 0; g < G; ++g) {
+      p.bwd_ds_off[g] = ws;
+      ws += align256(static_cast<int64_t>(p.bwd_ds_heads) * p.bwd_ds_qblocks[g] * p.bwd_ds_stages[g] * kBwdKS * 32 * 2);
+    }
+  }
   p.bwd_workspace_bytes = ws;
   auto seg_of = [&](int g, int32_t kind, int32_t frame) -> const SegRow& {
     for (const SegRow& r : p.segs)

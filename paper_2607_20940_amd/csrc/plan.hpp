@@ -115,11 +115,19 @@ struct Plan {
   Schedule sched;
   int64_t partial_off, partial_bytes;    // partial records and the range table in the workspace
   int64_t range_table_off;               // n_ranges + 1 int64 first tiles of the tail ranges
-  // Backward workspace: the forward's, then rowsum(dO * O) [heads, n_q]
-  // fp32, lse in log2 units [heads, n_q] fp32, then per group the fp32
-  // context gradients of K and V.
+  // Backward workspace: the forward's, then -rowsum(dO * O) [heads, n_q]
+  // fp32, -lse / scale [heads, n_q] fp32, then per group the fp32 context
+  // gradients of K and V, then (bf16) per group the dS tiles.
   int64_t bwd_dsum_off, bwd_lse2_off;
   std::vector<int64_t> bwd_dk_off, bwd_dv_off;  // bytes, per group
+  // bf16 plans: per group dS = P * (dP - rowsum) in bf16, written by the
+  // dK/dV kernel and read by the dQ kernel, in 4 KB tiles [head of the
+  // chunk][32-query block][64-key stage of the context's runs][64 key
+  // slots][32 queries], for bwd_ds_heads heads at a time.
+  int32_t bwd_ds_heads = 0;             // heads per backward chunk
+  std::vector<int64_t> bwd_ds_off;      // bytes, per group
+  std::vector<int32_t> bwd_ds_stages;   // 64-key stages of the group's runs
+  std::vector<int32_t> bwd_ds_qblocks;  // 32-query blocks, rounded up to an even count
   int64_t bwd_workspace_bytes;
   std::vector<ScatterJob> scatter_jobs;
 };

@@ -193,31 +193,56 @@ hipError_t launch_bwd_dot(const DotArgs& a, bool bf16, hipStream_t) {
   return hipSuccess;
 }
 
-hipError_t launch_bwd(const BwdArgs& a, int, int, int head_dim, bool bf16, hipStream_t) {
+// Heads the backward launches of one call have covered so far, in order.
+int64_t g_bwd_next_head = 0, g_bwd_heads = 0;
+
+hipError_t launch_bwd(const BwdArgs& a, int dq_blocks, int kv_blocks, int head_dim, bool bf16, hipStream_t) {
   const int64_t rb = a.ld * (bf16 ? 2 : 4);
-  if (a.ld != int64_t{a.num_heads} * head_dim) failure("backward: ld");
+  if (head_dim <= 0 || a.ld % head_dim != 0) failure("backward: ld");
+  const int64_t H = a.ld / head_dim;
+  if (a.head0 == 0) g_bwd_next_head = 0;
+  if (a.num_heads <= 0 || a.head0 != g_bwd_next_head || a.head0 + a.num_heads > H)
+    failure("backward: launch heads");
+  g_bwd_next_head = a.head0 + a.num_heads;
+  g_bwd_heads = H;
   check_range(a.q, a.n_q * rb, "backward q");
   check_range(a.d_out, a.n_q * rb, "backward d_out");
   check_range(a.dq, a.n_q * rb, "backward dq");
-  check_range(a.lse, int64_t{a.num_heads} * a.n_q * 4, "backward lse");
-  check_range(a.dsum, int64_t{a.num_heads} * a.n_q * 4, "backward dsum");
-  check_range(a.lse2, int64_t{a.num_heads} * a.n_q * 4, "backward lse2");
+  check_range(a.lse, H * a.n_q * 4, "backward lse");
+  check_range(a.dsum, H * a.n_q * 4, "backward dsum");
+  check_range(a.lse2, H * a.n_q * 4, "backward lse2");
+  int64_t qblocks = 0, kblocks = 0;
   for (int g = 0; g < a.n_groups; ++g) {
     const BwdGroupArgs& G = a.groups[g];
-    int64_t n = 0;
+    int64_t n = 0, stages = 0;
     for (int r = 0; r < G.n_runs; ++r) {
       check_range(G.runs[r].k, int64_t{G.runs[r].n_tok} * rb, "backward K run");
       check_range(G.runs[r].v, int64_t{G.runs[r].n_tok} * rb, "backward V run");
       n += G.runs[r].n_tok;
+      stages += ceil_div(int64_t{G.runs[r].n_tok}, int64_t{kBwdKS});
     }
     if (n != G.n_kv) failure("backward: runs do not cover the context");
     check_range(G.dk_ctx, int64_t{G.n_kv} * a.ld * 4, "backward dK context");
     check_range(G.dv_ctx, int64_t{G.n_kv} * a.ld * 4, "backward dV context");
+    if (G.dq_block_begin != qblocks || G.kv_block_begin != kblocks) failure("backward: block ranges");
+    qblocks += int64_t{G.n_qblocks} * a.num_heads;
+    kblocks += int64_t{G.n_kblocks} * a.num_heads;
+    if (bf16) {
+      // the dS tiles of every head of the launch, every 32-query block the
+      // dK/dV kernel's 64-query stages write, every 64-key stage of the runs
+      if (G.ds_stages != stages) failure("backward: dS stages");
+      if (int64_t{G.ds_qblocks} < 2 * ceil_div(int64_t{G.q_end - G.q_begin}, int64_t{kBwdQS}) ||
+          int64_t{G.n_qblocks} * kBwdQ > int64_t{G.ds_qblocks} * 32 + kBwdQ - 32)
+        failure("backward: dS query blocks");
+      check_range(G.ds, int64_t{a.num_heads} * G.ds_qblocks * G.ds_stages * kBwdKS * 32 * 2, "backward dS tiles");
+    }
   }
+  if (qblocks != dq_blocks || kblocks != kv_blocks) failure("backward: grid size");
   return hipSuccess;
 }
 
 hipError_t launch_scatter(const ScatterArgs& a, int n_blocks, bool bf16, hipStream_t) {
+  if (g_bwd_next_head != g_bwd_heads) failure("backward: heads not covered before the scatter");
   const int64_t rb = a.ld * (bf16 ? 2 : 4);
   int64_t blocks = 0;
   for (int j = 0; j < a.n_jobs; ++j) {

@@ -302,22 +302,80 @@ def test_tier_calls_checked():
     assert e.value.status == mssa.MSSA_ERR_INVALID_ARG
 
 
+def _context_runs(seg_rows):
+    """Token counts of a context's runs: maximal stretches of consecutive SEG
+    rows read from one buffer, i.e. of one class among sink frames, native
+    history frames, resampled frames (history or window, which share one
+    pooled block) and native window frames."""
+    runs, last = [], None
+    for _, kind, _, _, _, factor, n_tok, _ in seg_rows:
+        cls = "sink" if kind == 0 else ("pooled" if factor > 1 else ("hist" if kind == 1 else "win"))
+        if cls == last:
+            runs[-1] += int(n_tok)
+        else:
+            runs.append(int(n_tok))
+        last = cls
+    return runs
+
+
 def test_backward_workspace_layout():
     """The backward workspace is the forward's, then rowsum(dO * O) and lse in
     log2 units ([heads, n_q] fp32 each), then fp32 K and V context gradients
-    per query group, every region 256-byte aligned."""
+    per query group, then (bf16 plans) per group the dS tiles: 4 KB each, per
+    head, 32-query block (an even count) and 64-key stage of the context's
+    runs; every region 256-byte aligned."""
     def a256(x):
         return (x + 255) // 256 * 256
 
     for d in (128, 64):
-        desc = dict(num_states=4, scales=[1, 1, 2, 4], grid_h=10, grid_w=13, frames_per_state=2,
-                    sink_frames=1, hist_frames=3, num_heads=3, head_dim=d)
+        for dtype in ("bf16", "f32"):
+            desc = dict(num_states=4, scales=[1, 1, 2, 4], grid_h=10, grid_w=13, frames_per_state=2,
+                        sink_frames=1, hist_frames=3, num_heads=3, head_dim=d)
+            plan = mssa.mssa_plan_create(dict(desc, dtype=dtype))
+            info = plan.info()
+            nh, nq = desc["num_heads"], info["n_q"]
+            want = a256(info["workspace_bytes"]) + 2 * a256(nh * nq * 4)
+            want += sum(2 * a256(n_kv * nh * d * 4)
+                        for n_kv in info["n_kv"][: info["n_groups"]])
+            if dtype == "bf16":
+                want += _ds_bytes(plan, nh)
+            assert mssa.mssa_backward_workspace_size(plan) == want
+
+
+def _ds_bytes(plan, nh):
+    """dS tile bytes of a bf16 plan: per group, per head of a chunk, 32-query
+    block (an even count) and 64-key stage of the context's runs, 4 KB; a
+    chunk is as many whole heads as fit in 8 GiB, at least one."""
+    t = mssa.mssa_plan_tables(plan)
+    per_group = []
+    for scale, q0, q1, n_kv in t["QGRP"]:
+        runs = _context_runs([r for r in t["SEG"] if r[0] == scale])
+        assert sum(runs) == n_kv
+        stages = sum(-(-n // 64) for n in runs)
+        qblocks = 2 * -(-(q1 - q0) // 64)
+        per_group.append(qblocks * stages * 4096)
+    heads = max(1, min(nh, (8 << 30) // sum(per_group)))
+    return sum((heads * b + 255) // 256 * 256 for b in per_group)
+
+
+def test_backward_workspace_chunks_heads():
+    """At the three layer workloads the dS tiles of whole heads fit in 8 GiB:
+    all 12 heads of the 1.3B-shaped layer, 8 of the 21-frame history, 2 of the
+    14B-shaped 720p layer's 40."""
+    from paper_2607_20940_amd.workloads import WORKLOADS
+    for name, heads in (("wan13b_layer", 12), ("wan13b_longhist", 8), ("wan14b_720p", 2)):
+        desc = WORKLOADS[name]["desc"]
         plan = mssa.mssa_plan_create(dict(desc, dtype="bf16"))
         info = plan.info()
-        nh, nq = desc["num_heads"], info["n_q"]
-        want = a256(info["workspace_bytes"]) + 2 * a256(nh * nq * 4)
-        want += sum(2 * a256(n_kv * nh * d * 4) for n_kv in info["n_kv"][: info["n_groups"]])
-        assert mssa.mssa_backward_workspace_size(plan) == want
+        nh, nq, d = desc["num_heads"], info["n_q"], desc["head_dim"]
+        base = (info["workspace_bytes"] + 255) // 256 * 256 + 2 * ((nh * nq * 4 + 255) // 256 * 256)
+        base += sum(2 * ((n_kv * nh * d * 4 + 255) // 256 * 256) for n_kv in info["n_kv"][: info["n_groups"]])
+        ds = mssa.mssa_backward_workspace_size(plan) - base
+        assert ds == _ds_bytes(plan, nh)
+        t = mssa.mssa_plan_tables(plan)
+        per_head = sum(2 * -(-(q1 - q0) // 64) * sum(-(-n // 64) for n in _context_runs([r for r in t["SEG"] if r[0] == s]))
+                       * 4096 for s, q0, q1, _ in t["QGRP"])
+        assert heads * per_head <= ds < (heads + 1) * per_head and heads * per_head <= 8 << 30
 
 
 HEAD = mssa.MSSA_PLAN_HEAD_IN_RING
