@@ -193,7 +193,8 @@ void dq_kernel(BwdArgs a) {
   // Per-lane global offsets of this wave's K transfers (the same every
   // stage): transfer t = wave NK + i covers bytes 1024 t of the K rows,
   // logical chunk of the fixed LDS slot, zero past D.  The dS tile is copied
-  // as it lies, 1 KB per transfer.
+  // as it lies, 1 KB per transfer, non-temporal (each element is read once;
+  // -1 % against plain loads, K rows keep their L2 lines).
   const uint32_t row_bytes = static_cast<uint32_t>(ld) * 2;
   uint32_t voff[NK];
 #pragma unroll
@@ -221,8 +222,8 @@ void dq_kernel(BwdArgs a) {
         const i32x4 rd = rsrc_of(tile + j * (BN * 16), static_cast<uint32_t>(nv) * 32);
 #pragma unroll
         for (int i = 0; i < NDS / 2; ++i)
-          dma16(rd, i * 1024 + 16 * lane,
-                __builtin_amdgcn_readfirstlane(base + KT + wave * DT + j * (DT / 2) + i * 1024));
+          dma16_nt(rd, i * 1024 + 16 * lane,
+                   __builtin_amdgcn_readfirstlane(base + KT + wave * DT + j * (DT / 2) + i * 1024));
       }
     }
   };

@@ -50,6 +50,16 @@ __device__ inline void dma16(i32x4 rsrc, uint32_t voff, uint32_t lds_addr) {
 #pragma clang diagnostic pop
 }
 
+// As dma16 for data read once (nt: streamed past the caches' normal
+// retention, so it does not displace operands that are read again).
+__device__ inline void dma16_nt(i32x4 rsrc, uint32_t voff, uint32_t lds_addr) {
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen nt lds"
+               :: "s"(lds_addr), "v"(voff), "s"(rsrc) : "memory", "m0");
+#pragma clang diagnostic pop
+}
+
 // As dma16 for 4 bytes per lane (buffer_load_dword ... lds): lane i's dword
 // at buffer offset voff lands at LDS byte address lds_addr + 4 i.
 __device__ inline void dma4(i32x4 rsrc, uint32_t voff, uint32_t lds_addr) {
