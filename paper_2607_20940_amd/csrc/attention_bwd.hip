@@ -85,28 +85,36 @@ struct Lay {
 
 // ------------------------------------------------------------------ rowsum(dO * O)
 
+// One row (query, head) per group of L = head_dim * sizeof(T) / 16 lanes (8,
+// 16 or 32; rows are contiguous, so a wave reads 1-2 KB in one piece), each
+// lane 16 bytes of O and dO; the group's partial sums meet by lane
+// exchanges in a fixed order.
 template <typename T>
 __global__ __launch_bounds__(kDotThreads) void dot_kernel(DotArgs a) {
   constexpr int N = 16 / sizeof(T);
   typedef T vecT __attribute__((ext_vector_type(N)));
-  const int64_t r = static_cast<int64_t>(blockIdx.x) * kDotThreads + threadIdx.x;
-  if (r >= static_cast<int64_t>(a.n_q) * a.num_heads) return;
-  const int q = static_cast<int>(r / a.num_heads), h = static_cast<int>(r % a.num_heads);
-  const int64_t off = static_cast<int64_t>(q) * a.ld + static_cast<int64_t>(h) * a.head_dim;
-  const T* o = static_cast<const T*>(a.out) + off;
-  const T* g = static_cast<const T*>(a.d_out) + off;
+  const int L = a.head_dim / N;
+  const int64_t gt = static_cast<int64_t>(blockIdx.x) * kDotThreads + threadIdx.x;
+  const int64_t r = gt / L, rows = static_cast<int64_t>(a.n_q) * a.num_heads;
+  const int c = static_cast<int>(gt % L);
   float acc = 0.f;
-  for (int d = 0; d < a.head_dim; d += N) {
-    const vecT ov = *reinterpret_cast<const vecT*>(o + d);
-    const vecT gv = *reinterpret_cast<const vecT*>(g + d);
+  if (r < rows) {
+    // rows are contiguous: row r = (query r / heads, head r % heads) at r * head_dim
+    const int64_t off = r * a.head_dim + c * N;
+    const vecT ov = *reinterpret_cast<const vecT*>(static_cast<const T*>(a.out) + off);
+    const vecT gv = *reinterpret_cast<const vecT*>(static_cast<const T*>(a.d_out) + off);
 #pragma unroll
     for (int e = 0; e < N; ++e) acc = __builtin_fmaf(static_cast<float>(ov[e]), static_cast<float>(gv[e]), acc);
   }
-  // Both statistics are stored negated, as the dK/dV kernel's accumulator
-  // inputs: -rowsum, and -lse / scale (the row's log-sum-exp in units of the
-  // unscaled scores q k^T).
-  a.dsum[static_cast<int64_t>(h) * a.n_q + q] = -acc;
-  if (a.lse) a.lse2[static_cast<int64_t>(h) * a.n_q + q] = -a.lse[static_cast<int64_t>(h) * a.n_q + q] * a.inv_scale;
+  for (int m = L >> 1; m >= 1; m >>= 1) acc += __shfl_xor(acc, m);
+  if (r < rows && c == 0) {
+    const int q = static_cast<int>(r / a.num_heads), h = static_cast<int>(r % a.num_heads);
+    // Both statistics are stored negated, as the dK/dV kernel's accumulator
+    // inputs: -rowsum, and -lse / scale (the row's log-sum-exp in units of the
+    // unscaled scores q k^T).
+    a.dsum[static_cast<int64_t>(h) * a.n_q + q] = -acc;
+    if (a.lse) a.lse2[static_cast<int64_t>(h) * a.n_q + q] = -a.lse[static_cast<int64_t>(h) * a.n_q + q] * a.inv_scale;
+  }
 }
 
 // ------------------------------------------------------------------ bf16 kernels
@@ -757,7 +765,10 @@ __global__ __launch_bounds__(kPoolThreads) void scatter_kernel(ScatterArgs a) {
 hipError_t launch_bwd_dot(const DotArgs& a, bool bf16, hipStream_t stream) {
   const int64_t rows = static_cast<int64_t>(a.n_q) * a.num_heads;
   if (rows == 0) return hipSuccess;
-  const int blocks = static_cast<int>((rows + kDotThreads - 1) / kDotThreads);
+  if (a.ld != static_cast<int64_t>(a.num_heads) * a.head_dim) return hipErrorInvalidValue;
+  const int64_t threads = rows * (a.head_dim * (bf16 ? 2 : 4) / 16);
+  if ((threads + kDotThreads - 1) / kDotThreads > 0x7fffffff) return hipErrorInvalidValue;
+  const int blocks = static_cast<int>((threads + kDotThreads - 1) / kDotThreads);
   if (bf16)
     hipLaunchKernelGGL(dot_kernel<__bf16>, dim3(blocks), dim3(kDotThreads), 0, stream, a);
   else
