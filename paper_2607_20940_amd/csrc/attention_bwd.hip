@@ -146,8 +146,12 @@ void dq_kernel(BwdArgs a) {
   constexpr int BN = kBwdKS;                       // keys per stage
   constexpr int NW = kBwdQThreads / 64;            // waves of 32 queries
   constexpr int KT = BN * 256;                     // bytes of the stage's K rows (256-byte swizzled rows)
-  constexpr int DT = BN * 64;                      // bytes of one wave's dS tile (64-byte rows)
-  constexpr int STB = KT + NW * DT;
+  constexpr int DT = BN * 64;                      // bytes of one wave's dS tile
+  // The tile's LDS footprint: its second half sits 128 bytes further on, so
+  // that the two halves' rows a transposing read takes together fall in
+  // different banks.
+  constexpr int DTL = DT + 128;
+  constexpr int STB = KT + NW * DTL;
   constexpr int NK = KT / 1024 / NW;               // 1 KB K transfers per wave and stage
   constexpr int NDS = DT / 1024;                   // 1 KB dS transfers per wave and stage
   static_assert(NK * 1024 * NW == KT && NW * 32 == kBwdQ && BN % 32 == 0 && NDS % 2 == 0, "stage shape");
@@ -231,7 +235,7 @@ void dq_kernel(BwdArgs a) {
 #pragma unroll
         for (int i = 0; i < NDS / 2; ++i)
           dma16_nt(rd, i * 1024 + 16 * lane,
-                   __builtin_amdgcn_readfirstlane(base + KT + wave * DT + j * (DT / 2) + i * 1024));
+                   __builtin_amdgcn_readfirstlane(base + KT + wave * DTL + j * (DT / 2 + 128) + i * 1024));
       }
     }
   };
@@ -249,7 +253,7 @@ void dq_kernel(BwdArgs a) {
   int k_rd[DB][2], d_rd[2];
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
-    d_rd[h] = ((t_col >> 3) & 1) * (BN * 16) + (t_lane + 8 * h) * 16 + (t_col >> 4) * 8 + (t_col & 7);
+    d_rd[h] = ((t_col >> 3) & 1) * (BN * 16 + 64) + (t_lane + 8 * h) * 16 + (t_col >> 4) * 8 + (t_col & 7);
 #pragma unroll
     for (int db = 0; db < DB; ++db) k_rd[db][h] = swz(t_lane + 8 * h, db * 32 + t_col);
   }
@@ -260,7 +264,7 @@ void dq_kernel(BwdArgs a) {
   };
   auto stage = [&](int buf) {
     const __bf16* Ks = reinterpret_cast<const __bf16*>(lds + buf * STB);
-    const __bf16* Ds = reinterpret_cast<const __bf16*>(lds + buf * STB + KT + wave * DT);
+    const __bf16* Ds = reinterpret_cast<const __bf16*>(lds + buf * STB + KT + wave * DTL);
 #pragma unroll
     for (int rb = 0; rb < BN / 16; ++rb) {
       const bf16x8 dst = tr(Ds + rb * 16 * 16, d_rd[0], d_rd[1]);
