@@ -373,10 +373,13 @@ void dkdv_kernel(BwdArgs a) {
   const int64_t ld = a.ld, hoff = static_cast<int64_t>(head) * D;
   const float c = a.scale_log2e;
 
-  // Where B stores its key's dS: the key's run, 64-key stage of the run
-  // (the stages the dQ kernel walks) and slot in the stage; the lane's 16
-  // queries of a 32-query block at positions 16 hh .. 16 hh + 15 of the row.
-  __bf16* ds_lane = nullptr;
+  // Where B stores its key's dS: byte offset, in the tiles of a 32-query
+  // block, of the key's 64-key stage (its run's stages, as the dQ kernel
+  // walks them), slot and the lane's 8 queries of each tile half (16 hh,
+  // 16 hh + 8 .. of the row's 32 positions); the same offset every stage.
+  // Keys past the context point past the range: the range check drops
+  // their stores, so the store needs no branch.
+  uint32_t ds_voff = kPastEnd;
   if (role != 0 && k_ok) {
     int j = key, st = 0, r = 0;
     while (r + 1 < G.n_runs && j >= G.runs[r].n_tok) {
@@ -384,11 +387,11 @@ void dkdv_kernel(BwdArgs a) {
       j -= G.runs[r].n_tok;
       ++r;
     }
-    ds_lane = static_cast<__bf16*>(G.ds) +
-              (static_cast<int64_t>(hl) * G.ds_qblocks * G.ds_stages + st + j / kBwdKS) * (kBwdKS * 32) +
-              (j % kBwdKS) * 16 + 8 * hh;
+    ds_voff = static_cast<uint32_t>((st + j / kBwdKS) * (kBwdKS * 64) + (j % kBwdKS) * 32 + 16 * hh);
   }
-  const int64_t ds_qstride = static_cast<int64_t>(G.ds_stages) * (kBwdKS * 32);
+  const uint32_t ds_qbytes = static_cast<uint32_t>(G.ds_stages) * (kBwdKS * 64);  // one 32-query block's tiles
+  const __bf16* const ds_head =
+      static_cast<const __bf16*>(G.ds) + static_cast<int64_t>(hl) * G.ds_qblocks * G.ds_stages * (kBwdKS * 32);
 
   // B operand of the wave's row product: this lane's key (K for A, V for B),
   // 8 channels of its half-wave per k step.
@@ -406,7 +409,9 @@ void dkdv_kernel(BwdArgs a) {
   f32x16 acc[DB];  // dV^T (A) or dK^T (B)
 #pragma unroll
   for (int db = 0; db < DB; ++db) acc[db] = f32x16{};
-  f32x16 s[NQB];       // S_t (A) or dP_t (B)
+  f32x16 s[NQB];       // S_t (A) or dP_t (B); zero before the first stage
+#pragma unroll
+  for (int qb = 0; qb < NQB; ++qb) s[qb] = f32x16{};
   bf16x8 w[NQB][2];    // P_t (A) or dS_{t-1} (B), packed as the B operand of the accumulating product
 #pragma unroll
   for (int qb = 0; qb < NQB; ++qb) w[qb][0] = w[qb][1] = bf16x8{};
@@ -543,8 +548,12 @@ void dkdv_kernel(BwdArgs a) {
       for (int h = 0; h < 2; ++h) asm volatile("" : "+v"(w[qb][h]));
   };
   // B: dS = P dP' (dP' = dP - rowsum) of stage ts into w, and to the dS
-  // tiles of the stage's 32-query blocks 2 ts + qb for the dQ kernel.
+  // tiles of the stage's 32-query blocks 2 ts + qb for the dQ kernel.  Stage
+  // -1 (the first phase) computes exact zeros from the zeroed P block and
+  // dP registers, and its buffer range is empty, so nothing is stored.
   auto softmax_b = [&](int ts) {
+    const i32x4 rd = rsrc_of(ds_head + static_cast<int64_t>(NQB * max(ts, 0)) * G.ds_stages * (kBwdKS * 32),
+                             ts >= 0 ? NQB * ds_qbytes : 0u);
 #pragma unroll
     for (int qb = 0; qb < NQB; ++qb) {
       const bf16x8 p0 = pex[(qb * 2) * 64], p1 = pex[(qb * 2 + 1) * 64];
@@ -553,11 +562,8 @@ void dkdv_kernel(BwdArgs a) {
         const float p = static_cast<float>((e < 8 ? p0 : p1)[e & 7]);
         w[qb][e >> 3][e & 7] = static_cast<__bf16>(p * s[qb][e]);
       }
-      if (ds_lane) {
-        __bf16* dp = ds_lane + (NQB * ts + qb) * ds_qstride;
-        __builtin_nontemporal_store(w[qb][0], reinterpret_cast<bf16x8*>(dp));
-        __builtin_nontemporal_store(w[qb][1], reinterpret_cast<bf16x8*>(dp + kBwdKS * 16));
-      }
+      bstore16_nt<0>(__builtin_bit_cast(i32x4, w[qb][0]), rd, ds_voff, qb * ds_qbytes);
+      bstore16_nt<kBwdKS * 32>(__builtin_bit_cast(i32x4, w[qb][1]), rd, ds_voff, qb * ds_qbytes);
     }
 #pragma unroll
     for (int qb = 0; qb < NQB; ++qb)
@@ -578,6 +584,10 @@ void dkdv_kernel(BwdArgs a) {
     bf16x8* z = reinterpret_cast<bf16x8*>(lds + (NBUF - 1) * STB);
 #pragma unroll
     for (int i = 0; i < 2 * QT / 16 / kBwdKVThreads; ++i) z[tid + i * kBwdKVThreads] = bf16x8{};
+    bf16x8* zp = reinterpret_cast<bf16x8*>(lds + NBUF * STB);  // the P exchange blocks
+    static_assert(4 * PXB % (16 * kBwdKVThreads) == 0, "P blocks zeroed whole");
+#pragma unroll
+    for (int i = 0; i < 4 * PXB / 16 / kBwdKVThreads; ++i) zp[tid + i * kBwdKVThreads] = bf16x8{};
   }
   // this wave's transfers of one stage (the stage issued last may stay in flight)
   auto wait_all_but_last = [&]() {
@@ -613,7 +623,7 @@ void dkdv_kernel(BwdArgs a) {
       else
         wait_vmcnt<0>();
     } else {
-      if (t >= 1) softmax_b(t - 1);
+      softmax_b(t - 1);
     }
     __syncthreads();
   }

@@ -79,6 +79,15 @@ __device__ inline void dma16_soff(i32x4 rsrc, uint32_t voff, uint32_t soff, uint
 #pragma clang diagnostic pop
 }
 
+// Store of lane i's 16 bytes at buffer offset voff + soff + IMM
+// (buffer_store_dwordx4, non-temporal: data that another kernel reads once);
+// lanes whose offset is past the buffer's range store nothing.
+template <int IMM>
+__device__ inline void bstore16_nt(i32x4 data, i32x4 rsrc, uint32_t voff, uint32_t soff) {
+  asm volatile("buffer_store_dwordx4 %0, %1, %2, %3 offen offset:%4 nt"
+               :: "v"(data), "v"(voff), "s"(rsrc), "s"(soff), "n"(IMM) : "memory");
+}
+
 // s_waitcnt vmcnt(N) alone (gfx9 encoding: expcnt and lgkmcnt at their maxima).
 template <int N>
 __device__ inline void wait_vmcnt() {

@@ -290,7 +290,9 @@ mssa_status build_plan(const mssa_plan_desc& d, int slots, int attention_blocks,
       for (const Run& r : p.runs[g]) stages += (r.n_tok + kBwdKS - 1) / kBwdKS;
       const int64_t nq = p.groups[g].q_end - p.groups[g].q_begin;
       const int64_t qblocks = 2 * ((nq + kBwdQS - 1) / kBwdQS);
-      if (stages > 0x7fffffff || qblocks > 0x7fffffff) {
+      // the dK/dV kernel addresses a stage's two 32-query blocks of tiles
+      // with 32-bit offsets
+      if (stages * 2 * kBwdKS * 64 > 0xffffffffLL || qblocks > 0x7fffffff) {
         err = "backward dS buffer too large";
         return MSSA_ERR_UNSUPPORTED;
       }
