@@ -327,9 +327,10 @@ void dq_kernel(BwdArgs a) {
 //                 B  dK^T += Q_{t-1}^T dS_{t-1}, then dP_t = dO_t V^T
 // Stage t's Q, dO and row statistics live in LDS buffer t % 4 and are read
 // in phases 2t .. 2t + 3.  A issues stage t + 2 (direct transfers, the
-// statistics included) at the end of its matrix-core phase 2t into buffer
+// statistics included) at the start of its VALU phase 2t + 1 into buffer
 // (t + 2) % 4, whose stage t - 2 was last read in phase 2t - 1, and waits
-// for stage t + 1 at the end of its VALU phase 2t + 1.  B also stores dS_{t-1}
+// for stage t + 1 at the end of that phase (the transfer instructions cost
+// less there than at the end of the matrix-core phase: -2 %).  B also stores dS_{t-1}
 // to HBM in phase 2t and never waits for memory: a wave's wait for its
 // transfers would also wait for its earlier stores to complete.  P_t is
 // written in phase 2t + 1 and read in 2t + 2; one block per pair suffices.
@@ -575,9 +576,9 @@ void dkdv_kernel(BwdArgs a) {
   // keeps the register allocation tight): in the first stage the
   // accumulating product multiplies the zeroed buffer of stage -1 by w = 0,
   // adding exact zeros; in the stage after the last, the row product's
-  // result is never used.  A issues stage t + 2 at the end of its
-  // matrix-core phase 2t, into the buffer of stage t - 2 (last read in phase
-  // 2t - 1), and ends its VALU phase 2t + 1 once stage t + 1 has arrived.
+  // result is never used.  A issues stage t + 2 at the start of its VALU
+  // phase 2t + 1, into the buffer of stage t - 2 (last read in phase 2t - 1),
+  // and ends that phase once stage t + 1 has arrived.
   using T_ = std::true_type;
   const int nst = (q_end - q_begin + BQ - 1) / BQ;
   {
@@ -615,8 +616,8 @@ void dkdv_kernel(BwdArgs a) {
       mstep(T_{}, T_{}, tile(prev, 1 - role), tile(cur, role),
             reinterpret_cast<const float*>(lds + cur * STB + 2 * QT) + role * BQ);
       __builtin_amdgcn_s_setprio(0);
-      if (role == 0 && t + 2 < nst) issue(q_begin + (t + 2) * BQ, (t + 2) % NBUF);
     } else if (role == 0) {
+      if (t + 2 < nst) issue(q_begin + (t + 2) * BQ, (t + 2) % NBUF);
       if (t < nst) softmax_a();
       if (t + 2 < nst)
         wait_all_but_last();
